@@ -1,0 +1,358 @@
+"""Float64 reference of the PIPO pair-in/pair-out path: TEST INFRASTRUCTURE ONLY.
+
+Only the tests, ``__graft_entry__.smoke()`` and ``bench.py``'s ``cpu_baseline``
+leg may use this module.  It is deliberately plain: every function follows one
+definition of the paper, with NumPy matrix products as the only library steps,
+and there is no blocking or fusion beyond looping over independent heads and
+query rows.
+
+What the paper fixes (Sec. 3.1-3.2, App. B) and the readings taken where it is
+silent:
+
+* Pair-in (eq. 1, App. B.1 Table 4 "Linear"): ``z = W_c [x_a; x_b] + b_c``.
+  The configurations fix the Linear variant.  A prompt of odd length gets the
+  PAD token appended so that PAD sits at the odd slot of the last pair
+  (App. C.1, random PAD injection); a prompt of n tokens gives ceil(n/2)
+  latents.  PAD is the reserved last vocabulary row.
+* Backbone (eq. 2): a dense pre-norm decoder over latent positions:
+  ``x += W_o Attn(RoPE(W_q n), RoPE(W_k n), W_v n)`` with ``n = RMSNorm(x)``,
+  grouped-query attention with query head ``h`` reading KV group
+  ``h * n_kv // n_q``, scale ``1/sqrt(d)``, causal over latent positions;
+  then ``x += W_down(SiLU(W_gate n) * W_up n)``.  RoPE uses the latent index
+  as position, rotate-half pairs ``(j, j + d/2)`` and frequencies
+  ``base**(-2j/d)``.  No biases, no QK norm.
+* Pair-out (eqs. 3-5, App. B.2): ``h_b`` is the last residual state before the
+  final norm; ``logits_b = E RMSNorm(h_b; g_f)`` with the LM head tied to the
+  embedding E.  The MTP head is ``h_d = W_fc [RMSNorm(h_b; g_mh);
+  RMSNorm(E[b]; g_me)]`` with W_fc: 2H -> H; the decoder layer App. B.2
+  places after W_fc is omitted because the configurations fix a one-linear
+  MTP head; ``logits_d = E RMSNorm(h_d; g_mo)``.
+* Confidence (eq. 6, App. B.3): ``c = sigmoid(w_c . RMSNorm([h_b; h_d]; g_c))``;
+  a single linear replaces App. B.3's two-layer MLP, as the configurations
+  fix it.  The draft is accepted iff ``c >= tau`` (equality accepts), and the
+  next input pair is ``(b, d)`` if accepted else ``(b, PAD)`` (Sec. 3.2).
+* Token selection: greedy argmax with ties to the lowest id; or temperature
+  plus nucleus (top-p): ``p = softmax(logits / T)``; the threshold
+  ``theta*`` is the largest value among the ``p_j`` whose upper mass
+  ``sum_{p_j >= theta} p_j`` reaches ``top_p`` (all tokens if none does);
+  the nucleus is ``{j : p_j >= theta*}``, of mass ``M``; with ``t = u M`` the
+  token is the first id, scanning ids upwards through the nucleus, at which
+  the running mass exceeds ``t`` (the last nucleus id if rounding leaves
+  none).  ``u`` is an input.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from synth import rspec
+from synth.configs import ModelConfig, model_tensor_shapes
+
+F64 = np.float64
+
+
+# ---------------------------------------------------------------- primitives
+
+def rms_norm(x, g, eps):
+    """RMSNorm over the last axis: ``x / sqrt(mean(x^2) + eps) * g``."""
+    x = np.asarray(x, dtype=F64)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * np.asarray(g, F64)
+
+
+def rope_cos_sin(pos, head_dim, base):
+    """cos/sin of the angles ``p * base**(-2j/d)``, j < d/2, for positions ``pos``."""
+    half = head_dim // 2
+    j = np.arange(half, dtype=F64)
+    inv_freq = np.power(F64(base), -2.0 * j / head_dim)
+    ang = np.asarray(pos, dtype=F64)[..., None] * inv_freq
+    return np.cos(ang), np.sin(ang)
+
+
+def apply_rope(x, cos, sin):
+    """Rotate-half RoPE on the last axis of ``x`` (pairs ``j`` and ``j + d/2``).
+
+    ``cos``/``sin`` broadcast against ``x[..., :d/2]``.
+    """
+    half = x.shape[-1] // 2
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def silu(u):
+    """SiLU(u) = u / (1 + exp(-u))."""
+    return u / (1.0 + np.exp(-u))
+
+
+def softmax(s, axis=-1):
+    m = np.max(s, axis=axis, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=axis, keepdims=True)
+
+
+def prompt_pairs(tokens, pad_id):
+    """Eq. 1's pairing of a prompt: PAD appended at the odd slot if n is odd."""
+    t = [int(v) for v in tokens]
+    if len(t) % 2:
+        t.append(int(pad_id))
+    return np.asarray(t, dtype=np.int64).reshape(-1, 2)
+
+
+def compress(E, W_c, b_c, pairs):
+    """Pair-in compressor (eq. 1, Linear variant): ``W_c [E[a]; E[b]] + b_c``."""
+    pairs = np.asarray(pairs).reshape(-1, 2)
+    cat = np.concatenate([E[pairs[:, 0]], E[pairs[:, 1]]], axis=-1)
+    return cat @ np.asarray(W_c, F64).T + np.asarray(b_c, F64)
+
+
+def attention_decode(q, K, V):
+    """One query position against a causal prefix, grouped-query.
+
+    ``q``: [n_q, d]; ``K``, ``V``: [n_kv, T, d] holding positions 0..T-1 (the
+    query's own position last).  Returns ``o`` [n_q, d] and the probability
+    rows [n_q, T].
+    """
+    n_q, d = q.shape
+    n_kv = K.shape[0]
+    out = np.empty((n_q, d), dtype=F64)
+    probs = np.empty((n_q, K.shape[1]), dtype=F64)
+    for h in range(n_q):
+        g = h * n_kv // n_q
+        a = softmax(K[g] @ q[h] / np.sqrt(d))
+        probs[h] = a
+        out[h] = a @ V[g]
+    return out, probs
+
+
+def attention_causal(Q, K, V, block=2048):
+    """Causal grouped-query attention over a whole sequence.
+
+    ``Q``: [n_q, T, d]; ``K``, ``V``: [n_kv, T, d].  Query row ``i`` attends to
+    keys ``0..i``.  Rows are independent; they are processed ``block`` at a
+    time only to bound memory.
+    """
+    n_q, T, d = Q.shape
+    n_kv = K.shape[0]
+    out = np.empty_like(Q, dtype=F64)
+    for h in range(n_q):
+        g = h * n_kv // n_q
+        for r0 in range(0, T, block):
+            r1 = min(T, r0 + block)
+            s = Q[h, r0:r1] @ K[g, :r1].T / np.sqrt(d)
+            rows = np.arange(r0, r1)[:, None]
+            cols = np.arange(r1)[None, :]
+            s = np.where(cols <= rows, s, -np.inf)
+            out[h, r0:r1] = softmax(s) @ V[g, :r1]
+    return out
+
+
+def lm_logits(E, g, h, eps):
+    """Tied LM head (eq. 3): ``E RMSNorm(h; g)``."""
+    return rms_norm(h, g, eps) @ E.T
+
+
+def mtp_hidden(W_fc, g_h, g_e, h_b, e_tok, eps):
+    """MTP head (eq. 4, App. B.2, one linear): ``W_fc [RMSNorm(h_b); RMSNorm(x)]``."""
+    u = np.concatenate([rms_norm(h_b, g_h, eps), rms_norm(e_tok, g_e, eps)], axis=-1)
+    return u @ np.asarray(W_fc, F64).T
+
+
+def confidence(w_c, g_c, h_b, h_d, eps):
+    """Confidence head (eq. 6, App. B.3 as one linear): returns (s, sigmoid(s))."""
+    s = rms_norm(np.concatenate([h_b, h_d], axis=-1), g_c, eps) @ np.asarray(w_c, F64)
+    return s, 1.0 / (1.0 + np.exp(-s))
+
+
+def gate(c, tau):
+    """Accept the draft iff ``c >= tau`` (Sec. 3.2)."""
+    return bool(c >= tau)
+
+
+def select_greedy(logits):
+    """argmax; exact ties go to the lowest id."""
+    return int(np.argmax(logits))
+
+
+def select_top_p(logits, temperature, top_p, u):
+    """Temperature + nucleus sampling by inverse CDF in id order (see header)."""
+    y = np.asarray(logits, F64) / F64(temperature)
+    e = np.exp(y - np.max(y))
+    p = e / np.sum(e)
+    desc = np.sort(p)[::-1]
+    upper = np.cumsum(desc)
+    # mass(theta) counts every p_j >= theta, so a tie group contributes whole:
+    # evaluate the cumulative sum at the last member of each value's group.
+    last_of_group = np.searchsorted(-desc, -desc, side="right") - 1
+    ok = upper[last_of_group] >= top_p
+    theta = desc[np.argmax(ok)] if ok.any() else desc[-1]
+    nucleus = np.nonzero(p >= theta)[0]
+    mass = np.sum(p[nucleus])
+    t = u * mass
+    run = np.cumsum(p[nucleus])
+    hit = np.nonzero(run > t)[0]
+    return int(nucleus[hit[0]] if hit.size else nucleus[-1])
+
+
+# ------------------------------------------------------------------- weights
+
+class OracleWeights:
+    """All tensors of one model as float64 arrays in logical ``[out][in]`` order."""
+
+    def __init__(self, cfg: ModelConfig, tensors: dict):
+        self.cfg = cfg
+        self.t = {k: np.asarray(v, dtype=F64) for k, v in tensors.items()}
+
+    @classmethod
+    def generate(cls, cfg: ModelConfig, seed: int = 0, precision: str = "bf16"):
+        """R-spec weights; ``precision`` 'bf16' rounds matrices to bf16 first."""
+        tensors = {}
+        for name, shape in model_tensor_shapes(cfg).items():
+            tid = (rspec.TENSOR_IDS[name] if "." not in name
+                   else rspec.layer_tid(int(name.split(".")[0][1:]), name.split(".")[1]))
+            base = name.split(".")[-1]
+            if base.startswith("g_"):
+                v = rspec.gain_values(seed, tid, shape[0], cfg.gain_mode)
+            else:
+                v = rspec.weight_tensor(seed, tid, shape)
+            if precision == "bf16":
+                v = rspec.bf16_round(v)
+            tensors[name] = v.astype(F64)
+        return cls(cfg, tensors)
+
+    def __getitem__(self, k):
+        return self.t[k]
+
+    def layer(self, li):
+        return {k.split(".", 1)[1]: v for k, v in self.t.items() if k.startswith(f"l{li}.")}
+
+
+# ------------------------------------------------------------------ backbone
+
+def _layer_qkv(cfg, L, x, pos):
+    n = rms_norm(x, L["g_attn"], cfg.rms_eps)
+    T = n.shape[0]
+    q = (n @ L["wq"].T).reshape(T, cfg.n_q_heads, cfg.head_dim).transpose(1, 0, 2)
+    k = (n @ L["wk"].T).reshape(T, cfg.n_kv_heads, cfg.head_dim).transpose(1, 0, 2)
+    v = (n @ L["wv"].T).reshape(T, cfg.n_kv_heads, cfg.head_dim).transpose(1, 0, 2)
+    cos, sin = rope_cos_sin(pos, cfg.head_dim, cfg.rope_base)
+    return apply_rope(q, cos, sin), apply_rope(k, cos, sin), v
+
+
+def _layer_ffn(cfg, L, x):
+    n = rms_norm(x, L["g_ffn"], cfg.rms_eps)
+    return x + (silu(n @ L["wgate"].T) * (n @ L["wup"].T)) @ L["wdown"].T
+
+
+def backbone_full(W: OracleWeights, Z):
+    """Eq. 2 by brute force: all latent positions 0..T-1 from scratch.
+
+    Returns the final residual states [T, H] (before the final norm) and the
+    per-layer caches ``[(K, V)]`` with K, V of shape [n_kv, T, d].
+    """
+    cfg = W.cfg
+    x = np.asarray(Z, F64).copy()
+    T = x.shape[0]
+    caches = []
+    for li in range(cfg.n_layers):
+        L = W.layer(li)
+        q, k, v = _layer_qkv(cfg, L, x, np.arange(T))
+        o = attention_causal(q, k, v)
+        x = x + o.transpose(1, 0, 2).reshape(T, cfg.q_dim) @ L["wo"].T
+        x = _layer_ffn(cfg, L, x)
+        caches.append((k, v))
+    return x, caches
+
+
+def backbone_step(W: OracleWeights, z, pos, caches):
+    """Eq. 2 incrementally: one latent at position ``pos`` against the cache.
+
+    ``caches`` is a list per layer of ``[K, V]`` arrays [n_kv, pos, d]; the new
+    key/value are appended in place.  Returns the final residual state [H].
+    """
+    cfg = W.cfg
+    x = np.asarray(z, F64).reshape(1, -1).copy()
+    for li in range(cfg.n_layers):
+        L = W.layer(li)
+        q, k, v = _layer_qkv(cfg, L, x, np.array([pos]))
+        K = np.concatenate([caches[li][0], k], axis=1)
+        V = np.concatenate([caches[li][1], v], axis=1)
+        caches[li][0], caches[li][1] = K, V
+        o, _ = attention_decode(q[:, 0], K, V)
+        x = x + o.reshape(1, cfg.q_dim) @ L["wo"].T
+        x = _layer_ffn(cfg, L, x)
+    return x[0]
+
+
+# ------------------------------------------------------------------- session
+
+@dataclass
+class Sampling:
+    tau: float
+    temperature: float = 0.0       # <= 0: greedy
+    top_p: float = 1.0
+    seeds: tuple = ()              # one per sequence (sampling only)
+
+
+class PipoOracle:
+    """A batch of independent PIPO sequences: prefill, then pair-decode steps."""
+
+    def __init__(self, W: OracleWeights):
+        self.W = W
+        self.cfg = W.cfg
+
+    # heads: eqs. 3-6 and the gate, for one sequence
+    def heads(self, h_b, seq, step, force_b=None):
+        cfg, W, smp = self.cfg, self.W, self.sampling
+        eps = cfg.rms_eps
+        logits_b = lm_logits(W["embed"], W["g_final"], h_b, eps)
+        b = self._select(logits_b, seq, step, 0)
+        b_used = b if force_b is None else int(force_b)
+        h_d = mtp_hidden(W["w_fc"], W["g_mtp_h"], W["g_mtp_e"], h_b, W["embed"][b_used], eps)
+        logits_d = lm_logits(W["embed"], W["g_mtp_o"], h_d, eps)
+        d = self._select(logits_d, seq, step, 1)
+        s, c = confidence(W["w_conf"], W["g_conf"], h_b, h_d, eps)
+        return dict(tok_b=b, tok_d=d, s=float(s), conf=float(c), accept=gate(c, smp.tau),
+                    logits_b=logits_b, logits_d=logits_d, h_b=h_b, h_d=h_d)
+
+    def _select(self, logits, seq, step, slot):
+        smp = self.sampling
+        if smp.temperature <= 0:
+            return select_greedy(logits)
+        u = rspec.uniform_draw(smp.seeds[seq], step, slot)
+        return select_top_p(logits, smp.temperature, smp.top_p, u)
+
+    def prefill(self, prompts, sampling: Sampling, force_b=None):
+        """Compressed-prompt prefill of every sequence; returns the first pair."""
+        self.sampling = sampling
+        W, cfg = self.W, self.cfg
+        self.caches, self.length, self.step_idx, self.next_pairs = [], [], [], []
+        out = []
+        for i, prompt in enumerate(np.asarray(prompts)):
+            pairs = prompt_pairs(prompt, cfg.pad_id)
+            Z = compress(W["embed"], W["w_comp"], W["b_comp"], pairs)
+            X, caches = backbone_full(W, Z)
+            self.caches.append([[k, v] for k, v in caches])
+            self.length.append(len(pairs))
+            rec = self.heads(X[-1], i, 0, None if force_b is None else force_b[i])
+            out.append(rec)
+            self.step_idx.append(1)
+            self.next_pairs.append(self._next_pair(rec))
+        return out
+
+    def _next_pair(self, rec):
+        return (rec["tok_b"], rec["tok_d"] if rec["accept"] else self.cfg.pad_id)
+
+    def decode_step(self, in_pairs=None, force_b=None):
+        """One pair step for every sequence; ``in_pairs`` teacher-forces the input."""
+        W = self.W
+        out = []
+        for i in range(len(self.caches)):
+            pair = self.next_pairs[i] if in_pairs is None else tuple(int(v) for v in in_pairs[i])
+            z = compress(W["embed"], W["w_comp"], W["b_comp"], np.array([pair]))[0]
+            h_b = backbone_step(W, z, self.length[i], self.caches[i])
+            self.length[i] += 1
+            rec = self.heads(h_b, i, self.step_idx[i], None if force_b is None else force_b[i])
+            out.append(rec)
+            self.step_idx[i] += 1
+            self.next_pairs[i] = self._next_pair(rec)
+        return out

@@ -1,0 +1,408 @@
+"""Pins of the oracle against facts the paper and the mathematics fix.
+
+Each test checks one part of the oracle against something other than itself:
+published generator outputs, library routines that implement a textbook
+definition (PyTorch CPU float64), closed forms, invariants, brute force, and
+the paper's stated rules (latent length, PAD slot, gate at equality, tau
+extremes).  None of these tests needs a GPU.
+"""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from synth import rspec
+from synth.configs import ModelConfig, TINY
+from oracle import pipo_oracle as O
+
+SMALL = ModelConfig(n_layers=2, hidden=64, n_q_heads=4, n_kv_heads=2, head_dim=16,
+                    ffn=96, vocab=64, rope_base=1e4, rms_eps=1e-6, gain_mode=1)
+
+
+@pytest.fixture(scope="module")
+def small_w():
+    return O.OracleWeights.generate(SMALL, seed=3, precision="bf16")
+
+
+# ------------------------------------------------------------ input generator
+
+def test_splitmix64_published_outputs():
+    # SplitMix64 seeded with 0 returns these three words first (published
+    # reference outputs of the generator).
+    g = 0x9E3779B97F4A7C15
+    outs = [rspec.splitmix64((k * g) & ((1 << 64) - 1)) for k in range(3)]
+    assert outs == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+def test_weight_distribution_moments():
+    w = rspec.weight_values(0, 0, 0, 1 << 21).astype(np.float64)
+    assert abs(w.mean()) < 1e-4
+    assert abs(w.std() - 0.02) < 0.0002                        # sd within 1%
+    kurt = ((w - w.mean()) ** 4).mean() / w.var() ** 2 - 3.0
+    assert abs(kurt - (-0.3)) < 0.03                            # Irwin-Hall(4)
+    assert np.abs(w).max() <= 2 * 0.02 * np.sqrt(3) + 1e-7
+
+
+def test_weight_values_are_position_addressable():
+    a = rspec.weight_values(5, 7, 0, 1000)
+    b = rspec.weight_values(5, 7, 400, 100)
+    np.testing.assert_array_equal(a[400:500], b)
+    assert not np.array_equal(rspec.weight_values(5, 8, 0, 100), a[:100])
+
+
+def test_bf16_rounding_matches_torch():
+    x = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -8 + 2 ** -20, -3.14159,
+                  1e-30, 65504.0, 0.02], dtype=np.float32)
+    x = np.concatenate([x, rspec.weight_values(1, 2, 0, 4096)])
+    ours = rspec.bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(ours, ref)
+    assert rspec.bf16_round(np.float32([1.0 + 2 ** -8]))[0] == 1.0          # tie to even
+    assert rspec.bf16_round(np.float32([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
+
+
+def test_prompt_tokens_never_pad_and_roughly_uniform():
+    t = rspec.prompt_tokens(2, 200000, 64)
+    assert t.min() >= 0 and t.max() <= 62                      # PAD id 63 never drawn
+    counts = np.bincount(t.ravel(), minlength=63)
+    exp = t.size / 63
+    chi2 = ((counts - exp) ** 2 / exp).sum()
+    assert chi2 < 150                                          # 62 dof
+    assert not np.array_equal(t[0], t[1])
+
+
+# ---------------------------------------------------------------- primitives
+
+def test_rms_norm_matches_torch_and_is_scale_invariant():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((5, 64))
+    g = rng.standard_normal(64)
+    ref = F.rms_norm(torch.from_numpy(x), (64,), torch.from_numpy(g), eps=1e-6).numpy()
+    np.testing.assert_allclose(O.rms_norm(x, g, 1e-6), ref, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.rms_norm(7.5 * x, g, 0.0), O.rms_norm(x, g, 0.0), rtol=1e-12)
+
+
+def test_silu_matches_torch():
+    u = np.linspace(-30, 30, 1001)
+    np.testing.assert_allclose(O.silu(u), F.silu(torch.from_numpy(u)).numpy(), rtol=1e-13, atol=1e-300)
+
+
+def test_rope_identities():
+    rng = np.random.default_rng(1)
+    d = 16
+    x = rng.standard_normal(d)
+    c0, s0 = O.rope_cos_sin(np.array([0]), d, 1e4)
+    np.testing.assert_array_equal(O.apply_rope(x[None], c0, s0)[0], x)      # p = 0
+    c, s = O.rope_cos_sin(np.array([37]), d, 1e4)
+    y = O.apply_rope(x[None], c, s)[0]
+    assert abs(np.linalg.norm(y) - np.linalg.norm(x)) < 1e-12                # rotation
+    # complex form: (x_j + i x_{j+d/2}) * exp(i p w_j)
+    zc = (x[:d // 2] + 1j * x[d // 2:]) * np.exp(1j * 37 * 1e4 ** (-2 * np.arange(d // 2) / d))
+    np.testing.assert_allclose(y, np.concatenate([zc.real, zc.imag]), atol=1e-12)
+    # q_m . k_n depends only on m - n
+    q, k = rng.standard_normal(d), rng.standard_normal(d)
+
+    def dot(m, n):
+        cm, sm_ = O.rope_cos_sin(np.array([m]), d, 1e4)
+        cn, sn = O.rope_cos_sin(np.array([n]), d, 1e4)
+        return O.apply_rope(q[None], cm, sm_)[0] @ O.apply_rope(k[None], cn, sn)[0]
+    assert abs(dot(10, 3) - dot(107, 100)) < 1e-10
+    assert abs(dot(10, 3) - dot(3, 10)) > 1e-6                               # not symmetric
+
+
+def test_attention_matches_torch_sdpa_gqa():
+    rng = np.random.default_rng(2)
+    n_q, n_kv, T, d = 8, 2, 23, 16
+    Q = rng.standard_normal((n_q, T, d))
+    K = rng.standard_normal((n_kv, T, d))
+    V = rng.standard_normal((n_kv, T, d))
+    rep = n_q // n_kv
+    ref = F.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None], torch.from_numpy(K).repeat_interleave(rep, 0)[None],
+        torch.from_numpy(V).repeat_interleave(rep, 0)[None], is_causal=True)[0].numpy()
+    np.testing.assert_allclose(O.attention_causal(Q, K, V, block=7), ref, rtol=1e-11, atol=1e-12)
+    # the decode form at the last position agrees with the causal form
+    o, probs = O.attention_decode(Q[:, -1], K, V)
+    np.testing.assert_allclose(o, ref[:, -1], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(probs.sum(axis=1), 1.0, atol=1e-12)          # normalised
+
+
+def test_attention_single_key_and_zero_query():
+    rng = np.random.default_rng(3)
+    K = rng.standard_normal((2, 1, 8))
+    V = rng.standard_normal((2, 1, 8))
+    o, _ = O.attention_decode(rng.standard_normal((4, 8)), K, V)
+    np.testing.assert_array_equal(o[:2], np.repeat(V[0], 2, axis=0))       # exactly v_0
+    np.testing.assert_array_equal(o[2:], np.repeat(V[1], 2, axis=0))
+    K = rng.standard_normal((2, 9, 8))
+    V = rng.standard_normal((2, 9, 8))
+    o, _ = O.attention_decode(np.zeros((4, 8)), K, V)                        # W_q = 0
+    np.testing.assert_allclose(o[0], V[0].mean(axis=0), rtol=1e-12)
+    np.testing.assert_allclose(o[3], V[1].mean(axis=0), rtol=1e-12)
+
+
+def test_gqa_group_mapping():
+    # value rows of group g are constant g: head h must return h * n_kv // n_q
+    n_q, n_kv, T, d = 12, 3, 5, 4
+    V = np.stack([np.full((T, d), float(g)) for g in range(n_kv)])
+    K = np.random.default_rng(4).standard_normal((n_kv, T, d))
+    o, _ = O.attention_decode(np.ones((n_q, d)), K, V)
+    np.testing.assert_allclose(o[:, 0], [h // 4 for h in range(n_q)], atol=1e-12)
+
+
+# ------------------------------------------------------- pairs and compressor
+
+def test_prompt_pairs_pad_at_odd_slot_and_latent_length():
+    for n in (1, 2, 7, 8, 63, 64):
+        p = O.prompt_pairs(list(range(10, 10 + n)), pad_id=99)
+        assert p.shape == (-(-n // 2), 2)                                   # ceil(n/2)
+        assert p[0, 0] == 10
+        if n % 2:
+            assert p[-1, 1] == 99 and p[-1, 0] == 10 + n - 1
+        assert (p[:, 0] != 99).all()
+
+
+def test_compressor_closed_forms():
+    rng = np.random.default_rng(5)
+    H, V = 6, 10
+    E = rng.standard_normal((V, H))
+    W = np.concatenate([np.eye(H), np.eye(H)], axis=1)                      # f([a;b]) = a + b
+    pairs = np.array([[1, 2], [3, 9]])
+    np.testing.assert_allclose(O.compress(E, W, np.zeros(H), pairs), E[[1, 3]] + E[[2, 9]], rtol=1e-15)
+    b = rng.standard_normal(H)
+    np.testing.assert_allclose(O.compress(E, W, b, pairs), E[[1, 3]] + E[[2, 9]] + b, rtol=1e-14)
+    E[9] = 0.0                                                              # PAD row zero
+    np.testing.assert_allclose(O.compress(E, W, np.zeros(H), [[3, 9]])[0], E[3], rtol=1e-15)
+    # the two halves of W_c act on the first and second token respectively
+    W2 = np.concatenate([np.eye(H), 2 * np.eye(H)], axis=1)
+    np.testing.assert_allclose(O.compress(E, W2, np.zeros(H), [[1, 2]])[0], E[1] + 2 * E[2], rtol=1e-14)
+
+
+# ------------------------------------------------------------------- backbone
+
+def test_brute_force_equals_incremental(small_w):
+    rng = np.random.default_rng(6)
+    Z = rng.standard_normal((13, SMALL.hidden))
+    X_full, caches_full = O.backbone_full(small_w, Z)
+    caches = [[np.zeros((SMALL.n_kv_heads, 0, SMALL.head_dim))] * 2 for _ in range(SMALL.n_layers)]
+    for p in range(13):
+        h = O.backbone_step(small_w, Z[p], p, caches)
+        np.testing.assert_allclose(h, X_full[p], rtol=1e-10, atol=1e-12)
+    for li in range(SMALL.n_layers):
+        np.testing.assert_allclose(caches[li][0], caches_full[li][0], rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(caches[li][1], caches_full[li][1], rtol=1e-12, atol=1e-14)
+
+
+def test_causality(small_w):
+    rng = np.random.default_rng(7)
+    Z = rng.standard_normal((9, SMALL.hidden))
+    X, _ = O.backbone_full(small_w, Z)
+    Z2 = Z.copy()
+    Z2[6:] += rng.standard_normal((3, SMALL.hidden))
+    X2, _ = O.backbone_full(small_w, Z2)
+    np.testing.assert_array_equal(X2[:6], X[:6])                            # bit-unchanged
+    assert np.abs(X2[6:] - X[6:]).max() > 1e-3
+
+
+def test_zero_layers_is_identity():
+    cfg = SMALL.with_layers(0)
+    W = O.OracleWeights.generate(cfg, seed=1)
+    Z = np.random.default_rng(8).standard_normal((4, cfg.hidden))
+    X, _ = O.backbone_full(W, Z)
+    np.testing.assert_array_equal(X, Z)
+
+
+def test_layer_matches_torch_modules(small_w):
+    """One decoder layer, rebuilt from torch library modules in float64."""
+    cfg = SMALL
+    L = small_w.layer(0)
+    T = 11
+    x = np.random.default_rng(9).standard_normal((T, cfg.hidden))
+    X1, _ = O.backbone_full(O.OracleWeights(cfg.with_layers(1), {**{k: v for k, v in small_w.t.items() if not k.startswith("l1.")}}), x)
+    t = {k: torch.from_numpy(v) for k, v in L.items()}
+    xt = torch.from_numpy(x)
+    n = F.rms_norm(xt, (cfg.hidden,), t["g_attn"], eps=cfg.rms_eps)
+    q = F.linear(n, t["wq"]).view(T, cfg.n_q_heads, cfg.head_dim).transpose(0, 1)
+    k = F.linear(n, t["wk"]).view(T, cfg.n_kv_heads, cfg.head_dim).transpose(0, 1)
+    v = F.linear(n, t["wv"]).view(T, cfg.n_kv_heads, cfg.head_dim).transpose(0, 1)
+    half = cfg.head_dim // 2
+    inv = cfg.rope_base ** (-torch.arange(half, dtype=torch.float64) * 2 / cfg.head_dim)
+    ang = torch.arange(T, dtype=torch.float64)[:, None] * inv
+    cos, sin = torch.cat([ang.cos(), ang.cos()], -1), torch.cat([ang.sin(), ang.sin()], -1)
+
+    def rot(u):
+        return torch.cat([-u[..., half:], u[..., :half]], -1)
+    q, k = q * cos + rot(q) * sin, k * cos + rot(k) * sin
+    rep = cfg.n_q_heads // cfg.n_kv_heads
+    o = F.scaled_dot_product_attention(q[None], k.repeat_interleave(rep, 0)[None],
+                                       v.repeat_interleave(rep, 0)[None], is_causal=True)[0]
+    xt = xt + F.linear(o.transpose(0, 1).reshape(T, -1), t["wo"])
+    n = F.rms_norm(xt, (cfg.hidden,), t["g_ffn"], eps=cfg.rms_eps)
+    xt = xt + F.linear(F.silu(F.linear(n, t["wgate"])) * F.linear(n, t["wup"]), t["wdown"])
+    np.testing.assert_allclose(X1, xt.numpy(), rtol=1e-10, atol=1e-12)
+
+
+# ---------------------------------------------------------------------- heads
+
+def test_tied_head_closed_form():
+    H = 8
+    E = 0.5 * np.eye(H)
+    h = np.random.default_rng(10).standard_normal(H)
+    logits = O.lm_logits(E, np.ones(H), h, 0.0)
+    np.testing.assert_allclose(logits, 0.5 * h / np.sqrt(np.mean(h * h)), rtol=1e-14)
+    assert O.select_greedy(logits) == int(np.argmax(h))
+
+
+def test_mtp_closed_forms_and_dependence_on_backbone_token():
+    rng = np.random.default_rng(11)
+    H, V = 8, 12
+    E = rng.standard_normal((V, H))
+    h_b = rng.standard_normal(H)
+    g = rng.standard_normal(H)
+    I, Z = np.eye(H), np.zeros((H, H))
+    np.testing.assert_allclose(O.mtp_hidden(np.hstack([I, Z]), g, g, h_b, E[3], 1e-6),
+                               O.rms_norm(h_b, g, 1e-6), rtol=1e-14)
+    np.testing.assert_allclose(O.mtp_hidden(np.hstack([Z, I]), g, g, h_b, E[3], 1e-6),
+                               O.rms_norm(E[3], g, 1e-6), rtol=1e-14)
+
+
+def test_session_mtp_reads_the_backbone_token(small_w):
+    cfg = SMALL
+    prompt = rspec.prompt_tokens(1, 10, cfg.vocab)
+    smp = O.Sampling(tau=0.5)
+    a = O.PipoOracle(small_w).prefill(prompt, smp)[0]
+    W2 = O.OracleWeights(cfg, dict(small_w.t))
+    W2.t["embed"] = small_w["embed"].copy()
+    W2.t["embed"][a["tok_b"]] *= -1.0            # only E[b]'s row changes ...
+    b = O.PipoOracle(W2).prefill(prompt, smp)[0]
+    # ... the backbone logits move only at that row of the tied head
+    diff = np.abs(b["logits_b"] - a["logits_b"])
+    assert diff[a["tok_b"]] > 0
+    np.testing.assert_allclose(np.delete(diff, a["tok_b"]), 0.0, atol=1e-9)
+    assert np.abs(b["logits_d"] - a["logits_d"]).max() > 1e-3
+
+
+def test_confidence_closed_form_and_gate_rule():
+    rng = np.random.default_rng(12)
+    H = 6
+    h_b, h_d = rng.standard_normal(H), rng.standard_normal(H)
+    w = np.zeros(2 * H)
+    w[H + 2] = 1.0
+    s, c = O.confidence(w, np.ones(2 * H), h_b, h_d, 0.0)
+    cat = np.concatenate([h_b, h_d])
+    assert abs(s - cat[H + 2] / np.sqrt(np.mean(cat * cat))) < 1e-14
+    assert abs(c - 1 / (1 + np.exp(-s))) < 1e-15
+    assert O.gate(c, c)                            # equality accepts
+    assert O.gate(c, 0.0)                          # tau = 0: always accept
+    assert not O.gate(c, 1.0 + 1e-9)               # tau > 1: never accept
+    assert not O.gate(c, np.nextafter(c, 2.0))
+
+
+# -------------------------------------------------------------------- sampler
+
+def test_top_p_worked_example():
+    p = np.array([0.5, 0.3, 0.15, 0.05])
+    logits = np.log(p)
+    # top_p 0.8 -> nucleus {0, 1}, mass 0.8; u 0.7 -> t 0.56 -> running 0.5, 0.8.
+    # The mass of {0, 1} equals top_p exactly, so the example is posed with
+    # top_p a hair below 0.8: exp/log rounding must not decide the nucleus.
+    tp = 0.8 - 1e-9
+    assert O.select_top_p(logits, 1.0, tp, 0.7) == 1
+    assert O.select_top_p(logits, 1.0, tp, 0.6) == 0           # t = 0.48 < 0.5
+    assert O.select_top_p(logits, 1.0, 0.81, 0.999) == 2       # nucleus grows to {0,1,2}
+    assert O.select_top_p(logits, 1.0, 1.0, 0.999) == 3
+
+
+def test_top_p_limits_reduce_to_greedy():
+    logits = np.random.default_rng(13).standard_normal(50)
+    g = O.select_greedy(logits)
+    for u in (0.0, 0.3, 0.9999):
+        assert O.select_top_p(logits, 1.0, 1e-9, u) == g
+        assert O.select_top_p(logits, 1e-4, 0.95, u) == g
+
+
+def test_top_p_tie_group_is_whole():
+    logits = np.log(np.array([0.3, 0.3, 0.3, 0.1]))
+    # top_p 0.35 is reached inside the tie group: all three tied ids are in N
+    picks = {O.select_top_p(logits, 1.0, 0.35, u) for u in np.linspace(0, 0.999, 30)}
+    assert picks == {0, 1, 2}
+
+
+def test_top_p_inverse_cdf_distribution():
+    rng = np.random.default_rng(14)
+    logits = rng.standard_normal(8) * 1.5
+    T, top_p = 0.7, 0.9
+    p = np.exp(logits / T - np.max(logits / T))
+    p /= p.sum()
+    order = np.argsort(-p)
+    keep = order[: np.argmax(np.cumsum(p[order]) >= top_p) + 1]
+    target = np.zeros(8)
+    target[keep] = p[keep] / p[keep].sum()
+    N = 20000
+    draws = [O.select_top_p(logits, T, top_p, (i + 0.5) / N) for i in range(N)]
+    freq = np.bincount(draws, minlength=8) / N
+    np.testing.assert_allclose(freq, target, atol=2.0 / N)
+
+
+def test_greedy_ties_lowest_id():
+    assert O.select_greedy(np.array([0.1, 0.7, 0.2, 0.7])) == 1
+
+
+# --------------------------------------------------------------- the session
+
+def test_session_latent_length_and_pair_feedback(small_w):
+    cfg = SMALL
+    for tau in (0.0, 2.0):
+        orc = O.PipoOracle(small_w)
+        out = orc.prefill(rspec.prompt_tokens(2, 11, cfg.vocab), O.Sampling(tau=tau))
+        assert orc.length == [6, 6]                                         # ceil(11/2)
+        for k in range(3):
+            prev = orc.next_pairs[0]
+            rec = out[0]
+            expect = (rec["tok_b"], rec["tok_d"] if tau <= rec["conf"] else cfg.pad_id)
+            assert prev == expect
+            assert rec["accept"] == (tau == 0.0)
+            out = orc.decode_step()
+            assert orc.length == [6 + k + 1] * 2                           # +1 per step
+
+
+def test_session_decode_equals_brute_force(small_w):
+    """Prefill + decode steps reproduce a from-scratch pass over all latents."""
+    cfg = SMALL
+    prompt = rspec.prompt_tokens(1, 9, cfg.vocab)
+    orc = O.PipoOracle(small_w)
+    recs = [orc.prefill(prompt, O.Sampling(tau=0.5))[0]]
+    pairs = [tuple(p) for p in O.prompt_pairs(prompt[0], cfg.pad_id)]
+    for _ in range(4):
+        pairs.append(orc.next_pairs[0])
+        recs.append(orc.decode_step()[0])
+    Z = O.compress(small_w["embed"], small_w["w_comp"], small_w["b_comp"], np.array(pairs))
+    X, _ = O.backbone_full(small_w, Z)
+    for k, rec in enumerate(recs):
+        np.testing.assert_allclose(rec["h_b"], X[len(pairs) - len(recs) + k], rtol=1e-10, atol=1e-12)
+
+
+def test_teacher_forcing_reproduces_free_run(small_w):
+    cfg = SMALL
+    prompt = rspec.prompt_tokens(2, 8, cfg.vocab)
+    smp = O.Sampling(tau=0.4, temperature=0.8, top_p=0.9, seeds=(1000, 1001))
+    a = O.PipoOracle(small_w)
+    a.prefill(prompt, smp)
+    b = O.PipoOracle(small_w)
+    b.prefill(prompt, smp)
+    for _ in range(3):
+        forced = [a.next_pairs[i] for i in range(2)]
+        ra, rb = a.decode_step(), b.decode_step(in_pairs=forced)
+        for x, y in zip(ra, rb):
+            assert (x["tok_b"], x["tok_d"], x["accept"]) == (y["tok_b"], y["tok_d"], y["accept"])
+
+
+def test_tiny_workload_shapes_run():
+    """The tiny workload's model runs end to end in the oracle (smoke)."""
+    W = O.OracleWeights.generate(TINY, seed=0, precision="fp32")
+    orc = O.PipoOracle(W)
+    out = orc.prefill(rspec.prompt_tokens(1, 64, TINY.vocab), O.Sampling(tau=0.5))
+    assert orc.length == [32]
+    assert 0 <= out[0]["tok_b"] < TINY.vocab and 0 < out[0]["conf"] < 1
+    orc.decode_step()
+    assert orc.length == [33]

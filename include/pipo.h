@@ -1,0 +1,127 @@
+/*
+ * pipo.h - C ABI of the MI355X (gfx950) PIPO pair-in/pair-out library.
+ *
+ * PIPO (Pair-In, Pair-Out) decodes a token *pair* per backbone step (Sec. 3.1):
+ *   1. pair-in compressor   z = W_c [E[a]; E[b]] + b_c            (eq. 1, App. B.1 Linear)
+ *   2. backbone over latents h_b = Backbone(z^{<=i})              (eq. 2)
+ *   3. backbone token        b  ~ LMHead(RMSNorm(h_b))             (eq. 3, tied head)
+ *   4. MTP head + draft      h_d = W_fc[RMSNorm(h_b); RMSNorm(E[b])], d ~ LMHead(RMSNorm(h_d))
+ *                                                                  (eqs. 4-5, App. B.2, one linear)
+ *   5. confidence gate       c = sigmoid(w_c . RMSNorm([h_b; h_d])); accept iff c >= tau
+ *                            next input pair = accept ? (b, d) : (b, PAD)   (eq. 6, Sec. 3.2)
+ * Every step consumes exactly one latent position and emits one or two
+ * tokens; the prompt is compressed two tokens per latent (ceil(n/2) latents,
+ * PAD at the odd slot of an odd-length prompt).
+ *
+ * Conventions for every call:
+ *   - Pointers named d_* are device pointers (hipMalloc'd or torch CUDA
+ *     tensors' data_ptr()); the caller owns them.  Other pointers are host.
+ *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *     Every call is stream-ordered and asynchronous: outputs are valid once
+ *     the caller synchronises that stream.  One context must not be used
+ *     from two threads at once.
+ *   - Return value: PIPO_OK (0) or a negative PIPO_E* code.  Host-side
+ *     argument and capacity checks run before any device work, so a failed
+ *     call leaves the context unchanged.  A device fault from earlier work
+ *     surfaces as PIPO_EHIP.  Nothing aborts; no C++ exception crosses the ABI.
+ *   - pipo_last_error() returns the message of the most recent failure.
+ */
+#ifndef PIPO_H
+#define PIPO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PIPO_OK          0
+#define PIPO_EINVAL     -1   /* bad argument or unsupported shape            */
+#define PIPO_ENOMEM     -2   /* device allocation failed                     */
+#define PIPO_EHIP       -3   /* HIP runtime error (incl. earlier faults)     */
+#define PIPO_ECAPACITY  -4   /* batch or latent KV capacity exceeded         */
+#define PIPO_ESTATE     -5   /* decode before prefill                        */
+
+typedef struct pipo_ctx pipo_ctx;   /* opaque; owns weights, KV cache, workspaces */
+
+/* Model shape and capacities.  Constraints (PIPO_EINVAL otherwise):
+ * hidden % 32 == 0, ffn % 32 == 0, vocab % 16 == 0, head_dim in {64, 128},
+ * n_q_heads % n_kv_heads == 0 and n_q_heads / n_kv_heads <= 16,
+ * (n_q_heads*head_dim) % 32 == 0, 1 <= max_batch <= 32, max_latent >= 1,
+ * prefill_chunk a positive multiple of 16. */
+typedef struct {
+    int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
+    float   rope_base;       /* RoPE frequencies base^(-2j/d) over latent positions */
+    float   rms_eps;         /* RMSNorm epsilon                                     */
+    int32_t pad_id;          /* PAD token id; -1 selects vocab-1                    */
+    int32_t max_batch;       /* sequences per context                               */
+    int32_t max_latent;      /* KV capacity per sequence, in latent positions       */
+    int32_t prefill_chunk;   /* latent positions per prefill chunk (e.g. 4096)      */
+    int32_t gain_mode;       /* 0: RMSNorm gains 1; 1: gains 1 + 10*w (testing)     */
+} pipo_config;
+
+/* Token selection and the confidence gate (Sec. 3.2).  Read during the call,
+ * not retained except by value. */
+typedef struct {
+    float tau;               /* accept the draft iff sigmoid(s) >= tau             */
+    float temperature;       /* <= 0: greedy argmax, ties to the lowest id          */
+    float top_p;             /* nucleus mass in (0, 1]; used when temperature > 0   */
+    const uint64_t *seeds;   /* host [batch] per-sequence sampler seeds; may be NULL
+                                when greedy                                          */
+} pipo_sampling;
+
+/* One pair step's result for one sequence (16 bytes). */
+typedef struct {
+    int32_t tok_b;           /* backbone token x^{2i+2}                            */
+    int32_t tok_d;           /* draft token x^{2i+3}                               */
+    float   conf;            /* confidence c^i = sigmoid(s)                         */
+    int32_t accept;          /* 1 iff conf >= tau: the draft is emitted             */
+} pipo_pair;
+
+/* Create a context: allocate weights, KV cache and workspaces on the current
+ * device and fill every weight tensor from the counter-based generator
+ * (SplitMix64-derived, N(0, 0.02)-shaped, bf16 storage) for `seed`.
+ * On success *out receives the context (released by pipo_free).  Returns
+ * PIPO_EINVAL for a bad config, PIPO_ENOMEM if device memory runs out. */
+int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *stream, pipo_ctx **out);
+
+/* Compressed-prompt prefill (Sec. 4.3 TTFT path): start `batch` new
+ * sequences from d_tokens (device int32 [batch][n], row-major, ids in
+ * [0, vocab)), pair them (PAD appended to an odd n), run the backbone over
+ * the ceil(n/2) latents in chunks of prefill_chunk, and emit the first pair:
+ * d_out (device pipo_pair [batch]).  d_logits_b / d_logits_d (device float
+ * [batch][vocab]) receive the backbone / draft logits when non-NULL.
+ * Errors: PIPO_EINVAL (NULL pointers, n < 1, bad sampling values),
+ * PIPO_ECAPACITY (batch > max_batch or ceil(n/2) + 1 > max_latent). */
+int pipo_prefill(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, int32_t n,
+                 const pipo_sampling *smp, pipo_pair *d_out,
+                 float *d_logits_b, float *d_logits_d, void *stream);
+
+/* One pair-decode step for every sequence of the last prefill.  The input
+ * pair is d_in_pairs (device int32 [batch][2]) when non-NULL (teacher
+ * forcing), else the pair the previous call produced on the device:
+ * (tok_b, accept ? tok_d : pad_id).  Appends one latent per sequence.
+ * Outputs as for pipo_prefill.  Errors: PIPO_ESTATE (no prefill yet),
+ * PIPO_ECAPACITY (KV full). */
+int pipo_decode_step(pipo_ctx *ctx, const int32_t *d_in_pairs, pipo_pair *d_out,
+                     float *d_logits_b, float *d_logits_d, void *stream);
+
+/* Release a context and all its device memory.  NULL is a no-op (returns 0). */
+int pipo_free(pipo_ctx *ctx);
+
+/* Message of the most recent failure on ctx (or of pipo_init_weights when
+ * ctx is NULL).  Never NULL; valid until the next call on the same context. */
+const char *pipo_last_error(const pipo_ctx *ctx);
+
+/* Copy `count` elements, starting at logical element `start` of the
+ * row-major [out][in] tensor `name` (e.g. "embed", "w_comp", "l3.wq",
+ * "l0.g_attn"), to host memory as bf16 bit patterns, undoing the device
+ * packing.  Synchronous.  For verifying the device weight generator.
+ * Errors: PIPO_EINVAL (unknown name or range). */
+int pipo_read_weight(pipo_ctx *ctx, const char *name, int64_t start, int64_t count,
+                     uint16_t *host_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PIPO_H */

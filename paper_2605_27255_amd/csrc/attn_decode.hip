@@ -1,0 +1,149 @@
+// Grouped-query flash-decode over the latent KV cache (one query position per
+// sequence), split along the key axis.
+//
+// One wave per (sequence, KV group, split).  The group's query heads are the
+// 16 columns of the MFMA tiles (unused columns are zero): scores are computed
+// transposed, S^T[key][head] = K Q^T, 16 keys per tile, so each lane's
+// accumulator holds one head; online softmax runs per column; the
+// probabilities, held as (4g + v, 16 + 4g + v) for lane group g, are already
+// the B operand of O^T[dim][head] += V^T P^T because the V cache stores each
+// 32-key tile in that key order (see vslot in gemv.hip).  Per-split results
+// (m, l, o) go to a partial buffer; the last wave of a group to finish merges
+// them in split order.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace pipo {
+
+template <int D>
+__global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
+    constexpr int NC = D / 32;   // 32-wide d chunks (QK^T k-steps)
+    constexpr int NT = D / 16;   // 16-wide d tiles (PV output tiles)
+    __shared__ int s_last;
+    __shared__ float s_w[16 * 64];
+
+    const int lane = threadIdx.x, j = lane & 15, g = lane >> 4;
+    const int S = p.splits;
+    const int split = blockIdx.x % S;
+    const int bk = blockIdx.x / S;               // b * n_kv + kvh
+    const int b = bk / p.n_kv, kvh = bk - b * p.n_kv;
+    const int qpg = p.n_q / p.n_kv;
+    const int len = p.pos[b] + 1;
+    int chunk = (len + S - 1) / S;
+    chunk = (chunk + 31) & ~31;
+    const int k0 = split * chunk;
+    const int k1 = min(len, k0 + chunk);
+    const float scale = 1.4426950408889634f / sqrtf((float)D);
+
+    u32x4 qb[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        qb[c] = u32x4{0u, 0u, 0u, 0u};
+        if (j < qpg) qb[c] = *(const u32x4 *)(p.q + ((int64_t)b * p.n_q + kvh * qpg + j) * D + 32 * c + 8 * g);
+    }
+    const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
+    const uint16_t *vbase = p.vc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
+
+    f32x4 o[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    for (int kb = k0; kb < k1; kb += 32) {
+        f32x4 st[2];
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau) {
+            st[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const uint16_t *kr = kbase + (int64_t)(kb + 16 * tau + j) * D + 8 * g;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) st[tau] = mfma16(*(const u32x4 *)(kr + 32 * c), qb[c], st[tau]);
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int key = kb + 16 * tau + 4 * g + v;
+                const float sv = key < k1 ? st[tau][v] * scale : -INFINITY;
+                st[tau][v] = sv;
+                mx = fmaxf(mx, sv);
+            }
+        mx = col_max(mx);
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = exp2f(m_run - m_new);
+        float ps = 0.f;
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float e = exp2f(st[tau][v] - m_new);
+                st[tau][v] = e;
+                ps += e;
+            }
+        l_run = l_run * alpha + col_sum(ps);
+        m_run = m_new;
+        u32x4 pt;
+        pt[0] = pack_bf2(st[0][0], st[0][1]);
+        pt[1] = pack_bf2(st[0][2], st[0][3]);
+        pt[2] = pack_bf2(st[1][0], st[1][1]);
+        pt[3] = pack_bf2(st[1][2], st[1][3]);
+        const uint16_t *vt = vbase + (int64_t)(kb >> 5) * D * 32 + j * 32 + 8 * g;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            o[t] *= alpha;
+            o[t] = mfma16(*(const u32x4 *)(vt + t * 16 * 32), pt, o[t]);
+        }
+    }
+
+    // partial (o, m, l) of this split for each head of the group
+    if (j < qpg) {
+        float *pr = p.part + (((int64_t)b * p.n_q + kvh * qpg + j) * S + split) * (D + 2);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) *(f32x4 *)(pr + 16 * t + 4 * g) = o[t];
+        if (g == 0) {
+            pr[D] = m_run;
+            pr[D + 1] = l_run;
+        }
+    }
+    __threadfence();
+    __syncthreads();
+    if (lane == 0) {
+        const uint32_t prev = __hip_atomic_fetch_add(p.ctr + bk, 1u, __ATOMIC_ACQ_REL,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (prev == (uint32_t)(S - 1));
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    // merge: weights exp2(m_s - M) / L per (head, split), then a weighted sum
+    for (int h = 0; h < qpg; ++h) {
+        const float *ph = p.part + ((int64_t)b * p.n_q + kvh * qpg + h) * S * (D + 2);
+        float M = -INFINITY;
+        for (int sp = lane; sp < S; sp += 64) M = fmaxf(M, ph[sp * (D + 2) + D]);
+        M = wave_max(M);
+        float L = 0.f;
+        for (int sp = lane; sp < S; sp += 64) {
+            const float ms = ph[sp * (D + 2) + D];
+            const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
+            s_w[h * 64 + sp] = w;
+            L += w * ph[sp * (D + 2) + D + 1];
+        }
+        L = wave_sum(L);
+        __syncthreads();
+        const float inv = 1.0f / L;
+        for (int dim = lane; dim < D; dim += 64) {
+            float acc = 0.f;
+            for (int sp = 0; sp < S; ++sp) acc += s_w[h * 64 + sp] * ph[sp * (D + 2) + dim];
+            p.out[((int64_t)b * p.n_q + kvh * qpg + h) * D + dim] = (uint16_t)f2bf(acc * inv);
+        }
+    }
+    if (lane == 0) p.ctr[bk] = 0u;
+}
+
+void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s) {
+    const int grid = p.B * p.n_kv * p.splits;
+    if (p.d == 128) hipLaunchKernelGGL(k_attn_decode<128>, dim3(grid), dim3(64), 0, s, p);
+    else hipLaunchKernelGGL(k_attn_decode<64>, dim3(grid), dim3(64), 0, s, p);
+}
+
+}  // namespace pipo

@@ -1,0 +1,189 @@
+// Output side of a pair step: the confidence gate and next-pair builder
+// (eq. 6 and the PAD fallback of Sec. 3.2), and temperature / top-p token
+// selection.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace pipo {
+
+struct PairOut { int32_t tok_b, tok_d; float conf; int32_t accept; };
+
+// One workgroup per sequence: s = w_c . RMSNorm([h_b; h_d]) * g_c,
+// c = sigmoid(s), accept iff c >= tau; next pair = (b, accept ? d : PAD).
+__global__ __launch_bounds__(256) void k_gate(GateParams p) {
+    __shared__ float red[4];
+    __shared__ float s_sc;
+    const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int H = p.H;
+    if (wave == 0) {
+        float a = 0.f;
+        for (int i = lane; i < p.nss_b; i += 64) a += p.ss_b[b * p.nss_b + i];
+        for (int i = lane; i < p.nss_d; i += 64) a += p.ss_d[b * p.nss_d + i];
+        a = wave_sum(a);
+        if (lane == 0) s_sc = rsqrtf(a / (float)(2 * H) + p.eps);
+    }
+    float dot = 0.f;
+    for (int k = threadIdx.x; k < 2 * H; k += 256) {
+        const float u = k < H ? p.hb[(int64_t)b * H + k] : p.hd[(int64_t)b * H + k - H];
+        dot += p.w_conf[k] * p.g_conf[k] * u;
+    }
+    dot = wave_sum(dot);
+    if (lane == 0) red[wave] = dot;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const float s = (red[0] + red[1] + red[2] + red[3]) * s_sc;
+        const float c = 1.0f / (1.0f + expf(-s));
+        const int acc = c >= p.tau ? 1 : 0;
+        const int32_t tb = argmax_key_id(p.best_b[b]);
+        const int32_t td = argmax_key_id(p.best_d[b]);
+        PairOut *o = (PairOut *)p.out + b;
+        o->tok_b = tb;
+        o->tok_d = td;
+        o->conf = c;
+        o->accept = acc;
+        p.pairs[2 * b] = tb;
+        p.pairs[2 * b + 1] = acc ? td : p.pad_id;
+        if (p.advance) p.pos[b] += 1;
+        p.step[b] += 1;
+        p.best_b[b] = 0;
+        p.best_d[b] = 0;
+    }
+}
+
+void launch_gate(const GateParams &p, hipStream_t s) {
+    hipLaunchKernelGGL(k_gate, dim3(p.B), dim3(256), 0, s, p);
+}
+
+// ---------------------------------------------------------------------------
+// Temperature + top-p selection, one 1024-thread workgroup per sequence.
+//   e_j = exp((l_j - max l) / T); masses are fixed point, E_j = round(e_j 2^40),
+//   so every sum is an exact integer sum (order independent).
+//   theta* = the largest e-value whose upper mass sum_{e_i >= theta} E_i
+//   reaches top_p * sum E: found exactly by a 4-pass radix select over the
+//   float bit patterns of e (positive floats order like their bits).
+//   nucleus N = {j : e_j >= theta*}, mass M; t = floor(u M); the token is the
+//   first id, scanning upwards through N, whose running mass exceeds t.
+// ---------------------------------------------------------------------------
+constexpr int kSampThreads = 1024;
+
+__device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int d) {
+    uint32_t lo = __shfl_up((uint32_t)v, d), hi = __shfl_up((uint32_t)(v >> 32), d);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t fixed_mass(float e) {
+    return (uint64_t)__double2ull_rn((double)e * 1099511627776.0);   // 2^40
+}
+
+__global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
+    __shared__ unsigned long long hist[256];
+    __shared__ float s_red[kSampThreads / 64];
+    __shared__ unsigned long long s_u64[kSampThreads / 64];
+    __shared__ uint32_t s_prefix;
+    __shared__ unsigned long long s_above, s_mass;
+    __shared__ int s_all;
+
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float *lg = p.logits + (int64_t)b * p.V;
+    const int V = p.V;
+    const int per = (V + kSampThreads - 1) / kSampThreads;
+    const int j0 = min(V, tid * per), j1 = min(V, j0 + per);
+
+    float mx = -INFINITY;
+    for (int jj = j0; jj < j1; ++jj) mx = fmaxf(mx, lg[jj]);
+    mx = wave_max(mx);
+    if (lane == 0) s_red[wave] = mx;
+    __syncthreads();
+    mx = s_red[0];
+    for (int w = 1; w < kSampThreads / 64; ++w) mx = fmaxf(mx, s_red[w]);
+    const float kT = 1.4426950408889634f / p.temperature;
+
+    unsigned long long tot = 0;
+    for (int jj = j0; jj < j1; ++jj) tot += fixed_mass(exp2f((lg[jj] - mx) * kT));
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)tot, o), hi = __shfl_xor((uint32_t)(tot >> 32), o);
+        tot += ((unsigned long long)hi << 32) | lo;
+    }
+    if (lane == 0) s_u64[wave] = tot;
+    __syncthreads();
+    tot = 0;
+    for (int w = 0; w < kSampThreads / 64; ++w) tot += s_u64[w];
+    const double target = (double)p.top_p * (double)tot;
+
+    if (tid == 0) { s_prefix = 0; s_above = 0; s_all = 0; }
+    for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        if (tid < 256) hist[tid] = 0;
+        __syncthreads();
+        const uint32_t prefix = s_prefix;
+        for (int jj = j0; jj < j1; ++jj) {
+            const float e = exp2f((lg[jj] - mx) * kT);
+            const uint32_t key = __float_as_uint(e);
+            if (pass == 0 || (key >> (shift + 8)) == prefix)
+                atomicAdd(&hist[(key >> shift) & 255u], fixed_mass(e));
+        }
+        __syncthreads();
+        if (tid == 0) {
+            unsigned long long above = s_above;
+            int beta = -1;
+            for (int k = 255; k >= 0; --k) {
+                if ((double)(above + hist[k]) >= target) { beta = k; break; }
+                above += hist[k];
+            }
+            if (beta < 0) {   // no value reaches top_p (rounding): every token
+                s_all = 1;
+                beta = 0;
+                above = s_above;
+            }
+            if (!s_all) {
+                s_above = above;
+                s_prefix = (prefix << 8) | (uint32_t)beta;
+                s_mass = above + hist[beta];
+            }
+        }
+        __syncthreads();
+        if (s_all) break;
+    }
+    const uint32_t theta = s_all ? 0u : s_prefix;
+    const unsigned long long M = s_all ? tot : s_mass;
+
+    // u in [0,1) with 24 bits; t = floor(u * M)
+    const uint64_t r24 = splitmix64(rng_key(p.seeds[b], 1ull << 33) + 2ull * (uint64_t)p.step[b] + (uint64_t)p.slot) >> 40;
+    const unsigned long long t = __umul64hi(r24 << 40, M);
+
+    unsigned long long loc = 0;
+    for (int jj = j0; jj < j1; ++jj) {
+        const float e = exp2f((lg[jj] - mx) * kT);
+        if (__float_as_uint(e) >= theta) loc += fixed_mass(e);
+    }
+    // exclusive block scan of loc
+    unsigned long long inc = loc;
+    for (int d = 1; d < 64; d <<= 1) {
+        const unsigned long long o = shfl_up_u64(inc, d);
+        if (lane >= d) inc += o;
+    }
+    if (lane == 63) s_u64[wave] = inc;
+    __syncthreads();
+    unsigned long long base = 0;
+    for (int w = 0; w < wave; ++w) base += s_u64[w];
+    const unsigned long long excl = base + inc - loc;
+    if (loc > 0 && excl <= t && t < excl + loc) {
+        unsigned long long run = excl;
+        for (int jj = j0; jj < j1; ++jj) {
+            const float e = exp2f((lg[jj] - mx) * kT);
+            if (__float_as_uint(e) >= theta) {
+                run += fixed_mass(e);
+                if (run > t) {
+                    p.best[b] = (1ull << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)jj);
+                    break;
+                }
+            }
+        }
+    }
+}
+
+void launch_sample(const SampleParams &p, hipStream_t s) {
+    hipLaunchKernelGGL(k_sample, dim3(p.B), dim3(kSampThreads), 0, s, p);
+}
+
+}  // namespace pipo

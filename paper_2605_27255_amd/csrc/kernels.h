@@ -1,0 +1,138 @@
+// Launch interfaces of the gfx950 kernels (host side).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pipo {
+
+// ----------------------------------------------------------------------------
+// Weight-streaming skinny GEMM for the decode step:  Y^T[N][B] = W[N][K] X^T.
+// W is tiled (16x32 tiles, see device_common.h), X is produced on the fly by
+// the prologue into LDS as bf16, B <= 32.
+// ----------------------------------------------------------------------------
+enum GemvPro : int {
+    PRO_NORM = 0,   // X = bf16(RMSNorm(x) * gain): x fp32 [B][K], sum-of-squares parts
+    PRO_BF16 = 1,   // X = xb, bf16 [B][K]
+    PRO_PAIR = 2,   // X = [E[a]; E[b]] for int32 pairs [B][2] (pair-in compressor)
+    PRO_MTP  = 3,   // X = [RMSNorm(h_b) g1; RMSNorm(E[tok]) g2], tok from an argmax key
+};
+enum GemvEpi : int {
+    EPI_STORE  = 0,  // out fp32 [B][N] = acc (+ bias); sum-of-squares parts
+    EPI_RESID  = 1,  // out fp32 [B][N] += acc; sum-of-squares parts
+    EPI_SWIGLU = 2,  // act bf16 [B][N/2] = SiLU(gate) * up (gate/up strip-interleaved)
+    EPI_QKV    = 3,  // RoPE q,k; q bf16 [B][n_q][d]; k, v appended to the KV cache
+    EPI_LOGITS = 4,  // logits fp32 [B][N]; optional argmax key per row (greedy)
+};
+
+struct GemvParams {
+    const uint16_t *W;          // tiled [N][K]
+    int N, K, B;
+    int splits;                 // split-K factor (1 = none)
+    int ktiles_per_chunk;       // LDS staging chunk, in 32-wide k tiles
+    float *part;                // split-K partials [splits][B][N]
+    uint32_t *ctr;              // per strip-group arrival counters (zero between launches)
+    // prologue
+    const float *x; const uint16_t *xb; const float *ss; int nss; const float *gain;
+    const float *gain2; float eps; const int32_t *pairs; const uint16_t *embed; int H; int vocab;
+    const uint64_t *tokkey;
+    // epilogue
+    float *out; const float *bias; float *ss_out; uint16_t *act;
+    uint16_t *q; uint16_t *kc; uint16_t *vc; const int32_t *pos;
+    const float *rope_cos; const float *rope_sin;
+    int n_q, n_kv, d, lmax_pad;   // KV geometry of this layer
+    int64_t kv_bstride;           // elements between consecutive sequences' caches
+    uint64_t *best;               // argmax keys [B] (EPI_LOGITS; NULL: none)
+};
+void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s);
+int gemv_num_groups(int N);
+
+// ----------------------------------------------------------------------------
+// Split-K grouped-query flash-decode over the latent KV cache.
+// ----------------------------------------------------------------------------
+struct AttnDecodeParams {
+    const uint16_t *q;          // bf16 [B][n_q][d]
+    const uint16_t *kc, *vc;    // this layer's caches
+    int64_t kv_bstride;
+    const int32_t *pos;         // [B]: attend to keys 0..pos[b]
+    int B, n_q, n_kv, d, lmax_pad, splits;
+    float *part;                // [B][n_q][splits][d + 2]
+    uint32_t *ctr;              // [B][n_kv]
+    uint16_t *out;              // bf16 [B][n_q * d]
+};
+void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s);
+
+// ----------------------------------------------------------------------------
+// Heads: confidence gate, top-p sampler.
+// ----------------------------------------------------------------------------
+struct GateParams {
+    const float *hb, *hd; const float *ss_b, *ss_d; int nss_b, nss_d;
+    const float *w_conf, *g_conf; int H; float eps, tau;
+    uint64_t *best_b, *best_d; int32_t pad_id;
+    void *out;                  // pipo_pair [B]
+    int32_t *pairs, *pos, *step; int advance;
+    int B;
+};
+void launch_gate(const GateParams &p, hipStream_t s);
+
+struct SampleParams {
+    const float *logits; int V; int B;
+    float temperature, top_p;
+    const uint64_t *seeds; const int32_t *step; int slot;
+    uint64_t *best;
+};
+void launch_sample(const SampleParams &p, hipStream_t s);
+
+// ----------------------------------------------------------------------------
+// Initialisation: R-spec weights into packed layouts, RoPE table.
+// ----------------------------------------------------------------------------
+enum RowPerm : int { PERM_NONE = 0, PERM_QK = 1, PERM_GATEUP = 2 };
+// Fill a tiled [N][K] bf16 matrix: packed row r holds logical row L(r) of
+// tensor `tid` (rows [row_lo, row_hi) of the packed matrix); `perm` and
+// `half` describe L (see init.hip).
+void launch_init_tiled(uint16_t *dst, int64_t N, int64_t K, int64_t row_lo, int64_t row_hi,
+                       uint64_t seed, uint64_t tid, int perm, int half, int64_t tid_row0,
+                       uint64_t tid2, hipStream_t s);
+void launch_init_vec(float *dst, int64_t n, uint64_t seed, uint64_t tid, int kind, hipStream_t s);
+void launch_rope_table(float *cos_t, float *sin_t, int lmax, int d, double base, hipStream_t s);
+void launch_read_tiled(const uint16_t *src, int64_t N, int64_t K, int64_t start, int64_t count,
+                       int perm, int half, int64_t row_base, int64_t rows_total,
+                       uint16_t *dst, hipStream_t s);
+void launch_fill_u32(uint32_t *p, uint32_t v, int64_t n, hipStream_t s);
+void launch_copy_bytes(void *dst, const void *src, int64_t n, hipStream_t s);
+
+// ----------------------------------------------------------------------------
+// Prefill: gather, RMSNorm, MFMA GEMM, causal flash attention, last-row pick.
+// ----------------------------------------------------------------------------
+struct PrefillGeom {
+    int B;           // sequences
+    int c0, clen;    // chunk start latent and latents in this chunk
+    int mpad;        // per-sequence row stride (clen rounded up to 16)
+    int n_tok;       // prompt tokens per sequence
+};
+void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                         const PrefillGeom &g, uint16_t *xin, hipStream_t s);
+void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M,
+                          uint16_t *xn, hipStream_t s);
+struct GemmParams {
+    const uint16_t *W; const uint16_t *X;   // tiled [N][K], tiled [M][K]
+    int N, K, M;
+    int epi;                                // EPI_STORE (bias), EPI_RESID, EPI_SWIGLU, EPI_QKV
+    PrefillGeom g;
+    float *out; const float *bias; uint16_t *act;
+    uint16_t *q; uint16_t *kc; uint16_t *vc;
+    const float *rope_cos; const float *rope_sin;
+    int n_q, n_kv, d, lmax_pad; int64_t kv_bstride;
+};
+void launch_gemm(const GemmParams &p, hipStream_t s);
+struct AttnPrefillParams {
+    const uint16_t *q;          // bf16 [B][n_q][mpad][d]
+    const uint16_t *kc, *vc; int64_t kv_bstride;
+    PrefillGeom g;
+    int n_q, n_kv, d, lmax_pad;
+    uint16_t *out;              // tiled [B*mpad][n_q*d]
+};
+void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s);
+void launch_pick_last(const float *x, int H, const PrefillGeom &g, float *xdec, float *ss,
+                      int32_t *pos, int32_t *step, int latents, hipStream_t s);
+
+}  // namespace pipo

@@ -1,0 +1,401 @@
+// Compressed-prompt prefill: the pair step batched over a chunk of latent
+// positions of every sequence.  Activations that feed an MFMA GEMM are kept
+// in the 16x32 tiled bf16 layout so that both GEMM operands move as
+// contiguous 1 KB tiles from HBM to LDS to registers.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace pipo {
+
+__device__ __forceinline__ float silu_p(float u) { return u / (1.0f + __expf(-u)); }
+__device__ __forceinline__ int vslot_p(int kappa) {
+    return 8 * ((kappa & 15) >> 2) + 4 * (kappa >> 4) + (kappa & 3);
+}
+
+// ---- pair gather: X_in[m] = [E[a]; E[b]] for latent c0 + i of sequence b ----
+__global__ void k_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                               PrefillGeom g, uint16_t *xin) {
+    const int cpr = (2 * H) >> 3;
+    const int64_t total = (int64_t)g.B * g.mpad * cpr;
+    for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int m = (int)(idx / cpr);
+        const int k = (int)(idx - (int64_t)m * cpr) << 3;
+        const int b = m / g.mpad, i = m - b * g.mpad;
+        int row = pad_id;
+        if (i < g.clen) {
+            const int t = 2 * (g.c0 + i) + (k < H ? 0 : 1);
+            row = t < g.n_tok ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+        }
+        const u32x4 v = *(const u32x4 *)(embed + tiled_index(row, k < H ? k : k - H, H));
+        *(u32x4 *)(xin + tiled_index(m, k, 2 * H)) = v;
+    }
+}
+
+void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                         const PrefillGeom &g, uint16_t *xin, hipStream_t s) {
+    const int64_t total = (int64_t)g.B * g.mpad * ((2 * H) >> 3);
+    int grid = (int)((total + 255) / 256);
+    grid = grid > 65536 ? 65536 : grid;
+    hipLaunchKernelGGL(k_gather_pairs, dim3(grid), dim3(256), 0, s, tokens, embed, H, V, pad_id, g, xin);
+}
+
+// ---- RMSNorm of fp32 rows into the tiled bf16 layout (one wave per row) ----
+__global__ __launch_bounds__(256) void k_rmsnorm_tiled(const float *x, const float *gain, int H, float eps,
+                                                       int M, uint16_t *xn) {
+    const int lane = threadIdx.x & 63;
+    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (m >= M) return;
+    const float *xr = x + (int64_t)m * H;
+    float a = 0.f;
+    for (int k = lane * 4; k < H; k += 256) {
+        const float4 v = *(const float4 *)(xr + k);
+        a += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    a = wave_sum(a);
+    const float sc = rsqrtf(a / (float)H + eps);
+    for (int k = lane * 8; k < H; k += 512) {
+        const float4 x0 = *(const float4 *)(xr + k), x1 = *(const float4 *)(xr + k + 4);
+        const float4 g0 = *(const float4 *)(gain + k), g1 = *(const float4 *)(gain + k + 4);
+        u32x4 w;
+        w[0] = pack_bf2(x0.x * sc * g0.x, x0.y * sc * g0.y);
+        w[1] = pack_bf2(x0.z * sc * g0.z, x0.w * sc * g0.w);
+        w[2] = pack_bf2(x1.x * sc * g1.x, x1.y * sc * g1.y);
+        w[3] = pack_bf2(x1.z * sc * g1.z, x1.w * sc * g1.w);
+        *(u32x4 *)(xn + tiled_index(m, k, H)) = w;
+    }
+}
+
+void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M, uint16_t *xn,
+                          hipStream_t s) {
+    hipLaunchKernelGGL(k_rmsnorm_tiled, dim3((M + 3) / 4), dim3(256), 0, s, x, gain, H, eps, M, xn);
+}
+
+// ---- MFMA GEMM  C^T[N][M] = W[N][K] X[M][K]^T, both operands tiled ---------
+// Workgroup tile 128 (rows of W) x 128 (tokens) x 64 (k), four waves in a
+// 2x2 arrangement of 64x64, LDS double-buffered.
+constexpr int kGBN = 128, kGBM = 128, kGKT = 2;   // kGKT k-tiles (32 each) per stage
+constexpr int kGStripsN = kGBN / 16, kGStripsM = kGBM / 16;
+constexpr int kGStageElems = (kGStripsN + kGStripsM) * kGKT * 512;
+
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
+    __shared__ __align__(16) uint16_t lds[2][kGStageElems];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j = lane & 15, g = lane >> 4;
+    const int wn = wave >> 1, wm = wave & 1;
+    const int nblk_n = (p.N + kGBN - 1) / kGBN;
+    const int bn = blockIdx.x % nblk_n, bm = blockIdx.x / nblk_n;
+    const int KT = p.K >> 5;
+    const int NS = p.N >> 4, MS = p.M >> 4;   // strips
+
+    // each thread moves 8 x 16 B per stage: 4 for W, 4 for X
+    u32x4 reg[8];
+    auto gload = [&](int kt) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int c = tid + r * 256;                 // chunk 0..2047
+            const bool isw = c < 1024;
+            const int cc = isw ? c : c - 1024;
+            const int st = cc >> 7, within = cc & 127;   // strip, 16 B unit in its 2 tiles
+            const int kk = kt + (within >> 6);
+            const int strip = (isw ? bn * kGStripsN : bm * kGStripsM) + st;
+            const int nstr = isw ? NS : MS;
+            const uint16_t *src = isw ? p.W : p.X;
+            u32x4 v = u32x4{0u, 0u, 0u, 0u};
+            if (strip < nstr && kk < KT)
+                v = *(const u32x4 *)(src + ((int64_t)strip * KT + kk) * 512 + (within & 63) * 8);
+            reg[r] = v;
+        }
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int c = tid + r * 256;
+            *(u32x4 *)(&lds[buf][c * 8]) = reg[r];
+        }
+    };
+
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    gload(0);
+    sstore(0);
+    __syncthreads();
+    int buf = 0;
+    for (int kt = 0; kt < KT; kt += kGKT) {
+        const bool more = kt + kGKT < KT;
+        if (more) gload(kt + kGKT);
+#pragma unroll
+        for (int kk = 0; kk < kGKT; ++kk) {
+            u32x4 af[4], bf[4];
+#pragma unroll
+            for (int si = 0; si < 4; ++si)
+                af[si] = *(const u32x4 *)(&lds[buf][((4 * wn + si) * kGKT + kk) * 512 + lane * 8]);
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi)
+                bf[mi] = *(const u32x4 *)(&lds[buf][(kGStripsN * kGKT + (4 * wm + mi) * kGKT + kk) * 512 + lane * 8]);
+#pragma unroll
+            for (int si = 0; si < 4; ++si)
+#pragma unroll
+                for (int mi = 0; mi < 4; ++mi) acc[si][mi] = mfma16(af[si], bf[mi], acc[si][mi]);
+        }
+        if (more) {
+            sstore(buf ^ 1);
+            __syncthreads();
+            buf ^= 1;
+        }
+    }
+
+    // ---- epilogue -----------------------------------------------------------
+    const int d = p.d, hs = d >> 4;
+    const int qs = p.n_q * hs, ks = p.n_kv * hs;
+#pragma unroll
+    for (int si = 0; si < 4; ++si) {
+        const int strip = bn * kGStripsN + 4 * wn + si;
+        const int row0 = strip * 16 + 4 * g;
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi) {
+            const int m = bm * kGBM + (4 * wm + mi) * 16 + j;
+            f32x4 val = acc[si][mi];
+            f32x4 other;
+            if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(val[v], 32);
+            }
+            if (strip >= NS || m >= p.M) continue;
+            const int b = m / p.g.mpad, i = m - b * p.g.mpad;
+            if (i >= p.g.clen) continue;
+            if (EPI == EPI_STORE) {
+                if (p.bias) val += *(const f32x4 *)(p.bias + row0);
+                *(f32x4 *)(p.out + (int64_t)m * p.N + row0) = val;
+            } else if (EPI == EPI_RESID) {
+                f32x4 *o = (f32x4 *)(p.out + (int64_t)m * p.N + row0);
+                *o = *o + val;
+            } else if (EPI == EPI_SWIGLU) {
+                if (g < 2) {
+                    u32x2 w;
+                    w[0] = pack_bf2(silu_p(val[0]) * other[0], silu_p(val[1]) * other[1]);
+                    w[1] = pack_bf2(silu_p(val[2]) * other[2], silu_p(val[3]) * other[3]);
+                    *(u32x2 *)(p.act + tiled_index(m, strip * 8 + 4 * g, p.N >> 1)) = w;
+                }
+            } else if (EPI == EPI_QKV) {
+                const int pos = p.g.c0 + i;
+                if (strip < qs + ks) {
+                    const bool isq = strip < qs;
+                    const int sidx = isq ? strip : strip - qs;
+                    const int head = sidx / hs, t = sidx - head * hs;
+                    const int jr = 8 * t + 4 * (g & 1);
+                    const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
+                    const float *cs = p.rope_cos + (int64_t)pos * (d >> 1) + jr;
+                    const float *sn = p.rope_sin + (int64_t)pos * (d >> 1) + jr;
+                    float r[4];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        r[v] = (g < 2) ? val[v] * cs[v] - other[v] * sn[v] : val[v] * cs[v] + other[v] * sn[v];
+                    u32x2 w;
+                    w[0] = pack_bf2(r[0], r[1]);
+                    w[1] = pack_bf2(r[2], r[3]);
+                    uint16_t *dst = isq ? p.q + (((int64_t)b * p.n_q + head) * p.g.mpad + i) * d + dim0
+                                        : p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0;
+                    *(u32x2 *)dst = w;
+                } else {
+                    const int r0 = (strip - qs - ks) * 16 + 4 * g;
+                    const int kvh = r0 / d, dim = r0 - kvh * d;
+                    uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
+                                    ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot_p(pos & 31);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(val[v]);
+                }
+            }
+        }
+    }
+}
+
+void launch_gemm(const GemmParams &p, hipStream_t s) {
+    const int grid = ((p.N + kGBN - 1) / kGBN) * ((p.M + kGBM - 1) / kGBM);
+    switch (p.epi) {
+        case EPI_STORE: hipLaunchKernelGGL(k_gemm<EPI_STORE>, dim3(grid), dim3(256), 0, s, p); break;
+        case EPI_RESID: hipLaunchKernelGGL(k_gemm<EPI_RESID>, dim3(grid), dim3(256), 0, s, p); break;
+        case EPI_SWIGLU: hipLaunchKernelGGL(k_gemm<EPI_SWIGLU>, dim3(grid), dim3(256), 0, s, p); break;
+        default: hipLaunchKernelGGL(k_gemm<EPI_QKV>, dim3(grid), dim3(256), 0, s, p); break;
+    }
+}
+
+// ---- causal grouped-query flash attention for a chunk of queries ----------
+// One workgroup per (sequence, KV group, 32-query block); wave w computes head
+// kvh*qpg + w for all 32 queries (two 16-column MFMA tiles).  Keys and values
+// of 64 positions at a time are staged in LDS and shared by the group's heads.
+constexpr int kAQ = 32;         // queries per workgroup
+constexpr int kAK = 64;         // keys per LDS stage
+
+template <int D>
+__global__ __launch_bounds__(1024) void k_attn_prefill(AttnPrefillParams p) {
+    constexpr int NC = D / 32, NT = D / 16;
+    constexpr int KS = D + 8;           // padded K row (elements)
+    constexpr int VS = 40;              // padded V tile row (elements)
+    __shared__ __align__(16) uint16_t ks[kAK * KS];
+    __shared__ __align__(16) uint16_t vs[2 * D * VS];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nthr = blockDim.x;
+    const int j = lane & 15, g = lane >> 4;
+    const int qpg = p.n_q / p.n_kv;
+    const int nqb = (p.g.clen + kAQ - 1) / kAQ;
+    // heavy (late) query blocks first
+    const int qblk = nqb - 1 - (int)(blockIdx.x % nqb);
+    const int bk = blockIdx.x / nqb;
+    const int b = bk / p.n_kv, kvh = bk - b * p.n_kv;
+    const int head = kvh * qpg + wave;
+    const int q0 = qblk * kAQ;                 // chunk-local first query
+    const int qpos0 = p.g.c0 + q0;             // absolute position of the first query
+    const float scale = 1.4426950408889634f / sqrtf((float)D);
+
+    u32x4 qb[2][NC];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            qb[ct][c] = *(const u32x4 *)(p.q + (((int64_t)b * p.n_q + head) * p.g.mpad + q0 + 16 * ct + j) * D + 32 * c + 8 * g);
+
+    const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
+    const uint16_t *vbase = p.vc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
+
+    f32x4 o[2][NT];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) o[ct][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+
+    const int kend = qpos0 + kAQ;              // keys [0, kend) may be visible
+    for (int kb0 = 0; kb0 < kend; kb0 += kAK) {
+        __syncthreads();
+        // stage K rows kb0..kb0+63 and the two V tiles
+        for (int c = tid; c < kAK * D / 8; c += nthr) {
+            const int r = c / (D / 8), e = (c - r * (D / 8)) * 8;
+            *(u32x4 *)(&ks[r * KS + e]) = *(const u32x4 *)(kbase + (int64_t)(kb0 + r) * D + e);
+        }
+        for (int c = tid; c < 2 * D * 4; c += nthr) {
+            const int row = c >> 2, e = (c & 3) * 8;       // row = tile*D + dim
+            *(u32x4 *)(&vs[row * VS + e]) = *(const u32x4 *)(vbase + (int64_t)(kb0 >> 5) * D * 32 + (int64_t)row * 32 + e);
+        }
+        __syncthreads();
+        if (wave >= qpg) continue;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int kb = kb0 + 32 * half;
+            if (kb >= kend) break;
+            u32x4 kf[2][NC];
+#pragma unroll
+            for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    kf[tau][c] = *(const u32x4 *)(&ks[(32 * half + 16 * tau + j) * KS + 32 * c + 8 * g]);
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                const int qabs = qpos0 + 16 * ct + j;
+                f32x4 st[2];
+#pragma unroll
+                for (int tau = 0; tau < 2; ++tau) {
+                    st[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) st[tau] = mfma16(kf[tau][c], qb[ct][c], st[tau]);
+                }
+                float mx = -INFINITY;
+#pragma unroll
+                for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int key = kb + 16 * tau + 4 * g + v;
+                        const float sv = key <= qabs ? st[tau][v] * scale : -INFINITY;
+                        st[tau][v] = sv;
+                        mx = fmaxf(mx, sv);
+                    }
+                mx = col_max(mx);
+                const float m_new = fmaxf(m_run[ct], mx);
+                // a query row sees at least key 0 in the first block, so m_new is finite
+                const float alpha = exp2f(m_run[ct] - m_new);
+                float ps = 0.f;
+#pragma unroll
+                for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const float e = exp2f(st[tau][v] - m_new);
+                        st[tau][v] = e;
+                        ps += e;
+                    }
+                l_run[ct] = l_run[ct] * alpha + col_sum(ps);
+                m_run[ct] = m_new;
+                u32x4 pt;
+                pt[0] = pack_bf2(st[0][0], st[0][1]);
+                pt[1] = pack_bf2(st[0][2], st[0][3]);
+                pt[2] = pack_bf2(st[1][0], st[1][1]);
+                pt[3] = pack_bf2(st[1][2], st[1][3]);
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    o[ct][t] *= alpha;
+                    const u32x4 vf = *(const u32x4 *)(&vs[(half * D + 16 * t + j) * VS + 8 * g]);
+                    o[ct][t] = mfma16(vf, pt, o[ct][t]);
+                }
+            }
+        }
+    }
+    if (wave >= qpg) return;
+    const int qd = p.n_q * D;
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+        const int i = q0 + 16 * ct + j;
+        if (i >= p.g.clen) continue;
+        const float inv = 1.0f / l_run[ct];
+        const int64_t m = (int64_t)b * p.g.mpad + i;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            u32x2 w;
+            w[0] = pack_bf2(o[ct][t][0] * inv, o[ct][t][1] * inv);
+            w[1] = pack_bf2(o[ct][t][2] * inv, o[ct][t][3] * inv);
+            *(u32x2 *)(p.out + tiled_index(m, head * D + 16 * t + 4 * g, qd)) = w;
+        }
+    }
+}
+
+void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s) {
+    const int qpg = p.n_q / p.n_kv;
+    const int nqb = (p.g.clen + kAQ - 1) / kAQ;
+    const int grid = p.g.B * p.n_kv * nqb;
+    const int threads = 64 * qpg;
+    if (p.d == 128) hipLaunchKernelGGL(k_attn_prefill<128>, dim3(grid), dim3(threads), 0, s, p);
+    else hipLaunchKernelGGL(k_attn_prefill<64>, dim3(grid), dim3(threads), 0, s, p);
+}
+
+// ---- last latent of each sequence into the decode residual buffer --------
+__global__ __launch_bounds__(256) void k_pick_last(const float *x, int H, PrefillGeom g, float *xdec,
+                                                   float *ss, int32_t *pos, int32_t *step, int latents) {
+    __shared__ float red[4];
+    const int b = blockIdx.x;
+    const float *xr = x + ((int64_t)b * g.mpad + g.clen - 1) * H;
+    float a = 0.f;
+    for (int k = threadIdx.x; k < H; k += 256) {
+        const float v = xr[k];
+        xdec[(int64_t)b * H + k] = v;
+        a += v * v;
+    }
+    a = wave_sum(a);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        ss[b] = red[0] + red[1] + red[2] + red[3];
+        pos[b] = latents;
+        step[b] = 0;
+    }
+}
+
+void launch_pick_last(const float *x, int H, const PrefillGeom &g, float *xdec, float *ss, int32_t *pos,
+                      int32_t *step, int latents, hipStream_t s) {
+    hipLaunchKernelGGL(k_pick_last, dim3(g.B), dim3(256), 0, s, x, H, g, xdec, ss, pos, step, latents);
+}
+
+}  // namespace pipo

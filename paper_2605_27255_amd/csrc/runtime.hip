@@ -1,0 +1,572 @@
+// Host runtime behind the C ABI: owns device memory, builds the per-step
+// launch sequence, drives the chunked prefill and replays the decode step as
+// a HIP graph.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "pipo.h"
+#include "kernels.h"
+
+using namespace pipo;
+
+namespace {
+
+thread_local std::string g_init_error = "no error";
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+struct LayerW {
+    uint16_t *wqkv, *wo, *wgu, *wdown;
+    float *g_attn, *g_ffn;
+};
+
+struct Arena {
+    char *base = nullptr;
+    size_t used = 0, cap = 0;
+    template <class T>
+    T *take(int64_t n) {
+        size_t bytes = (size_t)round_up((int64_t)(n * sizeof(T)), 256);
+        T *p = (T *)(base + used);
+        used += bytes;
+        return p;
+    }
+};
+
+}  // namespace
+
+struct pipo_ctx {
+    pipo_config cfg;
+    uint64_t seed;
+    int H, F, V, nq, nkv, d, L, qdim, kvdim, nqkv, pad_id, Bmax, lmax_pad, chunk;
+    int64_t kv_bstride;    // elements between sequences in one layer's K (or V) cache
+    std::string err = "no error";
+
+    char *wmem = nullptr, *amem = nullptr;
+    uint16_t *embed, *w_comp, *w_fc;
+    float *b_comp, *w_conf, *g_final, *g_mtp_h, *g_mtp_e, *g_mtp_o, *g_conf;
+    std::vector<LayerW> layers;
+    uint16_t *kc, *vc;
+    float *rope_cos, *rope_sin;
+
+    // decode state and activations
+    float *x, *ss_x, *hd, *ss_hd, *logits_b, *logits_d, *gpart, *apart;
+    uint16_t *qbuf, *attn_out, *act;
+    uint64_t *best_b, *best_d, *seeds;
+    int32_t *pairs, *pos, *step;
+    pipo_pair *out;
+    uint32_t *gctr, *actr;
+    // prefill activations
+    uint16_t *p_xin, *p_xn, *p_q, *p_o, *p_act;
+    float *p_x;
+
+    uint64_t *h_seeds = nullptr;     // pinned staging for sampler seeds
+    hipEvent_t seeds_done = nullptr;
+    hipStream_t cap_stream = nullptr;
+
+    int batch = 0, len = 0;
+    bool prefilled = false;
+    float tau = 0.5f, temperature = 0.f, top_p = 1.f;
+
+    hipGraphExec_t graph = nullptr;
+    bool graph_dirty = true;
+    bool use_graph = true;
+};
+
+static int fail(pipo_ctx *c, int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (c) c->err = buf;
+    else g_init_error = buf;
+    return code;
+}
+
+#define HIP_TRY(ctx, expr)                                                                     \
+    do {                                                                                       \
+        hipError_t e_ = (expr);                                                                \
+        if (e_ != hipSuccess)                                                                  \
+            return fail((ctx), PIPO_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));     \
+    } while (0)
+
+static int check_config(const pipo_config *c) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "config is NULL");
+    if (c->n_layers < 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->ffn <= 0 ||
+        c->vocab <= 1)
+        return fail(nullptr, PIPO_EINVAL, "non-positive model dimension");
+    if (c->hidden % 32 || c->ffn % 32 || c->vocab % 16)
+        return fail(nullptr, PIPO_EINVAL, "hidden and ffn must be multiples of 32, vocab of 16");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(nullptr, PIPO_EINVAL, "head_dim must be 64 or 128");
+    if (c->n_q_heads % c->n_kv_heads || c->n_q_heads / c->n_kv_heads > 16)
+        return fail(nullptr, PIPO_EINVAL, "n_q_heads must be a multiple of n_kv_heads, at most 16x");
+    if ((c->n_q_heads * c->head_dim) % 32) return fail(nullptr, PIPO_EINVAL, "n_q_heads*head_dim % 32 != 0");
+    if (c->max_batch < 1 || c->max_batch > 32) return fail(nullptr, PIPO_EINVAL, "max_batch must be in [1, 32]");
+    if (c->max_latent < 1 || c->prefill_chunk < 1) return fail(nullptr, PIPO_EINVAL, "max_latent and prefill_chunk must be >= 1");
+    if (c->pad_id < -1 || c->pad_id >= c->vocab) return fail(nullptr, PIPO_EINVAL, "pad_id out of range");
+    if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return fail(nullptr, PIPO_EINVAL, "bad rms_eps or rope_base");
+    if (c->gain_mode != 0 && c->gain_mode != 1) return fail(nullptr, PIPO_EINVAL, "gain_mode must be 0 or 1");
+    return PIPO_OK;
+}
+
+// tensor ids of the weight generator (model-level; per layer 100 + 10 l + slot)
+enum { TID_EMBED = 0, TID_WCOMP = 1, TID_BCOMP = 2, TID_WFC = 3, TID_WCONF = 4, TID_GFINAL = 5,
+       TID_GMTPH = 6, TID_GMTPE = 7, TID_GMTPO = 8, TID_GCONF = 9 };
+static uint64_t layer_tid(int l, int slot) { return 100ull + 10ull * (uint64_t)l + (uint64_t)slot; }
+
+extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *stream, pipo_ctx **out) {
+    if (!out) return fail(nullptr, PIPO_EINVAL, "out is NULL");
+    *out = nullptr;
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    pipo_ctx *c = new pipo_ctx();
+    c->cfg = *cfg;
+    c->seed = seed;
+    c->H = cfg->hidden; c->F = cfg->ffn; c->V = cfg->vocab; c->nq = cfg->n_q_heads; c->nkv = cfg->n_kv_heads;
+    c->d = cfg->head_dim; c->L = cfg->n_layers; c->qdim = c->nq * c->d; c->kvdim = c->nkv * c->d;
+    c->nqkv = c->qdim + 2 * c->kvdim; c->pad_id = cfg->pad_id < 0 ? cfg->vocab - 1 : cfg->pad_id;
+    c->Bmax = cfg->max_batch;
+    // 128 positions of slack: prefill attention stages 64-key blocks that may
+    // extend up to 94 positions past the last latent.
+    c->lmax_pad = (int)round_up((int64_t)cfg->max_latent + 128, 64);
+    c->chunk = cfg->prefill_chunk;
+    c->kv_bstride = (int64_t)c->nkv * c->lmax_pad * c->d;
+    const int H = c->H, F = c->F, V = c->V, B = c->Bmax;
+
+    // ---- weights --------------------------------------------------------
+    Arena w;
+    for (int pass = 0; pass < 2; ++pass) {
+        w.used = 0;
+        c->embed = w.take<uint16_t>((int64_t)V * H);
+        c->w_comp = w.take<uint16_t>((int64_t)H * 2 * H);
+        c->w_fc = w.take<uint16_t>((int64_t)H * 2 * H);
+        c->b_comp = w.take<float>(H);
+        c->w_conf = w.take<float>(2 * H);
+        c->g_final = w.take<float>(H);
+        c->g_mtp_h = w.take<float>(H);
+        c->g_mtp_e = w.take<float>(H);
+        c->g_mtp_o = w.take<float>(H);
+        c->g_conf = w.take<float>(2 * H);
+        c->layers.assign(c->L, LayerW{});
+        for (auto &l : c->layers) {
+            l.wqkv = w.take<uint16_t>((int64_t)c->nqkv * H);
+            l.wo = w.take<uint16_t>((int64_t)H * c->qdim);
+            l.wgu = w.take<uint16_t>((int64_t)2 * F * H);
+            l.wdown = w.take<uint16_t>((int64_t)H * F);
+            l.g_attn = w.take<float>(H);
+            l.g_ffn = w.take<float>(H);
+        }
+        if (pass == 0) {
+            if (hipMalloc(&c->wmem, w.used) != hipSuccess) {
+                delete c;
+                return fail(nullptr, PIPO_ENOMEM, "weights: hipMalloc of %zu bytes failed", w.used);
+            }
+            w.base = c->wmem;
+        }
+    }
+
+    // ---- KV cache, RoPE table, activations ------------------------------
+    Arena a;
+    const int64_t mcap = (int64_t)B * round_up(c->chunk, 32);
+    const int S_att = 32, S_gemv = 16;
+    const int64_t nmax = std::max(std::max((int64_t)c->nqkv, (int64_t)2 * F), (int64_t)H);
+    const int64_t ngroups = gemv_num_groups((int)std::max(nmax, (int64_t)V));
+    for (int pass = 0; pass < 2; ++pass) {
+        a.used = 0;
+        c->kc = a.take<uint16_t>((int64_t)c->L * B * c->kv_bstride);
+        c->vc = a.take<uint16_t>((int64_t)c->L * B * c->kv_bstride);
+        c->rope_cos = a.take<float>((int64_t)c->lmax_pad * (c->d / 2));
+        c->rope_sin = a.take<float>((int64_t)c->lmax_pad * (c->d / 2));
+        c->x = a.take<float>((int64_t)B * H);
+        c->hd = a.take<float>((int64_t)B * H);
+        c->ss_x = a.take<float>((int64_t)B * (H / 16));
+        c->ss_hd = a.take<float>((int64_t)B * (H / 16));
+        c->logits_b = a.take<float>((int64_t)B * V);
+        c->logits_d = a.take<float>((int64_t)B * V);
+        c->qbuf = a.take<uint16_t>((int64_t)B * c->qdim);
+        c->attn_out = a.take<uint16_t>((int64_t)B * c->qdim);
+        c->act = a.take<uint16_t>((int64_t)B * F);
+        c->best_b = a.take<uint64_t>(B);
+        c->best_d = a.take<uint64_t>(B);
+        c->seeds = a.take<uint64_t>(B);
+        c->pairs = a.take<int32_t>(2 * B);
+        c->pos = a.take<int32_t>(B);
+        c->step = a.take<int32_t>(B);
+        c->out = a.take<pipo_pair>(B);
+        c->gpart = a.take<float>((int64_t)S_gemv * B * nmax);
+        c->gctr = a.take<uint32_t>(ngroups);
+        c->apart = a.take<float>((int64_t)B * c->nq * S_att * (c->d + 2));
+        c->actr = a.take<uint32_t>((int64_t)B * c->nkv);
+        c->p_xin = a.take<uint16_t>(mcap * 2 * H);
+        c->p_x = a.take<float>(mcap * H);
+        c->p_xn = a.take<uint16_t>(mcap * H);
+        c->p_q = a.take<uint16_t>(mcap * c->qdim);
+        c->p_o = a.take<uint16_t>(mcap * c->qdim);
+        c->p_act = a.take<uint16_t>(mcap * F);
+        if (pass == 0) {
+            if (hipMalloc(&c->amem, a.used) != hipSuccess) {
+                hipFree(c->wmem);
+                delete c;
+                return fail(nullptr, PIPO_ENOMEM, "KV cache and workspaces: hipMalloc of %zu bytes failed", a.used);
+            }
+            a.base = c->amem;
+        }
+    }
+    pipo_ctx *cc = c;
+    auto cleanup_fail = [&](int code) {
+        g_init_error = cc->err;
+        pipo_free(cc);
+        return code;
+    };
+    // Zero everything once (counters, argmax keys, the KV cache: attention
+    // reads whole 32-key tiles and relies on finite values past the length).
+    if (hipMemsetAsync(c->amem, 0, a.used, s) != hipSuccess) return cleanup_fail(fail(c, PIPO_EHIP, "memset failed"));
+
+    // ---- generate weights on the device --------------------------------
+    const uint64_t sd = seed;
+    launch_init_tiled(c->embed, V, H, 0, V, sd, TID_EMBED, PERM_NONE, 0, 0, 0, s);
+    launch_init_tiled(c->w_comp, H, 2 * H, 0, H, sd, TID_WCOMP, PERM_NONE, 0, 0, 0, s);
+    launch_init_tiled(c->w_fc, H, 2 * H, 0, H, sd, TID_WFC, PERM_NONE, 0, 0, 0, s);
+    launch_init_vec(c->b_comp, H, sd, TID_BCOMP, 0, s);
+    launch_init_vec(c->w_conf, 2 * H, sd, TID_WCONF, 0, s);
+    const int gk = cfg->gain_mode ? 2 : 1;
+    launch_init_vec(c->g_final, H, sd, TID_GFINAL, gk, s);
+    launch_init_vec(c->g_mtp_h, H, sd, TID_GMTPH, gk, s);
+    launch_init_vec(c->g_mtp_e, H, sd, TID_GMTPE, gk, s);
+    launch_init_vec(c->g_mtp_o, H, sd, TID_GMTPO, gk, s);
+    launch_init_vec(c->g_conf, 2 * H, sd, TID_GCONF, gk, s);
+    for (int l = 0; l < c->L; ++l) {
+        LayerW &lw = c->layers[l];
+        launch_init_tiled(lw.wqkv, c->nqkv, H, 0, c->qdim, sd, layer_tid(l, 0), PERM_QK, c->d / 2, 0, 0, s);
+        launch_init_tiled(lw.wqkv, c->nqkv, H, c->qdim, c->qdim + c->kvdim, sd, layer_tid(l, 1), PERM_QK, c->d / 2, 0, 0, s);
+        launch_init_tiled(lw.wqkv, c->nqkv, H, c->qdim + c->kvdim, c->nqkv, sd, layer_tid(l, 2), PERM_NONE, 0, 0, 0, s);
+        launch_init_tiled(lw.wo, H, c->qdim, 0, H, sd, layer_tid(l, 3), PERM_NONE, 0, 0, 0, s);
+        launch_init_tiled(lw.wgu, 2 * F, H, 0, 2 * F, sd, layer_tid(l, 4), PERM_GATEUP, 0, 0, layer_tid(l, 5), s);
+        launch_init_tiled(lw.wdown, H, F, 0, H, sd, layer_tid(l, 6), PERM_NONE, 0, 0, 0, s);
+        launch_init_vec(lw.g_attn, H, sd, layer_tid(l, 7), gk, s);
+        launch_init_vec(lw.g_ffn, H, sd, layer_tid(l, 8), gk, s);
+    }
+    launch_rope_table(c->rope_cos, c->rope_sin, c->lmax_pad, c->d, (double)cfg->rope_base, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return cleanup_fail(fail(c, PIPO_EHIP, "init launch: %s", hipGetErrorString(e)));
+    if (hipHostMalloc((void **)&c->h_seeds, sizeof(uint64_t) * B, hipHostMallocDefault) != hipSuccess ||
+        hipEventCreateWithFlags(&c->seeds_done, hipEventDisableTiming) != hipSuccess ||
+        hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess)
+        return cleanup_fail(fail(c, PIPO_EHIP, "host staging / event / stream creation failed"));
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return cleanup_fail(fail(c, PIPO_EHIP, "init: %s", hipGetErrorString(e)));
+    const char *ng = getenv("PIPO_NO_GRAPH");
+    c->use_graph = !(ng && ng[0] == '1');
+    *out = c;
+    return PIPO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The heads of a pair step (eqs. 3-6): LM head + selection of the backbone
+// token, MTP head, LM head + selection of the draft, confidence gate.
+// `nss` is the number of sum-of-squares parts describing x (h_b).
+static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t s) {
+    const int H = c->H;
+    const bool greedy = c->temperature <= 0.f;
+    GemvParams p{};
+    p.B = B; p.eps = c->cfg.rms_eps; p.H = H; p.part = c->gpart; p.ctr = c->gctr;
+    // LM head #1 on RMSNorm(h_b; g_final)
+    p.W = c->embed; p.N = c->V; p.K = H;
+    p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
+    p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
+    launch_gemv(p, PRO_NORM, EPI_LOGITS, s);
+    if (!greedy) {
+        SampleParams sp{c->logits_b, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 0, c->best_b};
+        launch_sample(sp, s);
+    }
+    // MTP head: W_fc [RMSNorm(h_b; g_mh); RMSNorm(E[b]; g_me)]
+    GemvParams m{};
+    m.B = B; m.eps = c->cfg.rms_eps; m.H = H; m.vocab = c->V; m.part = c->gpart; m.ctr = c->gctr;
+    m.W = c->w_fc; m.N = H; m.K = 2 * H;
+    m.x = c->x; m.ss = c->ss_x; m.nss = nss; m.gain = c->g_mtp_h; m.gain2 = c->g_mtp_e;
+    m.embed = c->embed; m.tokkey = c->best_b;
+    m.out = c->hd; m.ss_out = c->ss_hd;
+    launch_gemv(m, PRO_MTP, EPI_STORE, s);
+    // LM head #2 on RMSNorm(h_d; g_mo)
+    GemvParams q{};
+    q.B = B; q.eps = c->cfg.rms_eps; q.H = H; q.part = c->gpart; q.ctr = c->gctr;
+    q.W = c->embed; q.N = c->V; q.K = H;
+    q.x = c->hd; q.ss = c->ss_hd; q.nss = H / 16; q.gain = c->g_mtp_o;
+    q.out = c->logits_d; q.best = greedy ? c->best_d : nullptr;
+    launch_gemv(q, PRO_NORM, EPI_LOGITS, s);
+    if (!greedy) {
+        SampleParams sp{c->logits_d, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 1, c->best_d};
+        launch_sample(sp, s);
+    }
+    GateParams gp{};
+    gp.hb = c->x; gp.hd = c->hd; gp.ss_b = c->ss_x; gp.nss_b = nss; gp.ss_d = c->ss_hd; gp.nss_d = H / 16;
+    gp.w_conf = c->w_conf; gp.g_conf = c->g_conf; gp.H = H; gp.eps = c->cfg.rms_eps; gp.tau = c->tau;
+    gp.best_b = c->best_b; gp.best_d = c->best_d; gp.pad_id = c->pad_id; gp.out = c->out;
+    gp.pairs = c->pairs; gp.pos = c->pos; gp.step = c->step; gp.advance = advance; gp.B = B;
+    launch_gate(gp, s);
+}
+
+static int attn_splits(const pipo_ctx *c, int B) {
+    int sp = 512 / (B * c->nkv);
+    return sp < 1 ? 1 : (sp > 32 ? 32 : sp);
+}
+
+// One pair-decode step (eq. 1 on the pending pair, eq. 2 one position, heads).
+static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
+    const int B = c->batch, H = c->H;
+    GemvParams base{};
+    base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V; base.part = c->gpart; base.ctr = c->gctr;
+    {   // pair-in compressor
+        GemvParams p = base;
+        p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;
+        p.out = c->x; p.bias = c->b_comp; p.ss_out = c->ss_x;
+        launch_gemv(p, PRO_PAIR, EPI_STORE, s);
+    }
+    for (int l = 0; l < c->L; ++l) {
+        const LayerW &lw = c->layers[l];
+        uint16_t *kc = c->kc + (int64_t)l * c->Bmax * c->kv_bstride;
+        uint16_t *vc = c->vc + (int64_t)l * c->Bmax * c->kv_bstride;
+        GemvParams p = base;
+        p.W = lw.wqkv; p.N = c->nqkv; p.K = H;
+        p.x = c->x; p.ss = c->ss_x; p.nss = H / 16; p.gain = lw.g_attn;
+        p.q = c->qbuf; p.kc = kc; p.vc = vc; p.pos = c->pos; p.rope_cos = c->rope_cos; p.rope_sin = c->rope_sin;
+        p.n_q = c->nq; p.n_kv = c->nkv; p.d = c->d; p.lmax_pad = c->lmax_pad; p.kv_bstride = c->kv_bstride;
+        launch_gemv(p, PRO_NORM, EPI_QKV, s);
+
+        AttnDecodeParams ap{};
+        ap.q = c->qbuf; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.pos = c->pos;
+        ap.B = B; ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad;
+        ap.splits = attn_splits(c, B); ap.part = c->apart; ap.ctr = c->actr; ap.out = c->attn_out;
+        launch_attn_decode(ap, s);
+
+        p = base;
+        p.W = lw.wo; p.N = H; p.K = c->qdim; p.xb = c->attn_out; p.out = c->x; p.ss_out = c->ss_x;
+        launch_gemv(p, PRO_BF16, EPI_RESID, s);
+
+        p = base;
+        p.W = lw.wgu; p.N = 2 * c->F; p.K = H; p.x = c->x; p.ss = c->ss_x; p.nss = H / 16; p.gain = lw.g_ffn;
+        p.act = c->act;
+        launch_gemv(p, PRO_NORM, EPI_SWIGLU, s);
+
+        p = base;
+        p.W = lw.wdown; p.N = H; p.K = c->F; p.xb = c->act; p.out = c->x; p.ss_out = c->ss_x;
+        launch_gemv(p, PRO_BF16, EPI_RESID, s);
+    }
+    enqueue_heads(c, B, H / 16, 1, s);
+}
+
+static int check_sampling(pipo_ctx *c, const pipo_sampling *smp, int batch) {
+    if (!smp) return fail(c, PIPO_EINVAL, "sampling is NULL");
+    if (!(smp->tau == smp->tau)) return fail(c, PIPO_EINVAL, "tau is NaN");
+    if (smp->temperature > 0.f) {
+        if (!(smp->top_p > 0.f && smp->top_p <= 1.f)) return fail(c, PIPO_EINVAL, "top_p must be in (0, 1]");
+        if (!smp->seeds) return fail(c, PIPO_EINVAL, "sampling needs per-sequence seeds");
+    }
+    (void)batch;
+    return PIPO_OK;
+}
+
+static int copy_outputs(pipo_ctx *c, pipo_pair *d_out, float *d_lb, float *d_ld, hipStream_t s) {
+    const int B = c->batch;
+    HIP_TRY(c, hipMemcpyAsync(d_out, c->out, sizeof(pipo_pair) * B, hipMemcpyDeviceToDevice, s));
+    if (d_lb) HIP_TRY(c, hipMemcpyAsync(d_lb, c->logits_b, sizeof(float) * B * c->V, hipMemcpyDeviceToDevice, s));
+    if (d_ld) HIP_TRY(c, hipMemcpyAsync(d_ld, c->logits_d, sizeof(float) * B * c->V, hipMemcpyDeviceToDevice, s));
+    return PIPO_OK;
+}
+
+extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
+                            const pipo_sampling *smp, pipo_pair *d_out, float *d_logits_b, float *d_logits_d,
+                            void *stream) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (!d_tokens || !d_out) return fail(c, PIPO_EINVAL, "d_tokens and d_out must be non-NULL");
+    if (n < 1) return fail(c, PIPO_EINVAL, "prompt length must be >= 1 (got %d)", n);
+    if (batch < 1) return fail(c, PIPO_EINVAL, "batch must be >= 1 (got %d)", batch);
+    int rc = check_sampling(c, smp, batch);
+    if (rc) return rc;
+    if (batch > c->Bmax) return fail(c, PIPO_ECAPACITY, "batch %d exceeds max_batch %d", batch, c->Bmax);
+    const int latents = (n + 1) / 2;
+    if (latents + 1 > c->cfg.max_latent)
+        return fail(c, PIPO_ECAPACITY, "%d latents leave no room for a step (max_latent %d)", latents, c->cfg.max_latent);
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(c, hipGetLastError());
+
+    if (c->batch != batch || c->tau != smp->tau || c->temperature != smp->temperature || c->top_p != smp->top_p)
+        c->graph_dirty = true;
+    c->batch = batch;
+    c->tau = smp->tau;
+    c->temperature = smp->temperature;
+    c->top_p = smp->top_p;
+    if (smp->temperature > 0.f) {
+        HIP_TRY(c, hipEventSynchronize(c->seeds_done));
+        memcpy(c->h_seeds, smp->seeds, sizeof(uint64_t) * batch);
+        HIP_TRY(c, hipMemcpyAsync(c->seeds, c->h_seeds, sizeof(uint64_t) * batch, hipMemcpyHostToDevice, s));
+        HIP_TRY(c, hipEventRecord(c->seeds_done, s));
+    }
+    const int H = c->H, F = c->F;
+    PrefillGeom g{};
+    for (int c0 = 0; c0 < latents; c0 += c->chunk) {
+        g.B = batch; g.c0 = c0; g.clen = std::min(c->chunk, latents - c0);
+        g.mpad = (int)round_up(g.clen, 32); g.n_tok = n;
+        const int M = batch * g.mpad;
+        launch_gather_pairs(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_xin, s);
+        GemmParams gp{};
+        gp.g = g; gp.M = M;
+        gp.n_q = c->nq; gp.n_kv = c->nkv; gp.d = c->d; gp.lmax_pad = c->lmax_pad; gp.kv_bstride = c->kv_bstride;
+        gp.rope_cos = c->rope_cos; gp.rope_sin = c->rope_sin;
+        GemmParams p = gp;
+        p.W = c->w_comp; p.X = c->p_xin; p.N = H; p.K = 2 * H; p.epi = EPI_STORE; p.out = c->p_x; p.bias = c->b_comp;
+        launch_gemm(p, s);
+        for (int l = 0; l < c->L; ++l) {
+            const LayerW &lw = c->layers[l];
+            uint16_t *kc = c->kc + (int64_t)l * c->Bmax * c->kv_bstride;
+            uint16_t *vc = c->vc + (int64_t)l * c->Bmax * c->kv_bstride;
+            launch_rmsnorm_tiled(c->p_x, lw.g_attn, H, c->cfg.rms_eps, M, c->p_xn, s);
+            p = gp;
+            p.W = lw.wqkv; p.X = c->p_xn; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q; p.kc = kc; p.vc = vc;
+            launch_gemm(p, s);
+            AttnPrefillParams ap{};
+            ap.q = c->p_q; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.g = g;
+            ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad; ap.out = c->p_o;
+            launch_attn_prefill(ap, s);
+            p = gp;
+            p.W = lw.wo; p.X = c->p_o; p.N = H; p.K = c->qdim; p.epi = EPI_RESID; p.out = c->p_x;
+            launch_gemm(p, s);
+            launch_rmsnorm_tiled(c->p_x, lw.g_ffn, H, c->cfg.rms_eps, M, c->p_xn, s);
+            p = gp;
+            p.W = lw.wgu; p.X = c->p_xn; p.N = 2 * F; p.K = H; p.epi = EPI_SWIGLU; p.act = c->p_act;
+            launch_gemm(p, s);
+            p = gp;
+            p.W = lw.wdown; p.X = c->p_act; p.N = H; p.K = F; p.epi = EPI_RESID; p.out = c->p_x;
+            launch_gemm(p, s);
+        }
+    }
+    launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, latents, s);
+    enqueue_heads(c, batch, 1, 0, s);
+    HIP_TRY(c, hipGetLastError());
+    rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
+    if (rc) return rc;
+    c->len = latents;
+    c->prefilled = true;
+    return PIPO_OK;
+}
+
+extern "C" int pipo_decode_step(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pair *d_out, float *d_logits_b,
+                                float *d_logits_d, void *stream) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (!d_out) return fail(c, PIPO_EINVAL, "d_out must be non-NULL");
+    if (!c->prefilled) return fail(c, PIPO_ESTATE, "decode step before prefill");
+    if (c->len + 1 > c->cfg.max_latent)
+        return fail(c, PIPO_ECAPACITY, "KV cache full: %d latents, max_latent %d", c->len, c->cfg.max_latent);
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(c, hipGetLastError());
+    if (d_in_pairs)
+        HIP_TRY(c, hipMemcpyAsync(c->pairs, d_in_pairs, sizeof(int32_t) * 2 * c->batch, hipMemcpyDeviceToDevice, s));
+    if (c->use_graph) {
+        if (c->graph_dirty || !c->graph) {
+            if (c->graph) {
+                hipGraphExecDestroy(c->graph);
+                c->graph = nullptr;
+            }
+            hipGraph_t gr;
+            HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
+            enqueue_decode(c, c->cap_stream);
+            HIP_TRY(c, hipStreamEndCapture(c->cap_stream, &gr));
+            hipError_t e = hipGraphInstantiate(&c->graph, gr, nullptr, nullptr, 0);
+            hipGraphDestroy(gr);
+            if (e != hipSuccess) return fail(c, PIPO_EHIP, "graph instantiate: %s", hipGetErrorString(e));
+            c->graph_dirty = false;
+        }
+        HIP_TRY(c, hipGraphLaunch(c->graph, s));
+    } else {
+        enqueue_decode(c, s);
+        HIP_TRY(c, hipGetLastError());
+    }
+    int rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
+    if (rc) return rc;
+    c->len += 1;
+    return PIPO_OK;
+}
+
+extern "C" int pipo_free(pipo_ctx *c) {
+    if (!c) return PIPO_OK;
+    if (c->graph) hipGraphExecDestroy(c->graph);
+    if (c->cap_stream) hipStreamDestroy(c->cap_stream);
+    if (c->seeds_done) hipEventDestroy(c->seeds_done);
+    if (c->h_seeds) hipHostFree(c->h_seeds);
+    if (c->wmem) hipFree(c->wmem);
+    if (c->amem) hipFree(c->amem);
+    delete c;
+    return PIPO_OK;
+}
+
+extern "C" const char *pipo_last_error(const pipo_ctx *c) {
+    return c ? c->err.c_str() : g_init_error.c_str();
+}
+
+extern "C" int pipo_read_weight(pipo_ctx *c, const char *name, int64_t start, int64_t count, uint16_t *host_out) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (!name || !host_out || start < 0 || count < 0) return fail(c, PIPO_EINVAL, "bad arguments");
+    const int H = c->H, F = c->F;
+    const uint16_t *src = nullptr;
+    const float *vec = nullptr;
+    int64_t N = 0, K = 0, row_base = 0, rows_total = 0, off = 0;
+    int perm = PERM_NONE, half = 0;
+    std::string nm(name);
+    int layer = -1;
+    if (nm.size() > 1 && nm[0] == 'l' && nm.find('.') != std::string::npos) {
+        layer = atoi(nm.c_str() + 1);
+        if (layer < 0 || layer >= c->L) return fail(c, PIPO_EINVAL, "layer out of range in %s", name);
+        nm = nm.substr(nm.find('.') + 1);
+    }
+    if (layer < 0) {
+        if (nm == "embed") { src = c->embed; N = c->V; K = H; }
+        else if (nm == "w_comp") { src = c->w_comp; N = H; K = 2 * H; }
+        else if (nm == "w_fc") { src = c->w_fc; N = H; K = 2 * H; }
+        else if (nm == "b_comp") { vec = c->b_comp; N = H; }
+        else if (nm == "w_conf") { vec = c->w_conf; N = 2 * H; }
+        else if (nm == "g_final") { vec = c->g_final; N = H; }
+        else if (nm == "g_mtp_h") { vec = c->g_mtp_h; N = H; }
+        else if (nm == "g_mtp_e") { vec = c->g_mtp_e; N = H; }
+        else if (nm == "g_mtp_o") { vec = c->g_mtp_o; N = H; }
+        else if (nm == "g_conf") { vec = c->g_conf; N = 2 * H; }
+    } else {
+        const LayerW &lw = c->layers[layer];
+        if (nm == "wq") { src = lw.wqkv; N = c->qdim; K = H; perm = PERM_QK; half = c->d / 2; }
+        else if (nm == "wk") { src = lw.wqkv; N = c->kvdim; K = H; perm = PERM_QK; half = c->d / 2; row_base = c->qdim; }
+        else if (nm == "wv") { src = lw.wqkv; N = c->kvdim; K = H; row_base = c->qdim + c->kvdim; }
+        else if (nm == "wo") { src = lw.wo; N = H; K = c->qdim; }
+        else if (nm == "wgate") { src = lw.wgu; N = F; K = H; perm = PERM_GATEUP; rows_total = F; }
+        else if (nm == "wup") { src = lw.wgu; N = F; K = H; perm = PERM_GATEUP; rows_total = F; off = (int64_t)F * H; }
+        else if (nm == "wdown") { src = lw.wdown; N = H; K = F; }
+        else if (nm == "g_attn") { vec = lw.g_attn; N = H; }
+        else if (nm == "g_ffn") { vec = lw.g_ffn; N = H; }
+    }
+    if (!src && !vec) return fail(c, PIPO_EINVAL, "unknown tensor %s", name);
+    const int64_t total = vec ? N : N * K;
+    if (start + count > total) return fail(c, PIPO_EINVAL, "range past the end of %s", name);
+    if (count == 0) return PIPO_OK;
+    if (vec) {
+        std::vector<float> tmp(count);
+        HIP_TRY(c, hipMemcpy(tmp.data(), vec + start, sizeof(float) * count, hipMemcpyDeviceToHost));
+        for (int64_t i = 0; i < count; ++i) {
+            uint32_t u;
+            memcpy(&u, &tmp[i], 4);
+            host_out[i] = (uint16_t)(u >> 16);   // values are bf16-exact
+        }
+        return PIPO_OK;
+    }
+    uint16_t *dtmp = nullptr;
+    HIP_TRY(c, hipMalloc(&dtmp, sizeof(uint16_t) * count));
+    launch_read_tiled(src, N, K, start + off, count, perm, half, row_base, rows_total, dtmp, nullptr);
+    hipError_t e = hipMemcpy(host_out, dtmp, sizeof(uint16_t) * count, hipMemcpyDeviceToHost);
+    hipFree(dtmp);
+    if (e != hipSuccess) return fail(c, PIPO_EHIP, "read back: %s", hipGetErrorString(e));
+    return PIPO_OK;
+}

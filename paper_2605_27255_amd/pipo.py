@@ -1,0 +1,165 @@
+"""ctypes binding of ``libpipo.so`` (argument marshalling only).
+
+Every step of the PIPO path runs in the HIP library; this module only passes
+device pointers of torch CUDA tensors and the current HIP stream through the
+C ABI declared in ``include/pipo.h``.  It raises if the library is missing:
+there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libpipo.so")
+
+PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -1, -2, -3, -4, -5
+EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_free",
+            "pipo_last_error", "pipo_read_weight")
+
+
+class PipoError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"pipo error {code}: {msg}")
+        self.code = code
+
+
+class PipoConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("pad_id", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_latent", ctypes.c_int32),
+                ("prefill_chunk", ctypes.c_int32), ("gain_mode", ctypes.c_int32)]
+
+
+class PipoSampling(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("temperature", ctypes.c_float), ("top_p", ctypes.c_float),
+                ("seeds", ctypes.POINTER(ctypes.c_uint64))]
+
+
+class PipoPair(ctypes.Structure):
+    _fields_ = [("tok_b", ctypes.c_int32), ("tok_d", ctypes.c_int32), ("conf", ctypes.c_float),
+                ("accept", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the built library (raises FileNotFoundError if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is missing: build it with paper_2605_27255_amd/build.py")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.pipo_init_weights.argtypes = [ctypes.POINTER(PipoConfig), ctypes.c_uint64, vp, ctypes.POINTER(vp)]
+    lib.pipo_prefill.argtypes = [vp, i32, vp, i32, ctypes.POINTER(PipoSampling), vp, vp, vp, vp]
+    lib.pipo_decode_step.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.pipo_free.argtypes = [vp]
+    lib.pipo_last_error.argtypes = [vp]
+    lib.pipo_last_error.restype = ctypes.c_char_p
+    lib.pipo_read_weight.argtypes = [vp, ctypes.c_char_p, i64, i64, vp]
+    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_free", "pipo_read_weight"):
+        getattr(lib, fn).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def make_config(model, max_batch: int, max_latent: int, prefill_chunk: int = 4096) -> PipoConfig:
+    """A PipoConfig from any object with the model-shape attributes."""
+    return PipoConfig(model.n_layers, model.hidden, model.n_q_heads, model.n_kv_heads, model.head_dim,
+                      model.ffn, model.vocab, float(model.rope_base), float(model.rms_eps), -1,
+                      max_batch, max_latent, prefill_chunk, int(getattr(model, "gain_mode", 0)))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+class PipoModel:
+    """One PIPO context on the current CUDA (HIP) device."""
+
+    def __init__(self, model, seed: int = 0, max_batch: int = 1, max_latent: int = 4096,
+                 prefill_chunk: int = 4096):
+        import torch
+        self.torch = torch
+        self.lib = load_library()
+        self.model = model
+        self.cfg = make_config(model, max_batch, max_latent, prefill_chunk)
+        self.ctx = ctypes.c_void_p()
+        rc = self.lib.pipo_init_weights(ctypes.byref(self.cfg), ctypes.c_uint64(seed), self._stream(),
+                                        ctypes.byref(self.ctx))
+        if rc != PIPO_OK:
+            raise PipoError(rc, self.lib.pipo_last_error(None).decode())
+        self.batch = 0
+
+    def _stream(self):
+        return ctypes.c_void_p(self.torch.cuda.current_stream().cuda_stream)
+
+    def _check(self, rc):
+        if rc != PIPO_OK:
+            raise PipoError(rc, self.lib.pipo_last_error(self.ctx).decode())
+
+    def _outputs(self, B, logits):
+        t = self.torch
+        out = t.empty((B, 4), dtype=t.int32, device="cuda")
+        lb = t.empty((B, self.model.vocab), dtype=t.float32, device="cuda") if logits else None
+        ld = t.empty((B, self.model.vocab), dtype=t.float32, device="cuda") if logits else None
+        return out, lb, ld
+
+    def prefill(self, tokens, tau: float, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
+                logits: bool = False):
+        """tokens: int32 CUDA tensor [B, n].  Returns (pairs [B,4] int32, logits_b, logits_d)."""
+        t = self.torch
+        assert tokens.dtype == t.int32 and tokens.is_cuda and tokens.dim() == 2 and tokens.is_contiguous()
+        B, n = tokens.shape
+        seed_arr = None
+        if seeds is not None:
+            seed_arr = (ctypes.c_uint64 * len(seeds))(*[int(s) for s in seeds])
+        smp = PipoSampling(tau, temperature, top_p,
+                           ctypes.cast(seed_arr, ctypes.POINTER(ctypes.c_uint64)) if seed_arr else None)
+        out, lb, ld = self._outputs(B, logits)
+        self._check(self.lib.pipo_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(out),
+                                          _ptr(lb), _ptr(ld), self._stream()))
+        self.batch = B
+        self._keep = tokens
+        return out, lb, ld
+
+    def decode_step(self, in_pairs=None, logits: bool = False):
+        """One pair step; in_pairs: optional int32 CUDA tensor [B, 2] (teacher forcing)."""
+        out, lb, ld = self._outputs(self.batch, logits)
+        self._check(self.lib.pipo_decode_step(self.ctx, _ptr(in_pairs), _ptr(out), _ptr(lb), _ptr(ld),
+                                              self._stream()))
+        return out, lb, ld
+
+    def decode_into(self, out, in_pairs=None, logits_b=None, logits_d=None):
+        """decode_step writing into caller-provided tensors (no allocation)."""
+        self._check(self.lib.pipo_decode_step(self.ctx, _ptr(in_pairs), _ptr(out), _ptr(logits_b),
+                                              _ptr(logits_d), self._stream()))
+
+    def read_weight(self, name: str, start: int, count: int):
+        import numpy as np
+        buf = np.empty(count, dtype=np.uint16)
+        self._check(self.lib.pipo_read_weight(self.ctx, name.encode(), start, count,
+                                              buf.ctypes.data_as(ctypes.c_void_p)))
+        return buf
+
+    def close(self):
+        if self.ctx:
+            self.lib.pipo_free(self.ctx)
+            self.ctx = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def unpack_pairs(out):
+    """[B,4] int32 tensor -> (tok_b, tok_d, conf, accept) numpy arrays."""
+    import numpy as np
+    a = out.cpu().numpy()
+    return a[:, 0].copy(), a[:, 1].copy(), a[:, 2].copy().view(np.float32), a[:, 3].copy()

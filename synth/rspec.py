@@ -79,8 +79,32 @@ def _fields24(r):
     return (r >> np.uint64(40)) + ((r >> np.uint64(16)) & np.uint64(0xFFFFFF))
 
 
-def weight_values(seed: int, tid: int, start: int, count: int) -> np.ndarray:
+def _fast_lib():
+    """The OpenMP build of the same recipe (synth/rspec_fast.c), if compiled."""
+    global _FAST
+    if _FAST is None:
+        import ctypes
+        import os
+        so = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_rspec_fast.so")
+        _FAST = False
+        if os.path.exists(so):
+            lib = ctypes.CDLL(so)
+            lib.rspec_fill.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
+                                       ctypes.c_int64, ctypes.c_void_p]
+            _FAST = lib
+    return _FAST
+
+
+_FAST = None
+
+
+def weight_values(seed: int, tid: int, start: int, count: int, fast: bool = True) -> np.ndarray:
     """float32 values of elements ``[start, start+count)`` of tensor ``tid``."""
+    lib = _fast_lib() if fast else False
+    if lib:
+        out = np.empty(count, dtype=np.float32)
+        lib.rspec_fill(seed & _MASK64, tid & _MASK64, start, count, out.ctypes.data)
+        return out
     k = np.uint64(key(seed, tid))
     idx = np.arange(start, start + count, dtype=np.uint64)
     with np.errstate(over="ignore"):
@@ -90,7 +114,7 @@ def weight_values(seed: int, tid: int, start: int, count: int) -> np.ndarray:
     return centred.astype(np.float32) * WEIGHT_SCALE
 
 
-def weight_tensor(seed: int, tid: int, shape, chunk: int = 1 << 24) -> np.ndarray:
+def weight_tensor(seed: int, tid: int, shape, chunk: int = 1 << 26) -> np.ndarray:
     """A whole float32 tensor in logical row-major ``[out][in]`` order."""
     n = int(np.prod(shape))
     out = np.empty(n, dtype=np.float32)

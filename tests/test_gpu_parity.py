@@ -1,0 +1,187 @@
+"""GPU parity of the HIP path (through the C ABI) against the float64 oracle."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from synth import rspec
+from synth.configs import TINY, DENSE_4B, ModelConfig, model_tensor_shapes
+from oracle import pipo_oracle as O
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+from parity import run_parity  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    return t
+
+
+def _model(cfg, **kw):
+    from paper_2605_27255_amd import PipoModel
+    return PipoModel(cfg, **kw)
+
+
+def _expected_bits(cfg, name, seed, start, count):
+    shapes = model_tensor_shapes(cfg)
+    base = name.split(".")[-1]
+    tid = (rspec.TENSOR_IDS[name] if "." not in name
+           else rspec.layer_tid(int(name.split(".")[0][1:]), base))
+    if base.startswith("g_"):
+        v = rspec.gain_values(seed, tid, shapes[name][0], cfg.gain_mode)[start:start + count]
+    else:
+        v = rspec.weight_values(seed, tid, start, count)
+    return rspec.bf16_bits(v)
+
+
+def test_device_weights_bit_identical_tiny(torch):
+    for gm in (0, 1):
+        cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": gm})
+        m = _model(cfg, seed=5, max_batch=1, max_latent=40, prefill_chunk=16)
+        for name, shape in model_tensor_shapes(cfg).items():
+            n = int(np.prod(shape))
+            got = m.read_weight(name, 0, n)
+            np.testing.assert_array_equal(got, _expected_bits(cfg, name, 5, 0, n), err_msg=name)
+        m.close()
+
+
+def test_device_weights_bit_identical_4b_slices(torch):
+    cfg = DENSE_4B.with_layers(1)
+    m = _model(cfg, seed=0, max_batch=1, max_latent=64, prefill_chunk=64)
+    shapes = model_tensor_shapes(cfg)
+    rng = np.random.default_rng(0)
+    for name in ("embed", "w_comp", "w_fc", "b_comp", "w_conf", "l0.wq", "l0.wk", "l0.wv", "l0.wo",
+                 "l0.wgate", "l0.wup", "l0.wdown", "l0.g_attn"):
+        n = int(np.prod(shapes[name]))
+        cnt = min(4096, n)
+        for start in sorted({0, n - cnt, int(rng.integers(0, n - cnt + 1))}):
+            got = m.read_weight(name, start, cnt)
+            np.testing.assert_array_equal(got, _expected_bits(cfg, name, 0, start, cnt), err_msg=f"{name}@{start}")
+    m.close()
+
+
+def test_tiny_workload_parity_greedy(torch):
+    """Tiny model: 64-token prompt (32 latents, 2 chunks), 16 greedy pair steps,
+    against the oracle on the bf16-valued weights the device holds."""
+    n, steps, tau = 64, 16, 0.5
+    prompts = rspec.prompt_tokens(1, n, TINY.vocab)
+    m = _model(TINY, seed=0, max_batch=1, max_latent=32 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(TINY, seed=0, precision="bf16")
+    rep, host = run_parity(m, W, prompts, steps, O.Sampling(tau=tau), log)
+    rep.check()
+    m.close()
+
+
+def test_tiny_workload_against_fp32_weights(torch):
+    """The same run against the oracle on the unrounded float32 weights.  Storing
+    the weights in bf16 alone moves these logits by 4.5e-3 mean-relative (oracle
+    against oracle), so the mean-relative bound here is 1e-2; tokens, accept
+    flags, confidence (1e-3) and max-abs (2e-2) keep their bounds."""
+    n, steps, tau = 64, 16, 0.5
+    prompts = rspec.prompt_tokens(1, n, TINY.vocab)
+    m = _model(TINY, seed=0, max_batch=1, max_latent=32 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(TINY, seed=0, precision="fp32")
+    rep, host = run_parity(m, W, prompts, steps, O.Sampling(tau=tau), log, mean_rel_tol=1e-2)
+    rep.check()
+    m.close()
+
+
+def test_tiny_parity_odd_prompt_ragged_chunks_gains(torch):
+    """Odd prompt (PAD at the odd slot), ragged chunks, non-unit RMSNorm gains."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    n, steps, tau = 61, 6, 0.5
+    prompts = rspec.prompt_tokens(1, n, cfg.vocab, seed=3)
+    m = _model(cfg, seed=11, max_batch=1, max_latent=31 + steps + 1, prefill_chunk=8)
+    W = O.OracleWeights.generate(cfg, seed=11, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=tau), log)
+    rep.check()
+    m.close()
+
+
+def test_tiny_parity_batch_top_p(torch):
+    """Batch 3, temperature 0.6, top-p 0.95, tau 0.7, per-sequence seeds."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    B, n, steps = 3, 40, 5
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=4)
+    smp = O.Sampling(tau=0.7, temperature=0.6, top_p=0.95, seeds=tuple(1000 + b for b in range(B)))
+    m = _model(cfg, seed=2, max_batch=4, max_latent=20 + steps + 1, prefill_chunk=32)
+    W = O.OracleWeights.generate(cfg, seed=2, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, smp, log)
+    rep.check()
+    m.close()
+
+
+def test_tiny_parity_batch_greedy_tau_extremes(torch):
+    """tau = 0 accepts every draft, tau > 1 none (pair-in single-token decoding)."""
+    B, n, steps = 2, 30, 4
+    prompts = rspec.prompt_tokens(B, n, TINY.vocab, seed=6)
+    W = O.OracleWeights.generate(TINY, seed=1, precision="bf16")
+    for tau, expect in ((0.0, 1), (1.5, 0)):
+        m = _model(TINY, seed=1, max_batch=2, max_latent=15 + steps + 1, prefill_chunk=64)
+        rep, host = run_parity(m, W, prompts, steps, O.Sampling(tau=tau), log)
+        rep.check()
+        assert all((h[0][3] == expect).all() for h in host)
+        m.close()
+
+
+def test_4b_width_two_layers_2048_latents(torch):
+    """Full 4B-class width (hidden 2560, 32/8 heads of 128, FFN 9728, vocab 151936)
+    with two layers: 4096-token prompt (2048 latents, one chunk), 3 greedy steps."""
+    cfg = DENSE_4B.with_layers(2)
+    n, steps = 4096, 3
+    prompts = rspec.prompt_tokens(1, n, cfg.vocab)
+    m = _model(cfg, seed=0, max_batch=1, max_latent=2048 + steps + 1, prefill_chunk=4096)
+    log("generating oracle weights")
+    W = O.OracleWeights.generate(cfg, seed=0, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log)
+    rep.check()
+    m.close()
+
+
+def test_deterministic_repeat(torch):
+    prompts = torch.from_numpy(rspec.prompt_tokens(2, 50, TINY.vocab)).cuda()
+    res = []
+    for _ in range(2):
+        m = _model(TINY, seed=0, max_batch=2, max_latent=40, prefill_chunk=16)
+        outs = [m.prefill(prompts, 0.5, logits=True)]
+        for _ in range(4):
+            outs.append(m.decode_step(logits=True))
+        torch.cuda.synchronize()
+        res.append([(o.cpu().numpy(), lb.cpu().numpy(), ld.cpu().numpy()) for o, lb, ld in outs])
+        m.close()
+    for a, b in zip(*res):
+        for x, y in zip(a, b):
+            np.testing.assert_array_equal(x, y)
+
+
+def test_abi_state_and_capacity_errors(torch):
+    from paper_2605_27255_amd import PipoError, PIPO_ESTATE, PIPO_ECAPACITY
+    m = _model(TINY, seed=0, max_batch=2, max_latent=12, prefill_chunk=16)
+    with pytest.raises(PipoError) as e:
+        m.batch = 1
+        m.decode_step()
+    assert e.value.code == PIPO_ESTATE
+    toks = torch.from_numpy(rspec.prompt_tokens(3, 8, TINY.vocab)).cuda()
+    with pytest.raises(PipoError) as e:
+        m.prefill(toks, 0.5)
+    assert e.value.code == PIPO_ECAPACITY                       # batch 3 > 2
+    with pytest.raises(PipoError) as e:
+        m.prefill(torch.from_numpy(rspec.prompt_tokens(1, 23, TINY.vocab)).cuda(), 0.5)
+    assert e.value.code == PIPO_ECAPACITY                       # 12 latents + 1 > 12
+    m.prefill(torch.from_numpy(rspec.prompt_tokens(1, 20, TINY.vocab)).cuda(), 0.5)   # 10 latents
+    m.decode_step()                                              # 11 latents
+    m.decode_step()                                              # 12 latents: full
+    with pytest.raises(PipoError) as e:
+        m.decode_step()
+    torch.cuda.synchronize()
+    assert e.value.code == PIPO_ECAPACITY
+    m.close()

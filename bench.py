@@ -1,0 +1,247 @@
+#!/usr/bin/env python3
+"""PIPO pair-in/pair-out throughput on one MI355X.
+
+One timed step is one whole request of the workload: the compressed-prompt
+prefill (pair gather, compressor, backbone over ceil(n/2) latents, heads)
+followed by every pair-decode step (compressor, backbone over one latent, LM
+head, MTP head, LM head, confidence gate), with the prompt already resident
+in HBM.  ``value`` = emitted output tokens (1 + accept per sequence per pair
+step, the prefill's pair included) / wall time of the timed steps.
+
+Also reported on the same JSON line:
+  roofline      the weight-streaming GEMM kernel (k_gemv, the dominant
+                kernel of decode): algorithmic bytes of its launches in one
+                pair step / their summed duration, from HIP events recorded
+                around each launch on the library's stream (profiling pass);
+  cpu_baseline  the float64 oracle timed on this host on a bounded sample.
+Diagnostics go to stderr; stdout carries the one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "output tokens/s per step at bs=1/32 (4B-class); HBM GB/s and % roofline"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gemv_step_bytes(m, B):
+    """Algorithmic HBM bytes of the k_gemv launches of one pair step.
+
+    Every weight matrix once (bf16), except the tied embedding / LM head, which
+    is streamed twice (backbone token, then the draft token that depends on
+    it); plus each launch's activations read once and outputs written once.
+    """
+    h, f, v, L = m.hidden, m.ffn, m.vocab, m.n_layers
+    nqkv = m.q_dim + 2 * m.kv_dim
+    w = 2 * (L * (nqkv * h + h * m.q_dim + 2 * f * h + h * f) + 2 * (h * 2 * h) + 2 * v * h)
+    act = B * 4 * (L * (h + m.q_dim // 2 + h + f // 2) + 2 * h + 2 * h)        # inputs
+    act += B * 4 * (L * (nqkv // 2 + h + f // 2 + h) + h + h + 2 * v)         # outputs
+    return w + act
+
+
+def kv_step_bytes(m, B, length):
+    """KV-cache bytes one pair step reads at a context of ``length`` latents."""
+    return 2 * m.n_layers * B * m.n_kv_heads * (length + 1) * m.head_dim * 2
+
+
+def cpu_baseline(wl, accept_rate, budget_s=20.0):
+    """The oracle (float64, NumPy) on a bounded sample of one pair step.
+
+    Sample: the per-layer step (two decoder layers of the workload's shape over
+    synthetic KV caches at the workload's prompt length) and the heads (LM
+    head, MTP head, LM head, confidence) for one sequence; one pair step is
+    heads + layers/2 * (two-layer time); scaled to output tokens/s with the
+    acceptance the GPU run measured.
+    """
+    import numpy as np
+    from oracle import pipo_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    m2 = wl.model.with_layers(2)
+    W = O.OracleWeights.generate(m2, seed=wl.seed, precision="bf16")
+    rng = np.random.default_rng(0)
+    T = wl.latents
+    caches0 = [[rng.standard_normal((m2.n_kv_heads, T, m2.head_dim)),
+                rng.standard_normal((m2.n_kv_heads, T, m2.head_dim))] for _ in range(2)]
+    orc = O.PipoOracle(W)
+    orc.sampling = O.Sampling(tau=wl.tau, temperature=wl.temperature, top_p=wl.top_p,
+                              seeds=(wl.sample_seed_base,))
+    z = rng.standard_normal(m2.hidden)
+    t_layers, t_heads, reps = [], [], 0
+    t_start = time.perf_counter()
+    while reps < 1 or (time.perf_counter() - t_start < budget_s and reps < 3):
+        caches = [[c[0], c[1]] for c in caches0]
+        t0 = time.perf_counter()
+        h = O.backbone_step(W, z, T, caches)
+        t1 = time.perf_counter()
+        orc.heads(h, 0, 1)
+        t2 = time.perf_counter()
+        t_layers.append(t1 - t0)
+        t_heads.append(t2 - t1)
+        reps += 1
+    step_s = min(t_heads) + wl.model.n_layers / 2 * min(t_layers)
+    # the oracle runs the batch's sequences one after another: (1 + acceptance) tokens per step_s
+    return {"value": (1.0 + accept_rate) / step_s,
+            "unit": "output tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"float64 oracle, one sequence: {reps} repetitions of 2 decoder layers at "
+                       f"{T} cached latents plus the heads; pair step = heads + {wl.model.n_layers}/2 x "
+                       f"(2-layer time) = {step_s * 1e3:.1f} ms; batch sequences run one after another; "
+                       f"tokens per pair step 1 + {accept_rate:.3f} (GPU-measured acceptance)")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="4b-bs1-ctx2048")
+    ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's step count")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the PIPO decode path shards "
+              "as independent data-parallel replicas, one per GPU, with no inter-GPU traffic, so the "
+              "one-GPU figure is the per-GPU figure.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from dataclasses import replace
+    from paper_2605_27255_amd import PipoModel, unpack_pairs
+    from synth import rspec
+    from synth.configs import WORKLOADS
+
+    wl = WORKLOADS[args.workload]
+    if args.decode_steps is not None:
+        wl = replace(wl, decode_steps=args.decode_steps)
+    m = wl.model
+    B, steps = wl.batch, wl.decode_steps
+    torch.cuda.set_device(0)
+    log(f"workload {wl.name}: {m.n_layers}L h{m.hidden} B{B} prompt {wl.prompt_tokens} "
+        f"({wl.latents} latents) + {steps} pair steps")
+    t0 = time.perf_counter()
+    model = PipoModel(m, seed=wl.seed, max_batch=B, max_latent=wl.latents + steps + 1,
+                      prefill_chunk=wl.prefill_chunk)
+    prompts = torch.from_numpy(rspec.prompt_tokens(B, wl.prompt_tokens, m.vocab, wl.prompt_seed)).cuda()
+    seeds = [wl.sample_seed_base + b for b in range(B)] if wl.temperature > 0 else None
+    outs = torch.empty((steps, B, 4), dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    log(f"init (device weight generation) {time.perf_counter() - t0:.1f} s")
+
+    stream = torch.cuda.current_stream()
+
+    def job(ev=None):
+        if ev:
+            ev[0].record(stream)
+        first, _, _ = model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds)
+        if ev:
+            ev[1].record(stream)
+        for s in range(steps):
+            model.decode_into(outs[s])
+        if ev:
+            ev[2].record(stream)
+        return first
+
+    for _ in range(args.warmup):
+        job()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    emitted, accepts, pairs = 0, 0, 0
+    firsts = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        firsts.append(job(evs[k]))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    # emitted tokens: the last timed request's records (all requests are identical)
+    fb = unpack_pairs(firsts[-1])
+    acc_all = outs[:, :, 3].cpu().numpy()
+    accepts = int(acc_all.sum()) + int(fb[3].sum())
+    pairs = steps * B + B
+    emitted_per_job = pairs + accepts
+    value = emitted_per_job * args.steps / wall
+    ttft = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    dec_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ms_step = dec_ms / max(steps, 1)
+    acc_rate = accepts / pairs
+    kv_mean = float(np.mean([kv_step_bytes(m, B, wl.latents + s) for s in range(max(steps, 1))]))
+    step_bytes = gemv_step_bytes(m, B) + kv_mean
+    log(f"timed {args.steps} requests in {wall:.3f} s: TTFT {ttft:.2f} ms, decode {ms_step:.3f} ms/pair step, "
+        f"acceptance {acc_rate:.3f}, {value:.1f} output tokens/s")
+
+    result = {
+        "metric": METRIC, "value": round(value, 3), "unit": "output tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall / args.steps * 1e3, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (R-spec random-init weights and uniform random prompts)",
+        "config": {"workload": wl.name, "layers": m.n_layers, "hidden": m.hidden, "ffn": m.ffn,
+                   "heads_q_kv": [m.n_q_heads, m.n_kv_heads], "head_dim": m.head_dim, "vocab": m.vocab,
+                   "batch": B, "prompt_tokens": wl.prompt_tokens, "latents": wl.latents,
+                   "decode_steps": steps, "tau": wl.tau,
+                   "sampling": "greedy" if wl.temperature <= 0 else f"T{wl.temperature} top-p{wl.top_p}",
+                   "parallelism": "none (1 GPU)"},
+        "ttft_ms": round(ttft, 3),
+        "decode": {"ms_per_pair_step": round(ms_step, 4), "pair_steps_per_s": round(1e3 / ms_step, 2),
+                   "output_tokens_per_s": round(B * (1 + acc_rate) * 1e3 / ms_step, 2),
+                   "acceptance": round(acc_rate, 4),
+                   "algorithmic_gb_per_step": round(step_bytes / 1e9, 4),
+                   "hbm_gbs": round(step_bytes / ms_step / 1e6, 1),
+                   "hbm_frac": round(step_bytes / ms_step / 1e6 / HBM_PEAK_GBS, 4)},
+    }
+
+    if not args.no_profile:
+        psteps = min(steps, 16)
+        model.profile(True)
+        model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds)
+        torch.cuda.synchronize()
+        pre = model.profile_read()
+        model.profile(True)
+        for s in range(psteps):
+            model.decode_into(outs[s])
+        torch.cuda.synchronize()
+        prof = model.profile_read()
+        model.profile(False)
+        gemv_ms = sum(prof[k][0] for k in ("gemv_layer", "gemv_lmhead", "gemv_small")) / psteps
+        gemv_n = sum(prof[k][1] for k in ("gemv_layer", "gemv_lmhead", "gemv_small")) / psteps
+        gb = gemv_step_bytes(m, B)
+        achieved = gb / (gemv_ms * 1e-3) / 1e9
+        per_class = {k: {"ms_per_step": round(v[0] / psteps, 4), "launches_per_step": v[1] / psteps}
+                     for k, v in prof.items() if v[1]}
+        result["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                              "kernel": "k_gemv (decode weight-streaming GEMM, all launches of a pair step)",
+                              "bytes_per_launch": round(gb / gemv_n), "launches_per_step": gemv_n,
+                              "avg_launch_us": round(gemv_ms / gemv_n * 1e3, 3)}
+        result["kernel_ms_per_pair_step"] = per_class
+        result["prefill_kernel_ms"] = {k: round(v[0], 3) for k, v in pre.items() if v[1]}
+        log("per-class decode ms/step:", {k: v["ms_per_step"] for k, v in per_class.items()})
+        log("prefill kernel ms:", result["prefill_kernel_ms"])
+
+    model.close()
+    del model
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        result["cpu_baseline"] = cpu_baseline(wl, acc_rate)
+        log(f"cpu baseline {time.perf_counter() - t0:.1f} s: {result['cpu_baseline']['value']:.3f} tokens/s")
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -48,7 +48,7 @@ typedef struct pipo_ctx pipo_ctx;   /* opaque; owns weights, KV cache, workspace
  * hidden % 32 == 0, ffn % 32 == 0, vocab % 16 == 0, head_dim in {64, 128},
  * n_q_heads % n_kv_heads == 0 and n_q_heads / n_kv_heads <= 16,
  * (n_q_heads*head_dim) % 32 == 0, 1 <= max_batch <= 32, max_latent >= 1,
- * prefill_chunk a positive multiple of 16. */
+ * prefill_chunk >= 1. */
 typedef struct {
     int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
     float   rope_base;       /* RoPE frequencies base^(-2j/d) over latent positions */
@@ -120,6 +120,29 @@ const char *pipo_last_error(const pipo_ctx *ctx);
  * Errors: PIPO_EINVAL (unknown name or range). */
 int pipo_read_weight(pipo_ctx *ctx, const char *name, int64_t start, int64_t count,
                      uint16_t *host_out);
+
+/* Kernel classes of the profiling counters. */
+#define PIPO_K_GEMV_LAYER   0   /* decode weight-streaming GEMM: QKV, O, gate/up, down */
+#define PIPO_K_GEMV_LMHEAD  1   /* decode LM-head GEMM (both passes), argmax fused     */
+#define PIPO_K_GEMV_SMALL   2   /* decode compressor and MTP GEMMs                    */
+#define PIPO_K_ATTN_DECODE  3   /* split-K flash-decode (merge included)               */
+#define PIPO_K_SAMPLE       4   /* top-p sampler                                       */
+#define PIPO_K_GATE         5   /* confidence gate + next pair                         */
+#define PIPO_K_PREFILL_GEMM 6   /* prefill MFMA GEMMs                                  */
+#define PIPO_K_PREFILL_ATTN 7   /* prefill causal flash attention                      */
+#define PIPO_K_PREFILL_MISC 8   /* prefill gather, RMSNorm, last-latent pick           */
+#define PIPO_K_CLASSES      9
+
+/* Profiling: while on (on != 0), pipo_prefill and pipo_decode_step launch
+ * eagerly (no graph) with a HIP event recorded on the call's stream before
+ * and after every kernel; durations accumulate per kernel class.  Turning it
+ * on clears the accumulators.  Errors: PIPO_EINVAL (NULL ctx). */
+int pipo_profile_enable(pipo_ctx *ctx, int on);
+
+/* Synchronise the pending profiling events and return, for kernel class
+ * `kclass` (PIPO_K_*), the summed duration in milliseconds and the number of
+ * launches since profiling was turned on.  Errors: PIPO_EINVAL. */
+int pipo_profile_read(pipo_ctx *ctx, int kclass, double *total_ms, int64_t *launches);
 
 #ifdef __cplusplus
 }

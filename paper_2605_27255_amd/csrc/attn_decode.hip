@@ -8,8 +8,8 @@
 // probabilities, held as (4g + v, 16 + 4g + v) for lane group g, are already
 // the B operand of O^T[dim][head] += V^T P^T because the V cache stores each
 // 32-key tile in that key order (see vslot in gemv.hip).  Per-split results
-// (m, l, o) go to a partial buffer; the last wave of a group to finish merges
-// them in split order.
+// (m, l, o) go to a partial buffer; a second kernel merges them per head in
+// split order (the kernel boundary makes every split's partial visible).
 #include "device_common.h"
 #include "kernels.h"
 
@@ -19,9 +19,6 @@ template <int D>
 __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     constexpr int NC = D / 32;   // 32-wide d chunks (QK^T k-steps)
     constexpr int NT = D / 16;   // 16-wide d tiles (PV output tiles)
-    __shared__ int s_last;
-    __shared__ float s_w[16 * 64];
-
     const int lane = threadIdx.x, j = lane & 15, g = lane >> 4;
     const int S = p.splits;
     const int split = blockIdx.x % S;
@@ -105,45 +102,43 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
             pr[D + 1] = l_run;
         }
     }
-    __threadfence();
+}
+
+// merge: one wave per (sequence, query head): weights exp2(m_s - M), then the
+// weighted sum of the split outputs over L = sum_s w_s l_s, in split order.
+template <int D>
+__global__ __launch_bounds__(64) void k_attn_merge(AttnDecodeParams p) {
+    __shared__ float s_w[64];
+    const int lane = threadIdx.x;
+    const int S = p.splits;
+    const int bh = blockIdx.x;                        // b * n_q + head
+    const float *ph = p.part + (int64_t)bh * S * (D + 2);
+    const float ms = lane < S ? ph[lane * (D + 2) + D] : -INFINITY;
+    const float ls = lane < S ? ph[lane * (D + 2) + D + 1] : 0.f;
+    const float M = wave_max(ms);
+    const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
+    const float L = wave_sum(w * ls);
+    s_w[lane] = w;
     __syncthreads();
-    if (lane == 0) {
-        const uint32_t prev = __hip_atomic_fetch_add(p.ctr + bk, 1u, __ATOMIC_ACQ_REL,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (prev == (uint32_t)(S - 1));
+    const float inv = 1.0f / L;
+#pragma unroll
+    for (int dim = lane; dim < D; dim += 64) {
+        float acc = 0.f;
+#pragma unroll 8
+        for (int sp = 0; sp < S; ++sp) acc += s_w[sp] * ph[sp * (D + 2) + dim];
+        p.out[(int64_t)bh * D + dim] = acc * inv;
     }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    // merge: weights exp2(m_s - M) / L per (head, split), then a weighted sum
-    for (int h = 0; h < qpg; ++h) {
-        const float *ph = p.part + ((int64_t)b * p.n_q + kvh * qpg + h) * S * (D + 2);
-        float M = -INFINITY;
-        for (int sp = lane; sp < S; sp += 64) M = fmaxf(M, ph[sp * (D + 2) + D]);
-        M = wave_max(M);
-        float L = 0.f;
-        for (int sp = lane; sp < S; sp += 64) {
-            const float ms = ph[sp * (D + 2) + D];
-            const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
-            s_w[h * 64 + sp] = w;
-            L += w * ph[sp * (D + 2) + D + 1];
-        }
-        L = wave_sum(L);
-        __syncthreads();
-        const float inv = 1.0f / L;
-        for (int dim = lane; dim < D; dim += 64) {
-            float acc = 0.f;
-            for (int sp = 0; sp < S; ++sp) acc += s_w[h * 64 + sp] * ph[sp * (D + 2) + dim];
-            p.out[((int64_t)b * p.n_q + kvh * qpg + h) * D + dim] = (uint16_t)f2bf(acc * inv);
-        }
-    }
-    if (lane == 0) p.ctr[bk] = 0u;
 }
 
 void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s) {
     const int grid = p.B * p.n_kv * p.splits;
-    if (p.d == 128) hipLaunchKernelGGL(k_attn_decode<128>, dim3(grid), dim3(64), 0, s, p);
-    else hipLaunchKernelGGL(k_attn_decode<64>, dim3(grid), dim3(64), 0, s, p);
+    if (p.d == 128) {
+        hipLaunchKernelGGL(k_attn_decode<128>, dim3(grid), dim3(64), 0, s, p);
+        hipLaunchKernelGGL(k_attn_merge<128>, dim3(p.B * p.n_q), dim3(64), 0, s, p);
+    } else {
+        hipLaunchKernelGGL(k_attn_decode<64>, dim3(grid), dim3(64), 0, s, p);
+        hipLaunchKernelGGL(k_attn_merge<64>, dim3(p.B * p.n_q), dim3(64), 0, s, p);
+    }
 }
 
 }  // namespace pipo

@@ -25,6 +25,22 @@ __device__ __forceinline__ uint32_t f2bf(float f) {
 __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
     return f2bf(lo) | (f2bf(hi) << 16);
 }
+// x ~= bf(hi) + bf(lo): the bf16 rounding of x and of its remainder.
+__device__ __forceinline__ void split_bf(float x, uint32_t &hi, uint32_t &lo) {
+    hi = f2bf(x);
+    lo = f2bf(x - bf2f(hi));
+}
+// Eight floats into hi and lo bf16x8 words.
+__device__ __forceinline__ void split8(const float *v, u32x4 &hi, u32x4 &lo) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        uint32_t h0, l0, h1, l1;
+        split_bf(v[2 * i], h0, l0);
+        split_bf(v[2 * i + 1], h1, l1);
+        hi[i] = h0 | (h1 << 16);
+        lo[i] = l0 | (l1 << 16);
+    }
+}
 
 // ---- MFMA: C[16x16] += A[16x32] * B[32x16], bf16 in, fp32 accumulate ------
 // Lane l = 16*g + r supplies A row r and B column r, eight k-elements each

@@ -10,8 +10,8 @@ struct PairOut { int32_t tok_b, tok_d; float conf; int32_t accept; };
 
 // One workgroup per sequence: s = w_c . RMSNorm([h_b; h_d]) * g_c,
 // c = sigmoid(s), accept iff c >= tau; next pair = (b, accept ? d : PAD).
-__global__ __launch_bounds__(256) void k_gate(GateParams p) {
-    __shared__ float red[4];
+__global__ __launch_bounds__(512) void k_gate(GateParams p) {
+    __shared__ float red[8];
     __shared__ float s_sc;
     const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int H = p.H;
@@ -23,7 +23,8 @@ __global__ __launch_bounds__(256) void k_gate(GateParams p) {
         if (lane == 0) s_sc = rsqrtf(a / (float)(2 * H) + p.eps);
     }
     float dot = 0.f;
-    for (int k = threadIdx.x; k < 2 * H; k += 256) {
+#pragma unroll 4
+    for (int k = threadIdx.x; k < 2 * H; k += 512) {
         const float u = k < H ? p.hb[(int64_t)b * H + k] : p.hd[(int64_t)b * H + k - H];
         dot += p.w_conf[k] * p.g_conf[k] * u;
     }
@@ -31,7 +32,7 @@ __global__ __launch_bounds__(256) void k_gate(GateParams p) {
     if (lane == 0) red[wave] = dot;
     __syncthreads();
     if (threadIdx.x == 0) {
-        const float s = (red[0] + red[1] + red[2] + red[3]) * s_sc;
+        const float s = (((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7]))) * s_sc;
         const float c = 1.0f / (1.0f + expf(-s));
         const int acc = c >= p.tau ? 1 : 0;
         const int32_t tb = argmax_key_id(p.best_b[b]);
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(256) void k_gate(GateParams p) {
 }
 
 void launch_gate(const GateParams &p, hipStream_t s) {
-    hipLaunchKernelGGL(k_gate, dim3(p.B), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_gate, dim3(p.B), dim3(512), 0, s, p);
 }
 
 // ---------------------------------------------------------------------------

@@ -8,18 +8,19 @@ namespace pipo {
 // ----------------------------------------------------------------------------
 // Weight-streaming skinny GEMM for the decode step:  Y^T[N][B] = W[N][K] X^T.
 // W is tiled (16x32 tiles, see device_common.h), X is produced on the fly by
-// the prologue into LDS as bf16, B <= 32.
+// the prologue into LDS as a bf16 pair (hi + lo, about 16 significant bits),
+// B <= 32.
 // ----------------------------------------------------------------------------
 enum GemvPro : int {
     PRO_NORM = 0,   // X = bf16(RMSNorm(x) * gain): x fp32 [B][K], sum-of-squares parts
-    PRO_BF16 = 1,   // X = xb, bf16 [B][K]
+    PRO_F32  = 1,   // X = xf, fp32 [B][K]
     PRO_PAIR = 2,   // X = [E[a]; E[b]] for int32 pairs [B][2] (pair-in compressor)
     PRO_MTP  = 3,   // X = [RMSNorm(h_b) g1; RMSNorm(E[tok]) g2], tok from an argmax key
 };
 enum GemvEpi : int {
     EPI_STORE  = 0,  // out fp32 [B][N] = acc (+ bias); sum-of-squares parts
     EPI_RESID  = 1,  // out fp32 [B][N] += acc; sum-of-squares parts
-    EPI_SWIGLU = 2,  // act bf16 [B][N/2] = SiLU(gate) * up (gate/up strip-interleaved)
+    EPI_SWIGLU = 2,  // act fp32 [B][N/2] = SiLU(gate) * up (gate/up strip-interleaved)
     EPI_QKV    = 3,  // RoPE q,k; q bf16 [B][n_q][d]; k, v appended to the KV cache
     EPI_LOGITS = 4,  // logits fp32 [B][N]; optional argmax key per row (greedy)
 };
@@ -27,16 +28,13 @@ enum GemvEpi : int {
 struct GemvParams {
     const uint16_t *W;          // tiled [N][K]
     int N, K, B;
-    int splits;                 // split-K factor (1 = none)
-    int ktiles_per_chunk;       // LDS staging chunk, in 32-wide k tiles
-    float *part;                // split-K partials [splits][B][N]
-    uint32_t *ctr;              // per strip-group arrival counters (zero between launches)
+    int ktiles_per_chunk;       // LDS staging chunk, in 32-wide k tiles (set by launch_gemv)
     // prologue
-    const float *x; const uint16_t *xb; const float *ss; int nss; const float *gain;
+    const float *x; const float *xf; const float *ss; int nss; const float *gain;
     const float *gain2; float eps; const int32_t *pairs; const uint16_t *embed; int H; int vocab;
     const uint64_t *tokkey;
     // epilogue
-    float *out; const float *bias; float *ss_out; uint16_t *act;
+    float *out; const float *bias; float *ss_out; float *act;
     uint16_t *q; uint16_t *kc; uint16_t *vc; const int32_t *pos;
     const float *rope_cos; const float *rope_sin;
     int n_q, n_kv, d, lmax_pad;   // KV geometry of this layer
@@ -56,8 +54,7 @@ struct AttnDecodeParams {
     const int32_t *pos;         // [B]: attend to keys 0..pos[b]
     int B, n_q, n_kv, d, lmax_pad, splits;
     float *part;                // [B][n_q][splits][d + 2]
-    uint32_t *ctr;              // [B][n_kv]
-    uint16_t *out;              // bf16 [B][n_q * d]
+    float *out;                 // fp32 [B][n_q * d]
 };
 void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s);
 
@@ -112,13 +109,15 @@ struct PrefillGeom {
 void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
                          const PrefillGeom &g, uint16_t *xin, hipStream_t s);
 void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M,
-                          uint16_t *xn, hipStream_t s);
+                          uint16_t *xn_hi, uint16_t *xn_lo, hipStream_t s);
+// Activations of the prefill GEMMs are a pair of tiled bf16 planes, hi and lo
+// (x ~= hi + lo); Xlo == NULL means the activation is exact in bf16.
 struct GemmParams {
-    const uint16_t *W; const uint16_t *X;   // tiled [N][K], tiled [M][K]
+    const uint16_t *W; const uint16_t *X; const uint16_t *Xlo;   // tiled [N][K], tiled [M][K] x2
     int N, K, M;
     int epi;                                // EPI_STORE (bias), EPI_RESID, EPI_SWIGLU, EPI_QKV
     PrefillGeom g;
-    float *out; const float *bias; uint16_t *act;
+    float *out; const float *bias; uint16_t *act_hi, *act_lo;
     uint16_t *q; uint16_t *kc; uint16_t *vc;
     const float *rope_cos; const float *rope_sin;
     int n_q, n_kv, d, lmax_pad; int64_t kv_bstride;
@@ -129,7 +128,7 @@ struct AttnPrefillParams {
     const uint16_t *kc, *vc; int64_t kv_bstride;
     PrefillGeom g;
     int n_q, n_kv, d, lmax_pad;
-    uint16_t *out;              // tiled [B*mpad][n_q*d]
+    uint16_t *out_hi, *out_lo;  // tiled [B*mpad][n_q*d], hi and lo planes
 };
 void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s);
 void launch_pick_last(const float *x, int H, const PrefillGeom &g, float *xdec, float *ss,

@@ -1,7 +1,8 @@
 // Compressed-prompt prefill: the pair step batched over a chunk of latent
 // positions of every sequence.  Activations that feed an MFMA GEMM are kept
-// in the 16x32 tiled bf16 layout so that both GEMM operands move as
-// contiguous 1 KB tiles from HBM to LDS to registers.
+// in the 16x32 tiled bf16 layout, as two planes hi and lo (x ~= hi + lo,
+// about 16 significant bits), so that both GEMM operands move as contiguous
+// 1 KB tiles from HBM to LDS to registers.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -42,7 +43,7 @@ void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, in
 
 // ---- RMSNorm of fp32 rows into the tiled bf16 layout (one wave per row) ----
 __global__ __launch_bounds__(256) void k_rmsnorm_tiled(const float *x, const float *gain, int H, float eps,
-                                                       int M, uint16_t *xn) {
+                                                       int M, uint16_t *xh, uint16_t *xl) {
     const int lane = threadIdx.x & 63;
     const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (m >= M) return;
@@ -57,30 +58,34 @@ __global__ __launch_bounds__(256) void k_rmsnorm_tiled(const float *x, const flo
     for (int k = lane * 8; k < H; k += 512) {
         const float4 x0 = *(const float4 *)(xr + k), x1 = *(const float4 *)(xr + k + 4);
         const float4 g0 = *(const float4 *)(gain + k), g1 = *(const float4 *)(gain + k + 4);
-        u32x4 w;
-        w[0] = pack_bf2(x0.x * sc * g0.x, x0.y * sc * g0.y);
-        w[1] = pack_bf2(x0.z * sc * g0.z, x0.w * sc * g0.w);
-        w[2] = pack_bf2(x1.x * sc * g1.x, x1.y * sc * g1.y);
-        w[3] = pack_bf2(x1.z * sc * g1.z, x1.w * sc * g1.w);
-        *(u32x4 *)(xn + tiled_index(m, k, H)) = w;
+        const float f[8] = {x0.x * sc * g0.x, x0.y * sc * g0.y, x0.z * sc * g0.z, x0.w * sc * g0.w,
+                            x1.x * sc * g1.x, x1.y * sc * g1.y, x1.z * sc * g1.z, x1.w * sc * g1.w};
+        u32x4 hi, lo;
+        split8(f, hi, lo);
+        const int64_t at = tiled_index(m, k, H);
+        *(u32x4 *)(xh + at) = hi;
+        *(u32x4 *)(xl + at) = lo;
     }
 }
 
-void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M, uint16_t *xn,
-                          hipStream_t s) {
-    hipLaunchKernelGGL(k_rmsnorm_tiled, dim3((M + 3) / 4), dim3(256), 0, s, x, gain, H, eps, M, xn);
+void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M, uint16_t *xh,
+                          uint16_t *xl, hipStream_t s) {
+    hipLaunchKernelGGL(k_rmsnorm_tiled, dim3((M + 3) / 4), dim3(256), 0, s, x, gain, H, eps, M, xh, xl);
 }
 
 // ---- MFMA GEMM  C^T[N][M] = W[N][K] X[M][K]^T, both operands tiled ---------
-// Workgroup tile 128 (rows of W) x 128 (tokens) x 64 (k), four waves in a
-// 2x2 arrangement of 64x64, LDS double-buffered.
-constexpr int kGBN = 128, kGBM = 128, kGKT = 2;   // kGKT k-tiles (32 each) per stage
+// Workgroup tile 128 (rows of W) x 128 (tokens), one 32-wide k tile per
+// stage, four waves in a 2x2 arrangement of 64x64, LDS double-buffered.  With
+// a lo plane every W fragment meets the X hi and X lo fragments (two MFMAs).
+constexpr int kGBN = 128, kGBM = 128;
 constexpr int kGStripsN = kGBN / 16, kGStripsM = kGBM / 16;
-constexpr int kGStageElems = (kGStripsN + kGStripsM) * kGKT * 512;
 
-template <int EPI>
+template <int EPI, bool HASLO>
 __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
-    __shared__ __align__(16) uint16_t lds[2][kGStageElems];
+    constexpr int NOPS = HASLO ? 3 : 2;                       // W, X hi, (X lo)
+    constexpr int STAGE = (kGStripsN + (NOPS - 1) * kGStripsM) * 512;
+    constexpr int NCH = STAGE / 8 / 256;                      // 16 B chunks per thread
+    __shared__ __align__(16) uint16_t lds[2][STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = lane & 15, g = lane >> 4;
     const int wn = wave >> 1, wm = wave & 1;
@@ -89,31 +94,24 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
     const int KT = p.K >> 5;
     const int NS = p.N >> 4, MS = p.M >> 4;   // strips
 
-    // each thread moves 8 x 16 B per stage: 4 for W, 4 for X
-    u32x4 reg[8];
+    u32x4 reg[NCH];
     auto gload = [&](int kt) {
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-            const int c = tid + r * 256;                 // chunk 0..2047
-            const bool isw = c < 1024;
-            const int cc = isw ? c : c - 1024;
-            const int st = cc >> 7, within = cc & 127;   // strip, 16 B unit in its 2 tiles
-            const int kk = kt + (within >> 6);
-            const int strip = (isw ? bn * kGStripsN : bm * kGStripsM) + st;
-            const int nstr = isw ? NS : MS;
-            const uint16_t *src = isw ? p.W : p.X;
+        for (int r = 0; r < NCH; ++r) {
+            const int c = tid + r * 256;                 // 16 B chunk of the stage
+            const int op = c >> 9;                       // 512 chunks per operand (8 strips x 1 KB)
+            const int st = (c >> 6) & 7, within = c & 63;
+            const int strip = (op == 0 ? bn * kGStripsN : bm * kGStripsM) + st;
+            const int nstr = op == 0 ? NS : MS;
+            const uint16_t *src = op == 0 ? p.W : (op == 1 ? p.X : p.Xlo);
             u32x4 v = u32x4{0u, 0u, 0u, 0u};
-            if (strip < nstr && kk < KT)
-                v = *(const u32x4 *)(src + ((int64_t)strip * KT + kk) * 512 + (within & 63) * 8);
+            if (strip < nstr) v = *(const u32x4 *)(src + ((int64_t)strip * KT + kt) * 512 + within * 8);
             reg[r] = v;
         }
     };
     auto sstore = [&](int buf) {
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-            const int c = tid + r * 256;
-            *(u32x4 *)(&lds[buf][c * 8]) = reg[r];
-        }
+        for (int r = 0; r < NCH; ++r) *(u32x4 *)(&lds[buf][(tid + r * 256) * 8]) = reg[r];
     };
 
     f32x4 acc[4][4];
@@ -126,23 +124,24 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
     sstore(0);
     __syncthreads();
     int buf = 0;
-    for (int kt = 0; kt < KT; kt += kGKT) {
-        const bool more = kt + kGKT < KT;
-        if (more) gload(kt + kGKT);
+    for (int kt = 0; kt < KT; ++kt) {
+        const bool more = kt + 1 < KT;
+        if (more) gload(kt + 1);
+        u32x4 af[4], bf[4], bl[4];
 #pragma unroll
-        for (int kk = 0; kk < kGKT; ++kk) {
-            u32x4 af[4], bf[4];
+        for (int si = 0; si < 4; ++si) af[si] = *(const u32x4 *)(&lds[buf][(4 * wn + si) * 512 + lane * 8]);
 #pragma unroll
-            for (int si = 0; si < 4; ++si)
-                af[si] = *(const u32x4 *)(&lds[buf][((4 * wn + si) * kGKT + kk) * 512 + lane * 8]);
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-                bf[mi] = *(const u32x4 *)(&lds[buf][(kGStripsN * kGKT + (4 * wm + mi) * kGKT + kk) * 512 + lane * 8]);
-#pragma unroll
-            for (int si = 0; si < 4; ++si)
-#pragma unroll
-                for (int mi = 0; mi < 4; ++mi) acc[si][mi] = mfma16(af[si], bf[mi], acc[si][mi]);
+        for (int mi = 0; mi < 4; ++mi) {
+            bf[mi] = *(const u32x4 *)(&lds[buf][(kGStripsN + 4 * wm + mi) * 512 + lane * 8]);
+            if (HASLO) bl[mi] = *(const u32x4 *)(&lds[buf][(kGStripsN + kGStripsM + 4 * wm + mi) * 512 + lane * 8]);
         }
+#pragma unroll
+        for (int si = 0; si < 4; ++si)
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi) {
+                acc[si][mi] = mfma16(af[si], bf[mi], acc[si][mi]);
+                if (HASLO) acc[si][mi] = mfma16(af[si], bl[mi], acc[si][mi]);
+            }
         if (more) {
             sstore(buf ^ 1);
             __syncthreads();
@@ -177,10 +176,12 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
                 *o = *o + val;
             } else if (EPI == EPI_SWIGLU) {
                 if (g < 2) {
-                    u32x2 w;
-                    w[0] = pack_bf2(silu_p(val[0]) * other[0], silu_p(val[1]) * other[1]);
-                    w[1] = pack_bf2(silu_p(val[2]) * other[2], silu_p(val[3]) * other[3]);
-                    *(u32x2 *)(p.act + tiled_index(m, strip * 8 + 4 * g, p.N >> 1)) = w;
+                    uint32_t h[4], l[4];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) split_bf(silu_p(val[v]) * other[v], h[v], l[v]);
+                    const int64_t at = tiled_index(m, strip * 8 + 4 * g, p.N >> 1);
+                    *(u32x2 *)(p.act_hi + at) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+                    *(u32x2 *)(p.act_lo + at) = u32x2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
                 }
             } else if (EPI == EPI_QKV) {
                 const int pos = p.g.c0 + i;
@@ -217,23 +218,28 @@ __global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
 
 void launch_gemm(const GemmParams &p, hipStream_t s) {
     const int grid = ((p.N + kGBN - 1) / kGBN) * ((p.M + kGBM - 1) / kGBM);
+    if (!p.Xlo) {   // the gathered embedding pairs are exact in bf16
+        hipLaunchKernelGGL((k_gemm<EPI_STORE, false>), dim3(grid), dim3(256), 0, s, p);
+        return;
+    }
     switch (p.epi) {
-        case EPI_STORE: hipLaunchKernelGGL(k_gemm<EPI_STORE>, dim3(grid), dim3(256), 0, s, p); break;
-        case EPI_RESID: hipLaunchKernelGGL(k_gemm<EPI_RESID>, dim3(grid), dim3(256), 0, s, p); break;
-        case EPI_SWIGLU: hipLaunchKernelGGL(k_gemm<EPI_SWIGLU>, dim3(grid), dim3(256), 0, s, p); break;
-        default: hipLaunchKernelGGL(k_gemm<EPI_QKV>, dim3(grid), dim3(256), 0, s, p); break;
+        case EPI_STORE: hipLaunchKernelGGL((k_gemm<EPI_STORE, true>), dim3(grid), dim3(256), 0, s, p); break;
+        case EPI_RESID: hipLaunchKernelGGL((k_gemm<EPI_RESID, true>), dim3(grid), dim3(256), 0, s, p); break;
+        case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm<EPI_SWIGLU, true>), dim3(grid), dim3(256), 0, s, p); break;
+        default: hipLaunchKernelGGL((k_gemm<EPI_QKV, true>), dim3(grid), dim3(256), 0, s, p); break;
     }
 }
 
 // ---- causal grouped-query flash attention for a chunk of queries ----------
-// One workgroup per (sequence, KV group, 32-query block); wave w computes head
-// kvh*qpg + w for all 32 queries (two 16-column MFMA tiles).  Keys and values
-// of 64 positions at a time are staged in LDS and shared by the group's heads.
+// One workgroup per (sequence, KV group, group of up to four query heads,
+// 32-query block); wave w computes one head for all 32 queries (two 16-column
+// MFMA tiles).  Keys and values of 64 positions at a time are staged in LDS
+// and shared by the workgroup's heads.
 constexpr int kAQ = 32;         // queries per workgroup
 constexpr int kAK = 64;         // keys per LDS stage
 
 template <int D>
-__global__ __launch_bounds__(1024) void k_attn_prefill(AttnPrefillParams p) {
+__global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillParams p) {
     constexpr int NC = D / 32, NT = D / 16;
     constexpr int KS = D + 8;           // padded K row (elements)
     constexpr int VS = 40;              // padded V tile row (elements)
@@ -244,12 +250,16 @@ __global__ __launch_bounds__(1024) void k_attn_prefill(AttnPrefillParams p) {
     const int nthr = blockDim.x;
     const int j = lane & 15, g = lane >> 4;
     const int qpg = p.n_q / p.n_kv;
+    const int nhg = (qpg + 3) / 4;               // head groups per KV group
     const int nqb = (p.g.clen + kAQ - 1) / kAQ;
     // heavy (late) query blocks first
     const int qblk = nqb - 1 - (int)(blockIdx.x % nqb);
-    const int bk = blockIdx.x / nqb;
+    const int rest = blockIdx.x / nqb;
+    const int hg = rest % nhg, bk = rest / nhg;
     const int b = bk / p.n_kv, kvh = bk - b * p.n_kv;
-    const int head = kvh * qpg + wave;
+    const int hig = hg * 4 + wave;               // head index inside the KV group
+    const bool active = hig < qpg;
+    const int head = kvh * qpg + (active ? hig : 0);
     const int q0 = qblk * kAQ;                 // chunk-local first query
     const int qpos0 = p.g.c0 + q0;             // absolute position of the first query
     const float scale = 1.4426950408889634f / sqrtf((float)D);
@@ -284,7 +294,7 @@ __global__ __launch_bounds__(1024) void k_attn_prefill(AttnPrefillParams p) {
             *(u32x4 *)(&vs[row * VS + e]) = *(const u32x4 *)(vbase + (int64_t)(kb0 >> 5) * D * 32 + (int64_t)row * 32 + e);
         }
         __syncthreads();
-        if (wave >= qpg) continue;
+        if (!active) continue;
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int kb = kb0 + 32 * half;
@@ -344,7 +354,7 @@ __global__ __launch_bounds__(1024) void k_attn_prefill(AttnPrefillParams p) {
             }
         }
     }
-    if (wave >= qpg) return;
+    if (!active) return;
     const int qd = p.n_q * D;
 #pragma unroll
     for (int ct = 0; ct < 2; ++ct) {
@@ -354,19 +364,22 @@ __global__ __launch_bounds__(1024) void k_attn_prefill(AttnPrefillParams p) {
         const int64_t m = (int64_t)b * p.g.mpad + i;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            u32x2 w;
-            w[0] = pack_bf2(o[ct][t][0] * inv, o[ct][t][1] * inv);
-            w[1] = pack_bf2(o[ct][t][2] * inv, o[ct][t][3] * inv);
-            *(u32x2 *)(p.out + tiled_index(m, head * D + 16 * t + 4 * g, qd)) = w;
+            uint32_t h[4], l[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) split_bf(o[ct][t][v] * inv, h[v], l[v]);
+            const int64_t at = tiled_index(m, head * D + 16 * t + 4 * g, qd);
+            *(u32x2 *)(p.out_hi + at) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+            *(u32x2 *)(p.out_lo + at) = u32x2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
         }
     }
 }
 
 void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s) {
     const int qpg = p.n_q / p.n_kv;
+    const int nhg = (qpg + 3) / 4;
     const int nqb = (p.g.clen + kAQ - 1) / kAQ;
-    const int grid = p.g.B * p.n_kv * nqb;
-    const int threads = 64 * qpg;
+    const int grid = p.g.B * p.n_kv * nhg * nqb;
+    const int threads = 64 * (qpg < 4 ? qpg : 4);
     if (p.d == 128) hipLaunchKernelGGL(k_attn_prefill<128>, dim3(grid), dim3(threads), 0, s, p);
     else hipLaunchKernelGGL(k_attn_prefill<64>, dim3(grid), dim3(threads), 0, s, p);
 }

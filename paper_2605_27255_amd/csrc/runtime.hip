@@ -55,14 +55,14 @@ struct pipo_ctx {
     float *rope_cos, *rope_sin;
 
     // decode state and activations
-    float *x, *ss_x, *hd, *ss_hd, *logits_b, *logits_d, *gpart, *apart;
-    uint16_t *qbuf, *attn_out, *act;
+    float *x, *ss_x, *hd, *ss_hd, *logits_b, *logits_d, *apart;
+    uint16_t *qbuf;
+    float *attn_out, *act;
     uint64_t *best_b, *best_d, *seeds;
     int32_t *pairs, *pos, *step;
     pipo_pair *out;
-    uint32_t *gctr, *actr;
     // prefill activations
-    uint16_t *p_xin, *p_xn, *p_q, *p_o, *p_act;
+    uint16_t *p_xin, *p_xn, *p_xn_lo, *p_q, *p_o, *p_o_lo, *p_act, *p_act_lo;
     float *p_x;
 
     uint64_t *h_seeds = nullptr;     // pinned staging for sampler seeds
@@ -76,7 +76,39 @@ struct pipo_ctx {
     hipGraphExec_t graph = nullptr;
     bool graph_dirty = true;
     bool use_graph = true;
+
+    // profiling: events around every launch, summed per kernel class
+    bool prof_on = false;
+    std::vector<hipEvent_t> ev_pool;
+    size_t ev_next = 0;
+    std::vector<std::pair<int, size_t>> pending;   // (class, index of the start event)
+    double prof_ms[PIPO_K_CLASSES] = {};
+    int64_t prof_n[PIPO_K_CLASSES] = {};
 };
+
+// Launch bracket: record an event before and after a launch when profiling.
+struct ProfScope {
+    pipo_ctx *c; hipStream_t s; int cls; size_t i0 = 0;
+    ProfScope(pipo_ctx *c_, hipStream_t s_, int cls_) : c(c_), s(s_), cls(cls_) {
+        if (!c->prof_on) return;
+        while (c->ev_pool.size() < c->ev_next + 2) {
+            hipEvent_t e;
+            if (hipEventCreate(&e) != hipSuccess) { c->prof_on = false; return; }
+            c->ev_pool.push_back(e);
+        }
+        i0 = c->ev_next;
+        c->ev_next += 2;
+        hipEventRecord(c->ev_pool[i0], s);
+    }
+    ~ProfScope() {
+        if (!c->prof_on) return;
+        hipEventRecord(c->ev_pool[i0 + 1], s);
+        c->pending.push_back({cls, i0});
+    }
+};
+#define PROF_CAT2(a, b) a##b
+#define PROF_CAT(a, b) PROF_CAT2(a, b)
+#define PROF(cls) ProfScope PROF_CAT(prof_scope_, __LINE__)(c, s, cls)
 
 static int fail(pipo_ctx *c, int code, const char *fmt, ...) {
     char buf[512];
@@ -175,9 +207,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
     // ---- KV cache, RoPE table, activations ------------------------------
     Arena a;
     const int64_t mcap = (int64_t)B * round_up(c->chunk, 32);
-    const int S_att = 32, S_gemv = 16;
-    const int64_t nmax = std::max(std::max((int64_t)c->nqkv, (int64_t)2 * F), (int64_t)H);
-    const int64_t ngroups = gemv_num_groups((int)std::max(nmax, (int64_t)V));
+    const int S_att = 32;
     for (int pass = 0; pass < 2; ++pass) {
         a.used = 0;
         c->kc = a.take<uint16_t>((int64_t)c->L * B * c->kv_bstride);
@@ -191,8 +221,8 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->logits_b = a.take<float>((int64_t)B * V);
         c->logits_d = a.take<float>((int64_t)B * V);
         c->qbuf = a.take<uint16_t>((int64_t)B * c->qdim);
-        c->attn_out = a.take<uint16_t>((int64_t)B * c->qdim);
-        c->act = a.take<uint16_t>((int64_t)B * F);
+        c->attn_out = a.take<float>((int64_t)B * c->qdim);
+        c->act = a.take<float>((int64_t)B * F);
         c->best_b = a.take<uint64_t>(B);
         c->best_d = a.take<uint64_t>(B);
         c->seeds = a.take<uint64_t>(B);
@@ -200,16 +230,16 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->pos = a.take<int32_t>(B);
         c->step = a.take<int32_t>(B);
         c->out = a.take<pipo_pair>(B);
-        c->gpart = a.take<float>((int64_t)S_gemv * B * nmax);
-        c->gctr = a.take<uint32_t>(ngroups);
         c->apart = a.take<float>((int64_t)B * c->nq * S_att * (c->d + 2));
-        c->actr = a.take<uint32_t>((int64_t)B * c->nkv);
         c->p_xin = a.take<uint16_t>(mcap * 2 * H);
         c->p_x = a.take<float>(mcap * H);
         c->p_xn = a.take<uint16_t>(mcap * H);
+        c->p_xn_lo = a.take<uint16_t>(mcap * H);
         c->p_q = a.take<uint16_t>(mcap * c->qdim);
         c->p_o = a.take<uint16_t>(mcap * c->qdim);
+        c->p_o_lo = a.take<uint16_t>(mcap * c->qdim);
         c->p_act = a.take<uint16_t>(mcap * F);
+        c->p_act_lo = a.take<uint16_t>(mcap * F);
         if (pass == 0) {
             if (hipMalloc(&c->amem, a.used) != hipSuccess) {
                 hipFree(c->wmem);
@@ -225,7 +255,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         pipo_free(cc);
         return code;
     };
-    // Zero everything once (counters, argmax keys, the KV cache: attention
+    // Zero everything once (argmax keys, the KV cache: attention
     // reads whole 32-key tiles and relies on finite values past the length).
     if (hipMemsetAsync(c->amem, 0, a.used, s) != hipSuccess) return cleanup_fail(fail(c, PIPO_EHIP, "memset failed"));
 
@@ -276,33 +306,35 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     const int H = c->H;
     const bool greedy = c->temperature <= 0.f;
     GemvParams p{};
-    p.B = B; p.eps = c->cfg.rms_eps; p.H = H; p.part = c->gpart; p.ctr = c->gctr;
+    p.B = B; p.eps = c->cfg.rms_eps; p.H = H;
     // LM head #1 on RMSNorm(h_b; g_final)
     p.W = c->embed; p.N = c->V; p.K = H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
     p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
-    launch_gemv(p, PRO_NORM, EPI_LOGITS, s);
+    { PROF(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         SampleParams sp{c->logits_b, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 0, c->best_b};
+        PROF(PIPO_K_SAMPLE);
         launch_sample(sp, s);
     }
     // MTP head: W_fc [RMSNorm(h_b; g_mh); RMSNorm(E[b]; g_me)]
     GemvParams m{};
-    m.B = B; m.eps = c->cfg.rms_eps; m.H = H; m.vocab = c->V; m.part = c->gpart; m.ctr = c->gctr;
+    m.B = B; m.eps = c->cfg.rms_eps; m.H = H; m.vocab = c->V;
     m.W = c->w_fc; m.N = H; m.K = 2 * H;
     m.x = c->x; m.ss = c->ss_x; m.nss = nss; m.gain = c->g_mtp_h; m.gain2 = c->g_mtp_e;
     m.embed = c->embed; m.tokkey = c->best_b;
     m.out = c->hd; m.ss_out = c->ss_hd;
-    launch_gemv(m, PRO_MTP, EPI_STORE, s);
+    { PROF(PIPO_K_GEMV_SMALL); launch_gemv(m, PRO_MTP, EPI_STORE, s); }
     // LM head #2 on RMSNorm(h_d; g_mo)
     GemvParams q{};
-    q.B = B; q.eps = c->cfg.rms_eps; q.H = H; q.part = c->gpart; q.ctr = c->gctr;
+    q.B = B; q.eps = c->cfg.rms_eps; q.H = H;
     q.W = c->embed; q.N = c->V; q.K = H;
     q.x = c->hd; q.ss = c->ss_hd; q.nss = H / 16; q.gain = c->g_mtp_o;
     q.out = c->logits_d; q.best = greedy ? c->best_d : nullptr;
-    launch_gemv(q, PRO_NORM, EPI_LOGITS, s);
+    { PROF(PIPO_K_GEMV_LMHEAD); launch_gemv(q, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         SampleParams sp{c->logits_d, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 1, c->best_d};
+        PROF(PIPO_K_SAMPLE);
         launch_sample(sp, s);
     }
     GateParams gp{};
@@ -310,6 +342,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     gp.w_conf = c->w_conf; gp.g_conf = c->g_conf; gp.H = H; gp.eps = c->cfg.rms_eps; gp.tau = c->tau;
     gp.best_b = c->best_b; gp.best_d = c->best_d; gp.pad_id = c->pad_id; gp.out = c->out;
     gp.pairs = c->pairs; gp.pos = c->pos; gp.step = c->step; gp.advance = advance; gp.B = B;
+    PROF(PIPO_K_GATE);
     launch_gate(gp, s);
 }
 
@@ -322,11 +355,12 @@ static int attn_splits(const pipo_ctx *c, int B) {
 static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
     GemvParams base{};
-    base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V; base.part = c->gpart; base.ctr = c->gctr;
+    base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V;
     {   // pair-in compressor
         GemvParams p = base;
         p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;
         p.out = c->x; p.bias = c->b_comp; p.ss_out = c->ss_x;
+        PROF(PIPO_K_GEMV_SMALL);
         launch_gemv(p, PRO_PAIR, EPI_STORE, s);
     }
     for (int l = 0; l < c->L; ++l) {
@@ -338,26 +372,26 @@ static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
         p.x = c->x; p.ss = c->ss_x; p.nss = H / 16; p.gain = lw.g_attn;
         p.q = c->qbuf; p.kc = kc; p.vc = vc; p.pos = c->pos; p.rope_cos = c->rope_cos; p.rope_sin = c->rope_sin;
         p.n_q = c->nq; p.n_kv = c->nkv; p.d = c->d; p.lmax_pad = c->lmax_pad; p.kv_bstride = c->kv_bstride;
-        launch_gemv(p, PRO_NORM, EPI_QKV, s);
+        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_QKV, s); }
 
         AttnDecodeParams ap{};
         ap.q = c->qbuf; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.pos = c->pos;
         ap.B = B; ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad;
-        ap.splits = attn_splits(c, B); ap.part = c->apart; ap.ctr = c->actr; ap.out = c->attn_out;
-        launch_attn_decode(ap, s);
+        ap.splits = attn_splits(c, B); ap.part = c->apart; ap.out = c->attn_out;
+        { PROF(PIPO_K_ATTN_DECODE); launch_attn_decode(ap, s); }
 
         p = base;
-        p.W = lw.wo; p.N = H; p.K = c->qdim; p.xb = c->attn_out; p.out = c->x; p.ss_out = c->ss_x;
-        launch_gemv(p, PRO_BF16, EPI_RESID, s);
+        p.W = lw.wo; p.N = H; p.K = c->qdim; p.xf = c->attn_out; p.out = c->x; p.ss_out = c->ss_x;
+        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
 
         p = base;
         p.W = lw.wgu; p.N = 2 * c->F; p.K = H; p.x = c->x; p.ss = c->ss_x; p.nss = H / 16; p.gain = lw.g_ffn;
         p.act = c->act;
-        launch_gemv(p, PRO_NORM, EPI_SWIGLU, s);
+        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_SWIGLU, s); }
 
         p = base;
-        p.W = lw.wdown; p.N = H; p.K = c->F; p.xb = c->act; p.out = c->x; p.ss_out = c->ss_x;
-        launch_gemv(p, PRO_BF16, EPI_RESID, s);
+        p.W = lw.wdown; p.N = H; p.K = c->F; p.xf = c->act; p.out = c->x; p.ss_out = c->ss_x;
+        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
     }
     enqueue_heads(c, B, H / 16, 1, s);
 }
@@ -415,39 +449,39 @@ extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
         g.B = batch; g.c0 = c0; g.clen = std::min(c->chunk, latents - c0);
         g.mpad = (int)round_up(g.clen, 32); g.n_tok = n;
         const int M = batch * g.mpad;
-        launch_gather_pairs(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_xin, s);
+        { PROF(PIPO_K_PREFILL_MISC); launch_gather_pairs(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_xin, s); }
         GemmParams gp{};
         gp.g = g; gp.M = M;
         gp.n_q = c->nq; gp.n_kv = c->nkv; gp.d = c->d; gp.lmax_pad = c->lmax_pad; gp.kv_bstride = c->kv_bstride;
         gp.rope_cos = c->rope_cos; gp.rope_sin = c->rope_sin;
         GemmParams p = gp;
         p.W = c->w_comp; p.X = c->p_xin; p.N = H; p.K = 2 * H; p.epi = EPI_STORE; p.out = c->p_x; p.bias = c->b_comp;
-        launch_gemm(p, s);
+        { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
         for (int l = 0; l < c->L; ++l) {
             const LayerW &lw = c->layers[l];
             uint16_t *kc = c->kc + (int64_t)l * c->Bmax * c->kv_bstride;
             uint16_t *vc = c->vc + (int64_t)l * c->Bmax * c->kv_bstride;
-            launch_rmsnorm_tiled(c->p_x, lw.g_attn, H, c->cfg.rms_eps, M, c->p_xn, s);
+            { PROF(PIPO_K_PREFILL_MISC); launch_rmsnorm_tiled(c->p_x, lw.g_attn, H, c->cfg.rms_eps, M, c->p_xn, c->p_xn_lo, s); }
             p = gp;
-            p.W = lw.wqkv; p.X = c->p_xn; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q; p.kc = kc; p.vc = vc;
-            launch_gemm(p, s);
+            p.W = lw.wqkv; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q; p.kc = kc; p.vc = vc;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
             AttnPrefillParams ap{};
             ap.q = c->p_q; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.g = g;
-            ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad; ap.out = c->p_o;
-            launch_attn_prefill(ap, s);
+            ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad; ap.out_hi = c->p_o; ap.out_lo = c->p_o_lo;
+            { PROF(PIPO_K_PREFILL_ATTN); launch_attn_prefill(ap, s); }
             p = gp;
-            p.W = lw.wo; p.X = c->p_o; p.N = H; p.K = c->qdim; p.epi = EPI_RESID; p.out = c->p_x;
-            launch_gemm(p, s);
-            launch_rmsnorm_tiled(c->p_x, lw.g_ffn, H, c->cfg.rms_eps, M, c->p_xn, s);
+            p.W = lw.wo; p.X = c->p_o; p.Xlo = c->p_o_lo; p.N = H; p.K = c->qdim; p.epi = EPI_RESID; p.out = c->p_x;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+            { PROF(PIPO_K_PREFILL_MISC); launch_rmsnorm_tiled(c->p_x, lw.g_ffn, H, c->cfg.rms_eps, M, c->p_xn, c->p_xn_lo, s); }
             p = gp;
-            p.W = lw.wgu; p.X = c->p_xn; p.N = 2 * F; p.K = H; p.epi = EPI_SWIGLU; p.act = c->p_act;
-            launch_gemm(p, s);
+            p.W = lw.wgu; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = 2 * F; p.K = H; p.epi = EPI_SWIGLU; p.act_hi = c->p_act; p.act_lo = c->p_act_lo;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
             p = gp;
-            p.W = lw.wdown; p.X = c->p_act; p.N = H; p.K = F; p.epi = EPI_RESID; p.out = c->p_x;
-            launch_gemm(p, s);
+            p.W = lw.wdown; p.X = c->p_act; p.Xlo = c->p_act_lo; p.N = H; p.K = F; p.epi = EPI_RESID; p.out = c->p_x;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
         }
     }
-    launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, latents, s);
+    { PROF(PIPO_K_PREFILL_MISC); launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, latents, s); }
     enqueue_heads(c, batch, 1, 0, s);
     HIP_TRY(c, hipGetLastError());
     rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
@@ -468,7 +502,7 @@ extern "C" int pipo_decode_step(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pai
     HIP_TRY(c, hipGetLastError());
     if (d_in_pairs)
         HIP_TRY(c, hipMemcpyAsync(c->pairs, d_in_pairs, sizeof(int32_t) * 2 * c->batch, hipMemcpyDeviceToDevice, s));
-    if (c->use_graph) {
+    if (c->use_graph && !c->prof_on) {
         if (c->graph_dirty || !c->graph) {
             if (c->graph) {
                 hipGraphExecDestroy(c->graph);
@@ -494,8 +528,36 @@ extern "C" int pipo_decode_step(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pai
     return PIPO_OK;
 }
 
+extern "C" int pipo_profile_enable(pipo_ctx *c, int on) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    c->prof_on = on != 0;
+    c->pending.clear();
+    c->ev_next = 0;
+    for (int k = 0; k < PIPO_K_CLASSES; ++k) { c->prof_ms[k] = 0.0; c->prof_n[k] = 0; }
+    return PIPO_OK;
+}
+
+extern "C" int pipo_profile_read(pipo_ctx *c, int kclass, double *total_ms, int64_t *launches) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (kclass < 0 || kclass >= PIPO_K_CLASSES || !total_ms || !launches)
+        return fail(c, PIPO_EINVAL, "bad profiling arguments");
+    for (auto &pr : c->pending) {
+        HIP_TRY(c, hipEventSynchronize(c->ev_pool[pr.second + 1]));
+        float ms = 0.f;
+        HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_pool[pr.second], c->ev_pool[pr.second + 1]));
+        c->prof_ms[pr.first] += ms;
+        c->prof_n[pr.first] += 1;
+    }
+    c->pending.clear();
+    c->ev_next = 0;
+    *total_ms = c->prof_ms[kclass];
+    *launches = c->prof_n[kclass];
+    return PIPO_OK;
+}
+
 extern "C" int pipo_free(pipo_ctx *c) {
     if (!c) return PIPO_OK;
+    for (hipEvent_t e : c->ev_pool) hipEventDestroy(e);
     if (c->graph) hipGraphExecDestroy(c->graph);
     if (c->cap_stream) hipStreamDestroy(c->cap_stream);
     if (c->seeds_done) hipEventDestroy(c->seeds_done);

@@ -15,7 +15,10 @@ LIB_PATH = os.path.join(PKG_DIR, "libpipo.so")
 
 PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -1, -2, -3, -4, -5
 EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_free",
-            "pipo_last_error", "pipo_read_weight")
+            "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read")
+#: kernel classes of the profiling counters (PIPO_K_* in include/pipo.h)
+KERNEL_CLASSES = ("gemv_layer", "gemv_lmhead", "gemv_small", "attn_decode", "sample", "gate",
+                  "prefill_gemm", "prefill_attn", "prefill_misc")
 
 
 class PipoError(RuntimeError):
@@ -61,7 +64,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_last_error.argtypes = [vp]
     lib.pipo_last_error.restype = ctypes.c_char_p
     lib.pipo_read_weight.argtypes = [vp, ctypes.c_char_p, i64, i64, vp]
-    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_free", "pipo_read_weight"):
+    lib.pipo_profile_enable.argtypes = [vp, ctypes.c_int]
+    lib.pipo_profile_read.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
+    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_free", "pipo_read_weight",
+               "pipo_profile_enable", "pipo_profile_read"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -145,6 +151,19 @@ class PipoModel:
         self._check(self.lib.pipo_read_weight(self.ctx, name.encode(), start, count,
                                               buf.ctypes.data_as(ctypes.c_void_p)))
         return buf
+
+    def profile(self, on: bool):
+        """Per-kernel-class HIP-event timing (eager launches while on)."""
+        self._check(self.lib.pipo_profile_enable(self.ctx, 1 if on else 0))
+
+    def profile_read(self) -> dict:
+        """{class: (total_ms, launches)} since profiling was turned on."""
+        res = {}
+        for k, name in enumerate(KERNEL_CLASSES):
+            ms, n = ctypes.c_double(), ctypes.c_int64()
+            self._check(self.lib.pipo_profile_read(self.ctx, k, ctypes.byref(ms), ctypes.byref(n)))
+            res[name] = (ms.value, n.value)
+        return res
 
     def close(self):
         if self.ctx:

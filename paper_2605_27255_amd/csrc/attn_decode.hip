@@ -46,14 +46,27 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
 
-    for (int kb = k0; kb < k1; kb += 32) {
+    // K and V fragments of one 32-key block: K rows (16 keys per tile, 32 dims
+    // per MFMA step) and the 32-key V tile, 16 dims per output tile.
+    u32x4 kf[2][2][NC], vf[2][NT];
+    auto load_block = [&](int bsel, int kb) {
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau) {
+            const uint16_t *kr = kbase + (int64_t)(kb + 16 * tau + j) * D + 8 * g;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) kf[bsel][tau][c] = *(const u32x4 *)(kr + 32 * c);
+        }
+        const uint16_t *vt = vbase + (int64_t)(kb >> 5) * D * 32 + j * 32 + 8 * g;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) vf[bsel][t] = *(const u32x4 *)(vt + t * 16 * 32);
+    };
+    auto block = [&](int bsel, int kb) {
         f32x4 st[2];
 #pragma unroll
         for (int tau = 0; tau < 2; ++tau) {
             st[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const uint16_t *kr = kbase + (int64_t)(kb + 16 * tau + j) * D + 8 * g;
 #pragma unroll
-            for (int c = 0; c < NC; ++c) st[tau] = mfma16(*(const u32x4 *)(kr + 32 * c), qb[c], st[tau]);
+            for (int c = 0; c < NC; ++c) st[tau] = mfma16(kf[bsel][tau][c], qb[c], st[tau]);
         }
         float mx = -INFINITY;
 #pragma unroll
@@ -84,12 +97,21 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
         pt[1] = pack_bf2(st[0][2], st[0][3]);
         pt[2] = pack_bf2(st[1][0], st[1][1]);
         pt[3] = pack_bf2(st[1][2], st[1][3]);
-        const uint16_t *vt = vbase + (int64_t)(kb >> 5) * D * 32 + j * 32 + 8 * g;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             o[t] *= alpha;
-            o[t] = mfma16(*(const u32x4 *)(vt + t * 16 * 32), pt, o[t]);
+            o[t] = mfma16(vf[bsel][t], pt, o[t]);
         }
+    };
+    // ping-pong over 32-key blocks: the next block's loads are in flight
+    // while the current one is computed
+    if (k0 < k1) load_block(0, k0);
+    for (int kb = k0; kb < k1; kb += 64) {
+        if (kb + 32 < k1) load_block(1, kb + 32);
+        block(0, kb);
+        if (kb + 32 >= k1) break;
+        if (kb + 64 < k1) load_block(0, kb + 64);
+        block(1, kb + 32);
     }
 
     // partial (o, m, l) of this split for each head of the group

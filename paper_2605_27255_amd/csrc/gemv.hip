@@ -1,18 +1,23 @@
 // Weight-streaming skinny GEMM of the decode step (batch 1..32).
 //
 // Y^T[N][B] = W[N][K] X^T with W in 16x32 bf16 tiles.  A workgroup of eight
-// waves owns SG 16-row strips of W; the waves split the strips' K range
-// (wave w takes k-tiles w, w+8, w+16, ...) and stream each tile with one
-// contiguous 1 KB load as the MFMA A operand, two batches of loads in flight.
-// The activations X (B <= 32 rows) are staged in LDS as the B operand by a
-// fused prologue (RMSNorm gain, pair gather, MTP concat), as a pair of bf16
-// planes hi + lo (about 16 significant bits; two MFMAs per weight tile, the
-// matrix cores have the headroom); the RMSNorm scale is a per-row scalar, so
-// it is applied to the accumulators in the epilogue and staging never waits
-// for it.  The eight partial sums are reduced through
-// LDS in wave order (deterministic, no atomics, no cross-workgroup traffic)
-// and a fused epilogue writes the result (bias, residual add, SwiGLU, RoPE +
-// KV append, logits + argmax).
+// waves owns 8/KS 16-row strips of W, KS waves per strip splitting its K range
+// (wave k of a strip takes k-tiles k, k+KS, k+2KS, ...); every wave streams
+// its tiles with one contiguous 1 KB load each as the MFMA A operand.  KS is
+// chosen per matrix: tall matrices (the LM head) give every wave a whole
+// strip, short ones split K to keep enough loads in flight.
+//
+// Memory operations retire in issue order, so a wave first loads what the
+// prologue and epilogue need (the activation sources of the first LDS chunk,
+// RMSNorm partial sums, the residual rows), then issues two batches of weight
+// tiles, and only then waits: staging X in LDS never waits for weights, and
+// the weight stream never drains behind the prologue.  X is staged as a pair
+// of bf16 planes hi + lo (about 16 significant bits; two MFMAs per weight
+// tile, the matrix cores have the headroom).  The RMSNorm scale is a per-row
+// scalar applied to the accumulators in the epilogue.  The KS partial sums of
+// a strip are reduced through LDS in wave order (deterministic, no atomics,
+// no cross-workgroup traffic) and a fused epilogue writes the result (bias,
+// residual add, SwiGLU, RoPE + KV append, logits + argmax).
 #include "device_common.h"
 #include "kernels.h"
 
@@ -20,6 +25,7 @@ namespace pipo {
 
 constexpr int kNW = 8;                       // waves per workgroup
 constexpr int kGemvLdsBytes = 56 * 1024;     // dynamic LDS budget for the X chunk
+constexpr int kXR = 3;                       // prologue chunks per thread loaded ahead of the weights
 
 __device__ __forceinline__ float silu_f(float u) { return u / (1.0f + __expf(-u)); }
 
@@ -34,75 +40,147 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ u32x4 pack8(float4 a, float4 b) {
-    u32x4 v;
-    v[0] = pack_bf2(a.x, a.y);
-    v[1] = pack_bf2(a.z, a.w);
-    v[2] = pack_bf2(b.x, b.y);
-    v[3] = pack_bf2(b.z, b.w);
-    return v;
-}
+// The raw inputs of one 8-element prologue chunk, loaded early.
+struct XSrc {
+    float4 a0, a1;   // x (or x_f)
+    float4 g0, g1;   // gain
+    u32x4 e;         // gathered bf16 embedding
+};
 
 // MTP splits its K range: tiles below H/32 act on RMSNorm(h_b), the rest on
 // RMSNorm(E[b]); the two halves get different scales, so they accumulate apart.
 template <int PRO>
 struct NAcc { static constexpr int n = (PRO == PRO_MTP) ? 2 : 1; };
 
-template <int NBT, int SG, int PRO, int EPI>
+template <int PRO>
+__device__ __forceinline__ void load_src(const GemvParams &p, int b, int k, XSrc &s) {
+    if (PRO == PRO_PAIR) {
+        const bool first = k < p.H;
+        const int row = clamp_id(p.pairs[2 * b + (first ? 0 : 1)], p.vocab);
+        s.e = *(const u32x4 *)(p.embed + tiled_index(row, first ? k : k - p.H, p.H));
+    } else if (PRO == PRO_F32) {
+        const float4 *xp = (const float4 *)(p.xf + (int64_t)b * p.K + k);
+        s.a0 = xp[0];
+        s.a1 = xp[1];
+    } else if (PRO == PRO_NORM || k < p.H) {
+        const int stride = PRO == PRO_MTP ? p.H : p.K;
+        const float4 *xp = (const float4 *)(p.x + (int64_t)b * stride + k);
+        const float4 *gp = (const float4 *)(p.gain + k);
+        s.a0 = xp[0];
+        s.a1 = xp[1];
+        s.g0 = gp[0];
+        s.g1 = gp[1];
+    } else {   // PRO_MTP, second half: E[tok] * g_me
+        const int kh = k - p.H;
+        const int tok = clamp_id(argmax_key_id(p.tokkey[b]), p.vocab);
+        s.e = *(const u32x4 *)(p.embed + tiled_index(tok, kh, p.H));
+        const float4 *gp = (const float4 *)(p.gain2 + kh);
+        s.g0 = gp[0];
+        s.g1 = gp[1];
+    }
+}
+
+// hi / lo bf16 words of one chunk from its raw inputs
+template <int PRO>
+__device__ __forceinline__ void make_chunk(const GemvParams &p, int k, const XSrc &s, u32x4 &vh, u32x4 &vl) {
+    if (PRO == PRO_PAIR) {
+        vh = s.e;
+        vl = u32x4{0u, 0u, 0u, 0u};
+        return;
+    }
+    float f[8];
+    if (PRO == PRO_F32) {
+        f[0] = s.a0.x; f[1] = s.a0.y; f[2] = s.a0.z; f[3] = s.a0.w;
+        f[4] = s.a1.x; f[5] = s.a1.y; f[6] = s.a1.z; f[7] = s.a1.w;
+    } else if (PRO == PRO_NORM || k < p.H) {
+        f[0] = s.a0.x * s.g0.x; f[1] = s.a0.y * s.g0.y; f[2] = s.a0.z * s.g0.z; f[3] = s.a0.w * s.g0.w;
+        f[4] = s.a1.x * s.g1.x; f[5] = s.a1.y * s.g1.y; f[6] = s.a1.z * s.g1.z; f[7] = s.a1.w * s.g1.w;
+    } else {
+        f[0] = bf_lo(s.e[0]) * s.g0.x; f[1] = bf_hi(s.e[0]) * s.g0.y; f[2] = bf_lo(s.e[1]) * s.g0.z;
+        f[3] = bf_hi(s.e[1]) * s.g0.w; f[4] = bf_lo(s.e[2]) * s.g1.x; f[5] = bf_hi(s.e[2]) * s.g1.y;
+        f[6] = bf_lo(s.e[3]) * s.g1.z; f[7] = bf_hi(s.e[3]) * s.g1.w;
+    }
+    split8(f, vh, vl);
+}
+
+template <int NBT, int KS, int PRO, int EPI, int U = 4>
 __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
-    constexpr int U = 8 / SG;              // k-tiles per wave per load batch
+    // U: k-tiles per wave per load batch (two batches in flight)
+    constexpr int SPW = kNW / KS;          // strips per workgroup
     constexpr int NA = NAcc<PRO>::n;
     constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
+    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
     extern __shared__ __align__(16) uint16_t xs[];
     __shared__ float sc0[32], sc1[32];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
-    const int strip0 = blockIdx.x * SG;
+    const int ks = wave % KS;              // k-split index inside the strip
+    const int strip = blockIdx.x * SPW + wave / KS;
+    const bool sok = strip < nstrips;
+    const bool lead = ks == 0 && sok;      // the wave that reduces and writes the strip
     const int KT = p.K >> 5, HT = p.H >> 5;
     const int B = p.B;
     const int ktpc = p.ktiles_per_chunk;
     const int rstride = ktpc * 32 + 8;
-    uint16_t *xs_lo = xs + B * rstride;      // lo plane follows the hi plane
+    uint16_t *xs_lo = xs + B * rstride;    // lo plane follows the hi plane
+    const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
+    const int row0 = strip * 16 + 4 * g;   // first of this lane's four output rows
 
-    bool sok[SG];
-    const uint16_t *wp[SG];
+    // ---- 1. everything the prologue / epilogue read, before any weights -----
+    f32x4 resid[NBT];
 #pragma unroll
-    for (int s = 0; s < SG; ++s) {
-        sok[s] = strip0 + s < nstrips;
-        wp[s] = p.W + (int64_t)(sok[s] ? strip0 + s : 0) * KT * 512 + lane * 8;
+    for (int bt = 0; bt < NBT; ++bt) {
+        resid[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int b = bt * 16 + j;
+        if (EPI == EPI_RESID && lead && b < B) resid[bt] = *(const f32x4 *)(p.out + (int64_t)b * p.N + row0);
+    }
+    const int c1_first = min(KT, ktpc);
+    const int cpr_first = c1_first * 4;    // 8-element chunks per LDS row
+    XSrc src[kXR];
+#pragma unroll
+    for (int r = 0; r < kXR; ++r) {
+        const int idx = threadIdx.x + r * 512;
+        if (idx < B * cpr_first) {
+            const int b = idx / cpr_first;
+            load_src<PRO>(p, b, (idx - b * cpr_first) << 3, src[r]);
+        }
+    }
+    // RMSNorm scalars: wave w sums the partial sums of rows w, w+8, ...
+    float ssr[4] = {0.f, 0.f, 0.f, 0.f};
+    if (NORM) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int b = wave + r * kNW;
+            if (b < B)
+                for (int i = lane; i < p.nss; i += 64) ssr[r] += p.ss[b * p.nss + i];
+        }
     }
 
-    f32x4 acc[NA][SG][NBT];
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-#pragma unroll
-        for (int s = 0; s < SG; ++s)
-#pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) acc[a][s][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    u32x4 ra[2][U][SG];
+    // ---- 2. two batches of weight tiles in flight ----------------------------
+    u32x4 ra[2][U];
 #pragma unroll
     for (int bsel = 0; bsel < 2; ++bsel)
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int s = 0; s < SG; ++s) ra[bsel][u][s] = u32x4{0u, 0u, 0u, 0u};
-    // load batch: k-tiles kt_first + u*8 (u < U) of every strip into ra[BS]
+        for (int u = 0; u < U; ++u) ra[bsel][u] = u32x4{0u, 0u, 0u, 0u};
 #define GEMV_ISSUE(BS, kt_first, c1)                                                              \
     do {                                                                                          \
         _Pragma("unroll") for (int u = 0; u < U; ++u) {                                           \
-            const int kt_ = (kt_first) + u * kNW;                                                 \
-            _Pragma("unroll") for (int s = 0; s < SG; ++s) if (kt_ < (c1) && sok[s])              \
-                ra[BS][u][s] = __builtin_nontemporal_load((const u32x4 *)(wp[s] + (int64_t)kt_ * 512)); \
+            const int kt_ = (kt_first) + u * KS;                                                  \
+            if (kt_ < (c1) && sok)                                                                \
+                ra[BS][u] = __builtin_nontemporal_load((const u32x4 *)(wp + (int64_t)kt_ * 512)); \
         }                                                                                         \
     } while (0)
-    // MFMAs of one batch held in ra[BS] against the staged X chunk
+    f32x4 acc[NA][NBT];
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #define GEMV_CONSUME(BS, kt_first, c0, c1)                                                        \
     do {                                                                                          \
         _Pragma("unroll") for (int u = 0; u < U; ++u) {                                           \
-            const int k2 = (kt_first) + u * kNW;                                                  \
+            const int k2 = (kt_first) + u * KS;                                                   \
             if (k2 < (c1)) {                                                                      \
                 const bool hi_half = NA == 2 && k2 >= HT;                                         \
                 _Pragma("unroll") for (int bt = 0; bt < NBT; ++bt) {                              \
@@ -113,137 +191,128 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                         bop = *(const u32x4 *)(xs + xo);                                          \
                         if (HASLO) bol = *(const u32x4 *)(xs_lo + xo);                            \
                     }                                                                             \
-                    _Pragma("unroll") for (int s = 0; s < SG; ++s) {                              \
-                        f32x4 &ac = hi_half ? acc[NA - 1][s][bt] : acc[0][s][bt];                 \
-                        ac = mfma16(ra[BS][u][s], bop, ac);                                       \
-                        if (HASLO) ac = mfma16(ra[BS][u][s], bol, ac);                            \
-                    }                                                                             \
+                    f32x4 &ac = hi_half ? acc[NA - 1][bt] : acc[0][bt];                           \
+                    ac = mfma16(ra[BS][u], bop, ac);                                              \
+                    if (HASLO) ac = mfma16(ra[BS][u], bol, ac);                                   \
                 }                                                                                 \
             }                                                                                     \
         }                                                                                         \
     } while (0)
 
-    bool scalars_done = false;
-    for (int c0 = 0; c0 < KT; c0 += ktpc) {
-        const int c1 = min(KT, c0 + ktpc);
-        GEMV_ISSUE(0, c0 + wave, c1);          // weights first: independent of the activations
-        if (!scalars_done) {
-            scalars_done = true;
-            if (PRO == PRO_NORM || PRO == PRO_MTP) {
-                for (int b = wave; b < B; b += kNW) {
-                    float a = 0.f;
-                    for (int i = lane; i < p.nss; i += 64) a += p.ss[b * p.nss + i];
-                    a = wave_sum(a);
-                    const int kn = (PRO == PRO_MTP) ? p.H : p.K;
-                    if (lane == 0) sc0[b] = rsqrtf(a / (float)kn + p.eps);
-                    if (PRO == PRO_MTP) {
-                        const int tok = clamp_id(argmax_key_id(p.tokkey[b]), p.vocab);
-                        float e2 = 0.f;
-                        for (int k = lane * 8; k < p.H; k += 512) {
-                            const u32x4 w = *(const u32x4 *)(p.embed + tiled_index(tok, k, p.H));
+    GEMV_ISSUE(0, ks, c1_first);
+    GEMV_ISSUE(1, ks + U * KS, c1_first);
+
+    // ---- 3. scalars and the first LDS chunk (waits only on step 1's loads) --
+    if (NORM) {
 #pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                const float lo = bf_lo(w[i]), hi = bf_hi(w[i]);
-                                e2 += lo * lo + hi * hi;
-                            }
-                        }
-                        e2 = wave_sum(e2);
-                        if (lane == 0) sc1[b] = rsqrtf(e2 / (float)p.H + p.eps);
-                    }
-                }
-            }
+        for (int r = 0; r < 4; ++r) {
+            const int b = wave + r * kNW;
+            const float a = wave_sum(ssr[r]);
+            if (b < B && lane == 0) sc0[b] = rsqrtf(a / (float)(PRO == PRO_MTP ? p.H : p.K) + p.eps);
         }
-        __syncthreads();
-        const int cpr = (c1 - c0) * 4;        // 8-element chunks per LDS row
-        for (int idx = threadIdx.x; idx < B * cpr; idx += 512) {
-            const int b = idx / cpr;
-            const int kk = (idx - b * cpr) << 3;
-            const int k = c0 * 32 + kk;
-            u32x4 vh, vl = u32x4{0u, 0u, 0u, 0u};
-            float f[8];
-            if (PRO == PRO_PAIR) {
-                const bool first = k < p.H;
-                const int row = clamp_id(p.pairs[2 * b + (first ? 0 : 1)], p.vocab);
-                vh = *(const u32x4 *)(p.embed + tiled_index(row, first ? k : k - p.H, p.H));
-            } else {
-                if (PRO == PRO_NORM || (PRO == PRO_MTP && k < p.H)) {
-                    const int stride = PRO == PRO_MTP ? p.H : p.K;
-                    const float4 *xp = (const float4 *)(p.x + (int64_t)b * stride + k);
-                    const float4 *gp = (const float4 *)(p.gain + k);
-                    const float4 x0 = xp[0], x1 = xp[1], g0 = gp[0], g1 = gp[1];
-                    f[0] = x0.x * g0.x; f[1] = x0.y * g0.y; f[2] = x0.z * g0.z; f[3] = x0.w * g0.w;
-                    f[4] = x1.x * g1.x; f[5] = x1.y * g1.y; f[6] = x1.z * g1.z; f[7] = x1.w * g1.w;
-                } else if (PRO == PRO_F32) {
-                    const float4 *xp = (const float4 *)(p.xf + (int64_t)b * p.K + k);
-                    const float4 x0 = xp[0], x1 = xp[1];
-                    f[0] = x0.x; f[1] = x0.y; f[2] = x0.z; f[3] = x0.w;
-                    f[4] = x1.x; f[5] = x1.y; f[6] = x1.z; f[7] = x1.w;
-                } else {  // PRO_MTP, second half: E[tok] * g_me
-                    const int kh = k - p.H;
-                    const int tok = clamp_id(argmax_key_id(p.tokkey[b]), p.vocab);
-                    const u32x4 w = *(const u32x4 *)(p.embed + tiled_index(tok, kh, p.H));
-                    const float4 *gp = (const float4 *)(p.gain2 + kh);
-                    const float4 g0 = gp[0], g1 = gp[1];
-                    f[0] = bf_lo(w[0]) * g0.x; f[1] = bf_hi(w[0]) * g0.y; f[2] = bf_lo(w[1]) * g0.z;
-                    f[3] = bf_hi(w[1]) * g0.w; f[4] = bf_lo(w[2]) * g1.x; f[5] = bf_hi(w[2]) * g1.y;
-                    f[6] = bf_lo(w[3]) * g1.z; f[7] = bf_hi(w[3]) * g1.w;
+    }
+    if (PRO == PRO_MTP) {
+        // RMSNorm scale of E[tok] (a short row, read here after the weights)
+        for (int b = wave; b < B; b += kNW) {
+            const int tok = clamp_id(argmax_key_id(p.tokkey[b]), p.vocab);
+            float e2 = 0.f;
+            for (int k = lane * 8; k < p.H; k += 512) {
+                const u32x4 w = *(const u32x4 *)(p.embed + tiled_index(tok, k, p.H));
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float lo = bf_lo(w[i]), hi = bf_hi(w[i]);
+                    e2 += lo * lo + hi * hi;
                 }
-                split8(f, vh, vl);
             }
+            e2 = wave_sum(e2);
+            if (lane == 0) sc1[b] = rsqrtf(e2 / (float)p.H + p.eps);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kXR; ++r) {
+        const int idx = threadIdx.x + r * 512;
+        if (idx < B * cpr_first) {
+            const int b = idx / cpr_first;
+            const int kk = (idx - b * cpr_first) << 3;
+            u32x4 vh, vl;
+            make_chunk<PRO>(p, kk, src[r], vh, vl);
             *(u32x4 *)(xs + b * rstride + kk) = vh;
             if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
         }
-        __syncthreads();
-        // ping-pong: while one batch is consumed the next is in flight
-        int kt = c0 + wave;
+    }
+    for (int idx = threadIdx.x + kXR * 512; idx < B * cpr_first; idx += 512) {   // large B only
+        const int b = idx / cpr_first;
+        const int kk = (idx - b * cpr_first) << 3;
+        XSrc sx;
+        load_src<PRO>(p, b, kk, sx);
+        u32x4 vh, vl;
+        make_chunk<PRO>(p, kk, sx, vh, vl);
+        *(u32x4 *)(xs + b * rstride + kk) = vh;
+        if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
+    }
+    __syncthreads();
+
+    // ---- 4. stream: consume one batch while the next two are in flight ------
+    for (int c0 = 0; c0 < KT; c0 += ktpc) {
+        const int c1 = min(KT, c0 + ktpc);
+        if (c0 > 0) {   // later LDS chunks (batch > ~14 with long K)
+            __syncthreads();
+            const int cpr = (c1 - c0) * 4;
+            for (int idx = threadIdx.x; idx < B * cpr; idx += 512) {
+                const int b = idx / cpr;
+                const int kk = (idx - b * cpr) << 3;
+                XSrc sx;
+                load_src<PRO>(p, b, c0 * 32 + kk, sx);
+                u32x4 vh, vl;
+                make_chunk<PRO>(p, c0 * 32 + kk, sx, vh, vl);
+                *(u32x4 *)(xs + b * rstride + kk) = vh;
+                if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
+            }
+            __syncthreads();
+            GEMV_ISSUE(0, c0 + ks, c1);
+            GEMV_ISSUE(1, c0 + ks + U * KS, c1);
+        }
+        int kt = c0 + ks;
         while (kt < c1) {
-            int nxt = kt + U * kNW;
-            if (nxt < c1) GEMV_ISSUE(1, nxt, c1);
             GEMV_CONSUME(0, kt, c0, c1);
-            kt = nxt;
+            GEMV_ISSUE(0, kt + 2 * U * KS, c1);
+            kt += U * KS;
             if (kt >= c1) break;
-            nxt = kt + U * kNW;
-            if (nxt < c1) GEMV_ISSUE(0, nxt, c1);
             GEMV_CONSUME(1, kt, c0, c1);
-            kt = nxt;
+            GEMV_ISSUE(1, kt + 2 * U * KS, c1);
+            kt += U * KS;
         }
     }
 #undef GEMV_ISSUE
 #undef GEMV_CONSUME
 
-    // ---- reduce the eight waves' partial sums, strip by strip ---------------
-    // afterwards wave s < SG holds strip strip0 + s in fin[]
+    // ---- 5. reduce the KS partial sums of each strip (wave order) -----------
     f32x4 fin[NBT];
 #pragma unroll
-    for (int bt = 0; bt < NBT; ++bt) fin[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    f32x4 *red = (f32x4 *)xs;   // [kNW][NBT][64] f32x4, reusing the X chunk
-#pragma unroll
-    for (int s = 0; s < SG; ++s) {
-        __syncthreads();
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) {
-            f32x4 v = acc[0][s][bt];
-            if (NA == 2) {
-                const int b = bt * 16 + j;
-                const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
-                v = v * s0 + acc[NA - 1][s][bt] * s1;
-            }
-            red[(wave * NBT + bt) * 64 + lane] = v;
+    for (int bt = 0; bt < NBT; ++bt) {
+        f32x4 v = acc[0][bt];
+        if (NA == 2) {
+            const int b = bt * 16 + j;
+            const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
+            v = v * s0 + acc[NA - 1][bt] * s1;
         }
+        fin[bt] = v;
+    }
+    if (KS > 1) {
+        f32x4 *red = (f32x4 *)xs;   // [kNW][NBT][64] f32x4, reusing the X chunk
         __syncthreads();
-        if (wave == s) {
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
+        __syncthreads();
+        if (ks == 0) {
 #pragma unroll
             for (int bt = 0; bt < NBT; ++bt) {
-                f32x4 t = red[bt * 64 + lane];
 #pragma unroll
-                for (int w = 1; w < kNW; ++w) t += red[(w * NBT + bt) * 64 + lane];
-                fin[bt] = t;
+                for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
             }
         }
     }
-    if (wave >= SG) return;
-    const int strip = strip0 + wave;
-    if (strip >= nstrips) return;
+    if (EPI != EPI_LOGITS && !lead) return;
     if (PRO == PRO_NORM) {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
@@ -252,20 +321,16 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
         }
     }
 
-    // ---- fused epilogues (one wave per strip) -------------------------------
-    const int row0 = strip * 16 + 4 * g;   // first of this lane's four rows
+    // ---- 6. fused epilogues (one wave per strip) ----------------------------
     if (EPI == EPI_STORE || EPI == EPI_RESID) {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
             const int b = bt * 16 + j;
             const bool ok = b < B;
             f32x4 val = fin[bt];
-            float *o = p.out + (int64_t)b * p.N + row0;
-            if (ok) {
-                if (EPI == EPI_RESID) val += *(const f32x4 *)o;
-                else if (p.bias) val += *(const f32x4 *)(p.bias + row0);
-                *(f32x4 *)o = val;
-            }
+            if (EPI == EPI_RESID) val += resid[bt];
+            else if (p.bias) val += *(const f32x4 *)(p.bias + row0);
+            if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = val;
             float sq = val[0] * val[0] + val[1] * val[1] + val[2] * val[2] + val[3] * val[3];
             sq = col_sum(sq);
             if (ok && g == 0 && p.ss_out) p.ss_out[b * nstrips + strip] = sq;
@@ -287,7 +352,7 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
         }
     } else if (EPI == EPI_QKV) {
         const int d = p.d, hs = d >> 4;             // strips per head
-        const int qs = p.n_q * hs, ks = p.n_kv * hs;
+        const int qs = p.n_q * hs, kvs = p.n_kv * hs;
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
             const int b = bt * 16 + j;
@@ -296,7 +361,7 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
             for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(fin[bt][v], 32);
             if (b >= B) continue;
             const int pos = p.pos[b];
-            if (strip < qs + ks) {
+            if (strip < qs + kvs) {
                 const bool isq = strip < qs;
                 const int sidx = isq ? strip : strip - qs;
                 const int head = sidx / hs, t = sidx - head * hs;
@@ -316,7 +381,7 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                                     : p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0;
                 *(u32x2 *)dst = w;
             } else {
-                const int r0 = (strip - qs - ks) * 16 + 4 * g;
+                const int r0 = (strip - qs - kvs) * 16 + 4 * g;
                 const int kvh = r0 / d, dim = r0 - kvh * d;
                 uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
                                 ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot(pos & 31);
@@ -325,10 +390,12 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
             }
         }
     } else if (EPI == EPI_LOGITS) {
+        // every wave reaches here; waves without a strip contribute key 0
+        __shared__ uint64_t s_best[kNW][32];
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
             const int b = bt * 16 + j;
-            const bool ok = b < B;
+            const bool ok = lead && b < B;
             if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = fin[bt];
             if (p.best) {
                 uint64_t key = 0;
@@ -343,13 +410,22 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                 key = o > key ? o : key;
                 o = shfl_xor_u64(key, 32);
                 key = o > key ? o : key;
-                if (g == 0 && ok) atomicMax((unsigned long long *)(p.best + b), (unsigned long long)key);
+                if (g == 0) s_best[wave][b] = key;
+            }
+        }
+        if (p.best) {
+            __syncthreads();
+            if (threadIdx.x < B) {
+                uint64_t m = 0;
+#pragma unroll
+                for (int w = 0; w < kNW; ++w) m = s_best[w][threadIdx.x] > m ? s_best[w][threadIdx.x] : m;
+                if (m) atomicMax((unsigned long long *)(p.best + threadIdx.x), (unsigned long long)m);
             }
         }
     }
 }
 
-template <int NBT, int SG, int PRO, int EPI>
+template <int NBT, int KS, int PRO, int EPI>
 static void launch_t(const GemvParams &p, hipStream_t s) {
     GemvParams q = p;
     const int KT = q.K >> 5;
@@ -360,27 +436,30 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     int lds = planes * q.B * (ktpc * 32 + 8) * 2;
     const int red = kNW * NBT * 64 * 16;
     lds = lds > red ? lds : red;
-    const int grid = ((q.N >> 4) + SG - 1) / SG;
-    hipLaunchKernelGGL((k_gemv<NBT, SG, PRO, EPI>), dim3(grid), dim3(kNW * 64), lds, s, q);
+    constexpr int SPW = kNW / KS;
+    const int grid = ((q.N >> 4) + SPW - 1) / SPW;
+    hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI>), dim3(grid), dim3(kNW * 64), lds, s, q);
 }
 
-template <int SG, int PRO, int EPI>
+template <int KS, int PRO, int EPI>
 static void launch_nbt(const GemvParams &p, hipStream_t s) {
-    if (p.B <= 16) launch_t<1, SG, PRO, EPI>(p, s);
-    else launch_t<2, SG, PRO, EPI>(p, s);
+    if (p.B <= 16) launch_t<1, KS, PRO, EPI>(p, s);
+    else launch_t<2, KS, PRO, EPI>(p, s);
 }
 
-// One instantiation per (prologue, epilogue) pair the decode step uses; the
-// strips per workgroup follow the matrix height: the LM head (151936 rows)
-// and gate/up (19456) take 4 and 2 strips, the rest one.
+int gemv_num_groups(int N) { return N >> 4; }
+
+// One instantiation per (prologue, epilogue) pair the decode step uses.
+// Waves per strip (the K split), from a sweep on MI355X at batch 1: the LM
+// head (151936 rows) splits K in four, every other matrix in eight.
 void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s) {
-    if (pro == PRO_PAIR && epi == EPI_STORE) launch_nbt<1, PRO_PAIR, EPI_STORE>(p, s);
-    else if (pro == PRO_NORM && epi == EPI_QKV) launch_nbt<1, PRO_NORM, EPI_QKV>(p, s);
-    else if (pro == PRO_F32 && epi == EPI_RESID) launch_nbt<1, PRO_F32, EPI_RESID>(p, s);
-    else if (pro == PRO_NORM && epi == EPI_SWIGLU) launch_nbt<2, PRO_NORM, EPI_SWIGLU>(p, s);
+    if (pro == PRO_PAIR && epi == EPI_STORE) launch_nbt<8, PRO_PAIR, EPI_STORE>(p, s);
+    else if (pro == PRO_NORM && epi == EPI_QKV) launch_nbt<8, PRO_NORM, EPI_QKV>(p, s);
+    else if (pro == PRO_F32 && epi == EPI_RESID) launch_nbt<8, PRO_F32, EPI_RESID>(p, s);
+    else if (pro == PRO_NORM && epi == EPI_SWIGLU) launch_nbt<8, PRO_NORM, EPI_SWIGLU>(p, s);
     else if (pro == PRO_NORM && epi == EPI_LOGITS) launch_nbt<4, PRO_NORM, EPI_LOGITS>(p, s);
-    else if (pro == PRO_MTP && epi == EPI_STORE) launch_nbt<1, PRO_MTP, EPI_STORE>(p, s);
-    else if (pro == PRO_NORM && epi == EPI_STORE) launch_nbt<1, PRO_NORM, EPI_STORE>(p, s);
+    else if (pro == PRO_MTP && epi == EPI_STORE) launch_nbt<8, PRO_MTP, EPI_STORE>(p, s);
+    else if (pro == PRO_NORM && epi == EPI_STORE) launch_nbt<8, PRO_NORM, EPI_STORE>(p, s);
 }
 
 }  // namespace pipo

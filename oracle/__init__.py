@@ -11,5 +11,5 @@ from .pipo_oracle import (  # noqa: F401
     OracleWeights, PipoOracle, rms_norm, rope_cos_sin, apply_rope, silu,
     compress, attention_decode, attention_causal, backbone_full, lm_logits,
     mtp_hidden, confidence, gate, select_greedy, select_top_p, prompt_pairs,
-    Sampling,
+    Sampling, to_bf16,
 )

@@ -31,6 +31,10 @@ silent:
   a single linear replaces App. B.3's two-layer MLP, as the configurations
   fix it.  The draft is accepted iff ``c >= tau`` (equality accepts), and the
   next input pair is ``(b, d)`` if accepted else ``(b, PAD)`` (Sec. 3.2).
+* KV cache storage: the workloads fix a bf16 KV cache (like the bf16
+  weights, a storage format), so with ``kv_bf16`` the keys (after RoPE) and
+  values are rounded to bf16 (nearest even) as they enter the cache; every
+  other value stays float64.
 * Token selection: greedy argmax with ties to the lowest id; or temperature
   plus nucleus (top-p): ``p = softmax(logits / T)``; the threshold
   ``theta*`` is the largest value among the ``p_j`` whose upper mass
@@ -57,6 +61,7 @@ F64 = np.float64
 def rms_norm(x, g, eps):
     """RMSNorm over the last axis: ``x / sqrt(mean(x^2) + eps) * g``."""
     x = np.asarray(x, dtype=F64)
+    g = np.asarray(g, dtype=F64)
     return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * np.asarray(g, F64)
 
 
@@ -82,6 +87,13 @@ def apply_rope(x, cos, sin):
 def silu(u):
     """SiLU(u) = u / (1 + exp(-u))."""
     return u / (1.0 + np.exp(-u))
+
+
+def to_bf16(x):
+    """Nearest bf16 value (ties to even) of each element, via float32."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return u.astype(np.uint32).view(np.float32).astype(F64)
 
 
 def softmax(s, axis=-1):
@@ -196,15 +208,20 @@ def select_top_p(logits, temperature, top_p, u):
 # ------------------------------------------------------------------- weights
 
 class OracleWeights:
-    """All tensors of one model as float64 arrays in logical ``[out][in]`` order."""
+    """All tensors of one model in logical ``[out][in]`` order.
 
-    def __init__(self, cfg: ModelConfig, tensors: dict):
+    Values are held as float64, or as float32 when every value is exactly
+    representable in it (bf16-valued weights of large models, to halve the
+    memory); arithmetic is float64 either way (NumPy promotes the operands).
+    """
+
+    def __init__(self, cfg: ModelConfig, tensors: dict, storage=F64):
         self.cfg = cfg
-        self.t = {k: np.asarray(v, dtype=F64) for k, v in tensors.items()}
+        self.t = {k: np.asarray(v, dtype=storage) for k, v in tensors.items()}   # no copy if already
 
     @classmethod
-    def generate(cls, cfg: ModelConfig, seed: int = 0, precision: str = "bf16"):
-        """R-spec weights; ``precision`` 'bf16' rounds matrices to bf16 first."""
+    def generate(cls, cfg: ModelConfig, seed: int = 0, precision: str = "bf16", storage=F64):
+        """R-spec weights; ``precision`` 'bf16' rounds every tensor to bf16 first."""
         tensors = {}
         for name, shape in model_tensor_shapes(cfg).items():
             tid = (rspec.TENSOR_IDS[name] if "." not in name
@@ -212,12 +229,12 @@ class OracleWeights:
             base = name.split(".")[-1]
             if base.startswith("g_"):
                 v = rspec.gain_values(seed, tid, shape[0], cfg.gain_mode)
+                if precision == "bf16":
+                    v = rspec.bf16_round(v)
             else:
-                v = rspec.weight_tensor(seed, tid, shape)
-            if precision == "bf16":
-                v = rspec.bf16_round(v)
-            tensors[name] = v.astype(F64)
-        return cls(cfg, tensors)
+                v = rspec.weight_tensor(seed, tid, shape, bf16=precision == "bf16", dtype=storage)
+            tensors[name] = v
+        return cls(cfg, tensors, storage)
 
     def __getitem__(self, k):
         return self.t[k]
@@ -228,14 +245,17 @@ class OracleWeights:
 
 # ------------------------------------------------------------------ backbone
 
-def _layer_qkv(cfg, L, x, pos):
+def _layer_qkv(cfg, L, x, pos, kv_bf16=False):
     n = rms_norm(x, L["g_attn"], cfg.rms_eps)
     T = n.shape[0]
     q = (n @ L["wq"].T).reshape(T, cfg.n_q_heads, cfg.head_dim).transpose(1, 0, 2)
     k = (n @ L["wk"].T).reshape(T, cfg.n_kv_heads, cfg.head_dim).transpose(1, 0, 2)
     v = (n @ L["wv"].T).reshape(T, cfg.n_kv_heads, cfg.head_dim).transpose(1, 0, 2)
     cos, sin = rope_cos_sin(pos, cfg.head_dim, cfg.rope_base)
-    return apply_rope(q, cos, sin), apply_rope(k, cos, sin), v
+    q, k = apply_rope(q, cos, sin), apply_rope(k, cos, sin)
+    if kv_bf16:
+        k, v = to_bf16(k), to_bf16(v)
+    return q, k, v
 
 
 def _layer_ffn(cfg, L, x):
@@ -243,7 +263,7 @@ def _layer_ffn(cfg, L, x):
     return x + (silu(n @ L["wgate"].T) * (n @ L["wup"].T)) @ L["wdown"].T
 
 
-def backbone_full(W: OracleWeights, Z):
+def backbone_full(W: OracleWeights, Z, kv_bf16=False):
     """Eq. 2 by brute force: all latent positions 0..T-1 from scratch.
 
     Returns the final residual states [T, H] (before the final norm) and the
@@ -255,7 +275,7 @@ def backbone_full(W: OracleWeights, Z):
     caches = []
     for li in range(cfg.n_layers):
         L = W.layer(li)
-        q, k, v = _layer_qkv(cfg, L, x, np.arange(T))
+        q, k, v = _layer_qkv(cfg, L, x, np.arange(T), kv_bf16)
         o = attention_causal(q, k, v)
         x = x + o.transpose(1, 0, 2).reshape(T, cfg.q_dim) @ L["wo"].T
         x = _layer_ffn(cfg, L, x)
@@ -263,7 +283,7 @@ def backbone_full(W: OracleWeights, Z):
     return x, caches
 
 
-def backbone_step(W: OracleWeights, z, pos, caches):
+def backbone_step(W: OracleWeights, z, pos, caches, kv_bf16=False):
     """Eq. 2 incrementally: one latent at position ``pos`` against the cache.
 
     ``caches`` is a list per layer of ``[K, V]`` arrays [n_kv, pos, d]; the new
@@ -273,7 +293,7 @@ def backbone_step(W: OracleWeights, z, pos, caches):
     x = np.asarray(z, F64).reshape(1, -1).copy()
     for li in range(cfg.n_layers):
         L = W.layer(li)
-        q, k, v = _layer_qkv(cfg, L, x, np.array([pos]))
+        q, k, v = _layer_qkv(cfg, L, x, np.array([pos]), kv_bf16)
         K = np.concatenate([caches[li][0], k], axis=1)
         V = np.concatenate([caches[li][1], v], axis=1)
         caches[li][0], caches[li][1] = K, V
@@ -294,11 +314,14 @@ class Sampling:
 
 
 class PipoOracle:
-    """A batch of independent PIPO sequences: prefill, then pair-decode steps."""
+    """A batch of independent PIPO sequences: prefill, then pair-decode steps.
 
-    def __init__(self, W: OracleWeights):
+    ``kv_bf16``: store keys and values in bf16 (the workloads' KV format)."""
+
+    def __init__(self, W: OracleWeights, kv_bf16: bool = False):
         self.W = W
         self.cfg = W.cfg
+        self.kv_bf16 = kv_bf16
 
     # heads: eqs. 3-6 and the gate, for one sequence
     def heads(self, h_b, seq, step, force_b=None):
@@ -330,7 +353,7 @@ class PipoOracle:
         for i, prompt in enumerate(np.asarray(prompts)):
             pairs = prompt_pairs(prompt, cfg.pad_id)
             Z = compress(W["embed"], W["w_comp"], W["b_comp"], pairs)
-            X, caches = backbone_full(W, Z)
+            X, caches = backbone_full(W, Z, self.kv_bf16)
             self.caches.append([[k, v] for k, v in caches])
             self.length.append(len(pairs))
             rec = self.heads(X[-1], i, 0, None if force_b is None else force_b[i])
@@ -349,7 +372,7 @@ class PipoOracle:
         for i in range(len(self.caches)):
             pair = self.next_pairs[i] if in_pairs is None else tuple(int(v) for v in in_pairs[i])
             z = compress(W["embed"], W["w_comp"], W["b_comp"], np.array([pair]))[0]
-            h_b = backbone_step(W, z, self.length[i], self.caches[i])
+            h_b = backbone_step(W, z, self.length[i], self.caches[i], self.kv_bf16)
             self.length[i] += 1
             rec = self.heads(h_b, i, self.step_idx[i], None if force_b is None else force_b[i])
             out.append(rec)

@@ -7,7 +7,9 @@
 // accumulator holds one head; online softmax runs per column; the
 // probabilities, held as (4g + v, 16 + 4g + v) for lane group g, are already
 // the B operand of O^T[dim][head] += V^T P^T because the V cache stores each
-// 32-key tile in that key order (see vslot in gemv.hip).  Per-split results
+// 32-key tile in that key order (see vslot in gemv.hip).  The query and the
+// probabilities enter the MFMAs as bf16 pairs hi + lo (two MFMAs each), so
+// only the bf16 KV cache itself limits the precision.  Per-split results
 // (m, l, o) go to a partial buffer; a second kernel merges them per head in
 // split order (the kernel boundary makes every split's partial visible).
 #include "device_common.h"
@@ -32,11 +34,17 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     const int k1 = min(len, k0 + chunk);
     const float scale = 1.4426950408889634f / sqrtf((float)D);
 
-    u32x4 qb[NC];
+    u32x4 qh[NC], ql[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-        qb[c] = u32x4{0u, 0u, 0u, 0u};
-        if (j < qpg) qb[c] = *(const u32x4 *)(p.q + ((int64_t)b * p.n_q + kvh * qpg + j) * D + 32 * c + 8 * g);
+        qh[c] = u32x4{0u, 0u, 0u, 0u};
+        ql[c] = u32x4{0u, 0u, 0u, 0u};
+        if (j < qpg) {
+            const float4 *qp = (const float4 *)(p.q + ((int64_t)b * p.n_q + kvh * qpg + j) * D + 32 * c + 8 * g);
+            const float4 a = qp[0], bq = qp[1];
+            const float f[8] = {a.x, a.y, a.z, a.w, bq.x, bq.y, bq.z, bq.w};
+            split8(f, qh[c], ql[c]);
+        }
     }
     const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
     const uint16_t *vbase = p.vc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
@@ -66,7 +74,10 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
         for (int tau = 0; tau < 2; ++tau) {
             st[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < NC; ++c) st[tau] = mfma16(kf[bsel][tau][c], qb[c], st[tau]);
+            for (int c = 0; c < NC; ++c) {
+                st[tau] = mfma16(kf[bsel][tau][c], qh[c], st[tau]);
+                st[tau] = mfma16(kf[bsel][tau][c], ql[c], st[tau]);
+            }
         }
         float mx = -INFINITY;
 #pragma unroll
@@ -92,15 +103,14 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
             }
         l_run = l_run * alpha + col_sum(ps);
         m_run = m_new;
-        u32x4 pt;
-        pt[0] = pack_bf2(st[0][0], st[0][1]);
-        pt[1] = pack_bf2(st[0][2], st[0][3]);
-        pt[2] = pack_bf2(st[1][0], st[1][1]);
-        pt[3] = pack_bf2(st[1][2], st[1][3]);
+        const float pf[8] = {st[0][0], st[0][1], st[0][2], st[0][3], st[1][0], st[1][1], st[1][2], st[1][3]};
+        u32x4 ph, pl;
+        split8(pf, ph, pl);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             o[t] *= alpha;
-            o[t] = mfma16(vf[bsel][t], pt, o[t]);
+            o[t] = mfma16(vf[bsel][t], ph, o[t]);
+            o[t] = mfma16(vf[bsel][t], pl, o[t]);
         }
     };
     // ping-pong over 32-key blocks: the next block's loads are in flight

@@ -374,12 +374,14 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
                     r[v] = (g < 2) ? fin[bt][v] * c4[v] - other[v] * s4[v] : fin[bt][v] * c4[v] + other[v] * s4[v];
-                u32x2 w;
-                w[0] = pack_bf2(r[0], r[1]);
-                w[1] = pack_bf2(r[2], r[3]);
-                uint16_t *dst = isq ? p.q + ((int64_t)b * p.n_q + head) * d + dim0
-                                    : p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0;
-                *(u32x2 *)dst = w;
+                if (isq) {
+                    *(f32x4 *)(p.q + ((int64_t)b * p.n_q + head) * d + dim0) = f32x4{r[0], r[1], r[2], r[3]};
+                } else {
+                    u32x2 w;
+                    w[0] = pack_bf2(r[0], r[1]);
+                    w[1] = pack_bf2(r[2], r[3]);
+                    *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
+                }
             } else {
                 const int r0 = (strip - qs - kvs) * 16 + 4 * g;
                 const int kvh = r0 / d, dim = r0 - kvh * d;

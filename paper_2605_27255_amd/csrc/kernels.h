@@ -21,7 +21,7 @@ enum GemvEpi : int {
     EPI_STORE  = 0,  // out fp32 [B][N] = acc (+ bias); sum-of-squares parts
     EPI_RESID  = 1,  // out fp32 [B][N] += acc; sum-of-squares parts
     EPI_SWIGLU = 2,  // act fp32 [B][N/2] = SiLU(gate) * up (gate/up strip-interleaved)
-    EPI_QKV    = 3,  // RoPE q,k; q bf16 [B][n_q][d]; k, v appended to the KV cache
+    EPI_QKV    = 3,  // RoPE q,k; q fp32 [B][n_q][d]; k, v appended to the bf16 KV cache
     EPI_LOGITS = 4,  // logits fp32 [B][N]; optional argmax key per row (greedy)
 };
 
@@ -35,7 +35,7 @@ struct GemvParams {
     const uint64_t *tokkey;
     // epilogue
     float *out; const float *bias; float *ss_out; float *act;
-    uint16_t *q; uint16_t *kc; uint16_t *vc; const int32_t *pos;
+    float *q; uint16_t *kc; uint16_t *vc; const int32_t *pos;
     const float *rope_cos; const float *rope_sin;
     int n_q, n_kv, d, lmax_pad;   // KV geometry of this layer
     int64_t kv_bstride;           // elements between consecutive sequences' caches
@@ -48,7 +48,7 @@ int gemv_num_groups(int N);
 // Split-K grouped-query flash-decode over the latent KV cache.
 // ----------------------------------------------------------------------------
 struct AttnDecodeParams {
-    const uint16_t *q;          // bf16 [B][n_q][d]
+    const float *q;             // fp32 [B][n_q][d]
     const uint16_t *kc, *vc;    // this layer's caches
     int64_t kv_bstride;
     const int32_t *pos;         // [B]: attend to keys 0..pos[b]

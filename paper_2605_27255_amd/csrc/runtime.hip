@@ -56,8 +56,7 @@ struct pipo_ctx {
 
     // decode state and activations
     float *x, *ss_x, *hd, *ss_hd, *logits_b, *logits_d, *apart;
-    uint16_t *qbuf;
-    float *attn_out, *act;
+    float *qbuf, *attn_out, *act;
     uint64_t *best_b, *best_d, *seeds;
     int32_t *pairs, *pos, *step;
     pipo_pair *out;
@@ -220,7 +219,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->ss_hd = a.take<float>((int64_t)B * (H / 16));
         c->logits_b = a.take<float>((int64_t)B * V);
         c->logits_d = a.take<float>((int64_t)B * V);
-        c->qbuf = a.take<uint16_t>((int64_t)B * c->qdim);
+        c->qbuf = a.take<float>((int64_t)B * c->qdim);
         c->attn_out = a.take<float>((int64_t)B * c->qdim);
         c->act = a.take<float>((int64_t)B * F);
         c->best_b = a.take<uint64_t>(B);

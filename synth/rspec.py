@@ -90,7 +90,8 @@ def _fast_lib():
         if os.path.exists(so):
             lib = ctypes.CDLL(so)
             lib.rspec_fill.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
-                                       ctypes.c_int64, ctypes.c_void_p]
+                                       ctypes.c_int64, ctypes.c_void_p, ctypes.c_int]
+            lib.rspec_fill64.argtypes = lib.rspec_fill.argtypes
             _FAST = lib
     return _FAST
 
@@ -98,13 +99,17 @@ def _fast_lib():
 _FAST = None
 
 
-def weight_values(seed: int, tid: int, start: int, count: int, fast: bool = True) -> np.ndarray:
-    """float32 values of elements ``[start, start+count)`` of tensor ``tid``."""
+def weight_values(seed: int, tid: int, start: int, count: int, fast: bool = True,
+                  bf16: bool = False) -> np.ndarray:
+    """float32 values of elements ``[start, start+count)`` of tensor ``tid``
+    (rounded to bf16 when ``bf16``)."""
     lib = _fast_lib() if fast else False
     if lib:
         out = np.empty(count, dtype=np.float32)
-        lib.rspec_fill(seed & _MASK64, tid & _MASK64, start, count, out.ctypes.data)
+        lib.rspec_fill(seed & _MASK64, tid & _MASK64, start, count, out.ctypes.data, 1 if bf16 else 0)
         return out
+    if bf16:
+        return bf16_round(weight_values(seed, tid, start, count, fast=False))
     k = np.uint64(key(seed, tid))
     idx = np.arange(start, start + count, dtype=np.uint64)
     with np.errstate(over="ignore"):
@@ -114,14 +119,21 @@ def weight_values(seed: int, tid: int, start: int, count: int, fast: bool = True
     return centred.astype(np.float32) * WEIGHT_SCALE
 
 
-def weight_tensor(seed: int, tid: int, shape, chunk: int = 1 << 26) -> np.ndarray:
-    """A whole float32 tensor in logical row-major ``[out][in]`` order."""
+def weight_tensor(seed: int, tid: int, shape, chunk: int = 1 << 26, bf16: bool = False,
+                  dtype=np.float32) -> np.ndarray:
+    """A whole tensor in logical row-major ``[out][in]`` order (float32 values,
+    stored as ``dtype``)."""
     n = int(np.prod(shape))
+    lib = _fast_lib()
+    if lib and dtype == np.float64:
+        out = np.empty(n, dtype=np.float64)
+        lib.rspec_fill64(seed & _MASK64, tid & _MASK64, 0, n, out.ctypes.data, 1 if bf16 else 0)
+        return out.reshape(shape)
     out = np.empty(n, dtype=np.float32)
     for s in range(0, n, chunk):
         c = min(chunk, n - s)
-        out[s:s + c] = weight_values(seed, tid, s, c)
-    return out.reshape(shape)
+        out[s:s + c] = weight_values(seed, tid, s, c, bf16=bf16)
+    return out.reshape(shape).astype(dtype, copy=False)
 
 
 def gain_values(seed: int, tid: int, n: int, gain_mode: int) -> np.ndarray:

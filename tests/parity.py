@@ -1,7 +1,8 @@
 """Teacher-forced parity protocol between the HIP path and the oracle.
 
 The GPU runs free (each step's input pair is the pair its previous step
-produced on the device); the oracle replays exactly those input pairs and,
+produced on the device); the oracle, with the workloads' bf16 KV cache,
+replays exactly those input pairs and,
 inside each step, the GPU's backbone token as the MTP head's input, and every
 output is compared:
 
@@ -114,7 +115,7 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
     torch.cuda.synchronize()
     host = [(unpack_pairs(o), lb.cpu().numpy(), ld.cpu().numpy()) for o, lb, ld in outs]
     log(f"gpu done: {B} sequences, {steps} steps")
-    orc = O.PipoOracle(W)
+    orc = O.PipoOracle(W, kv_bf16=True)      # the device's KV cache is bf16, as the workloads state
     rep = ParityReport()
     for s, (o, lb, ld) in enumerate(host):
         force = [int(v) for v in o[0]]

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from synth import rspec
-from synth.configs import TINY, DENSE_4B, ModelConfig, model_tensor_shapes
+from synth.configs import TINY, DENSE_4B, DENSE_9B, ModelConfig, model_tensor_shapes
 from oracle import pipo_oracle as O
 
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
@@ -143,6 +143,72 @@ def test_4b_width_two_layers_2048_latents(torch):
     log("generating oracle weights")
     W = O.OracleWeights.generate(cfg, seed=0, precision="bf16")
     rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log)
+    rep.check()
+    m.close()
+
+
+def test_4b_full_depth_36_layers(torch):
+    """The whole 4B-class model (36 layers, bench launch configuration at batch 1):
+    a 40-token prompt (20 latents) and 3 greedy pair steps."""
+    n, steps = 40, 3
+    prompts = rspec.prompt_tokens(1, n, DENSE_4B.vocab)
+    m = _model(DENSE_4B, seed=0, max_batch=1, max_latent=2048 + 257, prefill_chunk=4096)
+    log("generating oracle weights (36 layers)")
+    W = O.OracleWeights.generate(DENSE_4B, seed=0, precision="bf16")
+    log("oracle weights ready")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log)
+    rep.check()
+    m.close()
+
+
+def test_4b_width_batch20_top_p(torch):
+    """4B width, two layers, 20 sequences (two 16-column MFMA tiles), T 0.6,
+    top-p 0.95, tau 0.7, per-sequence seeds."""
+    cfg = DENSE_4B.with_layers(2)
+    B, n, steps = 20, 64, 3
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=9)
+    smp = O.Sampling(tau=0.7, temperature=0.6, top_p=0.95, seeds=tuple(1000 + b for b in range(B)))
+    m = _model(cfg, seed=4, max_batch=32, max_latent=32 + steps + 1, prefill_chunk=4096)
+    W = O.OracleWeights.generate(cfg, seed=4, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, smp, log)
+    rep.check()
+    m.close()
+
+
+def test_9b_width_chunked_prefill(torch):
+    """9B-class width (hidden 4096, FFN 12288), one layer, batch 2, a 517-token
+    prompt (259 latents, odd) prefilled in chunks of 100 latents, 3 steps."""
+    cfg = DENSE_9B.with_layers(1)
+    B, n, steps = 2, 517, 3
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=5)
+    m = _model(cfg, seed=7, max_batch=2, max_latent=259 + steps + 1, prefill_chunk=100)
+    W = O.OracleWeights.generate(cfg, seed=7, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log)
+    rep.check()
+    m.close()
+
+
+def test_4b_width_long_prompt_four_chunks(torch):
+    """One 4B-width layer, 8192-token prompt (4096 latents) prefilled in four
+    1024-latent chunks (causal attention across chunks), then 3 steps."""
+    cfg = DENSE_4B.with_layers(1)
+    n, steps = 8192, 3
+    prompts = rspec.prompt_tokens(1, n, cfg.vocab, seed=2)
+    m = _model(cfg, seed=3, max_batch=1, max_latent=4096 + steps + 1, prefill_chunk=1024)
+    W = O.OracleWeights.generate(cfg, seed=3, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log)
+    rep.check()
+    m.close()
+
+
+def test_tiny_batch20_greedy_and_graph_replay(torch):
+    """Batch 20 on the tiny model, 6 steps: the decode graph replayed with the
+    device-side pair feedback."""
+    B, n, steps = 20, 24, 6
+    prompts = rspec.prompt_tokens(B, n, TINY.vocab, seed=8)
+    m = _model(TINY, seed=0, max_batch=20, max_latent=12 + steps + 1, prefill_chunk=8)
+    W = O.OracleWeights.generate(TINY, seed=0, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log)
     rep.check()
     m.close()
 

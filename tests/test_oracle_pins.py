@@ -82,6 +82,29 @@ def test_rms_norm_matches_torch_and_is_scale_invariant():
     np.testing.assert_allclose(O.rms_norm(7.5 * x, g, 0.0), O.rms_norm(x, g, 0.0), rtol=1e-12)
 
 
+def test_oracle_bf16_rounding_matches_torch():
+    x = np.random.default_rng(15).standard_normal(10000) * np.exp(np.random.default_rng(16).uniform(-20, 20, 10000))
+    x = np.concatenate([x, [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -0.0, 0.0]])
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.to_bf16(x), ref)
+
+
+def test_kv_bf16_rounds_exactly_the_cached_keys_and_values(small_w):
+    """With the bf16 KV cache, the cached K and V are the bf16 roundings of the
+    float64 ones, and the rounding changes the outputs only slightly."""
+    Z = np.random.default_rng(17).standard_normal((7, SMALL.hidden))
+    X, c64 = O.backbone_full(small_w, Z)
+    Xb, cb = O.backbone_full(small_w, Z, kv_bf16=True)
+    np.testing.assert_array_equal(cb[0][0], O.to_bf16(c64[0][0]))   # layer 0 sees identical inputs
+    np.testing.assert_array_equal(cb[0][1], O.to_bf16(c64[0][1]))
+    assert 0 < np.abs(Xb - X).max() < 1e-2 * np.abs(X).max()
+    # incremental decode with the bf16 cache equals brute force with it
+    caches = [[np.zeros((SMALL.n_kv_heads, 0, SMALL.head_dim))] * 2 for _ in range(SMALL.n_layers)]
+    for p in range(7):
+        h = O.backbone_step(small_w, Z[p], p, caches, kv_bf16=True)
+    np.testing.assert_allclose(h, Xb[-1], rtol=1e-10, atol=1e-12)
+
+
 def test_silu_matches_torch():
     u = np.linspace(-30, 30, 1001)
     np.testing.assert_allclose(O.silu(u), F.silu(torch.from_numpy(u)).numpy(), rtol=1e-13, atol=1e-300)

@@ -27,11 +27,11 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     const int bk = blockIdx.x / S;               // b * n_kv + kvh
     const int b = bk / p.n_kv, kvh = bk - b * p.n_kv;
     const int qpg = p.n_q / p.n_kv;
+    // splits own whole 32-key blocks: split s takes blocks [s*nb/S, (s+1)*nb/S)
     const int len = p.pos[b] + 1;
-    int chunk = (len + S - 1) / S;
-    chunk = (chunk + 31) & ~31;
-    const int k0 = split * chunk;
-    const int k1 = min(len, k0 + chunk);
+    const int nb = (len + 31) >> 5;
+    const int k0 = ((split * nb) / S) * 32;
+    const int k1 = min(len, (((split + 1) * nb) / S) * 32);
     const float scale = 1.4426950408889634f / sqrtf((float)D);
 
     u32x4 qh[NC], ql[NC];
@@ -136,37 +136,43 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     }
 }
 
-// merge: one wave per (sequence, query head): weights exp2(m_s - M), then the
-// weighted sum of the split outputs over L = sum_s w_s l_s, in split order.
+// merge: one workgroup of D threads per (sequence, query head); thread t
+// owns dimension t.  Weights exp2(m_s - M) and L = sum_s w_s l_s, then the
+// weighted sum of the split outputs in split order; every split's value is
+// requested before any is used.
 template <int D>
-__global__ __launch_bounds__(64) void k_attn_merge(AttnDecodeParams p) {
-    __shared__ float s_w[64];
-    const int lane = threadIdx.x;
+__global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
+    constexpr int SMAX = 64;
+    __shared__ float s_w[SMAX];
+    __shared__ float s_inv;
+    const int t = threadIdx.x;
     const int S = p.splits;
     const int bh = blockIdx.x;                        // b * n_q + head
     const float *ph = p.part + (int64_t)bh * S * (D + 2);
-    const float ms = lane < S ? ph[lane * (D + 2) + D] : -INFINITY;
-    const float ls = lane < S ? ph[lane * (D + 2) + D + 1] : 0.f;
-    const float M = wave_max(ms);
-    const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
-    const float L = wave_sum(w * ls);
-    s_w[lane] = w;
-    __syncthreads();
-    const float inv = 1.0f / L;
+    float ov[SMAX];
 #pragma unroll
-    for (int dim = lane; dim < D; dim += 64) {
-        float acc = 0.f;
-#pragma unroll 8
-        for (int sp = 0; sp < S; ++sp) acc += s_w[sp] * ph[sp * (D + 2) + dim];
-        p.out[(int64_t)bh * D + dim] = acc * inv;
+    for (int sp = 0; sp < SMAX; ++sp) ov[sp] = sp < S ? ph[sp * (D + 2) + t] : 0.f;
+    if (t < 64) {
+        const float ms = t < S ? ph[t * (D + 2) + D] : -INFINITY;
+        const float ls = t < S ? ph[t * (D + 2) + D + 1] : 0.f;
+        const float M = wave_max(ms);
+        const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
+        const float L = wave_sum(w * ls);
+        s_w[t] = w;
+        if (t == 0) s_inv = 1.0f / L;
     }
+    __syncthreads();
+    float acc = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < SMAX; ++sp) acc += s_w[sp] * ov[sp];
+    p.out[(int64_t)bh * D + t] = acc * s_inv;
 }
 
 void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s) {
     const int grid = p.B * p.n_kv * p.splits;
     if (p.d == 128) {
         hipLaunchKernelGGL(k_attn_decode<128>, dim3(grid), dim3(64), 0, s, p);
-        hipLaunchKernelGGL(k_attn_merge<128>, dim3(p.B * p.n_q), dim3(64), 0, s, p);
+        hipLaunchKernelGGL(k_attn_merge<128>, dim3(p.B * p.n_q), dim3(128), 0, s, p);
     } else {
         hipLaunchKernelGGL(k_attn_decode<64>, dim3(grid), dim3(64), 0, s, p);
         hipLaunchKernelGGL(k_attn_merge<64>, dim3(p.B * p.n_q), dim3(64), 0, s, p);

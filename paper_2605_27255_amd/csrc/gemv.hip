@@ -117,16 +117,19 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
     const int ks = wave % KS;              // k-split index inside the strip
-    const int strip = blockIdx.x * SPW + wave / KS;
-    const bool sok = strip < nstrips;
-    const bool lead = ks == 0 && sok;      // the wave that reduces and writes the strip
+    // a workgroup handles p.iters consecutive groups of SPW strips (iters > 1
+    // only when X fits in one LDS chunk), staging X once
+    const int iters = p.iters;
+    int strip = (blockIdx.x * iters) * SPW + wave / KS;
+    bool sok = strip < nstrips;
+    bool lead = ks == 0 && sok;            // the wave that reduces and writes the strip
     const int KT = p.K >> 5, HT = p.H >> 5;
     const int B = p.B;
     const int ktpc = p.ktiles_per_chunk;
     const int rstride = ktpc * 32 + 8;
     uint16_t *xs_lo = xs + B * rstride;    // lo plane follows the hi plane
     const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
-    const int row0 = strip * 16 + 4 * g;   // first of this lane's four output rows
+    int row0 = strip * 16 + 4 * g;         // first of this lane's four output rows
 
     // ---- 1. everything the prologue / epilogue read, before any weights -----
     f32x4 resid[NBT];
@@ -252,179 +255,219 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     }
     __syncthreads();
 
+    for (int it = 0; it < iters; ++it) {
     // ---- 4. stream: consume one batch while the next two are in flight ------
-    for (int c0 = 0; c0 < KT; c0 += ktpc) {
-        const int c1 = min(KT, c0 + ktpc);
-        if (c0 > 0) {   // later LDS chunks (batch > ~14 with long K)
-            __syncthreads();
-            const int cpr = (c1 - c0) * 4;
-            for (int idx = threadIdx.x; idx < B * cpr; idx += 512) {
-                const int b = idx / cpr;
-                const int kk = (idx - b * cpr) << 3;
-                XSrc sx;
-                load_src<PRO>(p, b, c0 * 32 + kk, sx);
-                u32x4 vh, vl;
-                make_chunk<PRO>(p, c0 * 32 + kk, sx, vh, vl);
-                *(u32x4 *)(xs + b * rstride + kk) = vh;
-                if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
+        for (int c0 = 0; c0 < KT; c0 += ktpc) {
+            const int c1 = min(KT, c0 + ktpc);
+            if (c0 > 0) {   // later LDS chunks (batch > ~14 with long K)
+                __syncthreads();
+                const int cpr = (c1 - c0) * 4;
+                for (int idx = threadIdx.x; idx < B * cpr; idx += 512) {
+                    const int b = idx / cpr;
+                    const int kk = (idx - b * cpr) << 3;
+                    XSrc sx;
+                    load_src<PRO>(p, b, c0 * 32 + kk, sx);
+                    u32x4 vh, vl;
+                    make_chunk<PRO>(p, c0 * 32 + kk, sx, vh, vl);
+                    *(u32x4 *)(xs + b * rstride + kk) = vh;
+                    if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
+                }
+                __syncthreads();
+                GEMV_ISSUE(0, c0 + ks, c1);
+                GEMV_ISSUE(1, c0 + ks + U * KS, c1);
             }
-            __syncthreads();
-            GEMV_ISSUE(0, c0 + ks, c1);
-            GEMV_ISSUE(1, c0 + ks + U * KS, c1);
+            int kt = c0 + ks;
+            while (kt < c1) {
+                GEMV_CONSUME(0, kt, c0, c1);
+                GEMV_ISSUE(0, kt + 2 * U * KS, c1);
+                kt += U * KS;
+                if (kt >= c1) break;
+                GEMV_CONSUME(1, kt, c0, c1);
+                GEMV_ISSUE(1, kt + 2 * U * KS, c1);
+                kt += U * KS;
+            }
         }
-        int kt = c0 + ks;
-        while (kt < c1) {
-            GEMV_CONSUME(0, kt, c0, c1);
-            GEMV_ISSUE(0, kt + 2 * U * KS, c1);
-            kt += U * KS;
-            if (kt >= c1) break;
-            GEMV_CONSUME(1, kt, c0, c1);
-            GEMV_ISSUE(1, kt + 2 * U * KS, c1);
-            kt += U * KS;
-        }
-    }
-#undef GEMV_ISSUE
-#undef GEMV_CONSUME
-
-    // ---- 5. reduce the KS partial sums of each strip (wave order) -----------
-    f32x4 fin[NBT];
-#pragma unroll
-    for (int bt = 0; bt < NBT; ++bt) {
-        f32x4 v = acc[0][bt];
-        if (NA == 2) {
-            const int b = bt * 16 + j;
-            const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
-            v = v * s0 + acc[NA - 1][bt] * s1;
-        }
-        fin[bt] = v;
-    }
-    if (KS > 1) {
-        f32x4 *red = (f32x4 *)xs;   // [kNW][NBT][64] f32x4, reusing the X chunk
-        __syncthreads();
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
-        __syncthreads();
-        if (ks == 0) {
+    #undef GEMV_ISSUE
+    #undef GEMV_CONSUME
+        // next group's first two batches and residual rows, before this
+        // group's reduction and epilogue
+        f32x4 resid_next[NBT];
+        const int strip_next = strip + SPW;
+        const bool more = it + 1 < iters;
+        if (more) {
+            const bool sok_n = strip_next < nstrips;
+            const uint16_t *wp_n = p.W + (int64_t)(sok_n ? strip_next : 0) * KT * 512 + lane * 8;
 #pragma unroll
             for (int bt = 0; bt < NBT; ++bt) {
-#pragma unroll
-                for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
+                resid_next[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+                const int b = bt * 16 + j;
+                if (EPI == EPI_RESID && ks == 0 && sok_n && b < B)
+                    resid_next[bt] = *(const f32x4 *)(p.out + (int64_t)b * p.N + strip_next * 16 + 4 * g);
             }
-        }
-    }
-    if (EPI != EPI_LOGITS && !lead) return;
-    if (PRO == PRO_NORM) {
 #pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) {
-            const int b = bt * 16 + j;
-            fin[bt] *= (b < B ? sc0[b] : 0.f);
-        }
-    }
-
-    // ---- 6. fused epilogues (one wave per strip) ----------------------------
-    if (EPI == EPI_STORE || EPI == EPI_RESID) {
+            for (int bsel = 0; bsel < 2; ++bsel)
 #pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) {
-            const int b = bt * 16 + j;
-            const bool ok = b < B;
-            f32x4 val = fin[bt];
-            if (EPI == EPI_RESID) val += resid[bt];
-            else if (p.bias) val += *(const f32x4 *)(p.bias + row0);
-            if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = val;
-            float sq = val[0] * val[0] + val[1] * val[1] + val[2] * val[2] + val[3] * val[3];
-            sq = col_sum(sq);
-            if (ok && g == 0 && p.ss_out) p.ss_out[b * nstrips + strip] = sq;
-        }
-    } else if (EPI == EPI_SWIGLU) {
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) {
-            const int b = bt * 16 + j;
-            f32x4 up;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) up[v] = __shfl_xor(fin[bt][v], 32);
-            if (b < B && g < 2) {
-                const f32x4 ga = fin[bt];
-                f32x4 w;
-#pragma unroll
-                for (int v = 0; v < 4; ++v) w[v] = silu_f(ga[v]) * up[v];
-                *(f32x4 *)(p.act + (int64_t)b * (p.N >> 1) + strip * 8 + 4 * g) = w;
-            }
-        }
-    } else if (EPI == EPI_QKV) {
-        const int d = p.d, hs = d >> 4;             // strips per head
-        const int qs = p.n_q * hs, kvs = p.n_kv * hs;
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) {
-            const int b = bt * 16 + j;
-            f32x4 other;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(fin[bt][v], 32);
-            if (b >= B) continue;
-            const int pos = p.pos[b];
-            if (strip < qs + kvs) {
-                const bool isq = strip < qs;
-                const int sidx = isq ? strip : strip - qs;
-                const int head = sidx / hs, t = sidx - head * hs;
-                const int jr = 8 * t + 4 * (g & 1);         // rotation index of v = 0
-                const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
-                const float4 cs = *(const float4 *)(p.rope_cos + (int64_t)pos * (d >> 1) + jr);
-                const float4 sn = *(const float4 *)(p.rope_sin + (int64_t)pos * (d >> 1) + jr);
-                const float c4[4] = {cs.x, cs.y, cs.z, cs.w}, s4[4] = {sn.x, sn.y, sn.z, sn.w};
-                float r[4];
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    r[v] = (g < 2) ? fin[bt][v] * c4[v] - other[v] * s4[v] : fin[bt][v] * c4[v] + other[v] * s4[v];
-                if (isq) {
-                    *(f32x4 *)(p.q + ((int64_t)b * p.n_q + head) * d + dim0) = f32x4{r[0], r[1], r[2], r[3]};
-                } else {
-                    u32x2 w;
-                    w[0] = pack_bf2(r[0], r[1]);
-                    w[1] = pack_bf2(r[2], r[3]);
-                    *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
+                for (int u = 0; u < U; ++u) {
+                    const int kt_ = ks + bsel * U * KS + u * KS;
+                    if (kt_ < KT && sok_n)
+                        ra[bsel][u] = __builtin_nontemporal_load((const u32x4 *)(wp_n + (int64_t)kt_ * 512));
                 }
-            } else {
-                const int r0 = (strip - qs - kvs) * 16 + 4 * g;
-                const int kvh = r0 / d, dim = r0 - kvh * d;
-                uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
-                                ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot(pos & 31);
-#pragma unroll
-                for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(fin[bt][v]);
-            }
         }
-    } else if (EPI == EPI_LOGITS) {
-        // every wave reaches here; waves without a strip contribute key 0
-        __shared__ uint64_t s_best[kNW][32];
-#pragma unroll
+    // ---- 5. reduce the KS partial sums of each strip (wave order) -----------
+        f32x4 fin[NBT];
+    #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
-            const int b = bt * 16 + j;
-            const bool ok = lead && b < B;
-            if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = fin[bt];
-            if (p.best) {
-                uint64_t key = 0;
-                if (ok) {
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const uint64_t kv = argmax_key(fin[bt][v], (uint32_t)(row0 + v));
-                        key = kv > key ? kv : key;
-                    }
-                }
-                uint64_t o = shfl_xor_u64(key, 16);
-                key = o > key ? o : key;
-                o = shfl_xor_u64(key, 32);
-                key = o > key ? o : key;
-                if (g == 0) s_best[wave][b] = key;
+            f32x4 v = acc[0][bt];
+            if (NA == 2) {
+                const int b = bt * 16 + j;
+                const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
+                v = v * s0 + acc[NA - 1][bt] * s1;
             }
+            fin[bt] = v;
         }
-        if (p.best) {
+        if (KS > 1) {
+            f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * B * rstride);   // [kNW][NBT][64] f32x4 after X
             __syncthreads();
-            if (threadIdx.x < B) {
-                uint64_t m = 0;
-#pragma unroll
-                for (int w = 0; w < kNW; ++w) m = s_best[w][threadIdx.x] > m ? s_best[w][threadIdx.x] : m;
-                if (m) atomicMax((unsigned long long *)(p.best + threadIdx.x), (unsigned long long)m);
+    #pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
+            __syncthreads();
+            if (ks == 0) {
+    #pragma unroll
+                for (int bt = 0; bt < NBT; ++bt) {
+    #pragma unroll
+                    for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
+                }
             }
         }
-    }
+        if (EPI == EPI_LOGITS || lead) {
+        if (PRO == PRO_NORM) {
+    #pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                fin[bt] *= (b < B ? sc0[b] : 0.f);
+            }
+        }
+    // ---- 6. fused epilogues (one wave per strip) ----------------------------
+        if (EPI == EPI_STORE || EPI == EPI_RESID) {
+    #pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                const bool ok = b < B;
+                f32x4 val = fin[bt];
+                if (EPI == EPI_RESID) val += resid[bt];
+                else if (p.bias) val += *(const f32x4 *)(p.bias + row0);
+                if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = val;
+                float sq = val[0] * val[0] + val[1] * val[1] + val[2] * val[2] + val[3] * val[3];
+                sq = col_sum(sq);
+                if (ok && g == 0 && p.ss_out) p.ss_out[b * nstrips + strip] = sq;
+            }
+        } else if (EPI == EPI_SWIGLU) {
+    #pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                f32x4 up;
+    #pragma unroll
+                for (int v = 0; v < 4; ++v) up[v] = __shfl_xor(fin[bt][v], 32);
+                if (b < B && g < 2) {
+                    const f32x4 ga = fin[bt];
+                    f32x4 w;
+    #pragma unroll
+                    for (int v = 0; v < 4; ++v) w[v] = silu_f(ga[v]) * up[v];
+                    *(f32x4 *)(p.act + (int64_t)b * (p.N >> 1) + strip * 8 + 4 * g) = w;
+                }
+            }
+        } else if (EPI == EPI_QKV) {
+            const int d = p.d, hs = d >> 4;             // strips per head
+            const int qs = p.n_q * hs, kvs = p.n_kv * hs;
+    #pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                f32x4 other;
+    #pragma unroll
+                for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(fin[bt][v], 32);
+                if (b >= B) continue;
+                const int pos = p.pos[b];
+                if (strip < qs + kvs) {
+                    const bool isq = strip < qs;
+                    const int sidx = isq ? strip : strip - qs;
+                    const int head = sidx / hs, t = sidx - head * hs;
+                    const int jr = 8 * t + 4 * (g & 1);         // rotation index of v = 0
+                    const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
+                    const float4 cs = *(const float4 *)(p.rope_cos + (int64_t)pos * (d >> 1) + jr);
+                    const float4 sn = *(const float4 *)(p.rope_sin + (int64_t)pos * (d >> 1) + jr);
+                    const float c4[4] = {cs.x, cs.y, cs.z, cs.w}, s4[4] = {sn.x, sn.y, sn.z, sn.w};
+                    float r[4];
+    #pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        r[v] = (g < 2) ? fin[bt][v] * c4[v] - other[v] * s4[v] : fin[bt][v] * c4[v] + other[v] * s4[v];
+                    if (isq) {
+                        *(f32x4 *)(p.q + ((int64_t)b * p.n_q + head) * d + dim0) = f32x4{r[0], r[1], r[2], r[3]};
+                    } else {
+                        u32x2 w;
+                        w[0] = pack_bf2(r[0], r[1]);
+                        w[1] = pack_bf2(r[2], r[3]);
+                        *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
+                    }
+                } else {
+                    const int r0 = (strip - qs - kvs) * 16 + 4 * g;
+                    const int kvh = r0 / d, dim = r0 - kvh * d;
+                    uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
+                                    ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot(pos & 31);
+    #pragma unroll
+                    for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(fin[bt][v]);
+                }
+            }
+        } else if (EPI == EPI_LOGITS) {
+            // every wave reaches here; waves without a strip contribute key 0
+            __shared__ uint64_t s_best[kNW][32];
+    #pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                const bool ok = lead && b < B;
+                if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = fin[bt];
+                if (p.best) {
+                    uint64_t key = 0;
+                    if (ok) {
+    #pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            const uint64_t kv = argmax_key(fin[bt][v], (uint32_t)(row0 + v));
+                            key = kv > key ? kv : key;
+                        }
+                    }
+                    uint64_t o = shfl_xor_u64(key, 16);
+                    key = o > key ? o : key;
+                    o = shfl_xor_u64(key, 32);
+                    key = o > key ? o : key;
+                    if (g == 0) s_best[wave][b] = key;
+                }
+            }
+            if (p.best) {
+                __syncthreads();
+                if (threadIdx.x < B) {
+                    uint64_t m = 0;
+    #pragma unroll
+                    for (int w = 0; w < kNW; ++w) m = s_best[w][threadIdx.x] > m ? s_best[w][threadIdx.x] : m;
+                    if (m) atomicMax((unsigned long long *)(p.best + threadIdx.x), (unsigned long long)m);
+                }
+            }
+            __syncthreads();   // s_best is rewritten by the next group
+        }
+        }   // lead
+        // advance to the next group
+#pragma unroll
+        for (int a = 0; a < NA; ++a)
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (more) {
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) resid[bt] = resid_next[bt];
+            strip = strip_next;
+            sok = strip < nstrips;
+            lead = ks == 0 && sok;
+            wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
+            row0 = strip * 16 + 4 * g;
+        }
+    }   // groups
 }
 
 template <int NBT, int KS, int PRO, int EPI>
@@ -435,11 +478,13 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     int ktpc = (kGemvLdsBytes / (2 * planes) / q.B - 8) / 32;
     ktpc = ktpc > KT ? KT : ktpc;
     q.ktiles_per_chunk = ktpc;
-    int lds = planes * q.B * (ktpc * 32 + 8) * 2;
-    const int red = kNW * NBT * 64 * 16;
-    lds = lds > red ? lds : red;
+    const int lds = planes * q.B * (ktpc * 32 + 8) * 2 + kNW * NBT * 64 * 16;   // X planes + reduction
     constexpr int SPW = kNW / KS;
-    const int grid = ((q.N >> 4) + SPW - 1) / SPW;
+    const int groups = ((q.N >> 4) + SPW - 1) / SPW;
+    // with X in one LDS chunk, a workgroup takes several strip groups so that
+    // all workgroups are resident at once (two per CU on 256 CUs)
+    q.iters = ktpc >= KT ? (groups + 511) / 512 : 1;
+    const int grid = (groups + q.iters - 1) / q.iters;
     hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI>), dim3(grid), dim3(kNW * 64), lds, s, q);
 }
 

@@ -206,7 +206,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
     // ---- KV cache, RoPE table, activations ------------------------------
     Arena a;
     const int64_t mcap = (int64_t)B * round_up(c->chunk, 32);
-    const int S_att = 32;
+    const int S_att = 64;
     for (int pass = 0; pass < 2; ++pass) {
         a.used = 0;
         c->kc = a.take<uint16_t>((int64_t)c->L * B * c->kv_bstride);
@@ -345,9 +345,15 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     launch_gate(gp, s);
 }
 
+// Key splits of the decode attention: at most two 32-key blocks per split at
+// full capacity (both blocks are prefetched), and no more splits than it takes
+// to give the machine about 1024 waves; at most 64 (the merge kernel's limit).
 static int attn_splits(const pipo_ctx *c, int B) {
-    int sp = 512 / (B * c->nkv);
-    return sp < 1 ? 1 : (sp > 32 ? 32 : sp);
+    const int blocks = (c->cfg.max_latent + 31) / 32;
+    int sp = (blocks + 1) / 2;
+    const int cap = (1024 + B * c->nkv - 1) / (B * c->nkv);
+    sp = sp < cap ? sp : cap;
+    return sp < 1 ? 1 : (sp > 64 ? 64 : sp);
 }
 
 // One pair-decode step (eq. 1 on the pending pair, eq. 2 one position, heads).

@@ -103,114 +103,65 @@ __device__ __forceinline__ void make_chunk(const GemvParams &p, int k, const XSr
     split8(f, vh, vl);
 }
 
-template <int NBT, int KS, int PRO, int EPI, int U = 4>
-__global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
-    // U: k-tiles per wave per load batch (two batches in flight)
-    constexpr int SPW = kNW / KS;          // strips per workgroup
-    constexpr int NA = NAcc<PRO>::n;
-    constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
-    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
-    extern __shared__ __align__(16) uint16_t xs[];
-    __shared__ float sc0[32], sc1[32];
-
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int j = lane & 15, g = lane >> 4;
-    const int nstrips = p.N >> 4;
-    const int ks = wave % KS;              // k-split index inside the strip
-    // a workgroup handles p.iters consecutive groups of SPW strips (iters > 1
-    // only when X fits in one LDS chunk), staging X once
-    const int iters = p.iters;
-    int strip = (blockIdx.x * iters) * SPW + wave / KS;
-    bool sok = strip < nstrips;
-    bool lead = ks == 0 && sok;            // the wave that reduces and writes the strip
-    const int KT = p.K >> 5, HT = p.H >> 5;
-    const int B = p.B;
-    const int ktpc = p.ktiles_per_chunk;
-    const int rstride = ktpc * 32 + 8;
-    uint16_t *xs_lo = xs + B * rstride;    // lo plane follows the hi plane
-    const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
-    int row0 = strip * 16 + 4 * g;         // first of this lane's four output rows
-
-    // ---- 1. everything the prologue / epilogue read, before any weights -----
+// Prologue: everything the first LDS chunk, the RMSNorm scalars and the
+// residual epilogue read, issued as unconditional loads (out-of-range indices
+// are clamped and the values discarded) so that the compiler's wait counts
+// stay exact and never cover the weight loads issued after them.
+template <int NBT, int PRO, int EPI>
+struct Pro {
+    static constexpr int RPW = 2 * NBT;    // RMSNorm rows per wave: b = wave + 8 r
     f32x4 resid[NBT];
+    float ssv[RPW][4];                     // sum-of-squares parts, 4 per lane (nss <= 256)
+    XSrc src[kXR];
+};
+
+template <int NBT, int PRO, int EPI>
+__device__ __forceinline__ void pro_load(const GemvParams &p, Pro<NBT, PRO, EPI> &pr, bool lead,
+                                         int row0, int cpr) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, j = lane & 15;
+    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
 #pragma unroll
     for (int bt = 0; bt < NBT; ++bt) {
-        resid[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
         const int b = bt * 16 + j;
-        if (EPI == EPI_RESID && lead && b < B) resid[bt] = *(const f32x4 *)(p.out + (int64_t)b * p.N + row0);
+        if (EPI == EPI_RESID)
+            pr.resid[bt] = *(const f32x4 *)(p.out + ((lead && b < p.B) ? (int64_t)b * p.N + row0 : 0));
     }
-    const int c1_first = min(KT, ktpc);
-    const int cpr_first = c1_first * 4;    // 8-element chunks per LDS row
-    XSrc src[kXR];
+    if (NORM) {
+#pragma unroll
+        for (int r = 0; r < Pro<NBT, PRO, EPI>::RPW; ++r)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int b = wave + r * kNW, i = lane + 64 * t;
+                pr.ssv[r][t] = p.ss[(b < p.B && i < p.nss) ? b * p.nss + i : 0];
+            }
+    }
 #pragma unroll
     for (int r = 0; r < kXR; ++r) {
-        const int idx = threadIdx.x + r * 512;
-        if (idx < B * cpr_first) {
-            const int b = idx / cpr_first;
-            load_src<PRO>(p, b, (idx - b * cpr_first) << 3, src[r]);
-        }
+        int idx = threadIdx.x + r * 512;
+        idx = idx < p.B * cpr ? idx : 0;
+        const int b = idx / cpr;
+        load_src<PRO>(p, b, (idx - b * cpr) << 3, pr.src[r]);
     }
-    // RMSNorm scalars: wave w sums the partial sums of rows w, w+8, ...
-    float ssr[4] = {0.f, 0.f, 0.f, 0.f};
+}
+
+// RMSNorm scalars into sc0 (and sc1 for the MTP's embedding half), then the
+// first LDS chunk of X (columns [0, 32 * c1)).
+template <int NBT, int PRO, int EPI>
+__device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, PRO, EPI> &pr, int c1,
+                                           uint16_t *xs, uint16_t *xs_lo, int rstride,
+                                           float *sc0, float *sc1) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
+    constexpr bool HASLO = PRO != PRO_PAIR;
+    const int B = p.B, cpr = c1 * 4;
     if (NORM) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
+        for (int r = 0; r < Pro<NBT, PRO, EPI>::RPW; ++r) {
             const int b = wave + r * kNW;
-            if (b < B)
-                for (int i = lane; i < p.nss; i += 64) ssr[r] += p.ss[b * p.nss + i];
-        }
-    }
-
-    // ---- 2. two batches of weight tiles in flight ----------------------------
-    u32x4 ra[2][U];
+            float a = 0.f;
 #pragma unroll
-    for (int bsel = 0; bsel < 2; ++bsel)
-#pragma unroll
-        for (int u = 0; u < U; ++u) ra[bsel][u] = u32x4{0u, 0u, 0u, 0u};
-#define GEMV_ISSUE(BS, kt_first, c1)                                                              \
-    do {                                                                                          \
-        _Pragma("unroll") for (int u = 0; u < U; ++u) {                                           \
-            const int kt_ = (kt_first) + u * KS;                                                  \
-            if (kt_ < (c1) && sok)                                                                \
-                ra[BS][u] = __builtin_nontemporal_load((const u32x4 *)(wp + (int64_t)kt_ * 512)); \
-        }                                                                                         \
-    } while (0)
-    f32x4 acc[NA][NBT];
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#define GEMV_CONSUME(BS, kt_first, c0, c1)                                                        \
-    do {                                                                                          \
-        _Pragma("unroll") for (int u = 0; u < U; ++u) {                                           \
-            const int k2 = (kt_first) + u * KS;                                                   \
-            if (k2 < (c1)) {                                                                      \
-                const bool hi_half = NA == 2 && k2 >= HT;                                         \
-                _Pragma("unroll") for (int bt = 0; bt < NBT; ++bt) {                              \
-                    const int b = bt * 16 + j;                                                    \
-                    u32x4 bop = u32x4{0u, 0u, 0u, 0u}, bol = u32x4{0u, 0u, 0u, 0u};               \
-                    const int xo = b * rstride + (k2 - (c0)) * 32 + g * 8;                        \
-                    if (b < B) {                                                                  \
-                        bop = *(const u32x4 *)(xs + xo);                                          \
-                        if (HASLO) bol = *(const u32x4 *)(xs_lo + xo);                            \
-                    }                                                                             \
-                    f32x4 &ac = hi_half ? acc[NA - 1][bt] : acc[0][bt];                           \
-                    ac = mfma16(ra[BS][u], bop, ac);                                              \
-                    if (HASLO) ac = mfma16(ra[BS][u], bol, ac);                                   \
-                }                                                                                 \
-            }                                                                                     \
-        }                                                                                         \
-    } while (0)
-
-    GEMV_ISSUE(0, ks, c1_first);
-    GEMV_ISSUE(1, ks + U * KS, c1_first);
-
-    // ---- 3. scalars and the first LDS chunk (waits only on step 1's loads) --
-    if (NORM) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int b = wave + r * kNW;
-            const float a = wave_sum(ssr[r]);
+            for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? pr.ssv[r][t] : 0.f;
+            a = wave_sum(a);
             if (b < B && lane == 0) sc0[b] = rsqrtf(a / (float)(PRO == PRO_MTP ? p.H : p.K) + p.eps);
         }
     }
@@ -234,18 +185,18 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 #pragma unroll
     for (int r = 0; r < kXR; ++r) {
         const int idx = threadIdx.x + r * 512;
-        if (idx < B * cpr_first) {
-            const int b = idx / cpr_first;
-            const int kk = (idx - b * cpr_first) << 3;
+        if (idx < B * cpr) {
+            const int b = idx / cpr;
+            const int kk = (idx - b * cpr) << 3;
             u32x4 vh, vl;
-            make_chunk<PRO>(p, kk, src[r], vh, vl);
+            make_chunk<PRO>(p, kk, pr.src[r], vh, vl);
             *(u32x4 *)(xs + b * rstride + kk) = vh;
             if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
         }
     }
-    for (int idx = threadIdx.x + kXR * 512; idx < B * cpr_first; idx += 512) {   // large B only
-        const int b = idx / cpr_first;
-        const int kk = (idx - b * cpr_first) << 3;
+    for (int idx = threadIdx.x + kXR * 512; idx < B * cpr; idx += 512) {   // large B only
+        const int b = idx / cpr;
+        const int kk = (idx - b * cpr) << 3;
         XSrc sx;
         load_src<PRO>(p, b, kk, sx);
         u32x4 vh, vl;
@@ -253,13 +204,132 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
         *(u32x4 *)(xs + b * rstride + kk) = vh;
         if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
     }
-    __syncthreads();
+}
 
-    for (int it = 0; it < iters; ++it) {
-    // ---- 4. stream: consume one batch while the next two are in flight ------
+// acc += W tile x X^T chunk for one 1 KB weight tile (kt is its k-tile, c0 the
+// first k-tile held in LDS); w is already zero for padding tiles.
+template <int NBT, int PRO>
+__device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 w, int kt, int c0, int HT, int B,
+                                         const uint16_t *xs, const uint16_t *xs_lo, int rstride) {
+    constexpr int NA = NAcc<PRO>::n;
+    constexpr bool HASLO = PRO != PRO_PAIR;
+    const int lane = threadIdx.x & 63, j = lane & 15, g = lane >> 4;
+    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) {
+        const int b = bt * 16 + j;
+        const bool bok = b < B;
+        const int xo = (bok ? b : 0) * rstride + (kt - c0) * 32 + g * 8;
+        u32x4 bop = *(const u32x4 *)(xs + xo), bol = zero;
+        if (HASLO) bol = *(const u32x4 *)(xs_lo + xo);
+        bop = bok ? bop : zero;
+        bol = bok ? bol : zero;
+        if (NA == 2) {
+            // MTP: tiles below H/32 act on RMSNorm(h_b), the rest on RMSNorm(E[b])
+            const bool hi_half = kt >= HT;
+            const u32x4 w0 = hi_half ? zero : w, w1 = hi_half ? w : zero;
+            acc[0][bt] = mfma16(w0, bop, acc[0][bt]);
+            acc[0][bt] = mfma16(w0, bol, acc[0][bt]);
+            acc[NA - 1][bt] = mfma16(w1, bop, acc[NA - 1][bt]);
+            acc[NA - 1][bt] = mfma16(w1, bol, acc[NA - 1][bt]);
+        } else {
+            acc[0][bt] = mfma16(w, bop, acc[0][bt]);
+            if (HASLO) acc[0][bt] = mfma16(w, bol, acc[0][bt]);
+        }
+    }
+}
+
+template <int NBT, int KS, int PRO, int EPI, int U, bool ONE>
+__global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
+    // U: k-tiles per wave per load batch (two batches in flight); ONE: X fits
+    // in one LDS chunk (ktiles_per_chunk >= K / 32)
+    constexpr int SPW = kNW / KS;          // strips per workgroup
+    constexpr int NA = NAcc<PRO>::n;
+    constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
+    extern __shared__ __align__(16) uint16_t xs[];
+    __shared__ float sc0[32], sc1[32];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15, g = lane >> 4;
+    const int nstrips = p.N >> 4;
+    const int ks = wave % KS;              // k-split index inside the strip
+    const int strip = blockIdx.x * SPW + wave / KS;
+    const bool sok = strip < nstrips;
+    const bool lead = ks == 0 && sok;      // the wave that reduces and writes the strip
+    const int KT = p.K >> 5, HT = p.H >> 5;
+    const int B = p.B;
+    const int ktpc = p.ktiles_per_chunk;
+    const int rstride = ktpc * 32 + 8;
+    uint16_t *xs_lo = xs + B * rstride;    // lo plane follows the hi plane
+    const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
+    const int row0 = strip * 16 + 4 * g;   // first of this lane's four output rows
+    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+
+    f32x4 acc[NA][NBT];
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // ---- 1. everything the prologue / epilogue read, before any weights -----
+    Pro<NBT, PRO, EPI> pr;
+    const int c1_first = min(KT, ktpc);
+    pro_load<NBT, PRO, EPI>(p, pr, lead, row0, c1_first * 4);
+
+    if (ONE) {
+        // ---- X fits in LDS: one pipelined pass over this wave's tiles ----------
+        // Wave tiles are kt = ks + KS i, i < n.  Loads are unconditional (tiles
+        // past the end read the matrix's first line and are multiplied as
+        // zero), so every batch keeps a fixed load count and the waits before
+        // each batch cover exactly that batch.
+        const int n = (KT - ks + KS - 1) / KS;
+        u32x4 ra[U], rb[U];
+#define GEMV_PTR(i) ((const u32x4 *)((i) < n ? wp + (int64_t)(ks + KS * (i)) * 512 : p.W))
+#pragma unroll
+        for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(u));
+#pragma unroll
+        for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(U + u));
+        // keep the prologue arithmetic (and its waits) after the weight loads
+        __builtin_amdgcn_sched_barrier(0);
+        pro_finish<NBT, PRO, EPI>(p, pr, KT, xs, xs_lo, rstride, sc0, sc1);
+        __syncthreads();
+        const int npair = (n + 2 * U - 1) / (2 * U);
+        int i0 = 0;
+        for (int it = 1; it < npair; ++it) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = i0 + u;
+                tile_mma<NBT, PRO>(acc, i < n ? ra[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 2 * U + u));
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = i0 + U + u;
+                tile_mma<NBT, PRO>(acc, i < n ? rb[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 3 * U + u));
+            i0 += 2 * U;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u;
+            tile_mma<NBT, PRO>(acc, i < n ? ra[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + U + u;
+            tile_mma<NBT, PRO>(acc, i < n ? rb[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
+        }
+#undef GEMV_PTR
+    } else {
+        // ---- X in several LDS chunks (large batch with long K) -----------------
+        // Per chunk: restage X, then stream the chunk's tiles of this wave.
+        pro_finish<NBT, PRO, EPI>(p, pr, c1_first, xs, xs_lo, rstride, sc0, sc1);
         for (int c0 = 0; c0 < KT; c0 += ktpc) {
             const int c1 = min(KT, c0 + ktpc);
-            if (c0 > 0) {   // later LDS chunks (batch > ~14 with long K)
+            if (c0 > 0) {
                 __syncthreads();
                 const int cpr = (c1 - c0) * 4;
                 for (int idx = threadIdx.x; idx < B * cpr; idx += 512) {
@@ -272,205 +342,167 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                     *(u32x4 *)(xs + b * rstride + kk) = vh;
                     if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
                 }
-                __syncthreads();
-                GEMV_ISSUE(0, c0 + ks, c1);
-                GEMV_ISSUE(1, c0 + ks + U * KS, c1);
             }
-            int kt = c0 + ks;
-            while (kt < c1) {
-                GEMV_CONSUME(0, kt, c0, c1);
-                GEMV_ISSUE(0, kt + 2 * U * KS, c1);
-                kt += U * KS;
-                if (kt >= c1) break;
-                GEMV_CONSUME(1, kt, c0, c1);
-                GEMV_ISSUE(1, kt + 2 * U * KS, c1);
-                kt += U * KS;
-            }
-        }
-    #undef GEMV_ISSUE
-    #undef GEMV_CONSUME
-        // next group's first two batches and residual rows, before this
-        // group's reduction and epilogue
-        f32x4 resid_next[NBT];
-        const int strip_next = strip + SPW;
-        const bool more = it + 1 < iters;
-        if (more) {
-            const bool sok_n = strip_next < nstrips;
-            const uint16_t *wp_n = p.W + (int64_t)(sok_n ? strip_next : 0) * KT * 512 + lane * 8;
-#pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) {
-                resid_next[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-                const int b = bt * 16 + j;
-                if (EPI == EPI_RESID && ks == 0 && sok_n && b < B)
-                    resid_next[bt] = *(const f32x4 *)(p.out + (int64_t)b * p.N + strip_next * 16 + 4 * g);
-            }
-#pragma unroll
-            for (int bsel = 0; bsel < 2; ++bsel)
+            __syncthreads();
+            for (int kt0 = c0 + ks; kt0 < c1; kt0 += U * KS) {
+                u32x4 rr[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    const int kt_ = ks + bsel * U * KS + u * KS;
-                    if (kt_ < KT && sok_n)
-                        ra[bsel][u] = __builtin_nontemporal_load((const u32x4 *)(wp_n + (int64_t)kt_ * 512));
+                    const int kt = kt0 + u * KS;
+                    rr[u] = __builtin_nontemporal_load((const u32x4 *)(kt < c1 ? wp + (int64_t)kt * 512 : p.W));
                 }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int kt = kt0 + u * KS;
+                    tile_mma<NBT, PRO>(acc, kt < c1 ? rr[u] : zero, kt < c1 ? kt : c0, c0, HT, B, xs, xs_lo, rstride);
+                }
+            }
         }
-    // ---- 5. reduce the KS partial sums of each strip (wave order) -----------
-        f32x4 fin[NBT];
-    #pragma unroll
+    }
+
+    // ---- 3. reduce the KS partial sums of each strip (wave order) -----------
+    f32x4 fin[NBT];
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) {
+        f32x4 v = acc[0][bt];
+        if (NA == 2) {
+            const int b = bt * 16 + j;
+            const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
+            v = v * s0 + acc[NA - 1][bt] * s1;
+        }
+        fin[bt] = v;
+    }
+    if (KS > 1) {
+        f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * B * rstride);   // [kNW][NBT][64] f32x4 after X
+        __syncthreads();
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
+        __syncthreads();
+        if (ks == 0) {
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+#pragma unroll
+                for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
+            }
+        }
+    }
+    if (PRO == PRO_NORM) {
+#pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
-            f32x4 v = acc[0][bt];
-            if (NA == 2) {
-                const int b = bt * 16 + j;
-                const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
-                v = v * s0 + acc[NA - 1][bt] * s1;
-            }
-            fin[bt] = v;
+            const int b = bt * 16 + j;
+            fin[bt] *= (b < B ? sc0[b] : 0.f);
         }
-        if (KS > 1) {
-            f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * B * rstride);   // [kNW][NBT][64] f32x4 after X
-            __syncthreads();
-    #pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
-            __syncthreads();
-            if (ks == 0) {
-    #pragma unroll
-                for (int bt = 0; bt < NBT; ++bt) {
-    #pragma unroll
-                    for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
-                }
-            }
-        }
-        if (EPI == EPI_LOGITS || lead) {
-        if (PRO == PRO_NORM) {
-    #pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) {
-                const int b = bt * 16 + j;
-                fin[bt] *= (b < B ? sc0[b] : 0.f);
-            }
-        }
-    // ---- 6. fused epilogues (one wave per strip) ----------------------------
-        if (EPI == EPI_STORE || EPI == EPI_RESID) {
-    #pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) {
-                const int b = bt * 16 + j;
-                const bool ok = b < B;
-                f32x4 val = fin[bt];
-                if (EPI == EPI_RESID) val += resid[bt];
-                else if (p.bias) val += *(const f32x4 *)(p.bias + row0);
-                if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = val;
-                float sq = val[0] * val[0] + val[1] * val[1] + val[2] * val[2] + val[3] * val[3];
-                sq = col_sum(sq);
-                if (ok && g == 0 && p.ss_out) p.ss_out[b * nstrips + strip] = sq;
-            }
-        } else if (EPI == EPI_SWIGLU) {
-    #pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) {
-                const int b = bt * 16 + j;
-                f32x4 up;
-    #pragma unroll
-                for (int v = 0; v < 4; ++v) up[v] = __shfl_xor(fin[bt][v], 32);
-                if (b < B && g < 2) {
-                    const f32x4 ga = fin[bt];
-                    f32x4 w;
-    #pragma unroll
-                    for (int v = 0; v < 4; ++v) w[v] = silu_f(ga[v]) * up[v];
-                    *(f32x4 *)(p.act + (int64_t)b * (p.N >> 1) + strip * 8 + 4 * g) = w;
-                }
-            }
-        } else if (EPI == EPI_QKV) {
-            const int d = p.d, hs = d >> 4;             // strips per head
-            const int qs = p.n_q * hs, kvs = p.n_kv * hs;
-    #pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) {
-                const int b = bt * 16 + j;
-                f32x4 other;
-    #pragma unroll
-                for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(fin[bt][v], 32);
-                if (b >= B) continue;
-                const int pos = p.pos[b];
-                if (strip < qs + kvs) {
-                    const bool isq = strip < qs;
-                    const int sidx = isq ? strip : strip - qs;
-                    const int head = sidx / hs, t = sidx - head * hs;
-                    const int jr = 8 * t + 4 * (g & 1);         // rotation index of v = 0
-                    const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
-                    const float4 cs = *(const float4 *)(p.rope_cos + (int64_t)pos * (d >> 1) + jr);
-                    const float4 sn = *(const float4 *)(p.rope_sin + (int64_t)pos * (d >> 1) + jr);
-                    const float c4[4] = {cs.x, cs.y, cs.z, cs.w}, s4[4] = {sn.x, sn.y, sn.z, sn.w};
-                    float r[4];
-    #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        r[v] = (g < 2) ? fin[bt][v] * c4[v] - other[v] * s4[v] : fin[bt][v] * c4[v] + other[v] * s4[v];
-                    if (isq) {
-                        *(f32x4 *)(p.q + ((int64_t)b * p.n_q + head) * d + dim0) = f32x4{r[0], r[1], r[2], r[3]};
-                    } else {
-                        u32x2 w;
-                        w[0] = pack_bf2(r[0], r[1]);
-                        w[1] = pack_bf2(r[2], r[3]);
-                        *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
-                    }
-                } else {
-                    const int r0 = (strip - qs - kvs) * 16 + 4 * g;
-                    const int kvh = r0 / d, dim = r0 - kvh * d;
-                    uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
-                                    ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot(pos & 31);
-    #pragma unroll
-                    for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(fin[bt][v]);
-                }
-            }
-        } else if (EPI == EPI_LOGITS) {
-            // every wave reaches here; waves without a strip contribute key 0
-            __shared__ uint64_t s_best[kNW][32];
-    #pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) {
-                const int b = bt * 16 + j;
-                const bool ok = lead && b < B;
-                if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = fin[bt];
-                if (p.best) {
-                    uint64_t key = 0;
-                    if (ok) {
-    #pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            const uint64_t kv = argmax_key(fin[bt][v], (uint32_t)(row0 + v));
-                            key = kv > key ? kv : key;
-                        }
-                    }
-                    uint64_t o = shfl_xor_u64(key, 16);
-                    key = o > key ? o : key;
-                    o = shfl_xor_u64(key, 32);
-                    key = o > key ? o : key;
-                    if (g == 0) s_best[wave][b] = key;
-                }
-            }
+    }
+    // ---- 4. fused epilogues (one wave per strip) ----------------------------
+    if (EPI == EPI_LOGITS) {
+        // every wave reaches here; waves without a strip contribute key 0
+        __shared__ uint64_t s_best[kNW][32];
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            const bool ok = lead && b < B;
+            if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = fin[bt];
             if (p.best) {
-                __syncthreads();
-                if (threadIdx.x < B) {
-                    uint64_t m = 0;
-    #pragma unroll
-                    for (int w = 0; w < kNW; ++w) m = s_best[w][threadIdx.x] > m ? s_best[w][threadIdx.x] : m;
-                    if (m) atomicMax((unsigned long long *)(p.best + threadIdx.x), (unsigned long long)m);
+                uint64_t key = 0;
+                if (ok) {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const uint64_t kv = argmax_key(fin[bt][v], (uint32_t)(row0 + v));
+                        key = kv > key ? kv : key;
+                    }
                 }
+                uint64_t o = shfl_xor_u64(key, 16);
+                key = o > key ? o : key;
+                o = shfl_xor_u64(key, 32);
+                key = o > key ? o : key;
+                if (g == 0) s_best[wave][b] = key;
             }
-            __syncthreads();   // s_best is rewritten by the next group
         }
-        }   // lead
-        // advance to the next group
+        if (p.best) {
+            __syncthreads();
+            if (threadIdx.x < B) {
+                uint64_t m = 0;
 #pragma unroll
-        for (int a = 0; a < NA; ++a)
-#pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (more) {
-#pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) resid[bt] = resid_next[bt];
-            strip = strip_next;
-            sok = strip < nstrips;
-            lead = ks == 0 && sok;
-            wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
-            row0 = strip * 16 + 4 * g;
+                for (int w = 0; w < kNW; ++w) m = s_best[w][threadIdx.x] > m ? s_best[w][threadIdx.x] : m;
+                if (m) atomicMax((unsigned long long *)(p.best + threadIdx.x), (unsigned long long)m);
+            }
         }
-    }   // groups
+        return;
+    }
+    if (!lead) return;
+    if (EPI == EPI_STORE || EPI == EPI_RESID) {
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            const bool ok = b < B;
+            f32x4 val = fin[bt];
+            if (EPI == EPI_RESID) val += pr.resid[bt];
+            else if (p.bias) val += *(const f32x4 *)(p.bias + row0);
+            if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = val;
+            float sq = val[0] * val[0] + val[1] * val[1] + val[2] * val[2] + val[3] * val[3];
+            sq = col_sum(sq);
+            if (ok && g == 0 && p.ss_out) p.ss_out[b * nstrips + strip] = sq;
+        }
+    } else if (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            f32x4 up;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) up[v] = __shfl_xor(fin[bt][v], 32);
+            if (b < B && g < 2) {
+                const f32x4 ga = fin[bt];
+                f32x4 w;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) w[v] = silu_f(ga[v]) * up[v];
+                *(f32x4 *)(p.act + (int64_t)b * (p.N >> 1) + strip * 8 + 4 * g) = w;
+            }
+        }
+    } else if (EPI == EPI_QKV) {
+        const int d = p.d, hs = d >> 4;             // strips per head
+        const int qs = p.n_q * hs, kvs = p.n_kv * hs;
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            f32x4 other;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(fin[bt][v], 32);
+            if (b >= B) continue;
+            const int pos = p.pos[b];
+            if (strip < qs + kvs) {
+                const bool isq = strip < qs;
+                const int sidx = isq ? strip : strip - qs;
+                const int head = sidx / hs, t = sidx - head * hs;
+                const int jr = 8 * t + 4 * (g & 1);         // rotation index of v = 0
+                const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
+                const float4 cs = *(const float4 *)(p.rope_cos + (int64_t)pos * (d >> 1) + jr);
+                const float4 sn = *(const float4 *)(p.rope_sin + (int64_t)pos * (d >> 1) + jr);
+                const float c4[4] = {cs.x, cs.y, cs.z, cs.w}, s4[4] = {sn.x, sn.y, sn.z, sn.w};
+                float r[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    r[v] = (g < 2) ? fin[bt][v] * c4[v] - other[v] * s4[v] : fin[bt][v] * c4[v] + other[v] * s4[v];
+                if (isq) {
+                    *(f32x4 *)(p.q + ((int64_t)b * p.n_q + head) * d + dim0) = f32x4{r[0], r[1], r[2], r[3]};
+                } else {
+                    u32x2 w;
+                    w[0] = pack_bf2(r[0], r[1]);
+                    w[1] = pack_bf2(r[2], r[3]);
+                    *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
+                }
+            } else {
+                const int r0 = (strip - qs - kvs) * 16 + 4 * g;
+                const int kvh = r0 / d, dim = r0 - kvh * d;
+                uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
+                                ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot(pos & 31);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(fin[bt][v]);
+            }
+        }
+    }
 }
 
-template <int NBT, int KS, int PRO, int EPI>
+template <int NBT, int KS, int PRO, int EPI, int U>
 static void launch_t(const GemvParams &p, hipStream_t s) {
     GemvParams q = p;
     const int KT = q.K >> 5;
@@ -478,20 +510,28 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     int ktpc = (kGemvLdsBytes / (2 * planes) / q.B - 8) / 32;
     ktpc = ktpc > KT ? KT : ktpc;
     q.ktiles_per_chunk = ktpc;
+    q.iters = 1;
     const int lds = planes * q.B * (ktpc * 32 + 8) * 2 + kNW * NBT * 64 * 16;   // X planes + reduction
     constexpr int SPW = kNW / KS;
-    const int groups = ((q.N >> 4) + SPW - 1) / SPW;
-    // with X in one LDS chunk, a workgroup takes several strip groups so that
-    // all workgroups are resident at once (two per CU on 256 CUs)
-    q.iters = ktpc >= KT ? (groups + 511) / 512 : 1;
-    const int grid = (groups + q.iters - 1) / q.iters;
-    hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI>), dim3(grid), dim3(kNW * 64), lds, s, q);
+    const int grid = ((q.N >> 4) + SPW - 1) / SPW;
+    if (ktpc >= KT) hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U, true>), dim3(grid), dim3(kNW * 64), lds, s, q);
+    else hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, 4, false>), dim3(grid), dim3(kNW * 64), lds, s, q);
+}
+
+// Batch size U: two batches of U tiles per wave are in flight.  Five when a
+// wave's tile count is a multiple of ten (K = 2560 with an eight-way split:
+// no padding tiles), four otherwise.
+template <int NBT, int KS, int PRO, int EPI>
+static void launch_u(const GemvParams &p, hipStream_t s) {
+    const int n = ((p.K >> 5) + KS - 1) / KS;
+    if (n % 10 == 0) launch_t<NBT, KS, PRO, EPI, 5>(p, s);
+    else launch_t<NBT, KS, PRO, EPI, 4>(p, s);
 }
 
 template <int KS, int PRO, int EPI>
 static void launch_nbt(const GemvParams &p, hipStream_t s) {
-    if (p.B <= 16) launch_t<1, KS, PRO, EPI>(p, s);
-    else launch_t<2, KS, PRO, EPI>(p, s);
+    if (p.B <= 16) launch_u<1, KS, PRO, EPI>(p, s);
+    else launch_u<2, KS, PRO, EPI>(p, s);
 }
 
 int gemv_num_groups(int N) { return N >> 4; }

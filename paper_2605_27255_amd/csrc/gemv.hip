@@ -24,7 +24,8 @@
 namespace pipo {
 
 constexpr int kNW = 8;                       // waves per workgroup
-constexpr int kGemvLdsBytes = 56 * 1024;     // dynamic LDS budget for the X chunk
+constexpr int kGemvLdsBytes = 56 * 1024;     // dynamic LDS budget for a shared X chunk
+constexpr int kGemvOneLdsBytes = 72 * 1024;  // budget for wave-private X (two workgroups per CU)
 constexpr int kXR = 3;                       // prologue chunks per thread loaded ahead of the weights
 
 __device__ __forceinline__ float silu_f(float u) { return u / (1.0f + __expf(-u)); }
@@ -103,6 +104,37 @@ __device__ __forceinline__ void make_chunk(const GemvParams &p, int k, const XSr
     split8(f, vh, vl);
 }
 
+// Where the 8-element chunks of X go in LDS.
+//  shared (several LDS chunks, large batch): the workgroup stages columns
+//    [32 c0, 32 c1) of every row cooperatively, row b at b * rstride.
+//  private (X fits): wave (strip, ks) multiplies only k-tiles ks + KS i, so it
+//    stages exactly those 32-column slices in its own region, row b at
+//    b * rstride, slice i at 32 i; no other wave reads them and no workgroup
+//    barrier is needed before the first MFMA.
+struct ChunkMap {
+    bool priv;
+    int per_row;        // chunks per row
+    int count;          // chunks in total
+    int ks, KS, KT;     // private: this wave's k-split
+    int rstride;
+    __device__ __forceinline__ int first() const { return priv ? (threadIdx.x & 63) : threadIdx.x; }
+    __device__ __forceinline__ int step() const { return priv ? 64 : 512; }
+    // chunk idx -> row b, global column k, LDS element offset (relative to the plane base)
+    __device__ __forceinline__ void map(int idx, int &b, int &k, int &off) const {
+        b = idx / per_row;
+        const int rem = idx - b * per_row;
+        if (priv) {
+            const int i = rem >> 2, q = rem & 3;
+            const int kt = ks + KS * i;
+            k = (kt < KT ? kt * 32 : 0) + q * 8;
+            off = b * rstride + i * 32 + q * 8;
+        } else {
+            k = rem << 3;
+            off = b * rstride + k;
+        }
+    }
+};
+
 // Prologue: everything the first LDS chunk, the RMSNorm scalars and the
 // residual epilogue read, issued as unconditional loads (out-of-range indices
 // are clamped and the values discarded) so that the compiler's wait counts
@@ -117,7 +149,7 @@ struct Pro {
 
 template <int NBT, int PRO, int EPI>
 __device__ __forceinline__ void pro_load(const GemvParams &p, Pro<NBT, PRO, EPI> &pr, bool lead,
-                                         int row0, int cpr) {
+                                         int row0, const ChunkMap &cm, int col0) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, j = lane & 15;
     constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
 #pragma unroll
@@ -137,23 +169,23 @@ __device__ __forceinline__ void pro_load(const GemvParams &p, Pro<NBT, PRO, EPI>
     }
 #pragma unroll
     for (int r = 0; r < kXR; ++r) {
-        int idx = threadIdx.x + r * 512;
-        idx = idx < p.B * cpr ? idx : 0;
-        const int b = idx / cpr;
-        load_src<PRO>(p, b, (idx - b * cpr) << 3, pr.src[r]);
+        int idx = cm.first() + r * cm.step();
+        idx = idx < cm.count ? idx : 0;
+        int b, k, off;
+        cm.map(idx, b, k, off);
+        load_src<PRO>(p, b, col0 + k, pr.src[r]);
     }
 }
 
 // RMSNorm scalars into sc0 (and sc1 for the MTP's embedding half), then the
-// first LDS chunk of X (columns [0, 32 * c1)).
+// chunks of X this thread loaded (and any beyond kXR per thread).
 template <int NBT, int PRO, int EPI>
-__device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, PRO, EPI> &pr, int c1,
-                                           uint16_t *xs, uint16_t *xs_lo, int rstride,
-                                           float *sc0, float *sc1) {
+__device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, PRO, EPI> &pr, const ChunkMap &cm,
+                                           int col0, uint16_t *xh, uint16_t *xl, float *sc0, float *sc1) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
     constexpr bool HASLO = PRO != PRO_PAIR;
-    const int B = p.B, cpr = c1 * 4;
+    const int B = p.B;
     if (NORM) {
 #pragma unroll
         for (int r = 0; r < Pro<NBT, PRO, EPI>::RPW; ++r) {
@@ -184,32 +216,33 @@ __device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, P
     }
 #pragma unroll
     for (int r = 0; r < kXR; ++r) {
-        const int idx = threadIdx.x + r * 512;
-        if (idx < B * cpr) {
-            const int b = idx / cpr;
-            const int kk = (idx - b * cpr) << 3;
+        const int idx = cm.first() + r * cm.step();
+        if (idx < cm.count) {
+            int b, k, off;
+            cm.map(idx, b, k, off);
             u32x4 vh, vl;
-            make_chunk<PRO>(p, kk, pr.src[r], vh, vl);
-            *(u32x4 *)(xs + b * rstride + kk) = vh;
-            if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
+            make_chunk<PRO>(p, col0 + k, pr.src[r], vh, vl);
+            *(u32x4 *)(xh + off) = vh;
+            if (HASLO) *(u32x4 *)(xl + off) = vl;
         }
     }
-    for (int idx = threadIdx.x + kXR * 512; idx < B * cpr; idx += 512) {   // large B only
-        const int b = idx / cpr;
-        const int kk = (idx - b * cpr) << 3;
+    for (int idx = cm.first() + kXR * cm.step(); idx < cm.count; idx += cm.step()) {   // large B only
+        int b, k, off;
+        cm.map(idx, b, k, off);
         XSrc sx;
-        load_src<PRO>(p, b, kk, sx);
+        load_src<PRO>(p, b, col0 + k, sx);
         u32x4 vh, vl;
-        make_chunk<PRO>(p, kk, sx, vh, vl);
-        *(u32x4 *)(xs + b * rstride + kk) = vh;
-        if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
+        make_chunk<PRO>(p, col0 + k, sx, vh, vl);
+        *(u32x4 *)(xh + off) = vh;
+        if (HASLO) *(u32x4 *)(xl + off) = vl;
     }
 }
 
-// acc += W tile x X^T chunk for one 1 KB weight tile (kt is its k-tile, c0 the
-// first k-tile held in LDS); w is already zero for padding tiles.
+// acc += W tile x X^T chunk for one 1 KB weight tile: kt is its k-tile, xcol
+// the LDS column where its 32 columns of X start; w is already zero for
+// padding tiles.
 template <int NBT, int PRO>
-__device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 w, int kt, int c0, int HT, int B,
+__device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 w, int kt, int xcol, int HT, int B,
                                          const uint16_t *xs, const uint16_t *xs_lo, int rstride) {
     constexpr int NA = NAcc<PRO>::n;
     constexpr bool HASLO = PRO != PRO_PAIR;
@@ -219,7 +252,7 @@ __device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 
     for (int bt = 0; bt < NBT; ++bt) {
         const int b = bt * 16 + j;
         const bool bok = b < B;
-        const int xo = (bok ? b : 0) * rstride + (kt - c0) * 32 + g * 8;
+        const int xo = (bok ? b : 0) * rstride + xcol + g * 8;
         u32x4 bop = *(const u32x4 *)(xs + xo), bol = zero;
         if (HASLO) bol = *(const u32x4 *)(xs_lo + xo);
         bop = bok ? bop : zero;
@@ -241,8 +274,10 @@ __device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 
 
 template <int NBT, int KS, int PRO, int EPI, int U, bool ONE>
 __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
-    // U: k-tiles per wave per load batch (two batches in flight); ONE: X fits
-    // in one LDS chunk (ktiles_per_chunk >= K / 32)
+    // U: k-tiles per wave per load batch (two batches in flight).  ONE: every
+    // wave's slices of X fit in LDS at once (wave-private staging); otherwise
+    // the workgroup stages X in shared chunks of ktiles_per_chunk k-tiles.
+    static_assert(KS > 1, "the strip reduction orders the RMSNorm scalars");
     constexpr int SPW = kNW / KS;          // strips per workgroup
     constexpr int NA = NAcc<PRO>::n;
     constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
@@ -258,12 +293,20 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     const bool lead = ks == 0 && sok;      // the wave that reduces and writes the strip
     const int KT = p.K >> 5, HT = p.H >> 5;
     const int B = p.B;
-    const int ktpc = p.ktiles_per_chunk;
-    const int rstride = ktpc * 32 + 8;
-    uint16_t *xs_lo = xs + B * rstride;    // lo plane follows the hi plane
     const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
     const int row0 = strip * 16 + 4 * g;   // first of this lane's four output rows
     const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+    // LDS: X hi planes, X lo planes, then the reduction buffer
+    int rstride, xplane;                   // row stride of a plane; elements per plane set
+    if (ONE) {
+        const int nmax = (KT + KS - 1) / KS;
+        rstride = nmax * 32 + 8;
+        xplane = kNW * B * rstride;
+    } else {
+        rstride = p.ktiles_per_chunk * 32 + 8;
+        xplane = B * rstride;
+    }
+    f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * xplane);   // [kNW][NBT][64] f32x4
 
     f32x4 acc[NA][NBT];
 #pragma unroll
@@ -271,18 +314,20 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // ---- 1. everything the prologue / epilogue read, before any weights -----
     Pro<NBT, PRO, EPI> pr;
-    const int c1_first = min(KT, ktpc);
-    pro_load<NBT, PRO, EPI>(p, pr, lead, row0, c1_first * 4);
-
     if (ONE) {
-        // ---- X fits in LDS: one pipelined pass over this wave's tiles ----------
+        // ---- wave-private X, one pipelined pass over this wave's tiles ----------
         // Wave tiles are kt = ks + KS i, i < n.  Loads are unconditional (tiles
         // past the end read the matrix's first line and are multiplied as
         // zero), so every batch keeps a fixed load count and the waits before
         // each batch cover exactly that batch.
         const int n = (KT - ks + KS - 1) / KS;
+        const int nmax = (KT + KS - 1) / KS;
+        ChunkMap cm{true, nmax * 4, B * nmax * 4, ks, KS, KT, rstride};
+        uint16_t *xh = xs + wave * B * rstride, *xl = xh + xplane;
+        // 1. prologue / epilogue inputs, before any weights
+        pro_load<NBT, PRO, EPI>(p, pr, lead, row0, cm, 0);
+        // 2. two batches of weights
         u32x4 ra[U], rb[U];
 #define GEMV_PTR(i) ((const u32x4 *)((i) < n ? wp + (int64_t)(ks + KS * (i)) * 512 : p.W))
 #pragma unroll
@@ -291,42 +336,41 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
         for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(U + u));
         // keep the prologue arithmetic (and its waits) after the weight loads
         __builtin_amdgcn_sched_barrier(0);
-        pro_finish<NBT, PRO, EPI>(p, pr, KT, xs, xs_lo, rstride, sc0, sc1);
-        __syncthreads();
+        // 3. scalars and this wave's slices of X; the MTP scales its halves
+        //    before the reduction, so it waits for every wave's scalars
+        pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
+        if (PRO == PRO_MTP) __syncthreads();
+        // 4. stream: consume one batch while the next is in flight
         const int npair = (n + 2 * U - 1) / (2 * U);
         int i0 = 0;
+#define GEMV_MMA(R, i)                                                                                  \
+        tile_mma<NBT, PRO>(acc, (i) < n ? R : zero, (i) < n ? ks + KS * (i) : 0, (i) < n ? 32 * (i) : 0, HT, B, \
+                           xh, xl, rstride)
         for (int it = 1; it < npair; ++it) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int i = i0 + u;
-                tile_mma<NBT, PRO>(acc, i < n ? ra[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
-            }
+            for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
 #pragma unroll
             for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 2 * U + u));
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int i = i0 + U + u;
-                tile_mma<NBT, PRO>(acc, i < n ? rb[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
-            }
+            for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
 #pragma unroll
             for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 3 * U + u));
             i0 += 2 * U;
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int i = i0 + u;
-            tile_mma<NBT, PRO>(acc, i < n ? ra[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
-        }
+        for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int i = i0 + U + u;
-            tile_mma<NBT, PRO>(acc, i < n ? rb[u] : zero, i < n ? ks + KS * i : 0, 0, HT, B, xs, xs_lo, rstride);
-        }
+        for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
+#undef GEMV_MMA
 #undef GEMV_PTR
     } else {
-        // ---- X in several LDS chunks (large batch with long K) -----------------
+        // ---- X in several shared LDS chunks (large batch with long K) ----------
         // Per chunk: restage X, then stream the chunk's tiles of this wave.
-        pro_finish<NBT, PRO, EPI>(p, pr, c1_first, xs, xs_lo, rstride, sc0, sc1);
+        const int ktpc = p.ktiles_per_chunk;
+        uint16_t *xh = xs, *xl = xs + xplane;
+        ChunkMap cm{false, min(KT, ktpc) * 4, B * min(KT, ktpc) * 4, 0, KS, KT, rstride};
+        pro_load<NBT, PRO, EPI>(p, pr, lead, row0, cm, 0);
+        pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
         for (int c0 = 0; c0 < KT; c0 += ktpc) {
             const int c1 = min(KT, c0 + ktpc);
             if (c0 > 0) {
@@ -339,8 +383,8 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                     load_src<PRO>(p, b, c0 * 32 + kk, sx);
                     u32x4 vh, vl;
                     make_chunk<PRO>(p, c0 * 32 + kk, sx, vh, vl);
-                    *(u32x4 *)(xs + b * rstride + kk) = vh;
-                    if (HASLO) *(u32x4 *)(xs_lo + b * rstride + kk) = vl;
+                    *(u32x4 *)(xh + b * rstride + kk) = vh;
+                    if (HASLO) *(u32x4 *)(xl + b * rstride + kk) = vl;
                 }
             }
             __syncthreads();
@@ -354,7 +398,8 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const int kt = kt0 + u * KS;
-                    tile_mma<NBT, PRO>(acc, kt < c1 ? rr[u] : zero, kt < c1 ? kt : c0, c0, HT, B, xs, xs_lo, rstride);
+                    tile_mma<NBT, PRO>(acc, kt < c1 ? rr[u] : zero, kt < c1 ? kt : c0, kt < c1 ? (kt - c0) * 32 : 0,
+                                       HT, B, xh, xl, rstride);
                 }
             }
         }
@@ -373,7 +418,6 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
         fin[bt] = v;
     }
     if (KS > 1) {
-        f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * B * rstride);   // [kNW][NBT][64] f32x4 after X
         __syncthreads();
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
@@ -507,15 +551,23 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     GemvParams q = p;
     const int KT = q.K >> 5;
     constexpr int planes = PRO == PRO_PAIR ? 1 : 2;
+    constexpr int SPW = kNW / KS;
+    const int grid = ((q.N >> 4) + SPW - 1) / SPW;
+    const int red = kNW * NBT * 64 * 16;
+    q.iters = 1;
+    // wave-private X when every wave's slices fit
+    const int nmax = (KT + KS - 1) / KS;
+    const int lds_one = planes * kNW * q.B * (nmax * 32 + 8) * 2 + red;
+    if (lds_one <= kGemvOneLdsBytes) {
+        q.ktiles_per_chunk = KT;
+        hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U, true>), dim3(grid), dim3(kNW * 64), lds_one, s, q);
+        return;
+    }
     int ktpc = (kGemvLdsBytes / (2 * planes) / q.B - 8) / 32;
     ktpc = ktpc > KT ? KT : ktpc;
     q.ktiles_per_chunk = ktpc;
-    q.iters = 1;
-    const int lds = planes * q.B * (ktpc * 32 + 8) * 2 + kNW * NBT * 64 * 16;   // X planes + reduction
-    constexpr int SPW = kNW / KS;
-    const int grid = ((q.N >> 4) + SPW - 1) / SPW;
-    if (ktpc >= KT) hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U, true>), dim3(grid), dim3(kNW * 64), lds, s, q);
-    else hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, 4, false>), dim3(grid), dim3(kNW * 64), lds, s, q);
+    const int lds = planes * q.B * (ktpc * 32 + 8) * 2 + red;
+    hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, 4, false>), dim3(grid), dim3(kNW * 64), lds, s, q);
 }
 
 // Batch size U: two batches of U tiles per wave are in flight.  Five when a

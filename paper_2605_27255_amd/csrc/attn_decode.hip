@@ -34,25 +34,20 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     const int k1 = min(len, (((split + 1) * nb) / S) * 32);
     const float scale = 1.4426950408889634f / sqrtf((float)D);
 
-    u32x4 qh[NC], ql[NC];
+    // the query rows (clamped for unused columns, zeroed below) and the first
+    // block are requested together, before any of them is waited for
+    float4 qr[NC][2];
+    {
+        const int jq = j < qpg ? j : 0;
+        const float4 *qp = (const float4 *)(p.q + ((int64_t)b * p.n_q + kvh * qpg + jq) * D + 8 * g);
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-        qh[c] = u32x4{0u, 0u, 0u, 0u};
-        ql[c] = u32x4{0u, 0u, 0u, 0u};
-        if (j < qpg) {
-            const float4 *qp = (const float4 *)(p.q + ((int64_t)b * p.n_q + kvh * qpg + j) * D + 32 * c + 8 * g);
-            const float4 a = qp[0], bq = qp[1];
-            const float f[8] = {a.x, a.y, a.z, a.w, bq.x, bq.y, bq.z, bq.w};
-            split8(f, qh[c], ql[c]);
+        for (int c = 0; c < NC; ++c) {
+            qr[c][0] = qp[8 * c];
+            qr[c][1] = qp[8 * c + 1];
         }
     }
     const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
     const uint16_t *vbase = p.vc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
-
-    f32x4 o[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;
 
     // K and V fragments of one 32-key block: K rows (16 keys per tile, 32 dims
     // per MFMA step) and the 32-key V tile, 16 dims per output tile.
@@ -68,6 +63,27 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) vf[bsel][t] = *(const u32x4 *)(vt + t * 16 * 32);
     };
+    // blocks k0 + 32 i, i < nblk; loads past the end re-read the first block
+    const int nblk = k0 < k1 ? (k1 - k0 + 31) >> 5 : 0;
+    auto blk = [&](int i) { return i < nblk ? k0 + 32 * i : 0; };
+    load_block(0, blk(0));
+    load_block(1, blk(1));
+    __builtin_amdgcn_sched_barrier(0);
+    u32x4 qh[NC], ql[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const float f[8] = {qr[c][0].x, qr[c][0].y, qr[c][0].z, qr[c][0].w,
+                            qr[c][1].x, qr[c][1].y, qr[c][1].z, qr[c][1].w};
+        split8(f, qh[c], ql[c]);
+        if (j >= qpg) {
+            qh[c] = u32x4{0u, 0u, 0u, 0u};
+            ql[c] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    f32x4 o[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
     auto block = [&](int bsel, int kb) {
         f32x4 st[2];
 #pragma unroll
@@ -113,16 +129,17 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
             o[t] = mfma16(vf[bsel][t], pl, o[t]);
         }
     };
-    // ping-pong over 32-key blocks: the next block's loads are in flight
-    // while the current one is computed
-    if (k0 < k1) load_block(0, k0);
-    for (int kb = k0; kb < k1; kb += 64) {
-        if (kb + 32 < k1) load_block(1, kb + 32);
-        block(0, kb);
-        if (kb + 32 >= k1) break;
-        if (kb + 64 < k1) load_block(0, kb + 64);
-        block(1, kb + 32);
+    // ping-pong over 32-key blocks: the next two blocks' loads are in flight
+    // while one is computed, with a fixed load count per step
+    int i = 0;
+    for (; i + 2 < nblk; i += 2) {
+        block(0, k0 + 32 * i);
+        load_block(0, blk(i + 2));
+        block(1, k0 + 32 * (i + 1));
+        load_block(1, blk(i + 3));
     }
+    if (i < nblk) block(0, k0 + 32 * i);
+    if (i + 1 < nblk) block(1, k0 + 32 * (i + 1));
 
     // partial (o, m, l) of this split for each head of the group
     if (j < qpg) {
@@ -151,10 +168,11 @@ __global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
     const float *ph = p.part + (int64_t)bh * S * (D + 2);
     float ov[SMAX];
 #pragma unroll
-    for (int sp = 0; sp < SMAX; ++sp) ov[sp] = sp < S ? ph[sp * (D + 2) + t] : 0.f;
+    for (int sp = 0; sp < SMAX; ++sp) ov[sp] = ph[(sp < S ? sp : 0) * (D + 2) + t];
     if (t < 64) {
-        const float ms = t < S ? ph[t * (D + 2) + D] : -INFINITY;
-        const float ls = t < S ? ph[t * (D + 2) + D + 1] : 0.f;
+        const float msr = ph[(t < S ? t : 0) * (D + 2) + D], lsr = ph[(t < S ? t : 0) * (D + 2) + D + 1];
+        const float ms = t < S ? msr : -INFINITY;
+        const float ls = t < S ? lsr : 0.f;
         const float M = wave_max(ms);
         const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
         const float L = wave_sum(w * ls);
@@ -164,7 +182,7 @@ __global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
     __syncthreads();
     float acc = 0.f;
 #pragma unroll
-    for (int sp = 0; sp < SMAX; ++sp) acc += s_w[sp] * ov[sp];
+    for (int sp = 0; sp < SMAX; ++sp) acc += sp < S ? s_w[sp] * ov[sp] : 0.f;
     p.out[(int64_t)bh * D + t] = acc * s_inv;
 }
 

@@ -24,8 +24,9 @@
 namespace pipo {
 
 constexpr int kNW = 8;                       // waves per workgroup
-constexpr int kGemvLdsBytes = 56 * 1024;     // dynamic LDS budget for a shared X chunk
 constexpr int kGemvOneLdsBytes = 72 * 1024;  // budget for wave-private X (two workgroups per CU)
+constexpr int kWideChunk = 8;                // k-tiles per shared X chunk (larger batches)
+constexpr int kWideTargetWgs = 128;          // workgroups the k-ranges aim for (fewer, longer ranges measured faster)
 constexpr int kXR = 3;                       // prologue chunks per thread loaded ahead of the weights
 
 __device__ __forceinline__ float silu_f(float u) { return u / (1.0f + __expf(-u)); }
@@ -272,172 +273,17 @@ __device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 
     }
 }
 
-template <int NBT, int KS, int PRO, int EPI, int U, bool ONE>
-__global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
-    // U: k-tiles per wave per load batch (two batches in flight).  ONE: every
-    // wave's slices of X fit in LDS at once (wave-private staging); otherwise
-    // the workgroup stages X in shared chunks of ktiles_per_chunk k-tiles.
-    static_assert(KS > 1, "the strip reduction orders the RMSNorm scalars");
-    constexpr int SPW = kNW / KS;          // strips per workgroup
-    constexpr int NA = NAcc<PRO>::n;
-    constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
-    extern __shared__ __align__(16) uint16_t xs[];
-    __shared__ float sc0[32], sc1[32];
-
+// Fused epilogues, one wave per strip (lanes (j, g) hold rows row0 + v of
+// column b = 16 bt + j): bias or residual add with sum-of-squares parts,
+// SwiGLU, RoPE + KV append, logits + argmax key.
+template <int NBT, int EPI>
+__device__ __forceinline__ void gemv_epilogue(const GemvParams &p, f32x4 (&fin)[NBT], const f32x4 (&resid)[NBT],
+                                              int strip, bool lead) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
-    const int ks = wave % KS;              // k-split index inside the strip
-    const int strip = blockIdx.x * SPW + wave / KS;
-    const bool sok = strip < nstrips;
-    const bool lead = ks == 0 && sok;      // the wave that reduces and writes the strip
-    const int KT = p.K >> 5, HT = p.H >> 5;
     const int B = p.B;
-    const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
-    const int row0 = strip * 16 + 4 * g;   // first of this lane's four output rows
-    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
-    // LDS: X hi planes, X lo planes, then the reduction buffer
-    int rstride, xplane;                   // row stride of a plane; elements per plane set
-    if (ONE) {
-        const int nmax = (KT + KS - 1) / KS;
-        rstride = nmax * 32 + 8;
-        xplane = kNW * B * rstride;
-    } else {
-        rstride = p.ktiles_per_chunk * 32 + 8;
-        xplane = B * rstride;
-    }
-    f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * xplane);   // [kNW][NBT][64] f32x4
-
-    f32x4 acc[NA][NBT];
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    Pro<NBT, PRO, EPI> pr;
-    if (ONE) {
-        // ---- wave-private X, one pipelined pass over this wave's tiles ----------
-        // Wave tiles are kt = ks + KS i, i < n.  Loads are unconditional (tiles
-        // past the end read the matrix's first line and are multiplied as
-        // zero), so every batch keeps a fixed load count and the waits before
-        // each batch cover exactly that batch.
-        const int n = (KT - ks + KS - 1) / KS;
-        const int nmax = (KT + KS - 1) / KS;
-        ChunkMap cm{true, nmax * 4, B * nmax * 4, ks, KS, KT, rstride};
-        uint16_t *xh = xs + wave * B * rstride, *xl = xh + xplane;
-        // 1. prologue / epilogue inputs, before any weights
-        pro_load<NBT, PRO, EPI>(p, pr, lead, row0, cm, 0);
-        // 2. two batches of weights
-        u32x4 ra[U], rb[U];
-#define GEMV_PTR(i) ((const u32x4 *)((i) < n ? wp + (int64_t)(ks + KS * (i)) * 512 : p.W))
-#pragma unroll
-        for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(u));
-#pragma unroll
-        for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(U + u));
-        // keep the prologue arithmetic (and its waits) after the weight loads
-        __builtin_amdgcn_sched_barrier(0);
-        // 3. scalars and this wave's slices of X; the MTP scales its halves
-        //    before the reduction, so it waits for every wave's scalars
-        pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
-        if (PRO == PRO_MTP) __syncthreads();
-        // 4. stream: consume one batch while the next is in flight
-        const int npair = (n + 2 * U - 1) / (2 * U);
-        int i0 = 0;
-#define GEMV_MMA(R, i)                                                                                  \
-        tile_mma<NBT, PRO>(acc, (i) < n ? R : zero, (i) < n ? ks + KS * (i) : 0, (i) < n ? 32 * (i) : 0, HT, B, \
-                           xh, xl, rstride)
-        for (int it = 1; it < npair; ++it) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
-#pragma unroll
-            for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 2 * U + u));
-#pragma unroll
-            for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
-#pragma unroll
-            for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 3 * U + u));
-            i0 += 2 * U;
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
-#pragma unroll
-        for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
-#undef GEMV_MMA
-#undef GEMV_PTR
-    } else {
-        // ---- X in several shared LDS chunks (large batch with long K) ----------
-        // Per chunk: restage X, then stream the chunk's tiles of this wave.
-        const int ktpc = p.ktiles_per_chunk;
-        uint16_t *xh = xs, *xl = xs + xplane;
-        ChunkMap cm{false, min(KT, ktpc) * 4, B * min(KT, ktpc) * 4, 0, KS, KT, rstride};
-        pro_load<NBT, PRO, EPI>(p, pr, lead, row0, cm, 0);
-        pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
-        for (int c0 = 0; c0 < KT; c0 += ktpc) {
-            const int c1 = min(KT, c0 + ktpc);
-            if (c0 > 0) {
-                __syncthreads();
-                const int cpr = (c1 - c0) * 4;
-                for (int idx = threadIdx.x; idx < B * cpr; idx += 512) {
-                    const int b = idx / cpr;
-                    const int kk = (idx - b * cpr) << 3;
-                    XSrc sx;
-                    load_src<PRO>(p, b, c0 * 32 + kk, sx);
-                    u32x4 vh, vl;
-                    make_chunk<PRO>(p, c0 * 32 + kk, sx, vh, vl);
-                    *(u32x4 *)(xh + b * rstride + kk) = vh;
-                    if (HASLO) *(u32x4 *)(xl + b * rstride + kk) = vl;
-                }
-            }
-            __syncthreads();
-            for (int kt0 = c0 + ks; kt0 < c1; kt0 += U * KS) {
-                u32x4 rr[U];
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int kt = kt0 + u * KS;
-                    rr[u] = __builtin_nontemporal_load((const u32x4 *)(kt < c1 ? wp + (int64_t)kt * 512 : p.W));
-                }
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int kt = kt0 + u * KS;
-                    tile_mma<NBT, PRO>(acc, kt < c1 ? rr[u] : zero, kt < c1 ? kt : c0, kt < c1 ? (kt - c0) * 32 : 0,
-                                       HT, B, xh, xl, rstride);
-                }
-            }
-        }
-    }
-
-    // ---- 3. reduce the KS partial sums of each strip (wave order) -----------
-    f32x4 fin[NBT];
-#pragma unroll
-    for (int bt = 0; bt < NBT; ++bt) {
-        f32x4 v = acc[0][bt];
-        if (NA == 2) {
-            const int b = bt * 16 + j;
-            const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
-            v = v * s0 + acc[NA - 1][bt] * s1;
-        }
-        fin[bt] = v;
-    }
-    if (KS > 1) {
-        __syncthreads();
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
-        __syncthreads();
-        if (ks == 0) {
-#pragma unroll
-            for (int bt = 0; bt < NBT; ++bt) {
-#pragma unroll
-                for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
-            }
-        }
-    }
-    if (PRO == PRO_NORM) {
-#pragma unroll
-        for (int bt = 0; bt < NBT; ++bt) {
-            const int b = bt * 16 + j;
-            fin[bt] *= (b < B ? sc0[b] : 0.f);
-        }
-    }
-    // ---- 4. fused epilogues (one wave per strip) ----------------------------
+    const int row0 = strip * 16 + 4 * g;
     if (EPI == EPI_LOGITS) {
         // every wave reaches here; waves without a strip contribute key 0
         __shared__ uint64_t s_best[kNW][32];
@@ -480,7 +326,7 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
             const int b = bt * 16 + j;
             const bool ok = b < B;
             f32x4 val = fin[bt];
-            if (EPI == EPI_RESID) val += pr.resid[bt];
+            if (EPI == EPI_RESID) val += resid[bt];
             else if (p.bias) val += *(const f32x4 *)(p.bias + row0);
             if (ok) *(f32x4 *)(p.out + (int64_t)b * p.N + row0) = val;
             float sq = val[0] * val[0] + val[1] * val[1] + val[2] * val[2] + val[3] * val[3];
@@ -547,6 +393,373 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 }
 
 template <int NBT, int KS, int PRO, int EPI, int U>
+__global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
+    // U: k-tiles per wave per load batch (two batches in flight).  Every
+    // wave's slices of X fit in LDS at once (wave-private staging).
+    static_assert(KS > 1, "the strip reduction orders the RMSNorm scalars");
+    constexpr int SPW = kNW / KS;          // strips per workgroup
+    constexpr int NA = NAcc<PRO>::n;
+    constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
+    extern __shared__ __align__(16) uint16_t xs[];
+    __shared__ float sc0[32], sc1[32];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15, g = lane >> 4;
+    const int nstrips = p.N >> 4;
+    const int ks = wave % KS;              // k-split index inside the strip
+    const int strip = blockIdx.x * SPW + wave / KS;
+    const bool sok = strip < nstrips;
+    const bool lead = ks == 0 && sok;      // the wave that reduces and writes the strip
+    const int KT = p.K >> 5, HT = p.H >> 5;
+    const int B = p.B;
+    const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
+    const int row0 = strip * 16 + 4 * g;   // first of this lane's four output rows
+    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+    // LDS: X hi planes, X lo planes, then the reduction buffer
+    const int rstride = ((KT + KS - 1) / KS) * 32 + 8;   // row stride of a wave's X slices
+    const int xplane = kNW * B * rstride;                 // elements per plane set
+    f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * xplane);   // [kNW][NBT][64] f32x4
+
+    f32x4 acc[NA][NBT];
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    Pro<NBT, PRO, EPI> pr;
+    {
+        // ---- wave-private X, one pipelined pass over this wave's tiles ----------
+        // Wave tiles are kt = ks + KS i, i < n.  Loads are unconditional (tiles
+        // past the end read the matrix's first line and are multiplied as
+        // zero), so every batch keeps a fixed load count and the waits before
+        // each batch cover exactly that batch.
+        const int n = (KT - ks + KS - 1) / KS;
+        const int nmax = (KT + KS - 1) / KS;
+        ChunkMap cm{true, nmax * 4, B * nmax * 4, ks, KS, KT, rstride};
+        uint16_t *xh = xs + wave * B * rstride, *xl = xh + xplane;
+        // 1. prologue / epilogue inputs, before any weights
+        pro_load<NBT, PRO, EPI>(p, pr, lead, row0, cm, 0);
+        // 2. two batches of weights
+        u32x4 ra[U], rb[U];
+#define GEMV_PTR(i) ((const u32x4 *)((i) < n ? wp + (int64_t)(ks + KS * (i)) * 512 : p.W))
+#pragma unroll
+        for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(u));
+#pragma unroll
+        for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(U + u));
+        // keep the prologue arithmetic (and its waits) after the weight loads
+        __builtin_amdgcn_sched_barrier(0);
+        // 3. scalars and this wave's slices of X; the MTP scales its halves
+        //    before the reduction, so it waits for every wave's scalars
+        pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
+        if (PRO == PRO_MTP) __syncthreads();
+        // 4. stream: consume one batch while the next is in flight
+        const int npair = (n + 2 * U - 1) / (2 * U);
+        int i0 = 0;
+#define GEMV_MMA(R, i)                                                                                  \
+        tile_mma<NBT, PRO>(acc, (i) < n ? R : zero, (i) < n ? ks + KS * (i) : 0, (i) < n ? 32 * (i) : 0, HT, B, \
+                           xh, xl, rstride)
+        for (int it = 1; it < npair; ++it) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
+#pragma unroll
+            for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 2 * U + u));
+#pragma unroll
+            for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
+#pragma unroll
+            for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 3 * U + u));
+            i0 += 2 * U;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
+#pragma unroll
+        for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
+#undef GEMV_MMA
+#undef GEMV_PTR
+    }
+
+    // ---- 3. reduce the KS partial sums of each strip (wave order) -----------
+    f32x4 fin[NBT];
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) {
+        f32x4 v = acc[0][bt];
+        if (NA == 2) {
+            const int b = bt * 16 + j;
+            const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
+            v = v * s0 + acc[NA - 1][bt] * s1;
+        }
+        fin[bt] = v;
+    }
+    if (KS > 1) {
+        __syncthreads();
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
+        __syncthreads();
+        if (ks == 0) {
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+#pragma unroll
+                for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
+            }
+        }
+    }
+    if (PRO == PRO_NORM) {
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            fin[bt] *= (b < B ? sc0[b] : 0.f);
+        }
+    }
+    gemv_epilogue<NBT, EPI>(p, fin, pr.resid, strip, lead);
+}
+
+// ---------------------------------------------------------------------------
+// Large batches.  k_xprep: one workgroup per row b writes X[b] = the GEMV
+// input with its RMSNorm scale(s) and gains applied, split into bf16 hi / lo
+// planes.  k_gemv_wide: a workgroup owns 128 weight rows (one 16-row strip
+// per wave) and a range of k-tiles; chunks of X (all B rows, hi and lo) pass
+// through LDS once per workgroup and are shared by its eight waves, which
+// keeps the X traffic well below the weight traffic for any batch up to 32.
+// Weights stream one chunk ahead of the chunk being multiplied.  With several
+// k-ranges the partial sums go to a workspace and k_gemv_fin adds them in
+// range order and runs the epilogue.
+template <int PRO>
+__global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
+    // workgroup (b, segment): columns [2048 seg, 2048 seg + 2048) of row b
+    const int b = blockIdx.x / p.xseg, seg = blockIdx.x - b * p.xseg;
+    const int K = p.K, H = p.H;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __shared__ float s_part[2][4];
+    float sc0 = 1.f, sc1 = 1.f;
+    if (PRO == PRO_NORM || PRO == PRO_MTP) {
+        // the row's sum of squares (and the MTP embedding row's), 8 values
+        // requested per thread per step
+        const int Kn = PRO == PRO_MTP ? H : K;
+        const float *xr = p.x + (int64_t)b * Kn;
+        float a = 0.f, e = 0.f;
+#pragma unroll 4
+        for (int k0 = threadIdx.x * 8; k0 < Kn; k0 += 256 * 8) {
+            const float4 u0 = *(const float4 *)(xr + k0), u1 = *(const float4 *)(xr + k0 + 4);
+            a += u0.x * u0.x + u0.y * u0.y + u0.z * u0.z + u0.w * u0.w;
+            a += u1.x * u1.x + u1.y * u1.y + u1.z * u1.z + u1.w * u1.w;
+        }
+        if (PRO == PRO_MTP) {
+            const int tok = clamp_id(argmax_key_id(p.tokkey[b]), p.vocab);
+#pragma unroll 4
+            for (int k0 = threadIdx.x * 8; k0 < H; k0 += 256 * 8) {
+                const u32x4 w = *(const u32x4 *)(p.embed + tiled_index(tok, k0, H));
+#pragma unroll
+                for (int i = 0; i < 4; ++i) e += bf_lo(w[i]) * bf_lo(w[i]) + bf_hi(w[i]) * bf_hi(w[i]);
+            }
+        }
+        a = wave_sum(a);
+        e = wave_sum(e);
+        if (lane == 0) {
+            s_part[0][wave] = a;
+            s_part[1][wave] = e;
+        }
+        __syncthreads();
+        sc0 = rsqrtf((s_part[0][0] + s_part[0][1] + s_part[0][2] + s_part[0][3]) / (float)Kn + p.eps);
+        sc1 = rsqrtf((s_part[1][0] + s_part[1][1] + s_part[1][2] + s_part[1][3]) / (float)H + p.eps);
+    }
+    {
+        const int k = seg * 2048 + threadIdx.x * 8;
+        if (k >= K) return;
+        XSrc sx;
+        load_src<PRO>(p, b, k, sx);
+        u32x4 vh, vl;
+        if (PRO == PRO_PAIR) {
+            vh = sx.e;
+            vl = u32x4{0u, 0u, 0u, 0u};
+        } else {
+            float f[8];
+            if (PRO == PRO_F32) {
+                f[0] = sx.a0.x; f[1] = sx.a0.y; f[2] = sx.a0.z; f[3] = sx.a0.w;
+                f[4] = sx.a1.x; f[5] = sx.a1.y; f[6] = sx.a1.z; f[7] = sx.a1.w;
+            } else if (PRO == PRO_NORM || k < H) {
+                f[0] = sx.a0.x * sx.g0.x; f[1] = sx.a0.y * sx.g0.y; f[2] = sx.a0.z * sx.g0.z; f[3] = sx.a0.w * sx.g0.w;
+                f[4] = sx.a1.x * sx.g1.x; f[5] = sx.a1.y * sx.g1.y; f[6] = sx.a1.z * sx.g1.z; f[7] = sx.a1.w * sx.g1.w;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) f[i] *= sc0;
+            } else {
+                f[0] = bf_lo(sx.e[0]) * sx.g0.x; f[1] = bf_hi(sx.e[0]) * sx.g0.y; f[2] = bf_lo(sx.e[1]) * sx.g0.z;
+                f[3] = bf_hi(sx.e[1]) * sx.g0.w; f[4] = bf_lo(sx.e[2]) * sx.g1.x; f[5] = bf_hi(sx.e[2]) * sx.g1.y;
+                f[6] = bf_lo(sx.e[3]) * sx.g1.z; f[7] = bf_hi(sx.e[3]) * sx.g1.w;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) f[i] *= sc1;
+            }
+            split8(f, vh, vl);
+        }
+        *(u32x4 *)(p.xh + (int64_t)b * K + k) = vh;
+        *(u32x4 *)(p.xl + (int64_t)b * K + k) = vl;
+    }
+}
+
+template <int NBT, int EPI>
+__global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
+    constexpr int CK = kWideChunk;         // k-tiles per X chunk
+    constexpr int RS = CK * 32 + 8;        // LDS row stride (elements) of a chunk plane
+    constexpr int XU = 2 * NBT;            // 16-byte X units per thread per chunk (2 B CK 4 / 512)
+    extern __shared__ __align__(16) uint16_t xsm[];   // [2 buffers][2 planes][B][RS]
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15, g = lane >> 4;
+    const int nstrips = p.N >> 4;
+    const int rtiles = (nstrips + kNW - 1) / kNW;
+    const int rt = blockIdx.x % rtiles, ksi = blockIdx.x / rtiles;
+    const int strip = rt * kNW + wave;
+    const bool sok = strip < nstrips;
+    const int KT = p.K >> 5, K = p.K, B = p.B;
+    const int NC = (KT + CK - 1) / CK;     // chunks over the whole K
+    const int c0 = (ksi * NC) / p.ksplit, c1 = ((ksi + 1) * NC) / p.ksplit;
+    const int nch = c1 - c0;
+    const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
+    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+    const int bufsz = 2 * B * RS;
+    // X unit u of a chunk: plane, row, 8-column group
+    const int units = 2 * B * (CK * 4);
+    auto x_src = [&](int c, int r) -> const u32x4 * {
+        int u = threadIdx.x + r * 512;
+        u = u < units ? u : 0;
+        const int plane = u / (B * CK * 4), rem = u - plane * B * CK * 4;
+        const int b = rem / (CK * 4), c8 = rem - b * CK * 4;
+        int col = (c0 + c) * CK * 32 + c8 * 8;
+        col = (c0 + c < c1 && col < K) ? col : 0;
+        return (const u32x4 *)((plane ? p.xl : p.xh) + (int64_t)b * K + col);
+    };
+    // units past the chunk land in a scratch line after the two buffers, so
+    // the store (like the load) is unconditional
+    auto x_put = [&](int buf, int r, u32x4 v) {
+        const int u = threadIdx.x + r * 512;
+        const int uc = u < units ? u : 0;
+        const int plane = uc / (B * CK * 4), rem = uc - plane * B * CK * 4;
+        const int b = rem / (CK * 4), c8 = rem - b * CK * 4;
+        const int off = u < units ? buf * bufsz + plane * B * RS + b * RS + c8 * 8 : 2 * bufsz;
+        *(u32x4 *)(xsm + off) = v;
+    };
+    // weight tile t of chunk c (tiles past K or past this range read the first line)
+    auto w_src = [&](int c, int t) -> const u32x4 * {
+        const int kt = (c0 + c) * CK + t;
+        return (const u32x4 *)((c0 + c < c1 && kt < KT) ? wp + (int64_t)kt * 512 : p.W);
+    };
+    f32x4 acc[NBT];
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto consume = [&](int buf, int c, const u32x4 (&w)[CK]) {
+        const uint16_t *xh = xsm + buf * bufsz, *xl = xh + B * RS;
+#pragma unroll
+        for (int t = 0; t < CK; ++t) {
+            const int kt = (c0 + c) * CK + t;
+            const u32x4 wt = kt < KT ? w[t] : zero;
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                const int xo = (b < B ? b : 0) * RS + t * 32 + g * 8;
+                u32x4 bh = *(const u32x4 *)(xh + xo), bl = *(const u32x4 *)(xl + xo);
+                bh = b < B ? bh : zero;
+                bl = b < B ? bl : zero;
+                acc[bt] = mfma16(wt, bh, acc[bt]);
+                acc[bt] = mfma16(wt, bl, acc[bt]);
+            }
+        }
+    };
+    f32x4 resid[NBT];
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) {
+        const int b = bt * 16 + j;
+        resid[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (EPI == EPI_RESID && p.ksplit == 1)
+            resid[bt] = *(const f32x4 *)(p.out + ((sok && b < B) ? (int64_t)b * p.N + strip * 16 + 4 * g : 0));
+    }
+    // chunk c: X regs loaded one chunk ahead and written to LDS buffer c % 2
+    // just before the barrier that opens chunk c; weights two chunks deep
+    u32x4 xr[XU], wa[CK], wb[CK];
+#pragma unroll
+    for (int r = 0; r < XU; ++r) xr[r] = *x_src(0, r);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int t = 0; t < CK; ++t) wa[t] = __builtin_nontemporal_load(w_src(0, t));
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int r = 0; r < XU; ++r) x_put(0, r, xr[r]);
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < XU; ++r) xr[r] = *x_src(1, r);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int t = 0; t < CK; ++t) wb[t] = __builtin_nontemporal_load(w_src(1, t));
+    __builtin_amdgcn_sched_barrier(0);
+    for (int c = 0; c < nch; c += 2) {
+        consume(0, c, wa);
+#pragma unroll
+        for (int r = 0; r < XU; ++r) x_put(1, r, xr[r]);
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < XU; ++r) xr[r] = *x_src(c + 2, r);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < CK; ++t) wa[t] = __builtin_nontemporal_load(w_src(c + 2, t));
+        __builtin_amdgcn_sched_barrier(0);
+        if (c + 1 < nch) consume(1, c + 1, wb);
+#pragma unroll
+        for (int r = 0; r < XU; ++r) x_put(0, r, xr[r]);
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < XU; ++r) xr[r] = *x_src(c + 3, r);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < CK; ++t) wb[t] = __builtin_nontemporal_load(w_src(c + 3, t));
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    f32x4 fin[NBT];
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) fin[bt] = acc[bt];
+    if (p.ksplit == 1) {
+        gemv_epilogue<NBT, EPI>(p, fin, resid, strip, sok);
+        return;
+    }
+    // partial sums of this k-range: part[ksi][b][row]
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) {
+        const int b = bt * 16 + j;
+        if (sok && b < B) *(f32x4 *)(p.part + ((int64_t)ksi * B + b) * p.N + strip * 16 + 4 * g) = fin[bt];
+    }
+}
+
+// Sum of the k-range partials in range order, then the fused epilogue.
+template <int NBT, int EPI>
+__global__ __launch_bounds__(512) void k_gemv_fin(GemvParams p) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15, g = lane >> 4;
+    const int nstrips = p.N >> 4;
+    const int strip = blockIdx.x * kNW + wave;
+    const bool sok = strip < nstrips;
+    const int B = p.B;
+    const int row0 = (sok ? strip : 0) * 16 + 4 * g;
+    f32x4 fin[NBT], resid[NBT];
+#pragma unroll
+    for (int bt = 0; bt < NBT; ++bt) {
+        const int b = bt * 16 + j;
+        const int bc = b < B ? b : 0;
+        resid[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (EPI == EPI_RESID) resid[bt] = *(const f32x4 *)(p.out + (int64_t)bc * p.N + row0);
+        // request 16 ranges at a time, add them in range order
+        f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int k0 = 0; k0 < p.ksplit; k0 += 16) {
+            f32x4 v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int k = min(k0 + u, p.ksplit - 1);
+                v[u] = *(const f32x4 *)(p.part + ((int64_t)k * B + bc) * p.N + row0);
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (k0 + u < p.ksplit) a += v[u];
+        }
+        fin[bt] = a;
+    }
+    gemv_epilogue<NBT, EPI>(p, fin, resid, strip, sok);
+}
+
+template <int NBT, int KS, int PRO, int EPI, int U>
 static void launch_t(const GemvParams &p, hipStream_t s) {
     GemvParams q = p;
     const int KT = q.K >> 5;
@@ -560,14 +773,22 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     const int lds_one = planes * kNW * q.B * (nmax * 32 + 8) * 2 + red;
     if (lds_one <= kGemvOneLdsBytes) {
         q.ktiles_per_chunk = KT;
-        hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U, true>), dim3(grid), dim3(kNW * 64), lds_one, s, q);
+        hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s, q);
         return;
     }
-    int ktpc = (kGemvLdsBytes / (2 * planes) / q.B - 8) / 32;
-    ktpc = ktpc > KT ? KT : ktpc;
-    q.ktiles_per_chunk = ktpc;
-    const int lds = planes * q.B * (ktpc * 32 + 8) * 2 + red;
-    hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, 4, false>), dim3(grid), dim3(kNW * 64), lds, s, q);
+    // otherwise: X planes, then 128-row workgroups over k-ranges
+    q.xseg = (q.K + 2047) / 2048;
+    hipLaunchKernelGGL((k_xprep<PRO>), dim3(q.B * q.xseg), dim3(256), 0, s, q);
+    const int rtiles = ((q.N >> 4) + kNW - 1) / kNW;
+    const int NC = (KT + kWideChunk - 1) / kWideChunk;
+    int ksplit = (kWideTargetWgs + rtiles - 1) / rtiles;
+    ksplit = ksplit < NC ? ksplit : NC;
+    const int64_t cap = q.part_cap / ((int64_t)q.B * q.N);
+    ksplit = ksplit < cap ? ksplit : (int)cap;
+    q.ksplit = ksplit < 1 ? 1 : ksplit;
+    const int lds_w = 2 * 2 * q.B * (kWideChunk * 32 + 8) * 2 + 16;
+    hipLaunchKernelGGL((k_gemv_wide<NBT, EPI>), dim3(rtiles * q.ksplit), dim3(kNW * 64), lds_w, s, q);
+    if (q.ksplit > 1) hipLaunchKernelGGL((k_gemv_fin<NBT, EPI>), dim3(rtiles), dim3(kNW * 64), 0, s, q);
 }
 
 // Batch size U: two batches of U tiles per wave are in flight.  Five when a

@@ -17,6 +17,9 @@ enum GemvPro : int {
     PRO_PAIR = 2,   // X = [E[a]; E[b]] for int32 pairs [B][2] (pair-in compressor)
     PRO_MTP  = 3,   // X = [RMSNorm(h_b) g1; RMSNorm(E[tok]) g2], tok from an argmax key
 };
+// Larger batches: a preparation kernel writes X (RMSNorm and gain applied) as
+// bf16 planes hi + lo [B][K] (GemvParams::xh / xl) and the GEMV streams its
+// B operands from them (cached in L2) next to the weight tiles.
 enum GemvEpi : int {
     EPI_STORE  = 0,  // out fp32 [B][N] = acc (+ bias); sum-of-squares parts
     EPI_RESID  = 1,  // out fp32 [B][N] += acc; sum-of-squares parts
@@ -41,6 +44,10 @@ struct GemvParams {
     int n_q, n_kv, d, lmax_pad;   // KV geometry of this layer
     int64_t kv_bstride;           // elements between consecutive sequences' caches
     uint64_t *best;               // argmax keys [B] (EPI_LOGITS; NULL: none)
+    uint16_t *xh, *xl;            // X planes workspace, [B][K] bf16 each (large batches)
+    float *part; int64_t part_cap;  // k-range partial sums workspace (floats)
+    int ksplit;                   // k-ranges (set by launch_gemv)
+    int xseg;                     // 2048-column segments per row of the X planes (set by launch_gemv)
 };
 void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s);
 int gemv_num_groups(int N);

@@ -57,6 +57,8 @@ struct pipo_ctx {
     // decode state and activations
     float *x, *ss_x, *hd, *ss_hd, *logits_b, *logits_d, *apart;
     float *qbuf, *attn_out, *act;
+    uint16_t *xh, *xl;    // decode GEMV input planes for larger batches [Bmax][Kmax]
+    float *gpart; int64_t gpart_cap;   // decode GEMV k-range partial sums
     uint64_t *best_b, *best_d, *seeds;
     int32_t *pairs, *pos, *step;
     pipo_pair *out;
@@ -222,6 +224,16 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->qbuf = a.take<float>((int64_t)B * c->qdim);
         c->attn_out = a.take<float>((int64_t)B * c->qdim);
         c->act = a.take<float>((int64_t)B * F);
+        {
+            const int64_t kmax = std::max<int64_t>(std::max<int64_t>(2 * H, F), c->qdim);
+            c->xh = a.take<uint16_t>((int64_t)B * kmax);
+            c->xl = a.take<uint16_t>((int64_t)B * kmax);
+            // k-range partial sums of the larger-batch GEMV: room for 16 ranges
+            // of the widest non-vocabulary output
+            const int64_t nmax = std::max<int64_t>(std::max<int64_t>(2 * F, c->nqkv), 2 * H);
+            c->gpart_cap = 16 * (int64_t)B * nmax;
+            c->gpart = a.take<float>(c->gpart_cap);
+        }
         c->best_b = a.take<uint64_t>(B);
         c->best_d = a.take<uint64_t>(B);
         c->seeds = a.take<uint64_t>(B);
@@ -305,7 +317,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     const int H = c->H;
     const bool greedy = c->temperature <= 0.f;
     GemvParams p{};
-    p.B = B; p.eps = c->cfg.rms_eps; p.H = H;
+    p.B = B; p.eps = c->cfg.rms_eps; p.H = H; p.xh = c->xh; p.xl = c->xl; p.part = c->gpart; p.part_cap = c->gpart_cap;
     // LM head #1 on RMSNorm(h_b; g_final)
     p.W = c->embed; p.N = c->V; p.K = H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
@@ -318,7 +330,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     }
     // MTP head: W_fc [RMSNorm(h_b; g_mh); RMSNorm(E[b]; g_me)]
     GemvParams m{};
-    m.B = B; m.eps = c->cfg.rms_eps; m.H = H; m.vocab = c->V;
+    m.B = B; m.eps = c->cfg.rms_eps; m.H = H; m.vocab = c->V; m.xh = c->xh; m.xl = c->xl; m.part = c->gpart; m.part_cap = c->gpart_cap;
     m.W = c->w_fc; m.N = H; m.K = 2 * H;
     m.x = c->x; m.ss = c->ss_x; m.nss = nss; m.gain = c->g_mtp_h; m.gain2 = c->g_mtp_e;
     m.embed = c->embed; m.tokkey = c->best_b;
@@ -326,7 +338,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     { PROF(PIPO_K_GEMV_SMALL); launch_gemv(m, PRO_MTP, EPI_STORE, s); }
     // LM head #2 on RMSNorm(h_d; g_mo)
     GemvParams q{};
-    q.B = B; q.eps = c->cfg.rms_eps; q.H = H;
+    q.B = B; q.eps = c->cfg.rms_eps; q.H = H; q.xh = c->xh; q.xl = c->xl; q.part = c->gpart; q.part_cap = c->gpart_cap;
     q.W = c->embed; q.N = c->V; q.K = H;
     q.x = c->hd; q.ss = c->ss_hd; q.nss = H / 16; q.gain = c->g_mtp_o;
     q.out = c->logits_d; q.best = greedy ? c->best_d : nullptr;
@@ -360,7 +372,7 @@ static int attn_splits(const pipo_ctx *c, int B) {
 static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
     GemvParams base{};
-    base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V;
+    base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V; base.xh = c->xh; base.xl = c->xl; base.part = c->gpart; base.part_cap = c->gpart_cap;
     {   // pair-in compressor
         GemvParams p = base;
         p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;

@@ -76,10 +76,16 @@ __device__ __forceinline__ uint64_t fixed_mass(float e) {
     return (uint64_t)__double2ull_rn((double)e * 1099511627776.0);   // 2^40
 }
 
+// Wave w of the workgroup owns the contiguous ids [w R, (w + 1) R), R a
+// multiple of 256, read as 256-element sub-tiles (lane l: ids base + 4 l ..
+// base + 4 l + 3, one float4), so every pass is coalesced and id order is
+// (wave, sub-tile, lane, element).
+constexpr int kSampWaves = kSampThreads / 64;
+
 __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
-    __shared__ unsigned long long hist[256];
-    __shared__ float s_red[kSampThreads / 64];
-    __shared__ unsigned long long s_u64[kSampThreads / 64];
+    __shared__ unsigned long long hist[kSampWaves][256];
+    __shared__ float s_red[kSampWaves];
+    __shared__ unsigned long long s_u64[kSampWaves];
     __shared__ uint32_t s_prefix;
     __shared__ unsigned long long s_above, s_mass;
     __shared__ int s_all;
@@ -87,20 +93,40 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
     const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const float *lg = p.logits + (int64_t)b * p.V;
     const int V = p.V;
-    const int per = (V + kSampThreads - 1) / kSampThreads;
-    const int j0 = min(V, tid * per), j1 = min(V, j0 + per);
+    const int R = ((V + kSampWaves * 256 - 1) / (kSampWaves * 256)) * 256;   // ids per wave
+    const int w0 = wave * R;
+    // the four logits of this lane in sub-tile t (ids past V read id 0, masked)
+    auto load4 = [&](int t, float (&v)[4]) {
+        const int id = w0 + t * 256 + 4 * lane;
+        const float4 q = *(const float4 *)(lg + (id + 3 < V ? id : 0));
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    };
+    auto valid = [&](int t, int e) { return w0 + t * 256 + 4 * lane + e < V; };
+    const int nt = R / 256;
 
     float mx = -INFINITY;
-    for (int jj = j0; jj < j1; ++jj) mx = fmaxf(mx, lg[jj]);
+#pragma unroll 4
+    for (int t = 0; t < nt; ++t) {
+        float v[4];
+        load4(t, v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = valid(t, e) ? fmaxf(mx, v[e]) : mx;
+    }
     mx = wave_max(mx);
     if (lane == 0) s_red[wave] = mx;
     __syncthreads();
     mx = s_red[0];
-    for (int w = 1; w < kSampThreads / 64; ++w) mx = fmaxf(mx, s_red[w]);
+    for (int w = 1; w < kSampWaves; ++w) mx = fmaxf(mx, s_red[w]);
     const float kT = 1.4426950408889634f / p.temperature;
 
     unsigned long long tot = 0;
-    for (int jj = j0; jj < j1; ++jj) tot += fixed_mass(exp2f((lg[jj] - mx) * kT));
+#pragma unroll 4
+    for (int t = 0; t < nt; ++t) {
+        float v[4];
+        load4(t, v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tot += valid(t, e) ? fixed_mass(exp2f((v[e] - mx) * kT)) : 0ull;
+    }
     for (int o = 32; o > 0; o >>= 1) {
         const uint32_t lo = __shfl_xor((uint32_t)tot, o), hi = __shfl_xor((uint32_t)(tot >> 32), o);
         tot += ((unsigned long long)hi << 32) | lo;
@@ -108,28 +134,40 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
     if (lane == 0) s_u64[wave] = tot;
     __syncthreads();
     tot = 0;
-    for (int w = 0; w < kSampThreads / 64; ++w) tot += s_u64[w];
+    for (int w = 0; w < kSampWaves; ++w) tot += s_u64[w];
     const double target = (double)p.top_p * (double)tot;
 
     if (tid == 0) { s_prefix = 0; s_above = 0; s_all = 0; }
     for (int pass = 0; pass < 4; ++pass) {
         const int shift = 24 - 8 * pass;
-        if (tid < 256) hist[tid] = 0;
+        for (int i = tid; i < kSampWaves * 256; i += kSampThreads) (&hist[0][0])[i] = 0;
         __syncthreads();
         const uint32_t prefix = s_prefix;
-        for (int jj = j0; jj < j1; ++jj) {
-            const float e = exp2f((lg[jj] - mx) * kT);
-            const uint32_t key = __float_as_uint(e);
-            if (pass == 0 || (key >> (shift + 8)) == prefix)
-                atomicAdd(&hist[(key >> shift) & 255u], fixed_mass(e));
+#pragma unroll 2
+        for (int t = 0; t < nt; ++t) {
+            float v[4];
+            load4(t, v);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float ev = exp2f((v[e] - mx) * kT);
+                const uint32_t key = __float_as_uint(ev);
+                if (valid(t, e) && (pass == 0 || (key >> (shift + 8)) == prefix))
+                    atomicAdd(&hist[wave][(key >> shift) & 255u], fixed_mass(ev));
+            }
+        }
+        __syncthreads();
+        if (tid < 256) {   // merge the per-wave histograms
+            unsigned long long h = 0;
+            for (int w = 0; w < kSampWaves; ++w) h += hist[w][tid];
+            hist[0][tid] = h;
         }
         __syncthreads();
         if (tid == 0) {
             unsigned long long above = s_above;
             int beta = -1;
             for (int k = 255; k >= 0; --k) {
-                if ((double)(above + hist[k]) >= target) { beta = k; break; }
-                above += hist[k];
+                if ((double)(above + hist[0][k]) >= target) { beta = k; break; }
+                above += hist[0][k];
             }
             if (beta < 0) {   // no value reaches top_p (rounding): every token
                 s_all = 1;
@@ -139,7 +177,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
             if (!s_all) {
                 s_above = above;
                 s_prefix = (prefix << 8) | (uint32_t)beta;
-                s_mass = above + hist[beta];
+                s_mass = above + hist[0][beta];
             }
         }
         __syncthreads();
@@ -150,36 +188,60 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
 
     // u in [0,1) with 24 bits; t = floor(u * M)
     const uint64_t r24 = splitmix64(rng_key(p.seeds[b], 1ull << 33) + 2ull * (uint64_t)p.step[b] + (uint64_t)p.slot) >> 40;
-    const unsigned long long t = __umul64hi(r24 << 40, M);
+    const unsigned long long tsel = __umul64hi(r24 << 40, M);
 
-    unsigned long long loc = 0;
-    for (int jj = j0; jj < j1; ++jj) {
-        const float e = exp2f((lg[jj] - mx) * kT);
-        if (__float_as_uint(e) >= theta) loc += fixed_mass(e);
+    // nucleus mass of each wave's id range, exclusive prefix over waves
+    unsigned long long wm = 0;
+#pragma unroll 4
+    for (int t = 0; t < nt; ++t) {
+        float v[4];
+        load4(t, v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float ev = exp2f((v[e] - mx) * kT);
+            wm += (valid(t, e) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
+        }
     }
-    // exclusive block scan of loc
-    unsigned long long inc = loc;
-    for (int d = 1; d < 64; d <<= 1) {
-        const unsigned long long o = shfl_up_u64(inc, d);
-        if (lane >= d) inc += o;
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)wm, o), hi = __shfl_xor((uint32_t)(wm >> 32), o);
+        wm += ((unsigned long long)hi << 32) | lo;
     }
-    if (lane == 63) s_u64[wave] = inc;
     __syncthreads();
-    unsigned long long base = 0;
-    for (int w = 0; w < wave; ++w) base += s_u64[w];
-    const unsigned long long excl = base + inc - loc;
-    if (loc > 0 && excl <= t && t < excl + loc) {
-        unsigned long long run = excl;
-        for (int jj = j0; jj < j1; ++jj) {
-            const float e = exp2f((lg[jj] - mx) * kT);
-            if (__float_as_uint(e) >= theta) {
-                run += fixed_mass(e);
-                if (run > t) {
-                    p.best[b] = (1ull << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)jj);
+    if (lane == 0) s_u64[wave] = wm;
+    __syncthreads();
+    unsigned long long run = 0;
+    for (int w = 0; w < wave; ++w) run += s_u64[w];
+    if (wm == 0 || tsel < run || tsel >= run + wm) return;
+    // this wave's range holds the target: walk its sub-tiles in id order
+    for (int t = 0; t < nt; ++t) {
+        float v[4];
+        load4(t, v);
+        unsigned long long m4[4], loc = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float ev = exp2f((v[e] - mx) * kT);
+            m4[e] = (valid(t, e) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
+            loc += m4[e];
+        }
+        unsigned long long inc = loc;
+        for (int d = 1; d < 64; d <<= 1) {
+            const unsigned long long o = shfl_up_u64(inc, d);
+            if (lane >= d) inc += o;
+        }
+        const unsigned long long excl = run + inc - loc;
+        if (loc > 0 && excl <= tsel && tsel < excl + loc) {
+            unsigned long long r = excl;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                r += m4[e];
+                if (m4[e] > 0 && r > tsel) {
+                    p.best[b] = (1ull << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)(w0 + t * 256 + 4 * lane + e));
                     break;
                 }
             }
         }
+        run += __shfl(inc, 63);
+        if (run > tsel) break;
     }
 }
 

@@ -25,6 +25,14 @@ __device__ __forceinline__ uint32_t f2bf(float f) {
 __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
     return f2bf(lo) | (f2bf(hi) << 16);
 }
+// Two floats into one bf16x2 word (element lo in the low half), rounded to
+// nearest even by the hardware conversion (v_cvt_pk_bf16_f32); for finite
+// inputs the same bits as f2bf.
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+__device__ __forceinline__ uint32_t pack_bf2_hw(float lo, float hi) {
+    const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
 // x ~= bf(hi) + bf(lo): the bf16 rounding of x and of its remainder.
 __device__ __forceinline__ void split_bf(float x, uint32_t &hi, uint32_t &lo) {
     hi = f2bf(x);
@@ -34,11 +42,9 @@ __device__ __forceinline__ void split_bf(float x, uint32_t &hi, uint32_t &lo) {
 __device__ __forceinline__ void split8(const float *v, u32x4 &hi, u32x4 &lo) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        uint32_t h0, l0, h1, l1;
-        split_bf(v[2 * i], h0, l0);
-        split_bf(v[2 * i + 1], h1, l1);
-        hi[i] = h0 | (h1 << 16);
-        lo[i] = l0 | (l1 << 16);
+        const uint32_t h = pack_bf2_hw(v[2 * i], v[2 * i + 1]);
+        hi[i] = h;
+        lo[i] = pack_bf2_hw(v[2 * i] - bf_lo(h), v[2 * i + 1] - bf_hi(h));
     }
 }
 

@@ -233,21 +233,27 @@ void launch_gemm(const GemmParams &p, hipStream_t s) {
 // ---- causal grouped-query flash attention for a chunk of queries ----------
 // One workgroup per (sequence, KV group, group of up to four query heads,
 // 32-query block); wave w computes one head for all 32 queries (two 16-column
-// MFMA tiles).  Keys and values of 64 positions at a time are staged in LDS
-// and shared by the workgroup's heads.
+// MFMA tiles).  Keys and values of 64 positions at a time are staged in LDS,
+// shared by the workgroup's heads and double-buffered: the next stage is
+// requested into registers before the current one is multiplied.  Per stage
+// the scores of all 64 keys are formed first (both query tiles), then one
+// online-softmax update per query tile (the causal mask only on stages that
+// reach the diagonal), so the accumulator rescale and the row max / sum
+// shuffles happen once per 64 keys.  Scores stay unscaled; the softmax scale
+// 1/sqrt(d) (times log2 e) enters through one fma per score in the exponent.
+// Two workgroups fit per CU so that one's softmax overlaps the other's MFMAs.
 constexpr int kAQ = 32;         // queries per workgroup
 constexpr int kAK = 64;         // keys per LDS stage
 
 template <int D>
-__global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillParams p) {
+__global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     constexpr int NC = D / 32, NT = D / 16;
     constexpr int KS = D + 8;           // padded K row (elements)
     constexpr int VS = 40;              // padded V tile row (elements)
-    __shared__ __align__(16) uint16_t ks[kAK * KS];
-    __shared__ __align__(16) uint16_t vs[2 * D * VS];
+    __shared__ __align__(16) uint16_t ks2[2][kAK * KS];
+    __shared__ __align__(16) uint16_t vs2[2][2 * D * VS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nthr = blockDim.x;
     const int j = lane & 15, g = lane >> 4;
     const int qpg = p.n_q / p.n_kv;
     const int nhg = (qpg + 3) / 4;               // head groups per KV group
@@ -282,77 +288,118 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillParams p) {
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
 
     const int kend = qpos0 + kAQ;              // keys [0, kend) may be visible
-    for (int kb0 = 0; kb0 < kend; kb0 += kAK) {
-        __syncthreads();
-        // stage K rows kb0..kb0+63 and the two V tiles
-        for (int c = tid; c < kAK * D / 8; c += nthr) {
-            const int r = c / (D / 8), e = (c - r * (D / 8)) * 8;
-            *(u32x4 *)(&ks[r * KS + e]) = *(const u32x4 *)(kbase + (int64_t)(kb0 + r) * D + e);
+    // K rows and V tiles of one 64-key stage, KU 16-byte chunks per thread
+    constexpr int KCH = kAK * D / 8, VCH = 2 * D * 4;   // chunks per stage
+    constexpr int KU = (KCH + VCH) / 256;
+    const int nstage = (kend + kAK - 1) / kAK;
+    u32x4 stg[KU];
+    auto stage_load = [&](int kb0) {
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int c = tid + u * 256;
+            const uint16_t *src;
+            if (u * 256 < KCH) {          // K rows (whole unrolled slots, KCH is a multiple of 256)
+                const int r = c / (D / 8), e = (c - r * (D / 8)) * 8;
+                src = kbase + (int64_t)(kb0 + r) * D + e;
+            } else {                      // V tiles: row = tile * D + dim
+                const int cv = c - KCH;
+                const int row = cv >> 2, e = (cv & 3) * 8;
+                src = vbase + (int64_t)(kb0 >> 5) * D * 32 + (int64_t)row * 32 + e;
+            }
+            stg[u] = *(const u32x4 *)src;
         }
-        for (int c = tid; c < 2 * D * 4; c += nthr) {
-            const int row = c >> 2, e = (c & 3) * 8;       // row = tile*D + dim
-            *(u32x4 *)(&vs[row * VS + e]) = *(const u32x4 *)(vbase + (int64_t)(kb0 >> 5) * D * 32 + (int64_t)row * 32 + e);
+    };
+    auto stage_store = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int c = tid + u * 256;
+            if (u * 256 < KCH) {
+                const int r = c / (D / 8), e = (c - r * (D / 8)) * 8;
+                *(u32x4 *)(&ks2[buf][r * KS + e]) = stg[u];
+            } else {
+                const int cv = c - KCH;
+                const int row = cv >> 2, e = (cv & 3) * 8;
+                *(u32x4 *)(&vs2[buf][row * VS + e]) = stg[u];
+            }
         }
-        __syncthreads();
-        if (!active) continue;
+    };
+    stage_load(0);
+    stage_store(0);
+    __syncthreads();
+    for (int st_i = 0; st_i < nstage; ++st_i) {
+        const int kb0 = st_i * kAK;
+        const int buf = st_i & 1;
+        // the next stage is always requested (one stage past the end stays
+        // inside the padded cache), so the load count per step is fixed
+        stage_load(kb0 + kAK);
+        const uint16_t *ks = ks2[buf], *vs = vs2[buf];
+        if (active) {
+            // scores S^T for 64 keys (four 16-key tiles) and both query tiles
+            f32x4 sc[2][4];
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const int kb = kb0 + 32 * half;
-            if (kb >= kend) break;
-            u32x4 kf[2][NC];
+            for (int tau = 0; tau < 4; ++tau) {
+                u32x4 kf[NC];
 #pragma unroll
-            for (int tau = 0; tau < 2; ++tau)
+                for (int c = 0; c < NC; ++c) kf[c] = *(const u32x4 *)(&ks[(16 * tau + j) * KS + 32 * c + 8 * g]);
 #pragma unroll
-                for (int c = 0; c < NC; ++c)
-                    kf[tau][c] = *(const u32x4 *)(&ks[(32 * half + 16 * tau + j) * KS + 32 * c + 8 * g]);
+                for (int ct = 0; ct < 2; ++ct) {
+                    sc[ct][tau] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) sc[ct][tau] = mfma16(kf[c], qb[ct][c], sc[ct][tau]);
+                }
+            }
+            const bool diag = kb0 + kAK - 1 > qpos0;   // some key may lie past some query
+            u32x4 pt[2][2];
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 const int qabs = qpos0 + 16 * ct + j;
-                f32x4 st[2];
-#pragma unroll
-                for (int tau = 0; tau < 2; ++tau) {
-                    st[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int c = 0; c < NC; ++c) st[tau] = mfma16(kf[tau][c], qb[ct][c], st[tau]);
-                }
                 float mx = -INFINITY;
 #pragma unroll
-                for (int tau = 0; tau < 2; ++tau)
+                for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        const int key = kb + 16 * tau + 4 * g + v;
-                        const float sv = key <= qabs ? st[tau][v] * scale : -INFINITY;
-                        st[tau][v] = sv;
+                        float sv = sc[ct][tau][v];
+                        if (diag) sv = kb0 + 16 * tau + 4 * g + v <= qabs ? sv : -INFINITY;
+                        sc[ct][tau][v] = sv;
                         mx = fmaxf(mx, sv);
                     }
                 mx = col_max(mx);
-                const float m_new = fmaxf(m_run[ct], mx);
-                // a query row sees at least key 0 in the first block, so m_new is finite
+                // a query row sees key 0 in the first stage, so m_new is finite
+                const float m_new = fmaxf(m_run[ct], mx * scale);
                 const float alpha = exp2f(m_run[ct] - m_new);
                 float ps = 0.f;
 #pragma unroll
-                for (int tau = 0; tau < 2; ++tau)
+                for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        const float e = exp2f(st[tau][v] - m_new);
-                        st[tau][v] = e;
+                        const float e = exp2f(fmaf(sc[ct][tau][v], scale, -m_new));
+                        sc[ct][tau][v] = e;
                         ps += e;
                     }
                 l_run[ct] = l_run[ct] * alpha + col_sum(ps);
                 m_run[ct] = m_new;
-                u32x4 pt;
-                pt[0] = pack_bf2(st[0][0], st[0][1]);
-                pt[1] = pack_bf2(st[0][2], st[0][3]);
-                pt[2] = pack_bf2(st[1][0], st[1][1]);
-                pt[3] = pack_bf2(st[1][2], st[1][3]);
 #pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    o[ct][t] *= alpha;
-                    const u32x4 vf = *(const u32x4 *)(&vs[(half * D + 16 * t + j) * VS + 8 * g]);
-                    o[ct][t] = mfma16(vf, pt, o[ct][t]);
+                for (int t = 0; t < NT; ++t) o[ct][t] *= alpha;
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    pt[ct][half][0] = pack_bf2_hw(sc[ct][2 * half][0], sc[ct][2 * half][1]);
+                    pt[ct][half][1] = pack_bf2_hw(sc[ct][2 * half][2], sc[ct][2 * half][3]);
+                    pt[ct][half][2] = pack_bf2_hw(sc[ct][2 * half + 1][0], sc[ct][2 * half + 1][1]);
+                    pt[ct][half][3] = pack_bf2_hw(sc[ct][2 * half + 1][2], sc[ct][2 * half + 1][3]);
                 }
             }
+            // O^T += V^T P^T, each V fragment serving both query tiles
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const u32x4 vf = *(const u32x4 *)(&vs[(half * D + 16 * t + j) * VS + 8 * g]);
+#pragma unroll
+                    for (int ct = 0; ct < 2; ++ct) o[ct][t] = mfma16(vf, pt[ct][half], o[ct][t]);
+                }
         }
+        stage_store(buf ^ 1);
+        __syncthreads();
     }
     if (!active) return;
     const int qd = p.n_q * D;
@@ -379,7 +426,7 @@ void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s) {
     const int nhg = (qpg + 3) / 4;
     const int nqb = (p.g.clen + kAQ - 1) / kAQ;
     const int grid = p.g.B * p.n_kv * nhg * nqb;
-    const int threads = 64 * (qpg < 4 ? qpg : 4);
+    const int threads = 256;   // four waves stage K/V even when the group has fewer heads
     if (p.d == 128) hipLaunchKernelGGL(k_attn_prefill<128>, dim3(grid), dim3(threads), 0, s, p);
     else hipLaunchKernelGGL(k_attn_prefill<64>, dim3(grid), dim3(threads), 0, s, p);
 }

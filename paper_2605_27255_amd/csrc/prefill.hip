@@ -74,159 +74,191 @@ void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, i
 }
 
 // ---- MFMA GEMM  C^T[N][M] = W[N][K] X[M][K]^T, both operands tiled ---------
-// Workgroup tile 128 (rows of W) x 128 (tokens), one 32-wide k tile per
-// stage, four waves in a 2x2 arrangement of 64x64, LDS double-buffered.  With
-// a lo plane every W fragment meets the X hi and X lo fragments (two MFMAs).
-constexpr int kGBN = 128, kGBM = 128;
-constexpr int kGStripsN = kGBN / 16, kGStripsM = kGBM / 16;
-
-template <int EPI, bool HASLO>
-__global__ __launch_bounds__(256) void k_gemm(GemmParams p) {
-    constexpr int NOPS = HASLO ? 3 : 2;                       // W, X hi, (X lo)
-    constexpr int STAGE = (kGStripsN + (NOPS - 1) * kGStripsM) * 512;
-    constexpr int NCH = STAGE / 8 / 256;                      // 16 B chunks per thread
-    __shared__ __align__(16) uint16_t lds[2][STAGE];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int j = lane & 15, g = lane >> 4;
-    const int wn = wave >> 1, wm = wave & 1;
-    const int nblk_n = (p.N + kGBN - 1) / kGBN;
-    const int bn = blockIdx.x % nblk_n, bm = blockIdx.x / nblk_n;
-    const int KT = p.K >> 5;
-    const int NS = p.N >> 4, MS = p.M >> 4;   // strips
-
-    u32x4 reg[NCH];
-    auto gload = [&](int kt) {
+// Fused epilogue of one 16x16 accumulator fragment: lane (j, g) holds rows
+// 16 strip + 4 g + v of token m.  Every lane takes part in the shuffles
+// before any of them returns.
+template <int EPI>
+__device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int strip, int m) {
+    const int lane = threadIdx.x & 63, g = lane >> 4;
+    f32x4 other;
+    if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
 #pragma unroll
-        for (int r = 0; r < NCH; ++r) {
-            const int c = tid + r * 256;                 // 16 B chunk of the stage
-            const int op = c >> 9;                       // 512 chunks per operand (8 strips x 1 KB)
-            const int st = (c >> 6) & 7, within = c & 63;
-            const int strip = (op == 0 ? bn * kGStripsN : bm * kGStripsM) + st;
-            const int nstr = op == 0 ? NS : MS;
-            const uint16_t *src = op == 0 ? p.W : (op == 1 ? p.X : p.Xlo);
-            u32x4 v = u32x4{0u, 0u, 0u, 0u};
-            if (strip < nstr) v = *(const u32x4 *)(src + ((int64_t)strip * KT + kt) * 512 + within * 8);
-            reg[r] = v;
-        }
-    };
-    auto sstore = [&](int buf) {
-#pragma unroll
-        for (int r = 0; r < NCH; ++r) *(u32x4 *)(&lds[buf][(tid + r * 256) * 8]) = reg[r];
-    };
-
-    f32x4 acc[4][4];
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    int buf = 0;
-    for (int kt = 0; kt < KT; ++kt) {
-        const bool more = kt + 1 < KT;
-        if (more) gload(kt + 1);
-        u32x4 af[4], bf[4], bl[4];
-#pragma unroll
-        for (int si = 0; si < 4; ++si) af[si] = *(const u32x4 *)(&lds[buf][(4 * wn + si) * 512 + lane * 8]);
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi) {
-            bf[mi] = *(const u32x4 *)(&lds[buf][(kGStripsN + 4 * wm + mi) * 512 + lane * 8]);
-            if (HASLO) bl[mi] = *(const u32x4 *)(&lds[buf][(kGStripsN + kGStripsM + 4 * wm + mi) * 512 + lane * 8]);
-        }
-#pragma unroll
-        for (int si = 0; si < 4; ++si)
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi) {
-                acc[si][mi] = mfma16(af[si], bf[mi], acc[si][mi]);
-                if (HASLO) acc[si][mi] = mfma16(af[si], bl[mi], acc[si][mi]);
-            }
-        if (more) {
-            sstore(buf ^ 1);
-            __syncthreads();
-            buf ^= 1;
-        }
+        for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(val[v], 32);
     }
-
-    // ---- epilogue -----------------------------------------------------------
-    const int d = p.d, hs = d >> 4;
-    const int qs = p.n_q * hs, ks = p.n_kv * hs;
+    if (strip >= (p.N >> 4) || m >= p.M) return;
+    const int b = m / p.g.mpad, i = m - b * p.g.mpad;
+    if (i >= p.g.clen) return;
+    const int row0 = strip * 16 + 4 * g;
+    if (EPI == EPI_STORE) {
+        if (p.bias) val += *(const f32x4 *)(p.bias + row0);
+        *(f32x4 *)(p.out + (int64_t)m * p.N + row0) = val;
+    } else if (EPI == EPI_RESID) {
+        f32x4 *o = (f32x4 *)(p.out + (int64_t)m * p.N + row0);
+        *o = *o + val;
+    } else if (EPI == EPI_SWIGLU) {
+        if (g < 2) {
+            uint32_t h[4], l[4];
 #pragma unroll
-    for (int si = 0; si < 4; ++si) {
-        const int strip = bn * kGStripsN + 4 * wn + si;
-        const int row0 = strip * 16 + 4 * g;
+            for (int v = 0; v < 4; ++v) split_bf(silu_p(val[v]) * other[v], h[v], l[v]);
+            const int64_t at = tiled_index(m, strip * 8 + 4 * g, p.N >> 1);
+            *(u32x2 *)(p.act_hi + at) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+            *(u32x2 *)(p.act_lo + at) = u32x2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
+        }
+    } else if (EPI == EPI_QKV) {
+        const int d = p.d, hs = d >> 4;
+        const int qs = p.n_q * hs, ks = p.n_kv * hs;
+        const int pos = p.g.c0 + i;
+        if (strip < qs + ks) {
+            const bool isq = strip < qs;
+            const int sidx = isq ? strip : strip - qs;
+            const int head = sidx / hs, t = sidx - head * hs;
+            const int jr = 8 * t + 4 * (g & 1);
+            const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
+            const float *cs = p.rope_cos + (int64_t)pos * (d >> 1) + jr;
+            const float *sn = p.rope_sin + (int64_t)pos * (d >> 1) + jr;
+            float r[4];
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi) {
-            const int m = bm * kGBM + (4 * wm + mi) * 16 + j;
-            f32x4 val = acc[si][mi];
-            f32x4 other;
-            if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+            for (int v = 0; v < 4; ++v)
+                r[v] = (g < 2) ? val[v] * cs[v] - other[v] * sn[v] : val[v] * cs[v] + other[v] * sn[v];
+            u32x2 w;
+            w[0] = pack_bf2(r[0], r[1]);
+            w[1] = pack_bf2(r[2], r[3]);
+            uint16_t *dst = isq ? p.q + (((int64_t)b * p.n_q + head) * p.g.mpad + i) * d + dim0
+                                : p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0;
+            *(u32x2 *)dst = w;
+        } else {
+            const int r0 = (strip - qs - ks) * 16 + 4 * g;
+            const int kvh = r0 / d, dim = r0 - kvh * d;
+            uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
+                            ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot_p(pos & 31);
 #pragma unroll
-                for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(val[v], 32);
-            }
-            if (strip >= NS || m >= p.M) continue;
-            const int b = m / p.g.mpad, i = m - b * p.g.mpad;
-            if (i >= p.g.clen) continue;
-            if (EPI == EPI_STORE) {
-                if (p.bias) val += *(const f32x4 *)(p.bias + row0);
-                *(f32x4 *)(p.out + (int64_t)m * p.N + row0) = val;
-            } else if (EPI == EPI_RESID) {
-                f32x4 *o = (f32x4 *)(p.out + (int64_t)m * p.N + row0);
-                *o = *o + val;
-            } else if (EPI == EPI_SWIGLU) {
-                if (g < 2) {
-                    uint32_t h[4], l[4];
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) split_bf(silu_p(val[v]) * other[v], h[v], l[v]);
-                    const int64_t at = tiled_index(m, strip * 8 + 4 * g, p.N >> 1);
-                    *(u32x2 *)(p.act_hi + at) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
-                    *(u32x2 *)(p.act_lo + at) = u32x2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
-                }
-            } else if (EPI == EPI_QKV) {
-                const int pos = p.g.c0 + i;
-                if (strip < qs + ks) {
-                    const bool isq = strip < qs;
-                    const int sidx = isq ? strip : strip - qs;
-                    const int head = sidx / hs, t = sidx - head * hs;
-                    const int jr = 8 * t + 4 * (g & 1);
-                    const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
-                    const float *cs = p.rope_cos + (int64_t)pos * (d >> 1) + jr;
-                    const float *sn = p.rope_sin + (int64_t)pos * (d >> 1) + jr;
-                    float r[4];
-#pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        r[v] = (g < 2) ? val[v] * cs[v] - other[v] * sn[v] : val[v] * cs[v] + other[v] * sn[v];
-                    u32x2 w;
-                    w[0] = pack_bf2(r[0], r[1]);
-                    w[1] = pack_bf2(r[2], r[3]);
-                    uint16_t *dst = isq ? p.q + (((int64_t)b * p.n_q + head) * p.g.mpad + i) * d + dim0
-                                        : p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0;
-                    *(u32x2 *)dst = w;
-                } else {
-                    const int r0 = (strip - qs - ks) * 16 + 4 * g;
-                    const int kvh = r0 / d, dim = r0 - kvh * d;
-                    uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
-                                    ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot_p(pos & 31);
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(val[v]);
-                }
-            }
+            for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(val[v]);
         }
     }
 }
 
+// Workgroup tile BN x BM = (GN WNT 16) x (GM WMT 16), GN x GM waves of
+// (WNT x WMT) 16x16 fragments each; one 32-wide k tile per stage, LDS
+// double-buffered, the next stage requested into registers before the
+// current stage's MFMAs.  Workgroups run token-tile fastest, so the ones in
+// flight share a few weight tiles (cache-resident) and sweep the tokens.
+// With a lo plane every W fragment meets the X hi and X lo fragments.
+template <int EPI, bool HASLO, int WNT, int WMT, int GN, int GM>
+__global__ __launch_bounds__(GN * GM * 64) void k_gemm(GemmParams p) {
+    constexpr int NT = GN * GM * 64;
+    constexpr int SN = GN * WNT, SM = GM * WMT;               // 16-row strips per tile
+    constexpr int NOPS = HASLO ? 3 : 2;                       // W, X hi, (X lo)
+    constexpr int TILES = SN + (NOPS - 1) * SM;               // 1 KB tiles per stage
+    constexpr int STAGE = TILES * 512;
+    constexpr int NCH = TILES * 64 / NT;                      // 16 B chunks per thread per stage
+    static_assert(TILES * 64 % NT == 0, "stage must split evenly over the threads");
+    extern __shared__ __align__(16) uint16_t lds[];           // [2][STAGE]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j = lane & 15;
+    const int wn = wave / GM, wm = wave - wn * GM;
+    const int nblk_m = (p.M + SM * 16 - 1) / (SM * 16);
+    const int bm = blockIdx.x % nblk_m, bn = blockIdx.x / nblk_m;
+    const int KT = p.K >> 5;
+    const int NS = p.N >> 4, MS = p.M >> 4;   // strips
+
+    // chunk c of a stage: tile c / 64 (W strips, then X hi, then X lo), 16 B c % 64
+    const uint16_t *src[NCH];
+#pragma unroll
+    for (int r = 0; r < NCH; ++r) {
+        const int c = tid + r * NT;
+        const int t = c >> 6, within = c & 63;
+        const bool isw = t < SN, ishi = !isw && t < SN + SM;
+        int strip = isw ? bn * SN + t : bm * SM + (t - SN - (ishi ? 0 : SM));
+        strip = strip < (isw ? NS : MS) ? strip : 0;          // padding strips read strip 0 (masked later)
+        const uint16_t *base = isw ? p.W : (ishi ? p.X : p.Xlo);
+        src[r] = base + (int64_t)strip * KT * 512 + within * 8;
+    }
+    u32x4 ra[NCH], rb[NCH];
+    // stages past K re-read the last stage (their products are never kept)
+    auto gload = [&](int kt, u32x4 (&reg)[NCH]) {
+        const int ktc = kt < KT ? kt : KT - 1;
+#pragma unroll
+        for (int r = 0; r < NCH; ++r) reg[r] = *(const u32x4 *)(src[r] + (int64_t)ktc * 512);
+    };
+    auto sstore = [&](int buf, const u32x4 (&reg)[NCH]) {
+#pragma unroll
+        for (int r = 0; r < NCH; ++r) *(u32x4 *)(&lds[buf * STAGE + (tid + r * NT) * 8]) = reg[r];
+    };
+
+    f32x4 acc[WNT][WMT];
+#pragma unroll
+    for (int a = 0; a < WNT; ++a)
+#pragma unroll
+        for (int c = 0; c < WMT; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](int buf) {
+        const uint16_t *L = lds + buf * STAGE;
+        u32x4 af[WNT], bh[WMT], bl[WMT];
+#pragma unroll
+        for (int si = 0; si < WNT; ++si) af[si] = *(const u32x4 *)(&L[(wn * WNT + si) * 512 + lane * 8]);
+#pragma unroll
+        for (int mi = 0; mi < WMT; ++mi) {
+            bh[mi] = *(const u32x4 *)(&L[(SN + wm * WMT + mi) * 512 + lane * 8]);
+            if (HASLO) bl[mi] = *(const u32x4 *)(&L[(SN + SM + wm * WMT + mi) * 512 + lane * 8]);
+        }
+#pragma unroll
+        for (int si = 0; si < WNT; ++si)
+#pragma unroll
+            for (int mi = 0; mi < WMT; ++mi) {
+                acc[si][mi] = mfma16(af[si], bh[mi], acc[si][mi]);
+                if (HASLO) acc[si][mi] = mfma16(af[si], bl[mi], acc[si][mi]);
+            }
+    };
+    // two stages in registers ahead of the one in LDS: stage kt + 2 is
+    // requested while stage kt is multiplied and written to LDS after kt + 1
+    gload(0, ra);
+    sstore(0, ra);
+    gload(1, rb);
+    __syncthreads();
+    gload(2, ra);
+    for (int kt = 0; kt < KT; kt += 2) {
+        compute(0);
+        sstore(1, rb);
+        __syncthreads();
+        gload(kt + 3, rb);
+        if (kt + 1 < KT) compute(1);
+        sstore(0, ra);
+        __syncthreads();
+        gload(kt + 4, ra);
+    }
+
+#pragma unroll
+    for (int si = 0; si < WNT; ++si)
+#pragma unroll
+        for (int mi = 0; mi < WMT; ++mi)
+            gemm_epi<EPI>(p, acc[si][mi], bn * SN + wn * WNT + si, bm * SM * 16 + (wm * WMT + mi) * 16 + j);
+}
+
+template <int EPI, bool HASLO, int WNT, int WMT, int GN, int GM>
+static void launch_gemm_t(const GemmParams &p, hipStream_t s) {
+    constexpr int SN = GN * WNT, SM = GM * WMT;
+    const int grid = ((p.N + SN * 16 - 1) / (SN * 16)) * ((p.M + SM * 16 - 1) / (SM * 16));
+    const int lds = 2 * (SN + (HASLO ? 2 : 1) * SM) * 512 * 2;
+    hipLaunchKernelGGL((k_gemm<EPI, HASLO, WNT, WMT, GN, GM>), dim3(grid), dim3(GN * GM * 64), lds, s, p);
+}
+
+// Tile (from a sweep on MI355X at 4096 tokens over the 4B shapes): 128
+// weight rows x 128 tokens, eight waves of 32 x 64, two waves per SIMD.
+template <int EPI, bool HASLO>
+static void launch_gemm_e(const GemmParams &p, hipStream_t s) {
+    launch_gemm_t<EPI, HASLO, 2, 4, 4, 2>(p, s);
+}
+
 void launch_gemm(const GemmParams &p, hipStream_t s) {
-    const int grid = ((p.N + kGBN - 1) / kGBN) * ((p.M + kGBM - 1) / kGBM);
     if (!p.Xlo) {   // the gathered embedding pairs are exact in bf16
-        hipLaunchKernelGGL((k_gemm<EPI_STORE, false>), dim3(grid), dim3(256), 0, s, p);
+        launch_gemm_e<EPI_STORE, false>(p, s);
         return;
     }
     switch (p.epi) {
-        case EPI_STORE: hipLaunchKernelGGL((k_gemm<EPI_STORE, true>), dim3(grid), dim3(256), 0, s, p); break;
-        case EPI_RESID: hipLaunchKernelGGL((k_gemm<EPI_RESID, true>), dim3(grid), dim3(256), 0, s, p); break;
-        case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm<EPI_SWIGLU, true>), dim3(grid), dim3(256), 0, s, p); break;
-        default: hipLaunchKernelGGL((k_gemm<EPI_QKV, true>), dim3(grid), dim3(256), 0, s, p); break;
+        case EPI_STORE: launch_gemm_e<EPI_STORE, true>(p, s); break;
+        case EPI_RESID: launch_gemm_e<EPI_RESID, true>(p, s); break;
+        case EPI_SWIGLU: launch_gemm_e<EPI_SWIGLU, true>(p, s); break;
+        default: launch_gemm_e<EPI_QKV, true>(p, s); break;
     }
 }
 

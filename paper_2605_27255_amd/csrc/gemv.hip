@@ -726,11 +726,13 @@ __global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
 
 // Sum of the k-range partials in range order, then the fused epilogue.
 template <int NBT, int EPI>
-__global__ __launch_bounds__(512) void k_gemv_fin(GemvParams p) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// One wave per strip (the vocabulary head never splits K, so the logits
+// epilogue's workgroup-wide argmax is not needed here).
+__global__ __launch_bounds__(64) void k_gemv_fin(GemvParams p) {
+    const int lane = threadIdx.x & 63;
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
-    const int strip = blockIdx.x * kNW + wave;
+    const int strip = blockIdx.x;
     const bool sok = strip < nstrips;
     const int B = p.B;
     const int row0 = (sok ? strip : 0) * 16 + 4 * g;
@@ -785,10 +787,10 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     ksplit = ksplit < NC ? ksplit : NC;
     const int64_t cap = q.part_cap / ((int64_t)q.B * q.N);
     ksplit = ksplit < cap ? ksplit : (int)cap;
-    q.ksplit = ksplit < 1 ? 1 : ksplit;
+    q.ksplit = (ksplit < 1 || EPI == EPI_LOGITS) ? 1 : ksplit;
     const int lds_w = 2 * 2 * q.B * (kWideChunk * 32 + 8) * 2 + 16;
     hipLaunchKernelGGL((k_gemv_wide<NBT, EPI>), dim3(rtiles * q.ksplit), dim3(kNW * 64), lds_w, s, q);
-    if (q.ksplit > 1) hipLaunchKernelGGL((k_gemv_fin<NBT, EPI>), dim3(rtiles), dim3(kNW * 64), 0, s, q);
+    if (q.ksplit > 1) hipLaunchKernelGGL((k_gemv_fin<NBT, EPI>), dim3(q.N >> 4), dim3(64), 0, s, q);
 }
 
 // Batch size U: two batches of U tiles per wave are in flight.  Five when a

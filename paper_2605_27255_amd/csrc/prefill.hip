@@ -140,8 +140,10 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
 // Workgroup tile BN x BM = (GN WNT 16) x (GM WMT 16), GN x GM waves of
 // (WNT x WMT) 16x16 fragments each; one 32-wide k tile per stage, LDS
 // double-buffered, the next stage requested into registers before the
-// current stage's MFMAs.  Workgroups run token-tile fastest, so the ones in
-// flight share a few weight tiles (cache-resident) and sweep the tokens.
+// current stage's MFMAs.  Workgroups run weight-tile fastest: the ones in
+// flight share a few token tiles, and the weight matrix (at most a few
+// hundred MB) is re-read from the memory-side cache rather than the token
+// activations (over a GB for a batch of long prompts) from HBM.
 // With a lo plane every W fragment meets the X hi and X lo fragments.
 template <int EPI, bool HASLO, int WNT, int WMT, int GN, int GM>
 __global__ __launch_bounds__(GN * GM * 64) void k_gemm(GemmParams p) {
@@ -156,8 +158,8 @@ __global__ __launch_bounds__(GN * GM * 64) void k_gemm(GemmParams p) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = lane & 15;
     const int wn = wave / GM, wm = wave - wn * GM;
-    const int nblk_m = (p.M + SM * 16 - 1) / (SM * 16);
-    const int bm = blockIdx.x % nblk_m, bn = blockIdx.x / nblk_m;
+    const int nblk_n = (p.N + SN * 16 - 1) / (SN * 16);
+    const int bn = blockIdx.x % nblk_n, bm = blockIdx.x / nblk_n;
     const int KT = p.K >> 5;
     const int NS = p.N >> 4, MS = p.M >> 4;   // strips
 

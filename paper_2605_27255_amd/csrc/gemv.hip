@@ -1,11 +1,14 @@
 // Weight-streaming skinny GEMM of the decode step (batch 1..32).
 //
-// Y^T[N][B] = W[N][K] X^T with W in 16x32 bf16 tiles.  A workgroup of eight
-// waves owns 8/KS 16-row strips of W, KS waves per strip splitting its K range
-// (wave k of a strip takes k-tiles k, k+KS, k+2KS, ...); every wave streams
-// its tiles with one contiguous 1 KB load each as the MFMA A operand.  KS is
-// chosen per matrix: tall matrices (the LM head) give every wave a whole
-// strip, short ones split K to keep enough loads in flight.
+// Y^T[N][B] = W[N][K] X^T with W in 16x32 bf16 tiles.  A strip group is 8/KS
+// 16-row strips of W handled by the eight waves of a workgroup, KS waves per
+// strip splitting its K range (wave k of a strip takes k-tiles k, k+KS,
+// k+2KS, ...); every wave streams its tiles with one contiguous 1 KB load
+// each as the MFMA A operand.  KS is chosen per matrix: tall matrices (the LM
+// head) give every wave a whole strip, short ones split K to keep enough
+// loads in flight.  The layer matrices run one workgroup per compute unit,
+// each taking every n-th strip group in one continuous weight stream (this
+// evens out the tail of the 1216-strip gate/up matrix).
 //
 // Memory operations retire in issue order, so a wave first loads what the
 // prologue and epilogue need (the activation sources of the first LDS chunk,
@@ -395,9 +398,12 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams &p, f32x4 (&fin)[
 template <int NBT, int KS, int PRO, int EPI, int U>
 __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     // U: k-tiles per wave per load batch (two batches in flight).  Every
-    // wave's slices of X fit in LDS at once (wave-private staging).
+    // wave's slices of X fit in LDS at once (wave-private staging).  A
+    // workgroup takes strip groups blockIdx.x, blockIdx.x + gridDim.x, ...:
+    // X is staged once and the weight stream runs on across strip groups,
+    // each group ending in its reduction and epilogue.
     static_assert(KS > 1, "the strip reduction orders the RMSNorm scalars");
-    constexpr int SPW = kNW / KS;          // strips per workgroup
+    constexpr int SPW = kNW / KS;          // strips per strip group
     constexpr int NA = NAcc<PRO>::n;
     constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
     extern __shared__ __align__(16) uint16_t xs[];
@@ -407,18 +413,22 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
     const int ks = wave % KS;              // k-split index inside the strip
-    const int strip = blockIdx.x * SPW + wave / KS;
-    const bool sok = strip < nstrips;
-    const bool lead = ks == 0 && sok;      // the wave that reduces and writes the strip
+    const int slot = wave / KS;            // strip of this wave inside a group
+    const int G = (nstrips + SPW - 1) / SPW;
+    const int ngrp = (G - 1 - (int)blockIdx.x) / (int)gridDim.x + 1;   // groups of this workgroup
     const int KT = p.K >> 5, HT = p.H >> 5;
     const int B = p.B;
-    const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
-    const int row0 = strip * 16 + 4 * g;   // first of this lane's four output rows
     const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
     // LDS: X hi planes, X lo planes, then the reduction buffer
-    const int rstride = ((KT + KS - 1) / KS) * 32 + 8;   // row stride of a wave's X slices
+    const int nmax = (KT + KS - 1) / KS;                  // k-tiles of a wave per strip (uniform)
+    const int n = (KT - ks + KS - 1) / KS;                // ... of which real for this wave
+    const int nb = (nmax + U - 1) / U;                    // load batches per strip
+    const int rstride = nmax * 32 + 8;                    // row stride of a wave's X slices
     const int xplane = kNW * B * rstride;                 // elements per plane set
     f32x4 *red = (f32x4 *)(xs + (HASLO ? 2 : 1) * xplane);   // [kNW][NBT][64] f32x4
+    auto strip_of = [&](int r) { return ((int)blockIdx.x + r * (int)gridDim.x) * SPW + slot; };
+    const int strip0 = strip_of(0);
+    const int row00 = strip0 * 16 + 4 * g;
 
     f32x4 acc[NA][NBT];
 #pragma unroll
@@ -426,70 +436,25 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // Strip group r ends: KS partial sums reduced in wave order, RMSNorm
+    // scalar, epilogue; the accumulators restart at zero.
     Pro<NBT, PRO, EPI> pr;
-    {
-        // ---- wave-private X, one pipelined pass over this wave's tiles ----------
-        // Wave tiles are kt = ks + KS i, i < n.  Loads are unconditional (tiles
-        // past the end read the matrix's first line and are multiplied as
-        // zero), so every batch keeps a fixed load count and the waits before
-        // each batch cover exactly that batch.
-        const int n = (KT - ks + KS - 1) / KS;
-        const int nmax = (KT + KS - 1) / KS;
-        ChunkMap cm{true, nmax * 4, B * nmax * 4, ks, KS, KT, rstride};
-        uint16_t *xh = xs + wave * B * rstride, *xl = xh + xplane;
-        // 1. prologue / epilogue inputs, before any weights
-        pro_load<NBT, PRO, EPI>(p, pr, lead, row0, cm, 0);
-        // 2. two batches of weights
-        u32x4 ra[U], rb[U];
-#define GEMV_PTR(i) ((const u32x4 *)((i) < n ? wp + (int64_t)(ks + KS * (i)) * 512 : p.W))
+    auto finish = [&](int r) {
+        f32x4 fin[NBT];
 #pragma unroll
-        for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(u));
-#pragma unroll
-        for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(U + u));
-        // keep the prologue arithmetic (and its waits) after the weight loads
-        __builtin_amdgcn_sched_barrier(0);
-        // 3. scalars and this wave's slices of X; the MTP scales its halves
-        //    before the reduction, so it waits for every wave's scalars
-        pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
-        if (PRO == PRO_MTP) __syncthreads();
-        // 4. stream: consume one batch while the next is in flight
-        const int npair = (n + 2 * U - 1) / (2 * U);
-        int i0 = 0;
-#define GEMV_MMA(R, i)                                                                                  \
-        tile_mma<NBT, PRO>(acc, (i) < n ? R : zero, (i) < n ? ks + KS * (i) : 0, (i) < n ? 32 * (i) : 0, HT, B, \
-                           xh, xl, rstride)
-        for (int it = 1; it < npair; ++it) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
-#pragma unroll
-            for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 2 * U + u));
-#pragma unroll
-            for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
-#pragma unroll
-            for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(GEMV_PTR(i0 + 3 * U + u));
-            i0 += 2 * U;
+        for (int bt = 0; bt < NBT; ++bt) {
+            f32x4 v = acc[0][bt];
+            if (NA == 2) {
+                const int b = bt * 16 + j;
+                const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
+                v = v * s0 + acc[NA - 1][bt] * s1;
+            }
+            fin[bt] = v;
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) GEMV_MMA(ra[u], i0 + u);
+        for (int a = 0; a < NA; ++a)
 #pragma unroll
-        for (int u = 0; u < U; ++u) GEMV_MMA(rb[u], i0 + U + u);
-#undef GEMV_MMA
-#undef GEMV_PTR
-    }
-
-    // ---- 3. reduce the KS partial sums of each strip (wave order) -----------
-    f32x4 fin[NBT];
-#pragma unroll
-    for (int bt = 0; bt < NBT; ++bt) {
-        f32x4 v = acc[0][bt];
-        if (NA == 2) {
-            const int b = bt * 16 + j;
-            const float s0 = b < B ? sc0[b] : 0.f, s1 = b < B ? sc1[b] : 0.f;
-            v = v * s0 + acc[NA - 1][bt] * s1;
-        }
-        fin[bt] = v;
-    }
-    if (KS > 1) {
+            for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
         __syncthreads();
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) red[(wave * NBT + bt) * 64 + lane] = fin[bt];
@@ -501,15 +466,79 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                 for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
             }
         }
-    }
-    if (PRO == PRO_NORM) {
+        if (PRO == PRO_NORM) {
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                fin[bt] *= (b < B ? sc0[b] : 0.f);
+            }
+        }
+        const int strip = strip_of(r);
+        const bool lead = ks == 0 && strip < nstrips;
+        f32x4 resid[NBT];
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
-            const int b = bt * 16 + j;
-            fin[bt] *= (b < B ? sc0[b] : 0.f);
+            resid[bt] = pr.resid[bt];
+            if (EPI == EPI_RESID && r > 0) {   // later groups read their residual rows here
+                const int b = bt * 16 + j;
+                resid[bt] = *(const f32x4 *)(p.out + ((lead && b < B) ? (int64_t)b * p.N + strip * 16 + 4 * g : 0));
+            }
         }
+        gemv_epilogue<NBT, EPI>(p, fin, resid, strip, lead);
+    };
+
+    // ---- wave-private X, then one pipelined pass over every group's tiles ----
+    // Batch q covers tiles i = U (q % nb) + u of strip group q / nb, at k-tile
+    // ks + KS i.  Loads are unconditional (tiles past a strip's end or past
+    // the last group read the matrix's first line and are multiplied as
+    // zero), so every batch keeps a fixed load count and the waits before
+    // each batch cover exactly that batch.
+    const int nq = ngrp * nb;
+    ChunkMap cm{true, nmax * 4, B * nmax * 4, ks, KS, KT, rstride};
+    uint16_t *xh = xs + wave * B * rstride, *xl = xh + xplane;
+    // 1. prologue / epilogue inputs, before any weights
+    pro_load<NBT, PRO, EPI>(p, pr, ks == 0 && strip0 < nstrips, row00, cm, 0);
+    // 2. two batches of weights
+    u32x4 ra[U], rb[U];
+    auto wptr = [&](int q, int u) -> const u32x4 * {
+        const int r = q / nb, i = (q - r * nb) * U + u;
+        const int strip = strip_of(r);
+        const bool ok = q < nq && i < n && strip < nstrips;
+        return (const u32x4 *)(ok ? p.W + ((int64_t)strip * KT + ks + KS * i) * 512 + lane * 8 : p.W);
+    };
+#pragma unroll
+    for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(wptr(0, u));
+#pragma unroll
+    for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(wptr(1, u));
+    // keep the prologue arithmetic (and its waits) after the weight loads
+    __builtin_amdgcn_sched_barrier(0);
+    // 3. scalars and this wave's slices of X; the MTP scales its halves
+    //    before the reduction, so it waits for every wave's scalars
+    pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
+    if (PRO == PRO_MTP) __syncthreads();
+    // 4. stream: consume one batch while the next is in flight
+    auto mma_batch = [&](const u32x4 (&R)[U], int q) {
+        const int r = q / nb, i0 = (q - r * nb) * U;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u;
+            const bool ok = q < nq && i < n;
+            tile_mma<NBT, PRO>(acc, ok ? R[u] : zero, ok ? ks + KS * i : 0, ok ? 32 * i : 0, HT, B, xh, xl, rstride);
+        }
+        if (q < nq && i0 + U >= nmax) finish(r);
+    };
+    // the last pair is peeled so that no load is left in flight at the end
+    int q = 0;
+    for (; q + 2 < nq; q += 2) {
+        mma_batch(ra, q);
+#pragma unroll
+        for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(wptr(q + 2, u));
+        mma_batch(rb, q + 1);
+#pragma unroll
+        for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(wptr(q + 3, u));
     }
-    gemv_epilogue<NBT, EPI>(p, fin, pr.resid, strip, lead);
+    mma_batch(ra, q);
+    mma_batch(rb, q + 1);
 }
 
 // ---------------------------------------------------------------------------
@@ -767,14 +796,13 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     const int KT = q.K >> 5;
     constexpr int planes = PRO == PRO_PAIR ? 1 : 2;
     constexpr int SPW = kNW / KS;
-    const int grid = ((q.N >> 4) + SPW - 1) / SPW;
+    int grid = ((q.N >> 4) + SPW - 1) / SPW;
     const int red = kNW * NBT * 64 * 16;
-    q.iters = 1;
     // wave-private X when every wave's slices fit
     const int nmax = (KT + KS - 1) / KS;
     const int lds_one = planes * kNW * q.B * (nmax * 32 + 8) * 2 + red;
     if (lds_one <= kGemvOneLdsBytes) {
-        q.ktiles_per_chunk = KT;
+        if (q.wg_cap > 0 && grid > q.wg_cap) grid = q.wg_cap;
         hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s, q);
         return;
     }

@@ -31,8 +31,8 @@ enum GemvEpi : int {
 struct GemvParams {
     const uint16_t *W;          // tiled [N][K]
     int N, K, B;
-    int ktiles_per_chunk;       // LDS staging chunk, in 32-wide k tiles (set by launch_gemv)
-    int iters;                  // strip groups per workgroup (set by launch_gemv)
+    int wg_cap;                 // workgroups of the batch-1 kernel, each taking every wg_cap-th
+                                // strip group (0: one workgroup per strip group)
     // prologue
     const float *x; const float *xf; const float *ss; int nss; const float *gain;
     const float *gain2; float eps; const int32_t *pairs; const uint16_t *embed; int H; int vocab;

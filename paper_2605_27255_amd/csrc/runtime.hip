@@ -59,6 +59,7 @@ struct pipo_ctx {
     float *qbuf, *attn_out, *act;
     uint16_t *xh, *xl;    // decode GEMV input planes for larger batches [Bmax][Kmax]
     float *gpart; int64_t gpart_cap;   // decode GEMV k-range partial sums
+    int n_cu;             // compute units: workgroups of the batch-1 GEMV
     uint64_t *best_b, *best_d, *seeds;
     int32_t *pairs, *pos, *step;
     pipo_pair *out;
@@ -303,6 +304,16 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         return cleanup_fail(fail(c, PIPO_EHIP, "host staging / event / stream creation failed"));
     e = hipStreamSynchronize(s);
     if (e != hipSuccess) return cleanup_fail(fail(c, PIPO_EHIP, "init: %s", hipGetErrorString(e)));
+    {
+        int dev = 0, ncu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu < 1)
+            return cleanup_fail(fail(c, PIPO_EHIP, "compute unit count query failed"));
+        c->n_cu = ncu;
+        // test hook: fewer GEMV workgroups, so small models run several strip groups per workgroup
+        const char *wc = getenv("PIPO_GEMV_WG_CAP");
+        if (wc && atoi(wc) > 0) c->n_cu = atoi(wc);
+    }
     const char *ng = getenv("PIPO_NO_GRAPH");
     c->use_graph = !(ng && ng[0] == '1');
     *out = c;
@@ -331,6 +342,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     // MTP head: W_fc [RMSNorm(h_b; g_mh); RMSNorm(E[b]; g_me)]
     GemvParams m{};
     m.B = B; m.eps = c->cfg.rms_eps; m.H = H; m.vocab = c->V; m.xh = c->xh; m.xl = c->xl; m.part = c->gpart; m.part_cap = c->gpart_cap;
+    m.wg_cap = c->n_cu;
     m.W = c->w_fc; m.N = H; m.K = 2 * H;
     m.x = c->x; m.ss = c->ss_x; m.nss = nss; m.gain = c->g_mtp_h; m.gain2 = c->g_mtp_e;
     m.embed = c->embed; m.tokkey = c->best_b;
@@ -373,6 +385,7 @@ static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
     GemvParams base{};
     base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V; base.xh = c->xh; base.xl = c->xl; base.part = c->gpart; base.part_cap = c->gpart_cap;
+    base.wg_cap = c->n_cu;
     {   // pair-in compressor
         GemvParams p = base;
         p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;

@@ -133,6 +133,25 @@ def test_tiny_parity_batch_greedy_tau_extremes(torch):
         m.close()
 
 
+def test_tiny_parity_gemv_workgroups_run_several_strip_groups(torch, monkeypatch):
+    """Decode GEMV workgroups capped at 3 (batch 1, greedy) and 7 (batch 3,
+    top-p): every workgroup streams several strip groups in a row, with the
+    reduction and epilogue of each in between, including the residual rows
+    that later groups read in their epilogue."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    W = O.OracleWeights.generate(cfg, seed=9, precision="bf16")
+    for cap, B, smp in ((3, 1, O.Sampling(tau=0.5)),
+                        (7, 3, O.Sampling(tau=0.7, temperature=0.6, top_p=0.95, seeds=(7, 8, 9)))):
+        monkeypatch.setenv("PIPO_GEMV_WG_CAP", str(cap))
+        n, steps = 36, 5
+        prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=cap)
+        m = _model(cfg, seed=9, max_batch=B, max_latent=18 + steps + 1, prefill_chunk=16)
+        log(f"wg_cap={cap} B={B}")
+        rep, _ = run_parity(m, W, prompts, steps, smp, log)
+        rep.check()
+        m.close()
+
+
 def test_4b_width_two_layers_2048_latents(torch):
     """Full 4B-class width (hidden 2560, 32/8 heads of 128, FFN 9728, vocab 151936)
     with two layers: 4096-token prompt (2048 latents, one chunk), 3 greedy steps."""

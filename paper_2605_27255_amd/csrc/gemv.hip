@@ -254,13 +254,12 @@ __device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 
     const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int bt = 0; bt < NBT; ++bt) {
+        // columns b >= B multiply row 0 again: MFMA columns are independent
+        // and every epilogue drops them
         const int b = bt * 16 + j;
-        const bool bok = b < B;
-        const int xo = (bok ? b : 0) * rstride + xcol + g * 8;
-        u32x4 bop = *(const u32x4 *)(xs + xo), bol = zero;
-        if (HASLO) bol = *(const u32x4 *)(xs_lo + xo);
-        bop = bok ? bop : zero;
-        bol = bok ? bol : zero;
+        const int xo = (b < B ? b : 0) * rstride + xcol + g * 8;
+        const u32x4 bop = *(const u32x4 *)(xs + xo);
+        const u32x4 bol = HASLO ? *(const u32x4 *)(xs_lo + xo) : zero;
         if (NA == 2) {
             // MTP: tiles below H/32 act on RMSNorm(h_b), the rest on RMSNorm(E[b])
             const bool hi_half = kt >= HT;

@@ -13,7 +13,11 @@ Also reported on the same JSON line:
                 kernel of decode): algorithmic bytes of its launches in one
                 pair step / their summed duration, from HIP events recorded
                 around each launch on the library's stream (profiling pass);
-  cpu_baseline  the float64 oracle timed on this host on a bounded sample.
+  cpu_baseline  the float64 oracle timed on this host on a bounded sample;
+  regular       regular one-token decoding on the same kernels and weights
+                (Sec. 4.3's baseline): the n prompt tokens prefilled as n
+                positions, then token steps; TTFT and per-token ratios
+                against the pair decoder on the same prompt.
 Diagnostics go to stderr; stdout carries the one JSON line.
 """
 from __future__ import annotations
@@ -118,6 +122,62 @@ def cpu_baseline(wl, accept_rate, budget_s=12.0):
                        f"tokens per pair step 1 + {accept_rate:.3f} (GPU-measured acceptance)")}
 
 
+def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_s, emitted, reps):
+    """Regular decoding of the same prompt on the same kernels: one timed job is
+    the n-position prefill plus as many token steps as the pair decoder ran
+    pair steps; ``reps`` timed jobs after one warm-up."""
+    import numpy as np
+    import torch
+    from paper_2605_27255_amd import PipoModel
+
+    m, B, steps = wl.model, wl.batch, wl.decode_steps
+    n = wl.prompt_tokens
+    t0 = time.perf_counter()
+    model = PipoModel(m, seed=wl.seed, max_batch=B, max_latent=n + steps + 1, prefill_chunk=wl.prefill_chunk)
+    toks = torch.empty((steps, B), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    log(f"regular decoding: init {time.perf_counter() - t0:.1f} s, prompt {n} positions + {steps} token steps")
+
+    def job(ev=None):
+        if ev:
+            ev[0].record(stream)
+        model.regular_prefill(prompts, wl.temperature, wl.top_p, seeds)
+        if ev:
+            ev[1].record(stream)
+        for s in range(steps):
+            model.regular_into(toks[s])
+        if ev:
+            ev[2].record(stream)
+
+    job()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    t_start = time.perf_counter()
+    for k in range(reps):
+        job(evs[k])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t_start) / reps
+    model.close()
+    del model
+    torch.cuda.empty_cache()
+    ttft = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    ms_tok = float(np.mean([e[1].elapsed_time(e[2]) for e in evs])) / max(steps, 1)
+    # the same number of output tokens as one pair-decoder job emitted
+    reg_same_out_s = (ttft + (emitted / B - 1) * ms_tok) * 1e-3
+    res = {"ttft_ms": round(ttft, 3), "ms_per_token_step": round(ms_tok, 4),
+           "output_tokens_per_s": round(B * 1e3 / ms_tok, 2), "job_s": round(wall, 4),
+           "ttft_speedup": round(ttft / pipo_ttft, 3),
+           "pair_step_cost_over_token_step": round(pipo_ms_step / ms_tok, 3),
+           "per_token_speedup_at_measured_acceptance": round(ms_tok * (1 + acc_rate) / pipo_ms_step, 3),
+           "per_token_speedup_two_slots_per_pair": round(ms_tok * 2 / pipo_ms_step, 3),
+           "end_to_end_speedup_same_output": round(reg_same_out_s / pipo_job_s, 3),
+           "paper_context": "Sec. 4.3 / Fig. 4 (4B model, HF backend; the paper names H20-141G GPUs): "
+                            "up to 2.64x TTFT, 2.07x TPOT counting both slots of a pair"}
+    log(f"regular decoding: TTFT {ttft:.2f} ms, {ms_tok:.3f} ms/token step; TTFT speedup "
+        f"{res['ttft_speedup']}x, pair step / token step {res['pair_step_cost_over_token_step']}")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,6 +187,7 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's step count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--no-regular", action="store_true", help="skip the regular-decoding baseline leg")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration) and exit")
     args = ap.parse_args()
@@ -265,6 +326,9 @@ def main():
     model.close()
     del model
     torch.cuda.empty_cache()
+    if not args.no_regular:
+        result["regular"] = regular_leg(wl, prompts, seeds, ttft, ms_step, acc_rate, wall / args.steps,
+                                        emitted_per_job, max(1, min(args.steps, 2)))
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         result["cpu_baseline"] = cpu_baseline(wl, acc_rate)

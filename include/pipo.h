@@ -106,6 +106,29 @@ int pipo_prefill(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, int32_t 
 int pipo_decode_step(pipo_ctx *ctx, const int32_t *d_in_pairs, pipo_pair *d_out,
                      float *d_logits_b, float *d_logits_d, void *stream);
 
+/* Regular one-token-per-step decoding on the same weights: the baseline the
+ * pair decoder is compared against (Sec. 4.3, Fig. 4: the backbone itself,
+ * one position per token, no compressor, MTP or confidence head).
+ * pipo_regular_prefill starts `batch` sequences from d_tokens (device int32
+ * [batch][n], row-major, ids in [0, vocab)) with the n embeddings as the
+ * backbone's positions and writes the first generated token to d_tok
+ * (device int32 [batch]); d_logits (device float [batch][vocab]) receives
+ * its logits when non-NULL.  Selection as in pipo_sampling (tau unused;
+ * top-p draws use slot 0 of each step).  A later pipo_decode_step needs a
+ * new pipo_prefill.  Errors: PIPO_EINVAL (NULL pointers, n < 1, bad
+ * sampling values), PIPO_ECAPACITY (batch > max_batch or n + 1 > max_latent). */
+int pipo_regular_prefill(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, int32_t n,
+                         const pipo_sampling *smp, int32_t *d_tok, float *d_logits,
+                         void *stream);
+
+/* One regular decoding step: feed one token per sequence, append one
+ * position, emit the next token.  The input is d_in_tok (device int32
+ * [batch]) when non-NULL (teacher forcing), else the token the previous
+ * call produced on the device.  Outputs as for pipo_regular_prefill.
+ * Errors: PIPO_ESTATE (no regular prefill yet), PIPO_ECAPACITY (KV full). */
+int pipo_regular_step(pipo_ctx *ctx, const int32_t *d_in_tok, int32_t *d_tok, float *d_logits,
+                      void *stream);
+
 /* Release a context and all its device memory.  NULL is a no-op (returns 0). */
 int pipo_free(pipo_ctx *ctx);
 
@@ -124,16 +147,16 @@ int pipo_read_weight(pipo_ctx *ctx, const char *name, int64_t start, int64_t cou
 /* Kernel classes of the profiling counters. */
 #define PIPO_K_GEMV_LAYER   0   /* decode weight-streaming GEMM: QKV, O, gate/up, down */
 #define PIPO_K_GEMV_LMHEAD  1   /* decode LM-head GEMM (both passes), argmax fused     */
-#define PIPO_K_GEMV_SMALL   2   /* decode compressor and MTP GEMMs                    */
+#define PIPO_K_GEMV_SMALL   2   /* decode compressor, MTP GEMM, regular embed gather  */
 #define PIPO_K_ATTN_DECODE  3   /* split-K flash-decode (merge included)               */
 #define PIPO_K_SAMPLE       4   /* top-p sampler                                       */
-#define PIPO_K_GATE         5   /* confidence gate + next pair                         */
+#define PIPO_K_GATE         5   /* confidence gate + next pair (regular: next token)   */
 #define PIPO_K_PREFILL_GEMM 6   /* prefill MFMA GEMMs                                  */
 #define PIPO_K_PREFILL_ATTN 7   /* prefill causal flash attention                      */
 #define PIPO_K_PREFILL_MISC 8   /* prefill gather, RMSNorm, last-latent pick           */
 #define PIPO_K_CLASSES      9
 
-/* Profiling: while on (on != 0), pipo_prefill and pipo_decode_step launch
+/* Profiling: while on (on != 0), the prefill and step calls of both decoders launch
  * eagerly (no graph) with a HIP event recorded on the call's stream before
  * and after every kernel; durations accumulate per kernel class.  Turning it
  * on clears the accumulators.  Errors: PIPO_EINVAL (NULL ctx). */

@@ -379,3 +379,59 @@ class PipoOracle:
             self.step_idx[i] += 1
             self.next_pairs[i] = self._next_pair(rec)
         return out
+
+
+class RegularOracle:
+    """Regular decoding on the same backbone, the baseline of Sec. 4.3 (Fig. 4).
+
+    Every token is one position: the backbone input is ``E[t]`` itself (no
+    compressor), the next token is selected from ``E RMSNorm(h; g_f)`` (eq. 3
+    on the last position) and fed back; neither the MTP nor the confidence
+    head runs.  Top-p draws use slot 0 of each step, step 0 being the prefill.
+    """
+
+    def __init__(self, W: OracleWeights, kv_bf16: bool = False):
+        self.W = W
+        self.cfg = W.cfg
+        self.kv_bf16 = kv_bf16
+
+    def _select(self, logits, seq, step):
+        smp = self.sampling
+        if smp.temperature <= 0:
+            return select_greedy(logits)
+        u = rspec.uniform_draw(smp.seeds[seq], step, 0)
+        return select_top_p(logits, smp.temperature, smp.top_p, u)
+
+    def _head(self, h, seq, step):
+        logits = lm_logits(self.W["embed"], self.W["g_final"], h, self.cfg.rms_eps)
+        return dict(tok=self._select(logits, seq, step), logits=logits, h=h)
+
+    def prefill(self, prompts, sampling: Sampling):
+        """The prompt's n tokens as n positions; returns the first generated token."""
+        self.sampling = sampling
+        W = self.W
+        self.caches, self.length, self.step_idx, self.next_tok = [], [], [], []
+        out = []
+        for i, prompt in enumerate(np.asarray(prompts)):
+            X, caches = backbone_full(W, W["embed"][np.asarray(prompt)], self.kv_bf16)
+            self.caches.append([[k, v] for k, v in caches])
+            self.length.append(len(prompt))
+            rec = self._head(X[-1], i, 0)
+            out.append(rec)
+            self.step_idx.append(1)
+            self.next_tok.append(rec["tok"])
+        return out
+
+    def step(self, in_tok=None):
+        """One token per sequence; ``in_tok`` teacher-forces the input."""
+        W = self.W
+        out = []
+        for i in range(len(self.caches)):
+            t = self.next_tok[i] if in_tok is None else int(in_tok[i])
+            h = backbone_step(W, W["embed"][t], self.length[i], self.caches[i], self.kv_bf16)
+            self.length[i] += 1
+            rec = self._head(h, i, self.step_idx[i])
+            out.append(rec)
+            self.step_idx[i] += 1
+            self.next_tok[i] = rec["tok"]
+        return out

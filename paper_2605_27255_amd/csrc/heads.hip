@@ -56,6 +56,55 @@ void launch_gate(const GateParams &p, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
+// Regular decoding on the same backbone (the paper's baseline, Sec. 4.3).
+// Step input: x[b] = E[tok_b] (fp32) with the sum-of-squares part of every
+// 16-element strip, as the RMSNorm prologue of the decode GEMM reads them.
+__global__ __launch_bounds__(256) void k_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V,
+                                                    float *x, float *ss) {
+    const int b = blockIdx.x;
+    const int row = clamp_id(pairs[2 * b], V);
+    for (int c = threadIdx.x; c < (H >> 3); c += 256) {
+        const int k = c << 3;
+        const u32x4 v = *(const u32x4 *)(embed + tiled_index(row, k, H));
+        const float f[8] = {bf_lo(v[0]), bf_hi(v[0]), bf_lo(v[1]), bf_hi(v[1]),
+                            bf_lo(v[2]), bf_hi(v[2]), bf_lo(v[3]), bf_hi(v[3])};
+        float4 *dst = (float4 *)(x + (int64_t)b * H + k);
+        dst[0] = make_float4(f[0], f[1], f[2], f[3]);
+        dst[1] = make_float4(f[4], f[5], f[6], f[7]);
+        float q = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) q += f[i] * f[i];
+        q += __shfl_xor(q, 1);          // the strip's other half (chunk c ^ 1)
+        if ((c & 1) == 0) ss[(int64_t)b * (H >> 4) + (c >> 1)] = q;
+    }
+}
+
+void launch_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V, float *x, float *ss, int B,
+                       hipStream_t s) {
+    hipLaunchKernelGGL(k_embed_step, dim3(B), dim3(256), 0, s, pairs, embed, H, V, x, ss);
+}
+
+// Step output: the selected token, which is also the next step's input.
+__global__ void k_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_t pad_id, int32_t *pos,
+                              int32_t *step, int advance, int B) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    const int32_t t = argmax_key_id(best[b]);
+    out_tok[b] = t;
+    pairs[2 * b] = t;
+    pairs[2 * b + 1] = pad_id;
+    if (advance) pos[b] += 1;
+    step[b] += 1;
+    best[b] = 0;
+}
+
+void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_t pad_id, int32_t *pos,
+                        int32_t *step, int advance, int B, hipStream_t s) {
+    hipLaunchKernelGGL(k_regular_out, dim3((B + 63) / 64), dim3(64), 0, s, best, out_tok, pairs, pad_id, pos, step,
+                       advance, B);
+}
+
+// ---------------------------------------------------------------------------
 // Temperature + top-p selection, one 1024-thread workgroup per sequence.
 //   e_j = exp((l_j - max l) / T); masses are fixed point, E_j = round(e_j 2^40),
 //   so every sum is an exact integer sum (order independent).

@@ -79,6 +79,12 @@ struct GateParams {
 };
 void launch_gate(const GateParams &p, hipStream_t s);
 
+// Regular decoding (no compressor, one token per position and step).
+void launch_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V, float *x, float *ss, int B,
+                       hipStream_t s);
+void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_t pad_id, int32_t *pos,
+                        int32_t *step, int advance, int B, hipStream_t s);
+
 struct SampleParams {
     const float *logits; int V; int B;
     float temperature, top_p;
@@ -116,6 +122,8 @@ struct PrefillGeom {
 };
 void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
                          const PrefillGeom &g, uint16_t *xin, hipStream_t s);
+void launch_gather_tokens(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                          const PrefillGeom &g, float *x, hipStream_t s);
 void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M,
                           uint16_t *xn_hi, uint16_t *xn_lo, hipStream_t s);
 // Activations of the prefill GEMMs are a pair of tiled bf16 planes, hi and lo

@@ -41,6 +41,35 @@ void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, in
     hipLaunchKernelGGL(k_gather_pairs, dim3(grid), dim3(256), 0, s, tokens, embed, H, V, pad_id, g, xin);
 }
 
+// ---- regular decoding: the prompt's tokens one per position, x = E[t] -----
+// Row (b, i) of the chunk holds token c0 + i of sequence b (rows past the
+// chunk hold E[pad_id]); fp32 residual rows [B * mpad][H].
+__global__ void k_gather_tokens(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                                PrefillGeom g, float *x) {
+    const int cpr = H >> 3;
+    const int64_t total = (int64_t)g.B * g.mpad * cpr;
+    for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int m = (int)(idx / cpr);
+        const int k = (int)(idx - (int64_t)m * cpr) << 3;
+        const int b = m / g.mpad, i = m - b * g.mpad;
+        const int t = g.c0 + i;
+        const int row = (i < g.clen && t < g.n_tok) ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+        const u32x4 v = *(const u32x4 *)(embed + tiled_index(row, k, H));
+        float4 *dst = (float4 *)(x + (int64_t)m * H + k);
+        dst[0] = make_float4(bf_lo(v[0]), bf_hi(v[0]), bf_lo(v[1]), bf_hi(v[1]));
+        dst[1] = make_float4(bf_lo(v[2]), bf_hi(v[2]), bf_lo(v[3]), bf_hi(v[3]));
+    }
+}
+
+void launch_gather_tokens(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                          const PrefillGeom &g, float *x, hipStream_t s) {
+    const int64_t total = (int64_t)g.B * g.mpad * (H >> 3);
+    int grid = (int)((total + 255) / 256);
+    grid = grid > 65536 ? 65536 : grid;
+    hipLaunchKernelGGL(k_gather_tokens, dim3(grid), dim3(256), 0, s, tokens, embed, H, V, pad_id, g, x);
+}
+
 // ---- RMSNorm of fp32 rows into the tiled bf16 layout (one wave per row) ----
 __global__ __launch_bounds__(256) void k_rmsnorm_tiled(const float *x, const float *gain, int H, float eps,
                                                        int M, uint16_t *xh, uint16_t *xl) {

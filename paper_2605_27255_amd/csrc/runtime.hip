@@ -73,6 +73,10 @@ struct pipo_ctx {
 
     int batch = 0, len = 0;
     bool prefilled = false;
+    bool regular = false;           // the last prefill was regular decoding
+    int32_t *out_tok = nullptr;     // regular decoding: selected token per sequence
+    hipGraphExec_t graph_reg = nullptr;
+    bool graph_reg_dirty = true;
     float tau = 0.5f, temperature = 0.f, top_p = 1.f;
 
     hipGraphExec_t graph = nullptr;
@@ -242,6 +246,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->pos = a.take<int32_t>(B);
         c->step = a.take<int32_t>(B);
         c->out = a.take<pipo_pair>(B);
+        c->out_tok = a.take<int32_t>(B);
         c->apart = a.take<float>((int64_t)B * c->nq * S_att * (c->d + 2));
         c->p_xin = a.take<uint16_t>(mcap * 2 * H);
         c->p_x = a.take<float>(mcap * H);
@@ -380,19 +385,12 @@ static int attn_splits(const pipo_ctx *c, int B) {
     return sp < 1 ? 1 : (sp > 64 ? 64 : sp);
 }
 
-// One pair-decode step (eq. 1 on the pending pair, eq. 2 one position, heads).
-static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
+// The backbone layers of one decode position (eq. 2) over the residual in x.
+static void enqueue_layers(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
     GemvParams base{};
     base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V; base.xh = c->xh; base.xl = c->xl; base.part = c->gpart; base.part_cap = c->gpart_cap;
     base.wg_cap = c->n_cu;
-    {   // pair-in compressor
-        GemvParams p = base;
-        p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;
-        p.out = c->x; p.bias = c->b_comp; p.ss_out = c->ss_x;
-        PROF(PIPO_K_GEMV_SMALL);
-        launch_gemv(p, PRO_PAIR, EPI_STORE, s);
-    }
     for (int l = 0; l < c->L; ++l) {
         const LayerW &lw = c->layers[l];
         uint16_t *kc = c->kc + (int64_t)l * c->Bmax * c->kv_bstride;
@@ -423,6 +421,21 @@ static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
         p.W = lw.wdown; p.N = H; p.K = c->F; p.xf = c->act; p.out = c->x; p.ss_out = c->ss_x;
         { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
     }
+}
+
+// One pair-decode step (eq. 1 on the pending pair, eq. 2 one position, heads).
+static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
+    const int B = c->batch, H = c->H;
+    {   // pair-in compressor
+        GemvParams p{};
+        p.B = B; p.eps = c->cfg.rms_eps; p.H = H; p.vocab = c->V; p.xh = c->xh; p.xl = c->xl; p.part = c->gpart; p.part_cap = c->gpart_cap;
+        p.wg_cap = c->n_cu;
+        p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;
+        p.out = c->x; p.bias = c->b_comp; p.ss_out = c->ss_x;
+        PROF(PIPO_K_GEMV_SMALL);
+        launch_gemv(p, PRO_PAIR, EPI_STORE, s);
+    }
+    enqueue_layers(c, s);
     enqueue_heads(c, B, H / 16, 1, s);
 }
 
@@ -445,24 +458,28 @@ static int copy_outputs(pipo_ctx *c, pipo_pair *d_out, float *d_lb, float *d_ld,
     return PIPO_OK;
 }
 
-extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
-                            const pipo_sampling *smp, pipo_pair *d_out, float *d_logits_b, float *d_logits_d,
-                            void *stream) {
-    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
-    if (!d_tokens || !d_out) return fail(c, PIPO_EINVAL, "d_tokens and d_out must be non-NULL");
+// The prompt prefill shared by both decoders: validation, sampling state,
+// the chunked backbone over `positions` (PIPO: ceil(n/2) latents of
+// compressed pairs, eq. 1; regular: the n tokens themselves), and the last
+// position's residual into x.
+static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
+                            const pipo_sampling *smp, bool regular, hipStream_t s) {
+    if (!d_tokens) return fail(c, PIPO_EINVAL, "d_tokens must be non-NULL");
     if (n < 1) return fail(c, PIPO_EINVAL, "prompt length must be >= 1 (got %d)", n);
     if (batch < 1) return fail(c, PIPO_EINVAL, "batch must be >= 1 (got %d)", batch);
     int rc = check_sampling(c, smp, batch);
     if (rc) return rc;
     if (batch > c->Bmax) return fail(c, PIPO_ECAPACITY, "batch %d exceeds max_batch %d", batch, c->Bmax);
-    const int latents = (n + 1) / 2;
-    if (latents + 1 > c->cfg.max_latent)
-        return fail(c, PIPO_ECAPACITY, "%d latents leave no room for a step (max_latent %d)", latents, c->cfg.max_latent);
-    hipStream_t s = (hipStream_t)stream;
+    const int positions = regular ? n : (n + 1) / 2;
+    if (positions + 1 > c->cfg.max_latent)
+        return fail(c, PIPO_ECAPACITY, "%d positions leave no room for a step (max_latent %d)", positions,
+                    c->cfg.max_latent);
     HIP_TRY(c, hipGetLastError());
 
-    if (c->batch != batch || c->tau != smp->tau || c->temperature != smp->temperature || c->top_p != smp->top_p)
+    if (c->batch != batch || c->tau != smp->tau || c->temperature != smp->temperature || c->top_p != smp->top_p) {
         c->graph_dirty = true;
+        c->graph_reg_dirty = true;
+    }
     c->batch = batch;
     c->tau = smp->tau;
     c->temperature = smp->temperature;
@@ -475,18 +492,23 @@ extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     }
     const int H = c->H, F = c->F;
     PrefillGeom g{};
-    for (int c0 = 0; c0 < latents; c0 += c->chunk) {
-        g.B = batch; g.c0 = c0; g.clen = std::min(c->chunk, latents - c0);
+    for (int c0 = 0; c0 < positions; c0 += c->chunk) {
+        g.B = batch; g.c0 = c0; g.clen = std::min(c->chunk, positions - c0);
         g.mpad = (int)round_up(g.clen, 32); g.n_tok = n;
         const int M = batch * g.mpad;
-        { PROF(PIPO_K_PREFILL_MISC); launch_gather_pairs(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_xin, s); }
         GemmParams gp{};
         gp.g = g; gp.M = M;
         gp.n_q = c->nq; gp.n_kv = c->nkv; gp.d = c->d; gp.lmax_pad = c->lmax_pad; gp.kv_bstride = c->kv_bstride;
         gp.rope_cos = c->rope_cos; gp.rope_sin = c->rope_sin;
         GemmParams p = gp;
-        p.W = c->w_comp; p.X = c->p_xin; p.N = H; p.K = 2 * H; p.epi = EPI_STORE; p.out = c->p_x; p.bias = c->b_comp;
-        { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+        if (regular) {
+            PROF(PIPO_K_PREFILL_MISC);
+            launch_gather_tokens(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_x, s);
+        } else {
+            { PROF(PIPO_K_PREFILL_MISC); launch_gather_pairs(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_xin, s); }
+            p.W = c->w_comp; p.X = c->p_xin; p.N = H; p.K = 2 * H; p.epi = EPI_STORE; p.out = c->p_x; p.bias = c->b_comp;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+        }
         for (int l = 0; l < c->L; ++l) {
             const LayerW &lw = c->layers[l];
             uint16_t *kc = c->kc + (int64_t)l * c->Bmax * c->kv_bstride;
@@ -511,13 +533,116 @@ extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
             { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
         }
     }
-    { PROF(PIPO_K_PREFILL_MISC); launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, latents, s); }
+    { PROF(PIPO_K_PREFILL_MISC); launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, positions, s); }
+    c->len = positions;
+    return PIPO_OK;
+}
+
+extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
+                            const pipo_sampling *smp, pipo_pair *d_out, float *d_logits_b, float *d_logits_d,
+                            void *stream) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (!d_out) return fail(c, PIPO_EINVAL, "d_out must be non-NULL");
+    hipStream_t s = (hipStream_t)stream;
+    c->prefilled = false;
+    int rc = prefill_backbone(c, batch, d_tokens, n, smp, false, s);
+    if (rc) return rc;
     enqueue_heads(c, batch, 1, 0, s);
     HIP_TRY(c, hipGetLastError());
     rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
     if (rc) return rc;
-    c->len = latents;
     c->prefilled = true;
+    c->regular = false;
+    return PIPO_OK;
+}
+
+// Regular decoding's heads: eq. 3 alone (tied LM head on RMSNorm(h; g_final),
+// greedy or top-p in sampler slot 0), then the token becomes the next input.
+static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t s) {
+    const bool greedy = c->temperature <= 0.f;
+    GemvParams p{};
+    p.B = B; p.eps = c->cfg.rms_eps; p.H = c->H; p.xh = c->xh; p.xl = c->xl; p.part = c->gpart; p.part_cap = c->gpart_cap;
+    p.W = c->embed; p.N = c->V; p.K = c->H;
+    p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
+    p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
+    { PROF(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
+    if (!greedy) {
+        SampleParams sp{c->logits_b, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 0, c->best_b};
+        PROF(PIPO_K_SAMPLE);
+        launch_sample(sp, s);
+    }
+    PROF(PIPO_K_GATE);
+    launch_regular_out(c->best_b, c->out_tok, c->pairs, c->pad_id, c->pos, c->step, advance, B, s);
+}
+
+// One regular decoding step: x = E[token] at the next position, the same
+// backbone layers as the pair step (eq. 2 for one position), the heads above.
+static void enqueue_regular_decode(pipo_ctx *c, hipStream_t s) {
+    const int B = c->batch, H = c->H;
+    { PROF(PIPO_K_GEMV_SMALL); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, s); }
+    enqueue_layers(c, s);
+    enqueue_regular_heads(c, B, H / 16, 1, s);
+}
+
+static int copy_tokens(pipo_ctx *c, int32_t *d_tok, float *d_logits, hipStream_t s) {
+    const int B = c->batch;
+    HIP_TRY(c, hipMemcpyAsync(d_tok, c->out_tok, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, s));
+    if (d_logits) HIP_TRY(c, hipMemcpyAsync(d_logits, c->logits_b, sizeof(float) * B * c->V, hipMemcpyDeviceToDevice, s));
+    return PIPO_OK;
+}
+
+extern "C" int pipo_regular_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
+                                    const pipo_sampling *smp, int32_t *d_tok, float *d_logits, void *stream) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (!d_tok) return fail(c, PIPO_EINVAL, "d_tok must be non-NULL");
+    hipStream_t s = (hipStream_t)stream;
+    c->prefilled = false;
+    int rc = prefill_backbone(c, batch, d_tokens, n, smp, true, s);
+    if (rc) return rc;
+    enqueue_regular_heads(c, batch, 1, 0, s);
+    HIP_TRY(c, hipGetLastError());
+    rc = copy_tokens(c, d_tok, d_logits, s);
+    if (rc) return rc;
+    c->prefilled = true;
+    c->regular = true;
+    return PIPO_OK;
+}
+
+extern "C" int pipo_regular_step(pipo_ctx *c, const int32_t *d_in_tok, int32_t *d_tok, float *d_logits,
+                                 void *stream) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (!d_tok) return fail(c, PIPO_EINVAL, "d_tok must be non-NULL");
+    if (!c->prefilled || !c->regular) return fail(c, PIPO_ESTATE, "regular step before a regular prefill");
+    if (c->len + 1 > c->cfg.max_latent)
+        return fail(c, PIPO_ECAPACITY, "KV cache full: %d positions, max_latent %d", c->len, c->cfg.max_latent);
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(c, hipGetLastError());
+    if (d_in_tok)   // teacher forcing: the input tokens into the first slot of each pair
+        HIP_TRY(c, hipMemcpy2DAsync(c->pairs, 2 * sizeof(int32_t), d_in_tok, sizeof(int32_t), sizeof(int32_t),
+                                    c->batch, hipMemcpyDeviceToDevice, s));
+    if (c->use_graph && !c->prof_on) {
+        if (c->graph_reg_dirty || !c->graph_reg) {
+            if (c->graph_reg) {
+                hipGraphExecDestroy(c->graph_reg);
+                c->graph_reg = nullptr;
+            }
+            hipGraph_t gr;
+            HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
+            enqueue_regular_decode(c, c->cap_stream);
+            HIP_TRY(c, hipStreamEndCapture(c->cap_stream, &gr));
+            hipError_t e = hipGraphInstantiate(&c->graph_reg, gr, nullptr, nullptr, 0);
+            hipGraphDestroy(gr);
+            if (e != hipSuccess) return fail(c, PIPO_EHIP, "graph instantiate: %s", hipGetErrorString(e));
+            c->graph_reg_dirty = false;
+        }
+        HIP_TRY(c, hipGraphLaunch(c->graph_reg, s));
+    } else {
+        enqueue_regular_decode(c, s);
+        HIP_TRY(c, hipGetLastError());
+    }
+    int rc = copy_tokens(c, d_tok, d_logits, s);
+    if (rc) return rc;
+    c->len += 1;
     return PIPO_OK;
 }
 
@@ -525,7 +650,7 @@ extern "C" int pipo_decode_step(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pai
                                 float *d_logits_d, void *stream) {
     if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
     if (!d_out) return fail(c, PIPO_EINVAL, "d_out must be non-NULL");
-    if (!c->prefilled) return fail(c, PIPO_ESTATE, "decode step before prefill");
+    if (!c->prefilled || c->regular) return fail(c, PIPO_ESTATE, "decode step before a PIPO prefill");
     if (c->len + 1 > c->cfg.max_latent)
         return fail(c, PIPO_ECAPACITY, "KV cache full: %d latents, max_latent %d", c->len, c->cfg.max_latent);
     hipStream_t s = (hipStream_t)stream;
@@ -589,6 +714,7 @@ extern "C" int pipo_free(pipo_ctx *c) {
     if (!c) return PIPO_OK;
     for (hipEvent_t e : c->ev_pool) hipEventDestroy(e);
     if (c->graph) hipGraphExecDestroy(c->graph);
+    if (c->graph_reg) hipGraphExecDestroy(c->graph_reg);
     if (c->cap_stream) hipStreamDestroy(c->cap_stream);
     if (c->seeds_done) hipEventDestroy(c->seeds_done);
     if (c->h_seeds) hipHostFree(c->h_seeds);

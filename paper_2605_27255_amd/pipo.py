@@ -14,8 +14,9 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libpipo.so")
 
 PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -1, -2, -3, -4, -5
-EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_free",
-            "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read")
+EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_regular_prefill",
+            "pipo_regular_step", "pipo_free", "pipo_last_error", "pipo_read_weight", "pipo_profile_enable",
+            "pipo_profile_read")
 #: kernel classes of the profiling counters (PIPO_K_* in include/pipo.h)
 KERNEL_CLASSES = ("gemv_layer", "gemv_lmhead", "gemv_small", "attn_decode", "sample", "gate",
                   "prefill_gemm", "prefill_attn", "prefill_misc")
@@ -60,14 +61,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_init_weights.argtypes = [ctypes.POINTER(PipoConfig), ctypes.c_uint64, vp, ctypes.POINTER(vp)]
     lib.pipo_prefill.argtypes = [vp, i32, vp, i32, ctypes.POINTER(PipoSampling), vp, vp, vp, vp]
     lib.pipo_decode_step.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.pipo_regular_prefill.argtypes = [vp, i32, vp, i32, ctypes.POINTER(PipoSampling), vp, vp, vp]
+    lib.pipo_regular_step.argtypes = [vp, vp, vp, vp, vp]
     lib.pipo_free.argtypes = [vp]
     lib.pipo_last_error.argtypes = [vp]
     lib.pipo_last_error.restype = ctypes.c_char_p
     lib.pipo_read_weight.argtypes = [vp, ctypes.c_char_p, i64, i64, vp]
     lib.pipo_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.pipo_profile_read.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
-    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_free", "pipo_read_weight",
-               "pipo_profile_enable", "pipo_profile_read"):
+    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_regular_prefill",
+               "pipo_regular_step", "pipo_free", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -115,17 +118,25 @@ class PipoModel:
         ld = t.empty((B, self.model.vocab), dtype=t.float32, device="cuda") if logits else None
         return out, lb, ld
 
-    def prefill(self, tokens, tau: float, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
-                logits: bool = False):
-        """tokens: int32 CUDA tensor [B, n].  Returns (pairs [B,4] int32, logits_b, logits_d)."""
-        t = self.torch
-        assert tokens.dtype == t.int32 and tokens.is_cuda and tokens.dim() == 2 and tokens.is_contiguous()
-        B, n = tokens.shape
+    @staticmethod
+    def _sampling(tau, temperature, top_p, seeds):
         seed_arr = None
         if seeds is not None:
             seed_arr = (ctypes.c_uint64 * len(seeds))(*[int(s) for s in seeds])
         smp = PipoSampling(tau, temperature, top_p,
                            ctypes.cast(seed_arr, ctypes.POINTER(ctypes.c_uint64)) if seed_arr else None)
+        return smp, seed_arr
+
+    def _tokens(self, tokens):
+        t = self.torch
+        assert tokens.dtype == t.int32 and tokens.is_cuda and tokens.dim() == 2 and tokens.is_contiguous()
+        return tokens.shape
+
+    def prefill(self, tokens, tau: float, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
+                logits: bool = False):
+        """tokens: int32 CUDA tensor [B, n].  Returns (pairs [B,4] int32, logits_b, logits_d)."""
+        B, n = self._tokens(tokens)
+        smp, _keep = self._sampling(tau, temperature, top_p, seeds)
         out, lb, ld = self._outputs(B, logits)
         self._check(self.lib.pipo_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(out),
                                           _ptr(lb), _ptr(ld), self._stream()))
@@ -144,6 +155,32 @@ class PipoModel:
         """decode_step writing into caller-provided tensors (no allocation)."""
         self._check(self.lib.pipo_decode_step(self.ctx, _ptr(in_pairs), _ptr(out), _ptr(logits_b),
                                               _ptr(logits_d), self._stream()))
+
+    def regular_prefill(self, tokens, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
+                        logits: bool = False):
+        """Regular decoding's prefill over the n prompt tokens.  Returns (tok [B] int32, logits)."""
+        t = self.torch
+        B, n = self._tokens(tokens)
+        smp, _keep = self._sampling(0.0, temperature, top_p, seeds)
+        tok = t.empty(B, dtype=t.int32, device="cuda")
+        lg = t.empty((B, self.model.vocab), dtype=t.float32, device="cuda") if logits else None
+        self._check(self.lib.pipo_regular_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(tok),
+                                                  _ptr(lg), self._stream()))
+        self.batch = B
+        self._keep = tokens
+        return tok, lg
+
+    def regular_step(self, in_tok=None, logits: bool = False):
+        """One regular decoding step; in_tok: optional int32 CUDA tensor [B] (teacher forcing)."""
+        t = self.torch
+        tok = t.empty(self.batch, dtype=t.int32, device="cuda")
+        lg = t.empty((self.batch, self.model.vocab), dtype=t.float32, device="cuda") if logits else None
+        self._check(self.lib.pipo_regular_step(self.ctx, _ptr(in_tok), _ptr(tok), _ptr(lg), self._stream()))
+        return tok, lg
+
+    def regular_into(self, tok, in_tok=None, logits=None):
+        """regular_step writing into caller-provided tensors (no allocation)."""
+        self._check(self.lib.pipo_regular_step(self.ctx, _ptr(in_tok), _ptr(tok), _ptr(logits), self._stream()))
 
     def read_weight(self, name: str, start: int, count: int):
         import numpy as np

@@ -130,3 +130,39 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
         f"max_mean_rel {rep.max_mean_rel:.3g} conf_err {rep.max_conf_err:.3g} "
         f"ambiguous tokens {rep.ambiguous_tokens} accepts {rep.ambiguous_accepts}")
     return rep, host
+
+
+def run_regular_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_MEAN_REL):
+    """Regular decoding: the GPU runs free for ``steps`` token steps after its
+    prefill; the oracle replays the GPU's tokens as inputs.  Logits and tokens
+    are held to the bounds of the pair path."""
+    import torch
+
+    B = prompts.shape[0]
+    seeds = list(smp.seeds) if smp.seeds else [0] * B
+    tokens = torch.from_numpy(np.ascontiguousarray(prompts, dtype=np.int32)).cuda()
+    outs = [gpu_model.regular_prefill(tokens, smp.temperature, smp.top_p,
+                                      seeds if smp.temperature > 0 else None, logits=True)]
+    for _ in range(steps):
+        outs.append(gpu_model.regular_step(logits=True))
+    torch.cuda.synchronize()
+    host = [(t.cpu().numpy(), lg.cpu().numpy()) for t, lg in outs]
+    log(f"gpu done (regular): {B} sequences, {steps} steps")
+    orc = O.RegularOracle(W, kv_bf16=True)
+    rep = ParityReport()
+    for s, (tok, lg) in enumerate(host):
+        recs = orc.prefill(prompts, smp) if s == 0 else orc.step(in_tok=[int(v) for v in host[s - 1][0]])
+        rep.steps += 1
+        for i, r in enumerate(recs):
+            rep.rows += 1
+            t = f"step {s} seq {i}"
+            ma, mr = _row_err(lg[i], r["logits"])
+            rep.max_abs = max(rep.max_abs, ma)
+            rep.max_mean_rel = max(rep.max_mean_rel, mr)
+            if ma > LOGIT_MAX_ABS or mr > mean_rel_tol:
+                rep.failures.append(f"{t} logits: max_abs {ma:.3g} mean_rel {mr:.3g}")
+            u = rspec.uniform_draw(seeds[i], s, 0) if smp.temperature > 0 else None
+            _check_token(rep, t, int(tok[i]), r["tok"], lg[i], r["logits"], ma, smp, u)
+    log(f"regular parity: steps {rep.steps} rows {rep.rows} max_abs {rep.max_abs:.3g} "
+        f"max_mean_rel {rep.max_mean_rel:.3g} ambiguous tokens {rep.ambiguous_tokens}")
+    return rep, host

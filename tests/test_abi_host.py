@@ -84,6 +84,8 @@ def test_null_arguments(lib):
     smp = pipo.PipoSampling(0.5, 0.0, 1.0, None)
     assert lib.pipo_prefill(None, 1, None, 4, ctypes.byref(smp), None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_decode_step(None, None, None, None, None, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_regular_prefill(None, 1, None, 4, ctypes.byref(smp), None, None, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_regular_step(None, None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_read_weight(None, b"embed", 0, 1, None) == pipo.PIPO_EINVAL
     assert lib.pipo_free(None) == pipo.PIPO_OK
     assert b"ctx" in lib.pipo_last_error(None)

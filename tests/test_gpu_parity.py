@@ -10,7 +10,7 @@ from synth.configs import TINY, DENSE_4B, DENSE_9B, ModelConfig, model_tensor_sh
 from oracle import pipo_oracle as O
 
 sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
-from parity import run_parity  # noqa: E402
+from parity import run_parity, run_regular_parity  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -269,4 +269,67 @@ def test_abi_state_and_capacity_errors(torch):
         m.decode_step()
     torch.cuda.synchronize()
     assert e.value.code == PIPO_ECAPACITY
+    m.close()
+
+
+# ------------------------------------------------- regular decoding baseline
+
+def test_tiny_regular_parity_greedy_ragged_chunks(torch):
+    """Regular decoding on the tiny model: 37-token prompt (3 ragged chunks of
+    16), 10 greedy token steps, the decode graph replayed."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    n, steps = 37, 10
+    prompts = rspec.prompt_tokens(1, n, cfg.vocab, seed=12)
+    m = _model(cfg, seed=7, max_batch=1, max_latent=n + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(cfg, seed=7, precision="bf16")
+    rep, _ = run_regular_parity(m, W, prompts, steps, O.Sampling(tau=0.0), log)
+    rep.check()
+    m.close()
+
+
+def test_tiny_regular_parity_batch_top_p(torch):
+    B, n, steps = 3, 20, 6
+    prompts = rspec.prompt_tokens(B, n, TINY.vocab, seed=13)
+    smp = O.Sampling(tau=0.0, temperature=0.7, top_p=0.9, seeds=tuple(77 + b for b in range(B)))
+    m = _model(TINY, seed=3, max_batch=4, max_latent=n + steps + 1, prefill_chunk=64)
+    W = O.OracleWeights.generate(TINY, seed=3, precision="bf16")
+    rep, _ = run_regular_parity(m, W, prompts, steps, smp, log)
+    rep.check()
+    m.close()
+
+
+def test_4b_width_regular_two_layers_1024_tokens(torch):
+    """4B widths (2 layers), a 1024-token prompt in two chunks, 4 greedy steps."""
+    cfg = DENSE_4B.with_layers(2)
+    n, steps = 1024, 4
+    prompts = rspec.prompt_tokens(1, n, cfg.vocab, seed=14)
+    m = _model(cfg, seed=0, max_batch=1, max_latent=n + steps + 1, prefill_chunk=512)
+    W = O.OracleWeights.generate(cfg, seed=0, precision="bf16")
+    rep, _ = run_regular_parity(m, W, prompts, steps, O.Sampling(tau=0.0), log)
+    rep.check()
+    m.close()
+
+
+def test_regular_and_pair_sessions_share_one_context(torch):
+    """One context serves both decoders in turn; a step of the other kind is
+    refused until its own prefill."""
+    from paper_2605_27255_amd import PipoError, PIPO_ESTATE, PIPO_ECAPACITY
+    W = O.OracleWeights.generate(TINY, seed=0, precision="bf16")
+    m = _model(TINY, seed=0, max_batch=2, max_latent=24, prefill_chunk=16)
+    prompts = rspec.prompt_tokens(2, 16, TINY.vocab, seed=15)
+    rep, _ = run_regular_parity(m, W, prompts, 3, O.Sampling(tau=0.0), log)
+    rep.check()
+    with pytest.raises(PipoError) as e:
+        m.decode_step()
+    assert e.value.code == PIPO_ESTATE
+    rep, _ = run_parity(m, W, prompts, 3, O.Sampling(tau=0.5), log)
+    rep.check()
+    with pytest.raises(PipoError) as e:
+        m.regular_step()
+    assert e.value.code == PIPO_ESTATE
+    with pytest.raises(PipoError) as e:
+        m.regular_prefill(torch.from_numpy(rspec.prompt_tokens(1, 24, TINY.vocab)).cuda())
+    assert e.value.code == PIPO_ECAPACITY                       # 24 positions + 1 > 24
+    rep, _ = run_regular_parity(m, W, prompts[:1], 2, O.Sampling(tau=0.0), log)
+    rep.check()
     m.close()

@@ -429,3 +429,62 @@ def test_tiny_workload_shapes_run():
     assert 0 <= out[0]["tok_b"] < TINY.vocab and 0 < out[0]["conf"] < 1
     orc.decode_step()
     assert orc.length == [33]
+
+
+# ------------------------------------------------- regular decoding baseline
+
+def test_regular_session_equals_brute_force(small_w):
+    """Regular prefill + steps reproduce a from-scratch pass over E[tokens]."""
+    cfg = SMALL
+    prompt = rspec.prompt_tokens(1, 7, cfg.vocab)
+    orc = O.RegularOracle(small_w)
+    recs = [orc.prefill(prompt, O.Sampling(tau=0.0))[0]]
+    toks = list(prompt[0])
+    assert orc.length == [7]
+    for k in range(4):
+        toks.append(orc.next_tok[0])
+        recs.append(orc.step()[0])
+        assert orc.length == [8 + k]
+    X, _ = O.backbone_full(small_w, small_w["embed"][np.array(toks)])
+    for k, rec in enumerate(recs):
+        np.testing.assert_allclose(rec["h"], X[6 + k], rtol=1e-10, atol=1e-12)
+        # the fed-back token is the greedy choice of the tied head on that position
+        logits = (F.rms_norm(torch.from_numpy(X[6 + k]), (cfg.hidden,), torch.from_numpy(small_w["g_final"]),
+                             cfg.rms_eps) @ torch.from_numpy(small_w["embed"]).T).numpy()
+        assert rec["tok"] == int(np.argmax(logits))
+
+
+def test_regular_zero_layers_is_the_tied_head_of_the_embedding():
+    cfg = ModelConfig(n_layers=0, hidden=32, n_q_heads=2, n_kv_heads=1, head_dim=16, ffn=48, vocab=40,
+                      rope_base=1e4, rms_eps=1e-6, gain_mode=1)
+    W = O.OracleWeights.generate(cfg, seed=5, precision="bf16")
+    orc = O.RegularOracle(W)
+    prompt = rspec.prompt_tokens(1, 3, cfg.vocab)
+    rec = orc.prefill(prompt, O.Sampling(tau=0.0))[0]
+    e = torch.from_numpy(W["embed"])
+    expect = F.rms_norm(e[int(prompt[0, -1])], (cfg.hidden,), torch.from_numpy(W["g_final"]), cfg.rms_eps) @ e.T
+    np.testing.assert_allclose(rec["logits"], expect.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_pipo_with_first_slot_compressor_is_regular_decoding_on_odd_tokens(small_w):
+    """With W_c = [I 0] and b_c = 0, eq. 1 passes E[a] through, so the pair
+    decoder over a prompt's pairs equals the regular decoder over its tokens
+    at even indices: the two sessions share one backbone."""
+    cfg = SMALL
+    t = dict(small_w.t)
+    t["w_comp"] = np.concatenate([np.eye(cfg.hidden), np.zeros((cfg.hidden, cfg.hidden))], axis=1)
+    t["b_comp"] = np.zeros(cfg.hidden)
+    W = O.OracleWeights(cfg, t)
+    prompt = rspec.prompt_tokens(2, 10, cfg.vocab)
+    p = O.PipoOracle(W)
+    rp = p.prefill(prompt, O.Sampling(tau=0.5))
+    r = O.RegularOracle(W)
+    rr = r.prefill(prompt[:, 0::2], O.Sampling(tau=0.0))
+    for a, b in zip(rp, rr):
+        np.testing.assert_allclose(a["h_b"], b["h"], rtol=1e-12, atol=1e-12)
+        assert a["tok_b"] == b["tok"]
+    forced = [[a["tok_b"], 5] for a in rp]
+    sp = p.decode_step(in_pairs=forced)
+    sr = r.step(in_tok=[f[0] for f in forced])
+    for a, b in zip(sp, sr):
+        np.testing.assert_allclose(a["h_b"], b["h"], rtol=1e-12, atol=1e-12)

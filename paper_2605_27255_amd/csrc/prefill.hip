@@ -2,7 +2,7 @@
 // positions of every sequence.  Activations that feed an MFMA GEMM are kept
 // in the 16x32 tiled bf16 layout, as two planes hi and lo (x ~= hi + lo,
 // about 16 significant bits), so that both GEMM operands move as contiguous
-// 1 KB tiles from HBM to LDS to registers.
+// 1 KB tiles (weights straight into registers, activations through LDS).
 #include "device_common.h"
 #include "kernels.h"
 
@@ -166,130 +166,166 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
     }
 }
 
-// Workgroup tile BN x BM = (GN WNT 16) x (GM WMT 16), GN x GM waves of
-// (WNT x WMT) 16x16 fragments each; one 32-wide k tile per stage, LDS
-// double-buffered, the next stage requested into registers before the
-// current stage's MFMAs.  Workgroups run weight-tile fastest: the ones in
-// flight share a few token tiles, and the weight matrix (at most a few
-// hundred MB) is re-read from the memory-side cache rather than the token
-// activations (over a GB for a batch of long prompts) from HBM.
-// With a lo plane every W fragment meets the X hi and X lo fragments.
-template <int EPI, bool HASLO, int WNT, int WMT, int GN, int GM>
-__global__ __launch_bounds__(GN * GM * 64) void k_gemm(GemmParams p) {
-    constexpr int NT = GN * GM * 64;
-    constexpr int SN = GN * WNT, SM = GM * WMT;               // 16-row strips per tile
-    constexpr int NOPS = HASLO ? 3 : 2;                       // W, X hi, (X lo)
-    constexpr int TILES = SN + (NOPS - 1) * SM;               // 1 KB tiles per stage
-    constexpr int STAGE = TILES * 512;
-    constexpr int NCH = TILES * 64 / NT;                      // 16 B chunks per thread per stage
-    static_assert(TILES * 64 % NT == 0, "stage must split evenly over the threads");
-    extern __shared__ __align__(16) uint16_t lds[];           // [2][STAGE]
+// ---- MFMA GEMM  C^T[N][M] = W[N][K] X[M][K]^T, both operands tiled ---------
+// Workgroup tile 256 weight rows x 64 tokens, four waves of 64 x 64 (4 x 4
+// fragments).  A wave's 64 weight rows are its own, so their 1 KB tiles go
+// from memory straight into its registers (one contiguous load per tile, no
+// LDS); the token tiles (X hi and lo, 16 KB per 64-wide k step) are shared by
+// the four waves through a double-buffered LDS stage.  One iteration covers
+// two 32-wide k tiles; the next iteration's weights and X are requested
+// before this one's MFMAs, and X is written to LDS after them.  MFMAs run the
+// hi plane over all 16 accumulators, then the lo plane, so dependent MFMAs
+// are 16 apart (and every accumulator sees hi, lo of one k tile before the
+// next k tile).
+// Workgroups are placed per XCD (workgroup i runs on XCD i % 8): each XCD
+// takes a contiguous run of tiles in grouped order (8 weight tiles by every
+// token tile), so the ~64 workgroups resident on one XCD cover about 8 x 8
+// tiles and share their weight and token tiles in that XCD's L2.
+constexpr int kWdRows = 256, kWdToks = 64, kWdGroup = 8;
+
+__device__ __forceinline__ bool wd_tile(int id, int nbn, int nbm, int &bn, int &bm) {
+    const int T = nbn * nbm;
+    const int chunk = (T + 7) / 8;
+    const int u = (id & 7) * chunk + (id >> 3);
+    if (u >= T) return false;
+    const int gsz = kWdGroup * nbm;
+    const int grp = u / gsz, r = u - grp * gsz;
+    const int first = grp * kWdGroup;
+    const int gs = min(kWdGroup, nbn - first);
+    bn = first + r % gs;
+    bm = r / gs;
+    return true;
+}
+
+template <int EPI, bool HASLO>
+__global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
+    constexpr int NP = HASLO ? 2 : 1;
+    constexpr int XT = NP * 2 * 4;                            // X tiles per stage: plane x k-tile x token strip
+    constexpr int XC = XT / 4;                                // 16-byte X chunks per thread per stage
+    extern __shared__ __align__(16) uint16_t lds[];           // [2][XT][512]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = lane & 15;
-    const int wn = wave / GM, wm = wave - wn * GM;
-    const int nblk_n = (p.N + SN * 16 - 1) / (SN * 16);
-    const int bn = blockIdx.x % nblk_n, bm = blockIdx.x / nblk_n;
+    const int nbn = (p.N + kWdRows - 1) / kWdRows, nbm = (p.M + kWdToks - 1) / kWdToks;
+    int bn, bm;
+    if (!wd_tile(blockIdx.x, nbn, nbm, bn, bm)) return;
     const int KT = p.K >> 5;
-    const int NS = p.N >> 4, MS = p.M >> 4;   // strips
+    const int NI = (KT + 1) >> 1;                              // iterations of two k tiles
+    const int NS = p.N >> 4, MS = p.M >> 4;
 
-    // chunk c of a stage: tile c / 64 (W strips, then X hi, then X lo), 16 B c % 64
-    const uint16_t *src[NCH];
+    // this wave's four weight strips (padding strips read strip 0, masked later)
+    const uint16_t *wsrc[4];
 #pragma unroll
-    for (int r = 0; r < NCH; ++r) {
-        const int c = tid + r * NT;
-        const int t = c >> 6, within = c & 63;
-        const bool isw = t < SN, ishi = !isw && t < SN + SM;
-        int strip = isw ? bn * SN + t : bm * SM + (t - SN - (ishi ? 0 : SM));
-        strip = strip < (isw ? NS : MS) ? strip : 0;          // padding strips read strip 0 (masked later)
-        const uint16_t *base = isw ? p.W : (ishi ? p.X : p.Xlo);
-        src[r] = base + (int64_t)strip * KT * 512 + within * 8;
+    for (int si = 0; si < 4; ++si) {
+        int strip = bn * 16 + wave * 4 + si;
+        strip = strip < NS ? strip : 0;
+        wsrc[si] = p.W + (int64_t)strip * KT * 512 + lane * 8;
     }
-    u32x4 ra[NCH], rb[NCH];
-    // stages past K re-read the last stage (their products are never kept)
-    auto gload = [&](int kt, u32x4 (&reg)[NCH]) {
-        const int ktc = kt < KT ? kt : KT - 1;
+    // X chunks of this thread: c = tid + 256 r, tile c / 64 = (plane, kk, ms)
+    const uint16_t *xsrc[XC];
 #pragma unroll
-        for (int r = 0; r < NCH; ++r) reg[r] = *(const u32x4 *)(src[r] + (int64_t)ktc * 512);
+    for (int r = 0; r < XC; ++r) {
+        const int c = tid + 256 * r, t = c >> 6, within = c & 63;
+        const int plane = t >> 3, kk = (t >> 2) & 1, ms = t & 3;
+        int strip = bm * 4 + ms;
+        strip = strip < MS ? strip : 0;
+        xsrc[r] = (plane ? p.Xlo : p.X) + ((int64_t)strip * KT + kk) * 512 + within * 8;
+    }
+    // k tiles past the end re-read the last one (their products are skipped)
+    auto kclamp = [&](int kt) { return kt < KT ? kt : KT - 1; };
+    auto load_w = [&](int it, u32x4 (&w)[2][4]) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int si = 0; si < 4; ++si)
+                w[kk][si] = *(const u32x4 *)(wsrc[si] + (int64_t)kclamp(2 * it + kk) * 512);
     };
-    auto sstore = [&](int buf, const u32x4 (&reg)[NCH]) {
+    auto load_x = [&](int it, u32x4 (&x)[XC]) {
 #pragma unroll
-        for (int r = 0; r < NCH; ++r) *(u32x4 *)(&lds[buf * STAGE + (tid + r * NT) * 8]) = reg[r];
-    };
-
-    f32x4 acc[WNT][WMT];
-#pragma unroll
-    for (int a = 0; a < WNT; ++a)
-#pragma unroll
-        for (int c = 0; c < WMT; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    auto compute = [&](int buf) {
-        const uint16_t *L = lds + buf * STAGE;
-        u32x4 af[WNT], bh[WMT], bl[WMT];
-#pragma unroll
-        for (int si = 0; si < WNT; ++si) af[si] = *(const u32x4 *)(&L[(wn * WNT + si) * 512 + lane * 8]);
-#pragma unroll
-        for (int mi = 0; mi < WMT; ++mi) {
-            bh[mi] = *(const u32x4 *)(&L[(SN + wm * WMT + mi) * 512 + lane * 8]);
-            if (HASLO) bl[mi] = *(const u32x4 *)(&L[(SN + SM + wm * WMT + mi) * 512 + lane * 8]);
+        for (int r = 0; r < XC; ++r) {
+            const int kk = ((tid + 256 * r) >> 8) & 1;
+            const int kt = kclamp(2 * it + kk) - kk;           // xsrc already holds the kk offset
+            x[r] = *(const u32x4 *)(xsrc[r] + (int64_t)kt * 512);
         }
-#pragma unroll
-        for (int si = 0; si < WNT; ++si)
-#pragma unroll
-            for (int mi = 0; mi < WMT; ++mi) {
-                acc[si][mi] = mfma16(af[si], bh[mi], acc[si][mi]);
-                if (HASLO) acc[si][mi] = mfma16(af[si], bl[mi], acc[si][mi]);
-            }
     };
-    // two stages in registers ahead of the one in LDS: stage kt + 2 is
-    // requested while stage kt is multiplied and written to LDS after kt + 1
-    gload(0, ra);
-    sstore(0, ra);
-    gload(1, rb);
+    auto store_x = [&](int buf, const u32x4 (&x)[XC]) {
+#pragma unroll
+        for (int r = 0; r < XC; ++r) *(u32x4 *)(&lds[(buf * XT * 64 + tid + 256 * r) * 8]) = x[r];
+    };
+
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto mma = [&](int buf, int it, const u32x4 (&w)[2][4]) {
+        const uint16_t *L = lds + buf * XT * 512;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            if (kk == 1 && 2 * it + 1 >= KT) break;            // odd K: no second tile
+            u32x4 bh[4], bl[4];
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi) {
+                bh[mi] = *(const u32x4 *)(&L[((0 * 2 + kk) * 4 + mi) * 512 + lane * 8]);
+                if (HASLO) bl[mi] = *(const u32x4 *)(&L[((1 * 2 + kk) * 4 + mi) * 512 + lane * 8]);
+            }
+#pragma unroll
+            for (int si = 0; si < 4; ++si)
+#pragma unroll
+                for (int mi = 0; mi < 4; ++mi) acc[si][mi] = mfma16(w[kk][si], bh[mi], acc[si][mi]);
+            if (HASLO) {
+#pragma unroll
+                for (int si = 0; si < 4; ++si)
+#pragma unroll
+                    for (int mi = 0; mi < 4; ++mi) acc[si][mi] = mfma16(w[kk][si], bl[mi], acc[si][mi]);
+            }
+        }
+    };
+
+    u32x4 wa[2][4], wb[2][4], xr[XC];
+    load_x(0, xr);
+    load_w(0, wa);
+    store_x(0, xr);
     __syncthreads();
-    gload(2, ra);
-    for (int kt = 0; kt < KT; kt += 2) {
-        compute(0);
-        sstore(1, rb);
+    // iteration it: request it + 1, multiply it, stage X of it + 1
+    for (int it = 0; it < NI; it += 2) {
+        load_x(it + 1, xr);
+        load_w(it + 1, wb);
+        mma(0, it, wa);
+        store_x(1, xr);
         __syncthreads();
-        gload(kt + 3, rb);
-        if (kt + 1 < KT) compute(1);
-        sstore(0, ra);
+        if (it + 1 >= NI) break;
+        load_x(it + 2, xr);
+        load_w(it + 2, wa);
+        mma(1, it + 1, wb);
+        store_x(0, xr);
         __syncthreads();
-        gload(kt + 4, ra);
     }
 
 #pragma unroll
-    for (int si = 0; si < WNT; ++si)
+    for (int si = 0; si < 4; ++si)
 #pragma unroll
-        for (int mi = 0; mi < WMT; ++mi)
-            gemm_epi<EPI>(p, acc[si][mi], bn * SN + wn * WNT + si, bm * SM * 16 + (wm * WMT + mi) * 16 + j);
+        for (int mi = 0; mi < 4; ++mi)
+            gemm_epi<EPI>(p, acc[si][mi], bn * 16 + wave * 4 + si, bm * kWdToks + mi * 16 + j);
 }
 
-template <int EPI, bool HASLO, int WNT, int WMT, int GN, int GM>
-static void launch_gemm_t(const GemmParams &p, hipStream_t s) {
-    constexpr int SN = GN * WNT, SM = GM * WMT;
-    const int grid = ((p.N + SN * 16 - 1) / (SN * 16)) * ((p.M + SM * 16 - 1) / (SM * 16));
-    const int lds = 2 * (SN + (HASLO ? 2 : 1) * SM) * 512 * 2;
-    hipLaunchKernelGGL((k_gemm<EPI, HASLO, WNT, WMT, GN, GM>), dim3(grid), dim3(GN * GM * 64), lds, s, p);
-}
-
-// Tile (from a sweep on MI355X at 4096 tokens over the 4B shapes): 128
-// weight rows x 128 tokens, eight waves of 32 x 64, two waves per SIMD.
 template <int EPI, bool HASLO>
-static void launch_gemm_e(const GemmParams &p, hipStream_t s) {
-    launch_gemm_t<EPI, HASLO, 2, 4, 4, 2>(p, s);
+static void launch_gemm_wd(const GemmParams &p, hipStream_t s) {
+    const int nbn = (p.N + kWdRows - 1) / kWdRows, nbm = (p.M + kWdToks - 1) / kWdToks;
+    const int grid = 8 * ((nbn * nbm + 7) / 8);
+    hipLaunchKernelGGL((k_gemm_wd<EPI, HASLO>), dim3(grid), dim3(256), 2 * (HASLO ? 16 : 8) * 1024, s, p);
 }
 
 void launch_gemm(const GemmParams &p, hipStream_t s) {
     if (!p.Xlo) {   // the gathered embedding pairs are exact in bf16
-        launch_gemm_e<EPI_STORE, false>(p, s);
+        launch_gemm_wd<EPI_STORE, false>(p, s);
         return;
     }
     switch (p.epi) {
-        case EPI_STORE: launch_gemm_e<EPI_STORE, true>(p, s); break;
-        case EPI_RESID: launch_gemm_e<EPI_RESID, true>(p, s); break;
-        case EPI_SWIGLU: launch_gemm_e<EPI_SWIGLU, true>(p, s); break;
-        default: launch_gemm_e<EPI_QKV, true>(p, s); break;
+        case EPI_STORE: launch_gemm_wd<EPI_STORE, true>(p, s); break;
+        case EPI_RESID: launch_gemm_wd<EPI_RESID, true>(p, s); break;
+        case EPI_SWIGLU: launch_gemm_wd<EPI_SWIGLU, true>(p, s); break;
+        default: launch_gemm_wd<EPI_QKV, true>(p, s); break;
     }
 }
 

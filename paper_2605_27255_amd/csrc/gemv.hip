@@ -29,7 +29,6 @@ namespace pipo {
 constexpr int kNW = 8;                       // waves per workgroup
 constexpr int kGemvOneLdsBytes = 72 * 1024;  // budget for wave-private X (two workgroups per CU)
 constexpr int kWideChunk = 8;                // k-tiles per shared X chunk (larger batches)
-constexpr int kWideTargetWgs = 128;          // workgroups the k-ranges aim for (fewer, longer ranges measured faster)
 constexpr int kXR = 3;                       // prologue chunks per thread loaded ahead of the weights
 
 __device__ __forceinline__ float silu_f(float u) { return u / (1.0f + __expf(-u)); }
@@ -541,15 +540,14 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Large batches.  k_xprep: one workgroup per row b writes X[b] = the GEMV
-// input with its RMSNorm scale(s) and gains applied, split into bf16 hi / lo
-// planes.  k_gemv_wide: a workgroup owns 128 weight rows (one 16-row strip
-// per wave) and a range of k-tiles; chunks of X (all B rows, hi and lo) pass
-// through LDS once per workgroup and are shared by its eight waves, which
-// keeps the X traffic well below the weight traffic for any batch up to 32.
-// Weights stream one chunk ahead of the chunk being multiplied.  With several
-// k-ranges the partial sums go to a workspace and k_gemv_fin adds them in
-// range order and runs the epilogue.
+// The vocabulary head at larger batches.  k_xprep: one workgroup per row b
+// writes X[b] = the GEMV input with its RMSNorm scale applied, split into
+// bf16 hi / lo planes.  k_gemv_wide: a workgroup owns 128 weight rows (one
+// 16-row strip per wave) over the whole K; chunks of X (all B rows, hi and
+// lo) pass through LDS once per workgroup and are shared by its eight waves.
+// Weights stream one chunk ahead of the chunk being multiplied.  (The kernel
+// can also take a k-range with partial sums for k_gemv_fin; the head never
+// splits K, since its argmax epilogue is workgroup-wide.)
 template <int PRO>
 __global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
     // workgroup (b, segment): columns [2048 seg, 2048 seg + 2048) of row b
@@ -752,6 +750,183 @@ __global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Batches whose X does not fit wave-private (k_gemv_kr).  K is cut into
+// ksplit ranges of krt k-tiles; workgroup w works on range w % ksplit,
+// stages that range's slice of X (all B rows, hi and lo) in LDS once, and
+// its eight waves then stream whole 16-row strips of the range, each wave on
+// its own strips: after the staging there is no barrier and no cross-wave
+// reduction.  A wave's tiles over all its strips form one stream in batches
+// of U, two batches in flight, loads unconditional (tiles past the stream
+// read the matrix's first line and are multiplied as zero).  With one range
+// the wave runs the fused epilogue per strip; otherwise it writes the
+// strip's partial sums (RMSNorm scale applied) and k_gemv_fin adds the
+// ranges in range order.
+constexpr int kKrLdsBytes = 128 * 1024;      // X slice budget of a k-range workgroup (one per CU)
+constexpr int kKrChunks = 8;                 // X chunks per thread: B * k-tiles * 4 <= 8 * 512
+template <int PRO>   // the MTP's chunks hold both halves' sources, so fewer fit in registers
+struct KrChunks { static constexpr int n = PRO == PRO_MTP ? 6 : kKrChunks; };
+constexpr int kKrWaves = 1280;               // streaming waves the ranges aim for (~20 MB in flight)
+template <int NBT, int PRO, int EPI, int U>
+__global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
+    constexpr int NA = NAcc<PRO>::n;
+    extern __shared__ __align__(16) uint16_t xs[];
+    __shared__ float sc0[32], sc1[32];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int j = lane & 15, g = lane >> 4;
+    const int nstrips = p.N >> 4;
+    const int KT = p.K >> 5, HT = p.H >> 5, B = p.B;
+    const int R = p.ksplit;
+    const int r = (int)blockIdx.x % R;                         // this workgroup's k-range
+    const int wr = ((int)gridDim.x - r + R - 1) / R;          // workgroups on range r
+    const int wid = ((int)blockIdx.x / R) * kNW + wave;       // this wave among the range's waves
+    const int nwr = wr * kNW;
+    const int kt0 = r * p.krt;
+    const int nt = min(p.krt, KT - kt0);                       // k-tiles of this range
+    const int rstride = p.krt * 32 + 8;
+    uint16_t *xh = xs, *xl = xs + B * rstride;
+    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+    const int ns = wid < nstrips ? (nstrips - 1 - wid) / nwr + 1 : 0;   // strips wid, wid + nwr, ...
+    const int nb = (nt + U - 1) / U;                          // batches per strip (the last one padded)
+    const int nq = ns * nb;
+    // tile u of batch q: strip q / nb, k-tile U (q % nb) + u of the range
+    auto wptr = [&](int q, int u) -> const u32x4 * {
+        const int sidx = q / nb, i = (q - sidx * nb) * U + u;
+        const int strip = wid + sidx * nwr;
+        return (const u32x4 *)(q < nq && i < nt ? p.W + ((int64_t)strip * KT + kt0 + i) * 512 + lane * 8 : p.W);
+    };
+    // 1. the whole X slice (at most KC 8-column chunks per thread) and
+    //    the RMSNorm inputs requested at once, then two weight batches
+    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
+    const int per_row = nt * 4, count = B * per_row;
+    const int col0 = kt0 * 32;
+    constexpr int KC = KrChunks<PRO>::n;
+    XSrc src[KC];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+        int idx = threadIdx.x + c * (kNW * 64);
+        idx = idx < count ? idx : 0;
+        const int b = idx / per_row;
+        load_src<PRO>(p, b, col0 + ((idx - b * per_row) << 3), src[c]);
+    }
+    constexpr int RPW = 2 * NBT;
+    float ssv[RPW][4];
+    if (NORM) {
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int b = wave + rr * kNW, i = lane + 64 * t;
+                ssv[rr][t] = p.ss[(b < B && i < p.nss) ? b * p.nss + i : 0];
+            }
+    }
+    u32x4 ra[U], rb[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(wptr(0, u));
+#pragma unroll
+    for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(wptr(1, u));
+    __builtin_amdgcn_sched_barrier(0);
+    // 2. the slice into LDS (shared by the eight waves), the RMSNorm scalars
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+        const int idx = threadIdx.x + c * (kNW * 64);
+        if (idx < count) {
+            const int b = idx / per_row, k = (idx - b * per_row) << 3;
+            u32x4 vh, vl;
+            make_chunk<PRO>(p, col0 + k, src[c], vh, vl);
+            *(u32x4 *)(xh + b * rstride + k) = vh;
+            if (PRO != PRO_PAIR) *(u32x4 *)(xl + b * rstride + k) = vl;
+        }
+    }
+    if (NORM) {
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr) {
+            const int b = wave + rr * kNW;
+            float a = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? ssv[rr][t] : 0.f;
+            a = wave_sum(a);
+            if (b < B && lane == 0) sc0[b] = rsqrtf(a / (float)(PRO == PRO_MTP ? p.H : p.K) + p.eps);
+        }
+    }
+    if (PRO == PRO_MTP) {   // RMSNorm scale of E[tok] (a short row)
+        for (int b = wave; b < B; b += kNW) {
+            const int tok = clamp_id(argmax_key_id(p.tokkey[b]), p.vocab);
+            float e2 = 0.f;
+            for (int k = lane * 8; k < p.H; k += 512) {
+                const u32x4 w = *(const u32x4 *)(p.embed + tiled_index(tok, k, p.H));
+#pragma unroll
+                for (int i = 0; i < 4; ++i) e2 += bf_lo(w[i]) * bf_lo(w[i]) + bf_hi(w[i]) * bf_hi(w[i]);
+            }
+            e2 = wave_sum(e2);
+            if (lane == 0) sc1[b] = rsqrtf(e2 / (float)p.H + p.eps);
+        }
+    }
+    __syncthreads();
+
+    f32x4 acc[NA][NBT];
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto finish = [&](int sidx) {
+        const int strip = wid + sidx * nwr;
+        f32x4 fin[NBT];
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            const float s0 = b < B ? sc0[b] : 0.f;
+            f32x4 v = acc[0][bt];
+            if (NA == 2) v = v * s0 + acc[NA - 1][bt] * (b < B ? sc1[b] : 0.f);
+            else if (PRO == PRO_NORM) v *= s0;
+            fin[bt] = v;
+        }
+#pragma unroll
+        for (int a = 0; a < NA; ++a)
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (R == 1) {
+            f32x4 resid[NBT];
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                resid[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (EPI == EPI_RESID)
+                    resid[bt] = *(const f32x4 *)(p.out + (b < B ? (int64_t)b * p.N + strip * 16 + 4 * g : 0));
+            }
+            gemv_epilogue<NBT, EPI>(p, fin, resid, strip, true);
+        } else {
+#pragma unroll
+            for (int bt = 0; bt < NBT; ++bt) {
+                const int b = bt * 16 + j;
+                if (b < B) *(f32x4 *)(p.part + ((int64_t)r * B + b) * p.N + strip * 16 + 4 * g) = fin[bt];
+            }
+        }
+    };
+    auto consume = [&](const u32x4 (&Rg)[U], int q) {
+        const int sidx = q / nb, i0 = (q - sidx * nb) * U;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u;
+            const bool ok = q < nq && i < nt;
+            tile_mma<NBT, PRO>(acc, ok ? Rg[u] : zero, ok ? kt0 + i : 0, ok ? 32 * i : 0, HT, B, xh, xl, rstride);
+        }
+        if (q < nq && i0 + U >= nt) finish(sidx);
+    };
+    // 3. stream; the last pair of batches is peeled so no load is left in flight
+    int q = 0;
+    for (; q + 2 < nq; q += 2) {
+        consume(ra, q);
+#pragma unroll
+        for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(wptr(q + 2, u));
+        consume(rb, q + 1);
+#pragma unroll
+        for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(wptr(q + 3, u));
+    }
+    consume(ra, q);
+    consume(rb, q + 1);
+}
+
 // Sum of the k-range partials in range order, then the fused epilogue.
 template <int NBT, int EPI>
 // One wave per strip (the vocabulary head never splits K, so the logits
@@ -805,19 +980,42 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
         hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s, q);
         return;
     }
-    // otherwise: X planes, then 128-row workgroups over k-ranges
+    // otherwise, below the vocabulary head: k-ranges whose X slices fit
+    if constexpr (EPI != EPI_LOGITS) {
+        // k-tiles per range: the X slice (hi + lo bf16) within the LDS budget
+        // and the per-thread chunk count, and enough ranges x strips for the
+        // streaming waves
+        int kmax = kKrLdsBytes / (2 * 2 * q.B * 32);
+        const int krt_c = KrChunks<PRO>::n * kNW * 64 / (4 * q.B);
+        kmax = (kmax < krt_c ? kmax : krt_c) / 8 * 8;            // whole load batches of 8 tiles
+        int R = (KT + kmax - 1) / kmax;
+        const int r_par = (kKrWaves + (q.N >> 4) - 1) / (q.N >> 4);
+        R = R > r_par ? R : r_par;
+        R = R < KT ? R : KT;
+        int krt = (KT + R - 1) / R;                              // even ranges, rounded to whole batches
+        krt = (krt + 7) / 8 * 8;
+        krt = krt < kmax ? krt : kmax;
+        R = (KT + krt - 1) / krt;
+        const bool partials = R > 1 && (int64_t)R * q.B * q.N <= q.part_cap;
+        if (kmax >= 8 && (R == 1 || partials)) {
+            q.ksplit = R;
+            q.krt = krt;
+            const int lds_kr = 2 * q.B * (krt * 32 + 8) * 2;
+            const int grid_kr = ((q.wg_cap > 0 ? q.wg_cap : 256) / R) * R;   // whole rounds of ranges
+            hipLaunchKernelGGL((k_gemv_kr<NBT, PRO, EPI, 8>), dim3(grid_kr > R ? grid_kr : R), dim3(kNW * 64),
+                               lds_kr, s, q);
+            if (R > 1) hipLaunchKernelGGL((k_gemv_fin<NBT, EPI>), dim3(q.N >> 4), dim3(64), 0, s, q);
+            return;
+        }
+    }
+    // the vocabulary head (and any matrix whose partials would not fit the
+    // workspace): X planes, then 128-row workgroups over the whole K
     q.xseg = (q.K + 2047) / 2048;
     hipLaunchKernelGGL((k_xprep<PRO>), dim3(q.B * q.xseg), dim3(256), 0, s, q);
     const int rtiles = ((q.N >> 4) + kNW - 1) / kNW;
-    const int NC = (KT + kWideChunk - 1) / kWideChunk;
-    int ksplit = (kWideTargetWgs + rtiles - 1) / rtiles;
-    ksplit = ksplit < NC ? ksplit : NC;
-    const int64_t cap = q.part_cap / ((int64_t)q.B * q.N);
-    ksplit = ksplit < cap ? ksplit : (int)cap;
-    q.ksplit = (ksplit < 1 || EPI == EPI_LOGITS) ? 1 : ksplit;
+    q.ksplit = 1;
     const int lds_w = 2 * 2 * q.B * (kWideChunk * 32 + 8) * 2 + 16;
-    hipLaunchKernelGGL((k_gemv_wide<NBT, EPI>), dim3(rtiles * q.ksplit), dim3(kNW * 64), lds_w, s, q);
-    if (q.ksplit > 1) hipLaunchKernelGGL((k_gemv_fin<NBT, EPI>), dim3(q.N >> 4), dim3(64), 0, s, q);
+    hipLaunchKernelGGL((k_gemv_wide<NBT, EPI>), dim3(rtiles), dim3(kNW * 64), lds_w, s, q);
 }
 
 // Batch size U: two batches of U tiles per wave are in flight.  Five when a

@@ -47,6 +47,7 @@ struct GemvParams {
     uint16_t *xh, *xl;            // X planes workspace, [B][K] bf16 each (large batches)
     float *part; int64_t part_cap;  // k-range partial sums workspace (floats)
     int ksplit;                   // k-ranges (set by launch_gemv)
+    int krt;                      // k-tiles per range of the k-range kernel (set by launch_gemv)
     int xseg;                     // 2048-column segments per row of the X planes (set by launch_gemv)
 };
 void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s);

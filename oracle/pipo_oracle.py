@@ -31,6 +31,16 @@ silent:
   a single linear replaces App. B.3's two-layer MLP, as the configurations
   fix it.  The draft is accepted iff ``c >= tau`` (equality accepts), and the
   next input pair is ``(b, d)`` if accepted else ``(b, PAD)`` (Sec. 3.2).
+* Paper-default heads (``ModelConfig.heads`` flags; the workloads use none):
+  the MLP compressor of Table 4, read as ``E[a] + E[b] + W2 SiLU(W1 [E[a];
+  E[b]])`` with an inner width of H: the paper initialises it to a + b by
+  zeroing "the residual branch", so the printed W2 SiLU(W1 .) is that branch
+  and a + b its skip path; the MTP head of App. B.2, W_fc followed by one
+  decoder layer shaped like the backbone's, with its own KV cache over latent
+  positions (RoPE at the latent index); during prefill, latent i < L-1 gets
+  the prompt token that follows its pair (x^{2i+2}) as the MTP input token,
+  the last latent the selected backbone token; the confidence head of App.
+  B.3, ``sigmoid(W2 SiLU(W1 RMSNorm([h_b; h_d]; g_c)))`` without biases.
 * KV cache storage: the workloads fix a bf16 KV cache (like the bf16
   weights, a storage format), so with ``kv_bf16`` the keys (after RoPE) and
   values are rounded to bf16 (nearest even) as they enter the cache; every
@@ -51,7 +61,8 @@ from dataclasses import dataclass
 import numpy as np
 
 from synth import rspec
-from synth.configs import ModelConfig, model_tensor_shapes
+from synth.configs import (ModelConfig, model_tensor_shapes, HEADS_MLP_COMPRESSOR, HEADS_MTP_LAYER,
+                           HEADS_MLP_CONFIDENCE)
 
 F64 = np.float64
 
@@ -117,6 +128,15 @@ def compress(E, W_c, b_c, pairs):
     return cat @ np.asarray(W_c, F64).T + np.asarray(b_c, F64)
 
 
+def compress_mlp(E, W1, W2, pairs):
+    """Pair-in compressor, MLP variant (Table 4, with its a + b skip path):
+    ``E[a] + E[b] + W2 SiLU(W1 [E[a]; E[b]])``."""
+    pairs = np.asarray(pairs).reshape(-1, 2)
+    a, b = E[pairs[:, 0]].astype(F64), E[pairs[:, 1]].astype(F64)
+    cat = np.concatenate([a, b], axis=-1)
+    return a + b + silu(cat @ np.asarray(W1, F64).T) @ np.asarray(W2, F64).T
+
+
 def attention_decode(q, K, V):
     """One query position against a causal prefix, grouped-query.
 
@@ -175,6 +195,14 @@ def confidence(w_c, g_c, h_b, h_d, eps):
     return s, 1.0 / (1.0 + np.exp(-s))
 
 
+def confidence_mlp(W1, w2, g_c, h_b, h_d, eps):
+    """Confidence head, App. B.3 form: s = w2 . SiLU(W1 RMSNorm([h_b; h_d]; g_c));
+    returns (s, sigmoid(s))."""
+    n = rms_norm(np.concatenate([h_b, h_d], axis=-1), g_c, eps)
+    s = silu(n @ np.asarray(W1, F64).T) @ np.asarray(w2, F64)
+    return s, 1.0 / (1.0 + np.exp(-s))
+
+
 def gate(c, tau):
     """Accept the draft iff ``c >= tau`` (Sec. 3.2)."""
     return bool(c >= tau)
@@ -224,8 +252,7 @@ class OracleWeights:
         """R-spec weights; ``precision`` 'bf16' rounds every tensor to bf16 first."""
         tensors = {}
         for name, shape in model_tensor_shapes(cfg).items():
-            tid = (rspec.TENSOR_IDS[name] if "." not in name
-                   else rspec.layer_tid(int(name.split(".")[0][1:]), name.split(".")[1]))
+            tid = rspec.tensor_id(name)
             base = name.split(".")[-1]
             if base.startswith("g_"):
                 v = rspec.gain_values(seed, tid, shape[0], cfg.gain_mode)
@@ -283,6 +310,32 @@ def backbone_full(W: OracleWeights, Z, kv_bf16=False):
     return x, caches
 
 
+def mtp_layer(W: OracleWeights):
+    """Weights of the MTP head's decoder layer (App. B.2) as a layer dict."""
+    return {k.split(".", 1)[1]: v for k, v in W.t.items() if k.startswith("mtp.")}
+
+
+def layer_full(cfg, L, X, kv_bf16=False):
+    """One decoder layer over positions 0..T-1 from scratch: (output, (K, V))."""
+    x = np.asarray(X, F64).copy()
+    T = x.shape[0]
+    q, k, v = _layer_qkv(cfg, L, x, np.arange(T), kv_bf16)
+    o = attention_causal(q, k, v)
+    x = x + o.transpose(1, 0, 2).reshape(T, cfg.q_dim) @ L["wo"].T
+    return _layer_ffn(cfg, L, x), (k, v)
+
+
+def layer_step(cfg, L, x, pos, cache, kv_bf16=False):
+    """One decoder layer for one position against ``cache`` = [K, V] (appended)."""
+    x = np.asarray(x, F64).reshape(1, -1).copy()
+    q, k, v = _layer_qkv(cfg, L, x, np.array([pos]), kv_bf16)
+    cache[0] = np.concatenate([cache[0], k], axis=1)
+    cache[1] = np.concatenate([cache[1], v], axis=1)
+    o, _ = attention_decode(q[:, 0], cache[0], cache[1])
+    x = x + o.reshape(1, cfg.q_dim) @ L["wo"].T
+    return _layer_ffn(cfg, L, x)[0]
+
+
 def backbone_step(W: OracleWeights, z, pos, caches, kv_bf16=False):
     """Eq. 2 incrementally: one latent at position ``pos`` against the cache.
 
@@ -323,17 +376,28 @@ class PipoOracle:
         self.cfg = W.cfg
         self.kv_bf16 = kv_bf16
 
-    # heads: eqs. 3-6 and the gate, for one sequence
-    def heads(self, h_b, seq, step, force_b=None):
+    def _compress(self, pairs):
+        W = self.W
+        if self.cfg.heads & HEADS_MLP_COMPRESSOR:
+            return compress_mlp(W["embed"], W["comp_w1"], W["comp_w2"], pairs)
+        return compress(W["embed"], W["w_comp"], W["b_comp"], pairs)
+
+    # heads: eqs. 3-6 and the gate, for one sequence; ``pos`` is h_b's latent index
+    def heads(self, h_b, seq, step, pos, force_b=None):
         cfg, W, smp = self.cfg, self.W, self.sampling
         eps = cfg.rms_eps
         logits_b = lm_logits(W["embed"], W["g_final"], h_b, eps)
         b = self._select(logits_b, seq, step, 0)
         b_used = b if force_b is None else int(force_b)
         h_d = mtp_hidden(W["w_fc"], W["g_mtp_h"], W["g_mtp_e"], h_b, W["embed"][b_used], eps)
+        if cfg.heads & HEADS_MTP_LAYER:
+            h_d = layer_step(cfg, mtp_layer(W), h_d, pos, self.mtp_caches[seq], self.kv_bf16)
         logits_d = lm_logits(W["embed"], W["g_mtp_o"], h_d, eps)
         d = self._select(logits_d, seq, step, 1)
-        s, c = confidence(W["w_conf"], W["g_conf"], h_b, h_d, eps)
+        if cfg.heads & HEADS_MLP_CONFIDENCE:
+            s, c = confidence_mlp(W["conf_w1"], W["conf_w2"], W["g_conf"], h_b, h_d, eps)
+        else:
+            s, c = confidence(W["w_conf"], W["g_conf"], h_b, h_d, eps)
         return dict(tok_b=b, tok_d=d, s=float(s), conf=float(c), accept=gate(c, smp.tau),
                     logits_b=logits_b, logits_d=logits_d, h_b=h_b, h_d=h_d)
 
@@ -348,15 +412,26 @@ class PipoOracle:
         """Compressed-prompt prefill of every sequence; returns the first pair."""
         self.sampling = sampling
         W, cfg = self.W, self.cfg
-        self.caches, self.length, self.step_idx, self.next_pairs = [], [], [], []
+        self.caches, self.length, self.step_idx, self.next_pairs, self.mtp_caches = [], [], [], [], []
         out = []
         for i, prompt in enumerate(np.asarray(prompts)):
             pairs = prompt_pairs(prompt, cfg.pad_id)
-            Z = compress(W["embed"], W["w_comp"], W["b_comp"], pairs)
+            Z = self._compress(pairs)
             X, caches = backbone_full(W, Z, self.kv_bf16)
             self.caches.append([[k, v] for k, v in caches])
             self.length.append(len(pairs))
-            rec = self.heads(X[-1], i, 0, None if force_b is None else force_b[i])
+            if cfg.heads & HEADS_MTP_LAYER:
+                # latents 0..L-2 take the prompt token after their pair as the MTP token
+                L = len(pairs)
+                U = np.stack([mtp_hidden(W["w_fc"], W["g_mtp_h"], W["g_mtp_e"], X[j], W["embed"][pairs[j + 1, 0]],
+                                         cfg.rms_eps) for j in range(L - 1)]) if L > 1 else np.zeros((0, cfg.hidden))
+                if L > 1:
+                    _, (k, v) = layer_full(cfg, mtp_layer(W), U, self.kv_bf16)
+                else:
+                    k = np.zeros((cfg.n_kv_heads, 0, cfg.head_dim))
+                    v = np.zeros((cfg.n_kv_heads, 0, cfg.head_dim))
+                self.mtp_caches.append([k, v])
+            rec = self.heads(X[-1], i, 0, len(pairs) - 1, None if force_b is None else force_b[i])
             out.append(rec)
             self.step_idx.append(1)
             self.next_pairs.append(self._next_pair(rec))
@@ -371,10 +446,11 @@ class PipoOracle:
         out = []
         for i in range(len(self.caches)):
             pair = self.next_pairs[i] if in_pairs is None else tuple(int(v) for v in in_pairs[i])
-            z = compress(W["embed"], W["w_comp"], W["b_comp"], np.array([pair]))[0]
-            h_b = backbone_step(W, z, self.length[i], self.caches[i], self.kv_bf16)
+            z = self._compress(np.array([pair]))[0]
+            pos = self.length[i]
+            h_b = backbone_step(W, z, pos, self.caches[i], self.kv_bf16)
             self.length[i] += 1
-            rec = self.heads(h_b, i, self.step_idx[i], None if force_b is None else force_b[i])
+            rec = self.heads(h_b, i, self.step_idx[i], pos, None if force_b is None else force_b[i])
             out.append(rec)
             self.step_idx[i] += 1
             self.next_pairs[i] = self._next_pair(rec)

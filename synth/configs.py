@@ -22,6 +22,7 @@ class ModelConfig:
     rope_base: float = 1e6
     rms_eps: float = 1e-6
     gain_mode: int = 0          # 0: RMSNorm gains are 1; 1: 1 + 10*R-spec
+    heads: int = 0              # paper-default heads (HEADS_* flags); 0: the one-linear forms
 
     @property
     def pad_id(self) -> int:
@@ -52,6 +53,13 @@ class ModelConfig:
         return 2 * self.n_layers * self.kv_dim * 2
 
 
+#: ``ModelConfig.heads`` flags: the App. B forms of the three heads.
+HEADS_MLP_COMPRESSOR = 1     # z = E[a] + E[b] + W2 SiLU(W1 [E[a]; E[b]])  (Table 4, MLP)
+HEADS_MTP_LAYER = 2          # h_d = Layer(W_fc [...]) with its own latent KV cache (App. B.2)
+HEADS_MLP_CONFIDENCE = 4     # c = sigmoid(W2 SiLU(W1 RMSNorm([h_b; h_d])))  (App. B.3)
+HEADS_PAPER = 7
+
+
 def model_tensor_shapes(cfg: ModelConfig) -> dict:
     """Logical ``[out][in]`` shapes of every tensor, keyed by name."""
     h = cfg.hidden
@@ -71,6 +79,17 @@ def model_tensor_shapes(cfg: ModelConfig) -> dict:
         shapes[f"l{li}.wdown"] = (h, cfg.ffn)
         shapes[f"l{li}.g_attn"] = (h,)
         shapes[f"l{li}.g_ffn"] = (h,)
+    if cfg.heads & HEADS_MLP_COMPRESSOR:
+        shapes["comp_w1"] = (h, 2 * h)
+        shapes["comp_w2"] = (h, h)
+    if cfg.heads & HEADS_MTP_LAYER:
+        for name, shp in (("wq", (cfg.q_dim, h)), ("wk", (cfg.kv_dim, h)), ("wv", (cfg.kv_dim, h)),
+                          ("wo", (h, cfg.q_dim)), ("wgate", (cfg.ffn, h)), ("wup", (cfg.ffn, h)),
+                          ("wdown", (h, cfg.ffn)), ("g_attn", (h,)), ("g_ffn", (h,))):
+            shapes[f"mtp.{name}"] = shp
+    if cfg.heads & HEADS_MLP_CONFIDENCE:
+        shapes["conf_w1"] = (h, 2 * h)
+        shapes["conf_w2"] = (h,)
     return shapes
 
 

@@ -50,6 +50,10 @@ TENSOR_IDS = {
     "g_mtp_e": 7,    # MTP RMSNorm gain on the token embedding [H]
     "g_mtp_o": 8,    # MTP output RMSNorm gain [H]
     "g_conf": 9,     # confidence RMSNorm gain [2H]
+    "comp_w1": 10,   # MLP compressor W1 [H, 2H]
+    "comp_w2": 11,   # MLP compressor W2 [H, H]
+    "conf_w1": 12,   # confidence MLP W1 [H, 2H]
+    "conf_w2": 13,   # confidence MLP W2 [H]
 }
 _LAYER_SLOTS = {"wq": 0, "wk": 1, "wv": 2, "wo": 3, "wgate": 4, "wup": 5,
                 "wdown": 6, "g_attn": 7, "g_ffn": 8}
@@ -57,6 +61,20 @@ _LAYER_SLOTS = {"wq": 0, "wk": 1, "wv": 2, "wo": 3, "wgate": 4, "wup": 5,
 
 def layer_tid(layer: int, name: str) -> int:
     return 100 + 10 * layer + _LAYER_SLOTS[name]
+
+
+def mtp_tid(name: str) -> int:
+    """Tensor id of the MTP head's decoder layer (the same slots as a layer)."""
+    return 90 + _LAYER_SLOTS[name]
+
+
+def tensor_id(name: str) -> int:
+    """Tensor id of a tensor named as in ``model_tensor_shapes``."""
+    if name.startswith("mtp."):
+        return mtp_tid(name[4:])
+    if "." in name:
+        return layer_tid(int(name.split(".")[0][1:]), name.split(".")[1])
+    return TENSOR_IDS[name]
 
 
 def splitmix64(x):

@@ -34,8 +34,7 @@ def _model(cfg, **kw):
 def _expected_bits(cfg, name, seed, start, count):
     shapes = model_tensor_shapes(cfg)
     base = name.split(".")[-1]
-    tid = (rspec.TENSOR_IDS[name] if "." not in name
-           else rspec.layer_tid(int(name.split(".")[0][1:]), base))
+    tid = rspec.tensor_id(name)
     if base.startswith("g_"):
         v = rspec.gain_values(seed, tid, shapes[name][0], cfg.gain_mode)[start:start + count]
     else:

@@ -488,3 +488,102 @@ def test_pipo_with_first_slot_compressor_is_regular_decoding_on_odd_tokens(small
     sr = r.step(in_tok=[f[0] for f in forced])
     for a, b in zip(sp, sr):
         np.testing.assert_allclose(a["h_b"], b["h"], rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------- paper-default heads (App. B)
+
+from synth.configs import HEADS_PAPER, HEADS_MTP_LAYER  # noqa: E402
+
+SMALL_P = ModelConfig(**{**SMALL.__dict__, "heads": HEADS_PAPER})
+
+
+@pytest.fixture(scope="module")
+def paper_w():
+    return O.OracleWeights.generate(SMALL_P, seed=4, precision="bf16")
+
+
+def test_mlp_compressor_zeroed_branch_is_the_sum(paper_w):
+    """The paper initialises the MLP compressor to a + b by zeroing its
+    residual branch: W2 = 0 (or W1 = 0, since SiLU(0) = 0) gives exactly a + b."""
+    E = paper_w["embed"]
+    pairs = np.array([[3, 7], [11, 2], [5, 5]])
+    for w1, w2 in ((paper_w["comp_w1"], np.zeros_like(paper_w["comp_w2"])),
+                   (np.zeros_like(paper_w["comp_w1"]), paper_w["comp_w2"])):
+        np.testing.assert_array_equal(O.compress_mlp(E, w1, w2, pairs), E[pairs[:, 0]] + E[pairs[:, 1]])
+
+
+def test_mlp_compressor_branch_is_linear_in_w2_and_symmetric_when_w1_is(paper_w):
+    E = paper_w["embed"]
+    pairs = np.array([[3, 7], [11, 2]])
+    base = E[pairs[:, 0]] + E[pairs[:, 1]]
+    f1 = O.compress_mlp(E, paper_w["comp_w1"], paper_w["comp_w2"], pairs) - base
+    f2 = O.compress_mlp(E, paper_w["comp_w1"], 2 * paper_w["comp_w2"], pairs) - base
+    np.testing.assert_allclose(f2, 2 * f1, rtol=1e-12, atol=1e-15)
+    assert np.abs(f1).max() > 0
+    # W1 = [M M] sees a + b only, so swapping the pair leaves z unchanged; a generic W1 does not
+    M = paper_w["comp_w1"][:, :SMALL.hidden]
+    w1s = np.concatenate([M, M], axis=1)
+    np.testing.assert_allclose(O.compress_mlp(E, w1s, paper_w["comp_w2"], pairs),
+                               O.compress_mlp(E, w1s, paper_w["comp_w2"], pairs[:, ::-1]), rtol=1e-12, atol=1e-15)
+    assert not np.allclose(O.compress_mlp(E, paper_w["comp_w1"], paper_w["comp_w2"], pairs),
+                           O.compress_mlp(E, paper_w["comp_w1"], paper_w["comp_w2"], pairs[:, ::-1]))
+
+
+def test_confidence_mlp_closed_forms(paper_w):
+    h_b = np.linspace(-1, 1, SMALL.hidden)
+    h_d = np.cos(np.arange(SMALL.hidden))
+    g = paper_w["g_conf"]
+    for w1, w2 in ((np.zeros_like(paper_w["conf_w1"]), paper_w["conf_w2"]),
+                   (paper_w["conf_w1"], np.zeros_like(paper_w["conf_w2"]))):
+        s, c = O.confidence_mlp(w1, w2, g, h_b, h_d, 1e-6)
+        assert s == 0.0 and c == 0.5
+    # worked example, H = 1: RMSNorm([3; 4]) = [3, 4] / sqrt(12.5 + eps), W1 = [[1, 0]], w2 = [2]
+    n0 = 3 / np.sqrt(12.5 + 1e-6)
+    s, c = O.confidence_mlp(np.array([[1.0, 0.0]]), np.array([2.0]), np.ones(2), np.array([3.0]), np.array([4.0]), 1e-6)
+    assert abs(s - 2 * n0 / (1 + np.exp(-n0))) < 1e-14 and abs(c - 1 / (1 + np.exp(-s))) < 1e-15
+
+
+def test_mtp_layer_with_zero_output_projections_is_the_linear_head():
+    """With the MTP layer's W_o and W_down zero the layer is the identity, so
+    the paper-default MTP head reduces to the one-linear form."""
+    cfg = ModelConfig(**{**SMALL.__dict__, "heads": HEADS_MTP_LAYER})
+    W = O.OracleWeights.generate(cfg, seed=6, precision="bf16")
+    W.t["mtp.wo"] = np.zeros_like(W.t["mtp.wo"])
+    W.t["mtp.wdown"] = np.zeros_like(W.t["mtp.wdown"])
+    W0 = O.OracleWeights(SMALL, {k: v for k, v in W.t.items() if not k.startswith("mtp.")})
+    prompt = rspec.prompt_tokens(1, 9, cfg.vocab, seed=8)
+    a, b = O.PipoOracle(W), O.PipoOracle(W0)
+    ra, rb = a.prefill(prompt, O.Sampling(tau=0.5)), b.prefill(prompt, O.Sampling(tau=0.5))
+    for _ in range(3):
+        np.testing.assert_allclose(ra[0]["h_d"], rb[0]["h_d"], rtol=1e-12, atol=1e-14)
+        assert (ra[0]["tok_b"], ra[0]["tok_d"]) == (rb[0]["tok_b"], rb[0]["tok_d"])
+        ra, rb = a.decode_step(), b.decode_step()
+
+
+def test_paper_heads_session_equals_brute_force(paper_w):
+    """Prefill + pair steps with all three App. B heads: the backbone states
+    equal a from-scratch pass over the compressed inputs, and the MTP states
+    equal a from-scratch pass of the MTP layer over its inputs (the prompt
+    token after each pair for the prompt's latents, the selected backbone
+    token afterwards)."""
+    cfg, W = SMALL_P, paper_w
+    prompt = rspec.prompt_tokens(1, 11, cfg.vocab, seed=9)
+    orc = O.PipoOracle(W)
+    recs = [orc.prefill(prompt, O.Sampling(tau=0.5))[0]]
+    pairs = [tuple(p) for p in O.prompt_pairs(prompt[0], cfg.pad_id)]
+    L0 = len(pairs)
+    for _ in range(4):
+        pairs.append(orc.next_pairs[0])
+        recs.append(orc.decode_step()[0])
+    Z = O.compress_mlp(W["embed"], W["comp_w1"], W["comp_w2"], np.array(pairs))
+    X, _ = O.backbone_full(W, Z)
+    for k, rec in enumerate(recs):
+        np.testing.assert_allclose(rec["h_b"], X[L0 - 1 + k], rtol=1e-10, atol=1e-12)
+    toks = [pairs[j + 1][0] for j in range(L0 - 1)] + [r["tok_b"] for r in recs]
+    U = np.stack([O.mtp_hidden(W["w_fc"], W["g_mtp_h"], W["g_mtp_e"], X[j], W["embed"][t], cfg.rms_eps)
+                  for j, t in enumerate(toks)])
+    Hd, _ = O.layer_full(cfg, O.mtp_layer(W), U)
+    for k, rec in enumerate(recs):
+        np.testing.assert_allclose(rec["h_d"], Hd[L0 - 1 + k], rtol=1e-10, atol=1e-12)
+        s, c = O.confidence_mlp(W["conf_w1"], W["conf_w2"], W["g_conf"], rec["h_b"], rec["h_d"], cfg.rms_eps)
+        assert abs(c - rec["conf"]) < 1e-15

@@ -58,7 +58,21 @@ typedef struct {
     int32_t max_latent;      /* KV capacity per sequence, in latent positions       */
     int32_t prefill_chunk;   /* latent positions per prefill chunk (e.g. 4096)      */
     int32_t gain_mode;       /* 0: RMSNorm gains 1; 1: gains 1 + 10*w (testing)     */
+    int32_t heads;           /* 0: one-linear compressor, MTP and confidence heads;
+                                else PIPO_HEADS_* flags for the App. B forms         */
 } pipo_config;
+
+/* The App. B forms of the three heads (pipo_config.heads):
+ * MLP compressor (Table 4): z = E[a] + E[b] + W2 SiLU(W1 [E[a]; E[b]]), W1 2H->H,
+ *   W2 H->H (the printed W2 SiLU(W1 .) is the residual branch of an a + b path);
+ * MTP layer (App. B.2): h_d = Layer(W_fc [RMSNorm(h_b); RMSNorm(E[b])]), Layer a
+ *   decoder layer shaped like the backbone's with its own KV cache over latent
+ *   positions; during prefill the prompt's latents other than the last take the
+ *   prompt token after their pair;
+ * MLP confidence (App. B.3): c = sigmoid(w2 . SiLU(W1 RMSNorm([h_b; h_d]))), W1 2H->H. */
+#define PIPO_HEADS_MLP_COMPRESSOR  1
+#define PIPO_HEADS_MTP_LAYER       2
+#define PIPO_HEADS_MLP_CONFIDENCE  4
 
 /* Token selection and the confidence gate (Sec. 3.2).  Read during the call,
  * not retained except by value. */

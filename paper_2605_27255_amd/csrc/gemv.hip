@@ -66,6 +66,13 @@ __device__ __forceinline__ void load_src(const GemvParams &p, int b, int k, XSrc
         const float4 *xp = (const float4 *)(p.xf + (int64_t)b * p.K + k);
         s.a0 = xp[0];
         s.a1 = xp[1];
+    } else if (PRO == PRO_CAT) {   // [x; x2] * gain over 2H
+        const float4 *xp = (const float4 *)(k < p.H ? p.x + (int64_t)b * p.H + k : p.x2 + (int64_t)b * p.H + k - p.H);
+        const float4 *gp = (const float4 *)(p.gain + k);
+        s.a0 = xp[0];
+        s.a1 = xp[1];
+        s.g0 = gp[0];
+        s.g1 = gp[1];
     } else if (PRO == PRO_NORM || k < p.H) {
         const int stride = PRO == PRO_MTP ? p.H : p.K;
         const float4 *xp = (const float4 *)(p.x + (int64_t)b * stride + k);
@@ -96,7 +103,7 @@ __device__ __forceinline__ void make_chunk(const GemvParams &p, int k, const XSr
     if (PRO == PRO_F32) {
         f[0] = s.a0.x; f[1] = s.a0.y; f[2] = s.a0.z; f[3] = s.a0.w;
         f[4] = s.a1.x; f[5] = s.a1.y; f[6] = s.a1.z; f[7] = s.a1.w;
-    } else if (PRO == PRO_NORM || k < p.H) {
+    } else if (PRO == PRO_NORM || PRO == PRO_CAT || k < p.H) {
         f[0] = s.a0.x * s.g0.x; f[1] = s.a0.y * s.g0.y; f[2] = s.a0.z * s.g0.z; f[3] = s.a0.w * s.g0.w;
         f[4] = s.a1.x * s.g1.x; f[5] = s.a1.y * s.g1.y; f[6] = s.a1.z * s.g1.z; f[7] = s.a1.w * s.g1.w;
     } else {
@@ -147,6 +154,7 @@ struct Pro {
     static constexpr int RPW = 2 * NBT;    // RMSNorm rows per wave: b = wave + 8 r
     f32x4 resid[NBT];
     float ssv[RPW][4];                     // sum-of-squares parts, 4 per lane (nss <= 256)
+    float ssv2[PRO == PRO_CAT ? RPW : 1][4];   // PRO_CAT: the second half's parts
     XSrc src[kXR];
 };
 
@@ -154,7 +162,7 @@ template <int NBT, int PRO, int EPI>
 __device__ __forceinline__ void pro_load(const GemvParams &p, Pro<NBT, PRO, EPI> &pr, bool lead,
                                          int row0, const ChunkMap &cm, int col0) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, j = lane & 15;
-    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
+    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP || PRO == PRO_CAT;
 #pragma unroll
     for (int bt = 0; bt < NBT; ++bt) {
         const int b = bt * 16 + j;
@@ -168,6 +176,7 @@ __device__ __forceinline__ void pro_load(const GemvParams &p, Pro<NBT, PRO, EPI>
             for (int t = 0; t < 4; ++t) {
                 const int b = wave + r * kNW, i = lane + 64 * t;
                 pr.ssv[r][t] = p.ss[(b < p.B && i < p.nss) ? b * p.nss + i : 0];
+                if (PRO == PRO_CAT) pr.ssv2[r][t] = p.ss2[(b < p.B && i < p.nss) ? b * p.nss + i : 0];
             }
     }
 #pragma unroll
@@ -186,7 +195,7 @@ template <int NBT, int PRO, int EPI>
 __device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, PRO, EPI> &pr, const ChunkMap &cm,
                                            int col0, uint16_t *xh, uint16_t *xl, float *sc0, float *sc1) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
+    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP || PRO == PRO_CAT;
     constexpr bool HASLO = PRO != PRO_PAIR;
     const int B = p.B;
     if (NORM) {
@@ -196,6 +205,10 @@ __device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, P
             float a = 0.f;
 #pragma unroll
             for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? pr.ssv[r][t] : 0.f;
+            if (PRO == PRO_CAT) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? pr.ssv2[r][t] : 0.f;
+            }
             a = wave_sum(a);
             if (b < B && lane == 0) sc0[b] = rsqrtf(a / (float)(PRO == PRO_MTP ? p.H : p.K) + p.eps);
         }
@@ -334,6 +347,17 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams &p, f32x4 (&fin)[
             sq = col_sum(sq);
             if (ok && g == 0 && p.ss_out) p.ss_out[b * nstrips + strip] = sq;
         }
+    } else if (EPI == EPI_SILU) {
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            if (b < B) {
+                f32x4 w;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) w[v] = silu_f(fin[bt][v]);
+                *(f32x4 *)(p.act + (int64_t)b * p.N + row0) = w;
+            }
+        }
     } else if (EPI == EPI_SWIGLU) {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
@@ -464,7 +488,7 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                 for (int w = 1; w < KS; ++w) fin[bt] += red[((wave + w) * NBT + bt) * 64 + lane];
             }
         }
-        if (PRO == PRO_NORM) {
+        if (PRO == PRO_NORM || PRO == PRO_CAT) {
 #pragma unroll
             for (int bt = 0; bt < NBT; ++bt) {
                 const int b = bt * 16 + j;
@@ -556,10 +580,10 @@ __global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     __shared__ float s_part[2][4];
     float sc0 = 1.f, sc1 = 1.f;
-    if (PRO == PRO_NORM || PRO == PRO_MTP) {
+    if (PRO == PRO_NORM || PRO == PRO_MTP || PRO == PRO_CAT) {
         // the row's sum of squares (and the MTP embedding row's), 8 values
         // requested per thread per step
-        const int Kn = PRO == PRO_MTP ? H : K;
+        const int Kn = PRO == PRO_NORM ? K : H;
         const float *xr = p.x + (int64_t)b * Kn;
         float a = 0.f, e = 0.f;
 #pragma unroll 4
@@ -567,6 +591,14 @@ __global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
             const float4 u0 = *(const float4 *)(xr + k0), u1 = *(const float4 *)(xr + k0 + 4);
             a += u0.x * u0.x + u0.y * u0.y + u0.z * u0.z + u0.w * u0.w;
             a += u1.x * u1.x + u1.y * u1.y + u1.z * u1.z + u1.w * u1.w;
+        }
+        if (PRO == PRO_CAT) {
+            const float *x2 = p.x2 + (int64_t)b * H;
+            for (int k0 = threadIdx.x * 8; k0 < H; k0 += 256 * 8) {
+                const float4 u0 = *(const float4 *)(x2 + k0), u1 = *(const float4 *)(x2 + k0 + 4);
+                a += u0.x * u0.x + u0.y * u0.y + u0.z * u0.z + u0.w * u0.w;
+                a += u1.x * u1.x + u1.y * u1.y + u1.z * u1.z + u1.w * u1.w;
+            }
         }
         if (PRO == PRO_MTP) {
             const int tok = clamp_id(argmax_key_id(p.tokkey[b]), p.vocab);
@@ -584,7 +616,8 @@ __global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
             s_part[1][wave] = e;
         }
         __syncthreads();
-        sc0 = rsqrtf((s_part[0][0] + s_part[0][1] + s_part[0][2] + s_part[0][3]) / (float)Kn + p.eps);
+        sc0 = rsqrtf((s_part[0][0] + s_part[0][1] + s_part[0][2] + s_part[0][3]) / (float)(PRO == PRO_CAT ? K : Kn) +
+                     p.eps);
         sc1 = rsqrtf((s_part[1][0] + s_part[1][1] + s_part[1][2] + s_part[1][3]) / (float)H + p.eps);
     }
     {
@@ -601,7 +634,7 @@ __global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
             if (PRO == PRO_F32) {
                 f[0] = sx.a0.x; f[1] = sx.a0.y; f[2] = sx.a0.z; f[3] = sx.a0.w;
                 f[4] = sx.a1.x; f[5] = sx.a1.y; f[6] = sx.a1.z; f[7] = sx.a1.w;
-            } else if (PRO == PRO_NORM || k < H) {
+            } else if (PRO == PRO_NORM || PRO == PRO_CAT || k < H) {
                 f[0] = sx.a0.x * sx.g0.x; f[1] = sx.a0.y * sx.g0.y; f[2] = sx.a0.z * sx.g0.z; f[3] = sx.a0.w * sx.g0.w;
                 f[4] = sx.a1.x * sx.g1.x; f[5] = sx.a1.y * sx.g1.y; f[6] = sx.a1.z * sx.g1.z; f[7] = sx.a1.w * sx.g1.w;
 #pragma unroll
@@ -797,7 +830,7 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
     };
     // 1. the whole X slice (at most KC 8-column chunks per thread) and
     //    the RMSNorm inputs requested at once, then two weight batches
-    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP;
+    constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP || PRO == PRO_CAT;
     const int per_row = nt * 4, count = B * per_row;
     const int col0 = kt0 * 32;
     constexpr int KC = KrChunks<PRO>::n;
@@ -810,7 +843,7 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
         load_src<PRO>(p, b, col0 + ((idx - b * per_row) << 3), src[c]);
     }
     constexpr int RPW = 2 * NBT;
-    float ssv[RPW][4];
+    float ssv[RPW][4], ssv2[PRO == PRO_CAT ? RPW : 1][4];
     if (NORM) {
 #pragma unroll
         for (int rr = 0; rr < RPW; ++rr)
@@ -818,6 +851,7 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
             for (int t = 0; t < 4; ++t) {
                 const int b = wave + rr * kNW, i = lane + 64 * t;
                 ssv[rr][t] = p.ss[(b < B && i < p.nss) ? b * p.nss + i : 0];
+                if (PRO == PRO_CAT) ssv2[rr][t] = p.ss2[(b < B && i < p.nss) ? b * p.nss + i : 0];
             }
     }
     u32x4 ra[U], rb[U];
@@ -845,6 +879,10 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
             float a = 0.f;
 #pragma unroll
             for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? ssv[rr][t] : 0.f;
+            if (PRO == PRO_CAT) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? ssv2[rr][t] : 0.f;
+            }
             a = wave_sum(a);
             if (b < B && lane == 0) sc0[b] = rsqrtf(a / (float)(PRO == PRO_MTP ? p.H : p.K) + p.eps);
         }
@@ -878,7 +916,7 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
             const float s0 = b < B ? sc0[b] : 0.f;
             f32x4 v = acc[0][bt];
             if (NA == 2) v = v * s0 + acc[NA - 1][bt] * (b < B ? sc1[b] : 0.f);
-            else if (PRO == PRO_NORM) v *= s0;
+            else if (PRO == PRO_NORM || PRO == PRO_CAT) v *= s0;
             fin[bt] = v;
         }
 #pragma unroll
@@ -1047,6 +1085,8 @@ void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s) {
     else if (pro == PRO_NORM && epi == EPI_LOGITS) launch_nbt<4, PRO_NORM, EPI_LOGITS>(p, s);
     else if (pro == PRO_MTP && epi == EPI_STORE) launch_nbt<8, PRO_MTP, EPI_STORE>(p, s);
     else if (pro == PRO_NORM && epi == EPI_STORE) launch_nbt<8, PRO_NORM, EPI_STORE>(p, s);
+    else if (pro == PRO_PAIR && epi == EPI_SILU) launch_nbt<8, PRO_PAIR, EPI_SILU>(p, s);
+    else if (pro == PRO_CAT && epi == EPI_SILU) launch_nbt<8, PRO_CAT, EPI_SILU>(p, s);
 }
 
 }  // namespace pipo

@@ -15,18 +15,24 @@ __global__ __launch_bounds__(512) void k_gate(GateParams p) {
     __shared__ float s_sc;
     const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int H = p.H;
+    const bool mlp = p.conf_h != nullptr;   // App. B.3: w2 . SiLU(W1 RMSNorm([h_b; h_d])), hidden precomputed
     if (wave == 0) {
         float a = 0.f;
         for (int i = lane; i < p.nss_b; i += 64) a += p.ss_b[b * p.nss_b + i];
         for (int i = lane; i < p.nss_d; i += 64) a += p.ss_d[b * p.nss_d + i];
         a = wave_sum(a);
-        if (lane == 0) s_sc = rsqrtf(a / (float)(2 * H) + p.eps);
+        if (lane == 0) s_sc = mlp ? 1.0f : rsqrtf(a / (float)(2 * H) + p.eps);
     }
     float dot = 0.f;
+    if (mlp) {
 #pragma unroll 4
-    for (int k = threadIdx.x; k < 2 * H; k += 512) {
-        const float u = k < H ? p.hb[(int64_t)b * H + k] : p.hd[(int64_t)b * H + k - H];
-        dot += p.w_conf[k] * p.g_conf[k] * u;
+        for (int k = threadIdx.x; k < H; k += 512) dot += p.conf_w2[k] * p.conf_h[(int64_t)b * H + k];
+    } else {
+#pragma unroll 4
+        for (int k = threadIdx.x; k < 2 * H; k += 512) {
+            const float u = k < H ? p.hb[(int64_t)b * H + k] : p.hd[(int64_t)b * H + k - H];
+            dot += p.w_conf[k] * p.g_conf[k] * u;
+        }
     }
     dot = wave_sum(dot);
     if (lane == 0) red[wave] = dot;
@@ -56,18 +62,26 @@ void launch_gate(const GateParams &p, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// Regular decoding on the same backbone (the paper's baseline, Sec. 4.3).
-// Step input: x[b] = E[tok_b] (fp32) with the sum-of-squares part of every
-// 16-element strip, as the RMSNorm prologue of the decode GEMM reads them.
+// Embedding rows of the step's input tokens: x[b] = E[first token] (regular
+// decoding, the paper's baseline of Sec. 4.3), or E[a] + E[b] of the pending
+// pair (`both`: the skip path of the MLP compressor), in fp32 with the
+// sum-of-squares part of every 16-element strip, as the RMSNorm prologue of
+// the decode GEMM reads them.
 __global__ __launch_bounds__(256) void k_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V,
-                                                    float *x, float *ss) {
+                                                    float *x, float *ss, int both) {
     const int b = blockIdx.x;
     const int row = clamp_id(pairs[2 * b], V);
+    const int row2 = clamp_id(pairs[2 * b + 1], V);
     for (int c = threadIdx.x; c < (H >> 3); c += 256) {
         const int k = c << 3;
         const u32x4 v = *(const u32x4 *)(embed + tiled_index(row, k, H));
-        const float f[8] = {bf_lo(v[0]), bf_hi(v[0]), bf_lo(v[1]), bf_hi(v[1]),
-                            bf_lo(v[2]), bf_hi(v[2]), bf_lo(v[3]), bf_hi(v[3])};
+        float f[8] = {bf_lo(v[0]), bf_hi(v[0]), bf_lo(v[1]), bf_hi(v[1]),
+                      bf_lo(v[2]), bf_hi(v[2]), bf_lo(v[3]), bf_hi(v[3])};
+        if (both) {
+            const u32x4 w = *(const u32x4 *)(embed + tiled_index(row2, k, H));
+            f[0] += bf_lo(w[0]); f[1] += bf_hi(w[0]); f[2] += bf_lo(w[1]); f[3] += bf_hi(w[1]);
+            f[4] += bf_lo(w[2]); f[5] += bf_hi(w[2]); f[6] += bf_lo(w[3]); f[7] += bf_hi(w[3]);
+        }
         float4 *dst = (float4 *)(x + (int64_t)b * H + k);
         dst[0] = make_float4(f[0], f[1], f[2], f[3]);
         dst[1] = make_float4(f[4], f[5], f[6], f[7]);
@@ -80,8 +94,8 @@ __global__ __launch_bounds__(256) void k_embed_step(const int32_t *pairs, const 
 }
 
 void launch_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V, float *x, float *ss, int B,
-                       hipStream_t s) {
-    hipLaunchKernelGGL(k_embed_step, dim3(B), dim3(256), 0, s, pairs, embed, H, V, x, ss);
+                       int both, hipStream_t s) {
+    hipLaunchKernelGGL(k_embed_step, dim3(B), dim3(256), 0, s, pairs, embed, H, V, x, ss, both);
 }
 
 // Step output: the selected token, which is also the next step's input.

@@ -16,6 +16,7 @@ enum GemvPro : int {
     PRO_F32  = 1,   // X = xf, fp32 [B][K]
     PRO_PAIR = 2,   // X = [E[a]; E[b]] for int32 pairs [B][2] (pair-in compressor)
     PRO_MTP  = 3,   // X = [RMSNorm(h_b) g1; RMSNorm(E[tok]) g2], tok from an argmax key
+    PRO_CAT  = 4,   // X = RMSNorm([x; x2]) * gain over 2H (one scale): the MLP confidence head
 };
 // Larger batches: a preparation kernel writes X (RMSNorm and gain applied) as
 // bf16 planes hi + lo [B][K] (GemvParams::xh / xl) and the GEMV streams its
@@ -26,6 +27,7 @@ enum GemvEpi : int {
     EPI_SWIGLU = 2,  // act fp32 [B][N/2] = SiLU(gate) * up (gate/up strip-interleaved)
     EPI_QKV    = 3,  // RoPE q,k; q fp32 [B][n_q][d]; k, v appended to the bf16 KV cache
     EPI_LOGITS = 4,  // logits fp32 [B][N]; optional argmax key per row (greedy)
+    EPI_SILU   = 5,  // act fp32 [B][N] = SiLU(acc)
 };
 
 struct GemvParams {
@@ -35,6 +37,7 @@ struct GemvParams {
                                 // strip group (0: one workgroup per strip group)
     // prologue
     const float *x; const float *xf; const float *ss; int nss; const float *gain;
+    const float *x2; const float *ss2;   // PRO_CAT: second half [B][H] and its sum-of-squares parts
     const float *gain2; float eps; const int32_t *pairs; const uint16_t *embed; int H; int vocab;
     const uint64_t *tokkey;
     // epilogue
@@ -73,6 +76,7 @@ void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s);
 struct GateParams {
     const float *hb, *hd; const float *ss_b, *ss_d; int nss_b, nss_d;
     const float *w_conf, *g_conf; int H; float eps, tau;
+    const float *conf_h, *conf_w2;   // MLP confidence head: s = conf_w2 . conf_h[b] (H each); NULL: one linear
     uint64_t *best_b, *best_d; int32_t pad_id;
     void *out;                  // pipo_pair [B]
     int32_t *pairs, *pos, *step; int advance;
@@ -82,7 +86,7 @@ void launch_gate(const GateParams &p, hipStream_t s);
 
 // Regular decoding (no compressor, one token per position and step).
 void launch_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V, float *x, float *ss, int B,
-                       hipStream_t s);
+                       int both, hipStream_t s);
 void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_t pad_id, int32_t *pos,
                         int32_t *step, int advance, int B, hipStream_t s);
 
@@ -123,6 +127,11 @@ struct PrefillGeom {
 };
 void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
                          const PrefillGeom &g, uint16_t *xin, hipStream_t s);
+void launch_gather_pair_sum(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                            const PrefillGeom &g, float *x, hipStream_t s);
+void launch_mtp_rows(const float *xb, const int32_t *tokens, const uint16_t *embed, const float *gh, const float *ge,
+                     int H, int V, int pad_id, float eps, const PrefillGeom &g, int M, uint16_t *xh, uint16_t *xl,
+                     hipStream_t s);
 void launch_gather_tokens(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
                           const PrefillGeom &g, float *x, hipStream_t s);
 void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M,
@@ -132,7 +141,7 @@ void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, i
 struct GemmParams {
     const uint16_t *W; const uint16_t *X; const uint16_t *Xlo;   // tiled [N][K], tiled [M][K] x2
     int N, K, M;
-    int epi;                                // EPI_STORE (bias), EPI_RESID, EPI_SWIGLU, EPI_QKV
+    int epi;                                // EPI_STORE (bias), EPI_RESID, EPI_SWIGLU, EPI_QKV, EPI_SILU
     PrefillGeom g;
     float *out; const float *bias; uint16_t *act_hi, *act_lo;
     uint16_t *q; uint16_t *kc; uint16_t *vc;

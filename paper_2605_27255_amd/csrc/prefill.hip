@@ -41,6 +41,96 @@ void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, in
     hipLaunchKernelGGL(k_gather_pairs, dim3(grid), dim3(256), 0, s, tokens, embed, H, V, pad_id, g, xin);
 }
 
+// ---- MLP compressor's skip path: x[m] = E[a] + E[b] for latent c0 + i -------
+__global__ void k_gather_pair_sum(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                                  PrefillGeom g, float *x) {
+    const int cpr = H >> 3;
+    const int64_t total = (int64_t)g.B * g.mpad * cpr;
+    for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int m = (int)(idx / cpr);
+        const int k = (int)(idx - (int64_t)m * cpr) << 3;
+        const int b = m / g.mpad, i = m - b * g.mpad;
+        int ra = pad_id, rb = pad_id;
+        if (i < g.clen) {
+            const int t = 2 * (g.c0 + i);
+            ra = t < g.n_tok ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+            rb = t + 1 < g.n_tok ? clamp_id(tokens[(int64_t)b * g.n_tok + t + 1], V) : pad_id;
+        }
+        const u32x4 va = *(const u32x4 *)(embed + tiled_index(ra, k, H));
+        const u32x4 vb = *(const u32x4 *)(embed + tiled_index(rb, k, H));
+        float4 *dst = (float4 *)(x + (int64_t)m * H + k);
+        dst[0] = make_float4(bf_lo(va[0]) + bf_lo(vb[0]), bf_hi(va[0]) + bf_hi(vb[0]),
+                             bf_lo(va[1]) + bf_lo(vb[1]), bf_hi(va[1]) + bf_hi(vb[1]));
+        dst[1] = make_float4(bf_lo(va[2]) + bf_lo(vb[2]), bf_hi(va[2]) + bf_hi(vb[2]),
+                             bf_lo(va[3]) + bf_lo(vb[3]), bf_hi(va[3]) + bf_hi(vb[3]));
+    }
+}
+
+void launch_gather_pair_sum(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
+                            const PrefillGeom &g, float *x, hipStream_t s) {
+    const int64_t total = (int64_t)g.B * g.mpad * (H >> 3);
+    int grid = (int)((total + 255) / 256);
+    grid = grid > 65536 ? 65536 : grid;
+    hipLaunchKernelGGL(k_gather_pair_sum, dim3(grid), dim3(256), 0, s, tokens, embed, H, V, pad_id, g, x);
+}
+
+// ---- MTP layer inputs of the prompt's latents (one wave per row) -----------
+// Row (b, i) = [RMSNorm(h_b; g_mh); RMSNorm(E[t]; g_me)] with t the prompt token
+// after latent c0 + i's pair (PAD where there is none: the last latent, whose
+// row is recomputed with the selected token once it is known), written as
+// tiled hi / lo planes of width 2H.
+__global__ __launch_bounds__(256) void k_mtp_rows(const float *xb, const int32_t *tokens, const uint16_t *embed,
+                                                  const float *gh, const float *ge, int H, int V, int pad_id,
+                                                  float eps, PrefillGeom g, int M, uint16_t *xh, uint16_t *xl) {
+    const int lane = threadIdx.x & 63;
+    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (m >= M) return;
+    const int b = m / g.mpad, i = m - b * g.mpad;
+    const int t = 2 * (g.c0 + i) + 2;
+    const int tok = (i < g.clen && t < g.n_tok) ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+    const float *xr = xb + (int64_t)m * H;
+    float a = 0.f, e = 0.f;
+    for (int k = lane * 8; k < H; k += 512) {
+        const float4 x0 = *(const float4 *)(xr + k), x1 = *(const float4 *)(xr + k + 4);
+        a += x0.x * x0.x + x0.y * x0.y + x0.z * x0.z + x0.w * x0.w + x1.x * x1.x + x1.y * x1.y + x1.z * x1.z +
+             x1.w * x1.w;
+        const u32x4 w = *(const u32x4 *)(embed + tiled_index(tok, k, H));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) e += bf_lo(w[q]) * bf_lo(w[q]) + bf_hi(w[q]) * bf_hi(w[q]);
+    }
+    a = wave_sum(a);
+    e = wave_sum(e);
+    const float s1 = rsqrtf(a / (float)H + eps), s2 = rsqrtf(e / (float)H + eps);
+    for (int k = lane * 8; k < H; k += 512) {
+        const float4 x0 = *(const float4 *)(xr + k), x1 = *(const float4 *)(xr + k + 4);
+        const float4 g0 = *(const float4 *)(gh + k), g1 = *(const float4 *)(gh + k + 4);
+        const float f[8] = {x0.x * s1 * g0.x, x0.y * s1 * g0.y, x0.z * s1 * g0.z, x0.w * s1 * g0.w,
+                            x1.x * s1 * g1.x, x1.y * s1 * g1.y, x1.z * s1 * g1.z, x1.w * s1 * g1.w};
+        u32x4 hi, lo;
+        split8(f, hi, lo);
+        const int64_t at = tiled_index(m, k, 2 * H);
+        *(u32x4 *)(xh + at) = hi;
+        *(u32x4 *)(xl + at) = lo;
+        const u32x4 w = *(const u32x4 *)(embed + tiled_index(tok, k, H));
+        const float4 e0 = *(const float4 *)(ge + k), e1 = *(const float4 *)(ge + k + 4);
+        const float fe[8] = {bf_lo(w[0]) * s2 * e0.x, bf_hi(w[0]) * s2 * e0.y, bf_lo(w[1]) * s2 * e0.z,
+                             bf_hi(w[1]) * s2 * e0.w, bf_lo(w[2]) * s2 * e1.x, bf_hi(w[2]) * s2 * e1.y,
+                             bf_lo(w[3]) * s2 * e1.z, bf_hi(w[3]) * s2 * e1.w};
+        split8(fe, hi, lo);
+        const int64_t at2 = tiled_index(m, H + k, 2 * H);
+        *(u32x4 *)(xh + at2) = hi;
+        *(u32x4 *)(xl + at2) = lo;
+    }
+}
+
+void launch_mtp_rows(const float *xb, const int32_t *tokens, const uint16_t *embed, const float *gh, const float *ge,
+                     int H, int V, int pad_id, float eps, const PrefillGeom &g, int M, uint16_t *xh, uint16_t *xl,
+                     hipStream_t s) {
+    hipLaunchKernelGGL(k_mtp_rows, dim3((M + 3) / 4), dim3(256), 0, s, xb, tokens, embed, gh, ge, H, V, pad_id, eps,
+                       g, M, xh, xl);
+}
+
 // ---- regular decoding: the prompt's tokens one per position, x = E[t] -----
 // Row (b, i) of the chunk holds token c0 + i of sequence b (rows past the
 // chunk hold E[pad_id]); fp32 residual rows [B * mpad][H].
@@ -124,6 +214,13 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
     } else if (EPI == EPI_RESID) {
         f32x4 *o = (f32x4 *)(p.out + (int64_t)m * p.N + row0);
         *o = *o + val;
+    } else if (EPI == EPI_SILU) {
+        uint32_t h[4], l[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) split_bf(silu_p(val[v]), h[v], l[v]);
+        const int64_t at = tiled_index(m, row0, p.N);
+        *(u32x2 *)(p.act_hi + at) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+        *(u32x2 *)(p.act_lo + at) = u32x2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
     } else if (EPI == EPI_SWIGLU) {
         if (g < 2) {
             uint32_t h[4], l[4];
@@ -318,7 +415,8 @@ static void launch_gemm_wd(const GemmParams &p, hipStream_t s) {
 
 void launch_gemm(const GemmParams &p, hipStream_t s) {
     if (!p.Xlo) {   // the gathered embedding pairs are exact in bf16
-        launch_gemm_wd<EPI_STORE, false>(p, s);
+        if (p.epi == EPI_SILU) launch_gemm_wd<EPI_SILU, false>(p, s);
+        else launch_gemm_wd<EPI_STORE, false>(p, s);
         return;
     }
     switch (p.epi) {
@@ -531,23 +629,23 @@ void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s) {
 }
 
 // ---- last latent of each sequence into the decode residual buffer --------
+// The last position's residual becomes the decode state x (with the
+// sum-of-squares part of every 16-element strip, as the decode GEMVs read
+// them); pos is set to that position, so the heads that follow run there and
+// advance it, and the step counter restarts.
 __global__ __launch_bounds__(256) void k_pick_last(const float *x, int H, PrefillGeom g, float *xdec,
                                                    float *ss, int32_t *pos, int32_t *step, int latents) {
-    __shared__ float red[4];
     const int b = blockIdx.x;
     const float *xr = x + ((int64_t)b * g.mpad + g.clen - 1) * H;
-    float a = 0.f;
-    for (int k = threadIdx.x; k < H; k += 256) {
-        const float v = xr[k];
-        xdec[(int64_t)b * H + k] = v;
-        a += v * v;
+    for (int k = threadIdx.x; k < H; k += 256) xdec[(int64_t)b * H + k] = xr[k];
+    for (int st = threadIdx.x; st < (H >> 4); st += 256) {
+        float a = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) a += xr[16 * st + i] * xr[16 * st + i];
+        ss[(int64_t)b * (H >> 4) + st] = a;
     }
-    a = wave_sum(a);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
-    __syncthreads();
     if (threadIdx.x == 0) {
-        ss[b] = red[0] + red[1] + red[2] + red[3];
-        pos[b] = latents;
+        pos[b] = latents - 1;
         step[b] = 0;
     }
 }

@@ -52,6 +52,13 @@ struct pipo_ctx {
     float *b_comp, *w_conf, *g_final, *g_mtp_h, *g_mtp_e, *g_mtp_o, *g_conf;
     std::vector<LayerW> layers;
     uint16_t *kc, *vc;
+    // App. B heads (pipo_config.heads): MLP compressor, MTP decoder layer with
+    // its KV cache, MLP confidence head
+    int heads = 0;
+    uint16_t *comp_w1 = nullptr, *comp_w2 = nullptr, *conf_w1 = nullptr;
+    float *conf_w2 = nullptr;
+    LayerW mtp{};
+    uint16_t *kc_mtp = nullptr, *vc_mtp = nullptr;
     float *rope_cos, *rope_sin;
 
     // decode state and activations
@@ -150,13 +157,17 @@ static int check_config(const pipo_config *c) {
     if (c->pad_id < -1 || c->pad_id >= c->vocab) return fail(nullptr, PIPO_EINVAL, "pad_id out of range");
     if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return fail(nullptr, PIPO_EINVAL, "bad rms_eps or rope_base");
     if (c->gain_mode != 0 && c->gain_mode != 1) return fail(nullptr, PIPO_EINVAL, "gain_mode must be 0 or 1");
+    if (c->heads & ~(PIPO_HEADS_MLP_COMPRESSOR | PIPO_HEADS_MTP_LAYER | PIPO_HEADS_MLP_CONFIDENCE))
+        return fail(nullptr, PIPO_EINVAL, "unknown heads flags 0x%x", (unsigned)c->heads);
     return PIPO_OK;
 }
 
 // tensor ids of the weight generator (model-level; per layer 100 + 10 l + slot)
 enum { TID_EMBED = 0, TID_WCOMP = 1, TID_BCOMP = 2, TID_WFC = 3, TID_WCONF = 4, TID_GFINAL = 5,
-       TID_GMTPH = 6, TID_GMTPE = 7, TID_GMTPO = 8, TID_GCONF = 9 };
+       TID_GMTPH = 6, TID_GMTPE = 7, TID_GMTPO = 8, TID_GCONF = 9, TID_COMPW1 = 10, TID_COMPW2 = 11,
+       TID_CONFW1 = 12, TID_CONFW2 = 13 };
 static uint64_t layer_tid(int l, int slot) { return 100ull + 10ull * (uint64_t)l + (uint64_t)slot; }
+static uint64_t mtp_tid(int slot) { return 90ull + (uint64_t)slot; }   // the MTP head's decoder layer
 
 extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *stream, pipo_ctx **out) {
     if (!out) return fail(nullptr, PIPO_EINVAL, "out is NULL");
@@ -176,6 +187,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
     c->lmax_pad = (int)round_up((int64_t)cfg->max_latent + 128, 64);
     c->chunk = cfg->prefill_chunk;
     c->kv_bstride = (int64_t)c->nkv * c->lmax_pad * c->d;
+    c->heads = cfg->heads;
     const int H = c->H, F = c->F, V = c->V, B = c->Bmax;
 
     // ---- weights --------------------------------------------------------
@@ -193,13 +205,23 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->g_mtp_o = w.take<float>(H);
         c->g_conf = w.take<float>(2 * H);
         c->layers.assign(c->L, LayerW{});
-        for (auto &l : c->layers) {
+        auto take_layer = [&](LayerW &l) {
             l.wqkv = w.take<uint16_t>((int64_t)c->nqkv * H);
             l.wo = w.take<uint16_t>((int64_t)H * c->qdim);
             l.wgu = w.take<uint16_t>((int64_t)2 * F * H);
             l.wdown = w.take<uint16_t>((int64_t)H * F);
             l.g_attn = w.take<float>(H);
             l.g_ffn = w.take<float>(H);
+        };
+        for (auto &l : c->layers) take_layer(l);
+        if (c->heads & PIPO_HEADS_MLP_COMPRESSOR) {
+            c->comp_w1 = w.take<uint16_t>((int64_t)H * 2 * H);
+            c->comp_w2 = w.take<uint16_t>((int64_t)H * H);
+        }
+        if (c->heads & PIPO_HEADS_MTP_LAYER) take_layer(c->mtp);
+        if (c->heads & PIPO_HEADS_MLP_CONFIDENCE) {
+            c->conf_w1 = w.take<uint16_t>((int64_t)H * 2 * H);
+            c->conf_w2 = w.take<float>(H);
         }
         if (pass == 0) {
             if (hipMalloc(&c->wmem, w.used) != hipSuccess) {
@@ -218,6 +240,10 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         a.used = 0;
         c->kc = a.take<uint16_t>((int64_t)c->L * B * c->kv_bstride);
         c->vc = a.take<uint16_t>((int64_t)c->L * B * c->kv_bstride);
+        if (c->heads & PIPO_HEADS_MTP_LAYER) {
+            c->kc_mtp = a.take<uint16_t>((int64_t)B * c->kv_bstride);
+            c->vc_mtp = a.take<uint16_t>((int64_t)B * c->kv_bstride);
+        }
         c->rope_cos = a.take<float>((int64_t)c->lmax_pad * (c->d / 2));
         c->rope_sin = a.take<float>((int64_t)c->lmax_pad * (c->d / 2));
         c->x = a.take<float>((int64_t)B * H);
@@ -289,16 +315,25 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
     launch_init_vec(c->g_mtp_e, H, sd, TID_GMTPE, gk, s);
     launch_init_vec(c->g_mtp_o, H, sd, TID_GMTPO, gk, s);
     launch_init_vec(c->g_conf, 2 * H, sd, TID_GCONF, gk, s);
-    for (int l = 0; l < c->L; ++l) {
-        LayerW &lw = c->layers[l];
-        launch_init_tiled(lw.wqkv, c->nqkv, H, 0, c->qdim, sd, layer_tid(l, 0), PERM_QK, c->d / 2, 0, 0, s);
-        launch_init_tiled(lw.wqkv, c->nqkv, H, c->qdim, c->qdim + c->kvdim, sd, layer_tid(l, 1), PERM_QK, c->d / 2, 0, 0, s);
-        launch_init_tiled(lw.wqkv, c->nqkv, H, c->qdim + c->kvdim, c->nqkv, sd, layer_tid(l, 2), PERM_NONE, 0, 0, 0, s);
-        launch_init_tiled(lw.wo, H, c->qdim, 0, H, sd, layer_tid(l, 3), PERM_NONE, 0, 0, 0, s);
-        launch_init_tiled(lw.wgu, 2 * F, H, 0, 2 * F, sd, layer_tid(l, 4), PERM_GATEUP, 0, 0, layer_tid(l, 5), s);
-        launch_init_tiled(lw.wdown, H, F, 0, H, sd, layer_tid(l, 6), PERM_NONE, 0, 0, 0, s);
-        launch_init_vec(lw.g_attn, H, sd, layer_tid(l, 7), gk, s);
-        launch_init_vec(lw.g_ffn, H, sd, layer_tid(l, 8), gk, s);
+    auto init_layer = [&](LayerW &lw, auto tid) {
+        launch_init_tiled(lw.wqkv, c->nqkv, H, 0, c->qdim, sd, tid(0), PERM_QK, c->d / 2, 0, 0, s);
+        launch_init_tiled(lw.wqkv, c->nqkv, H, c->qdim, c->qdim + c->kvdim, sd, tid(1), PERM_QK, c->d / 2, 0, 0, s);
+        launch_init_tiled(lw.wqkv, c->nqkv, H, c->qdim + c->kvdim, c->nqkv, sd, tid(2), PERM_NONE, 0, 0, 0, s);
+        launch_init_tiled(lw.wo, H, c->qdim, 0, H, sd, tid(3), PERM_NONE, 0, 0, 0, s);
+        launch_init_tiled(lw.wgu, 2 * F, H, 0, 2 * F, sd, tid(4), PERM_GATEUP, 0, 0, tid(5), s);
+        launch_init_tiled(lw.wdown, H, F, 0, H, sd, tid(6), PERM_NONE, 0, 0, 0, s);
+        launch_init_vec(lw.g_attn, H, sd, tid(7), gk, s);
+        launch_init_vec(lw.g_ffn, H, sd, tid(8), gk, s);
+    };
+    for (int l = 0; l < c->L; ++l) init_layer(c->layers[l], [l](int slot) { return layer_tid(l, slot); });
+    if (c->heads & PIPO_HEADS_MLP_COMPRESSOR) {
+        launch_init_tiled(c->comp_w1, H, 2 * H, 0, H, sd, TID_COMPW1, PERM_NONE, 0, 0, 0, s);
+        launch_init_tiled(c->comp_w2, H, H, 0, H, sd, TID_COMPW2, PERM_NONE, 0, 0, 0, s);
+    }
+    if (c->heads & PIPO_HEADS_MTP_LAYER) init_layer(c->mtp, [](int slot) { return mtp_tid(slot); });
+    if (c->heads & PIPO_HEADS_MLP_CONFIDENCE) {
+        launch_init_tiled(c->conf_w1, H, 2 * H, 0, H, sd, TID_CONFW1, PERM_NONE, 0, 0, 0, s);
+        launch_init_vec(c->conf_w2, H, sd, TID_CONFW2, 0, s);
     }
     launch_rope_table(c->rope_cos, c->rope_sin, c->lmax_pad, c->d, (double)cfg->rope_base, s);
     hipError_t e = hipGetLastError();
@@ -323,6 +358,64 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
     c->use_graph = !(ng && ng[0] == '1');
     *out = c;
     return PIPO_OK;
+}
+
+// Key splits of the decode attention: at most two 32-key blocks per split at
+// full capacity (both blocks are prefetched), and no more splits than it takes
+// to give the machine about 1024 waves; at most 64 (the merge kernel's limit).
+static int attn_splits(const pipo_ctx *c, int B) {
+    const int blocks = (c->cfg.max_latent + 31) / 32;
+    int sp = (blocks + 1) / 2;
+    const int cap = (1024 + B * c->nkv - 1) / (B * c->nkv);
+    sp = sp < cap ? sp : cap;
+    return sp < 1 ? 1 : (sp > 64 ? 64 : sp);
+}
+
+static GemvParams gemv_base(const pipo_ctx *c, int B) {
+    GemvParams p{};
+    p.B = B; p.eps = c->cfg.rms_eps; p.H = c->H; p.vocab = c->V; p.xh = c->xh; p.xl = c->xl; p.part = c->gpart;
+    p.part_cap = c->gpart_cap; p.wg_cap = c->n_cu;
+    return p;
+}
+
+// One decoder layer (eq. 2) at the current positions over the residual xres
+// (with its sum-of-squares parts ssres): a backbone layer, or the MTP head's.
+static void enqueue_layer(pipo_ctx *c, const LayerW &lw, uint16_t *kc, uint16_t *vc, float *xres, float *ssres,
+                          hipStream_t s) {
+    const int B = c->batch, H = c->H;
+    const GemvParams base = gemv_base(c, B);
+    GemvParams p = base;
+    p.W = lw.wqkv; p.N = c->nqkv; p.K = H;
+    p.x = xres; p.ss = ssres; p.nss = H / 16; p.gain = lw.g_attn;
+    p.q = c->qbuf; p.kc = kc; p.vc = vc; p.pos = c->pos; p.rope_cos = c->rope_cos; p.rope_sin = c->rope_sin;
+    p.n_q = c->nq; p.n_kv = c->nkv; p.d = c->d; p.lmax_pad = c->lmax_pad; p.kv_bstride = c->kv_bstride;
+    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_QKV, s); }
+
+    AttnDecodeParams ap{};
+    ap.q = c->qbuf; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.pos = c->pos;
+    ap.B = B; ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad;
+    ap.splits = attn_splits(c, B); ap.part = c->apart; ap.out = c->attn_out;
+    { PROF(PIPO_K_ATTN_DECODE); launch_attn_decode(ap, s); }
+
+    p = base;
+    p.W = lw.wo; p.N = H; p.K = c->qdim; p.xf = c->attn_out; p.out = xres; p.ss_out = ssres;
+    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+
+    p = base;
+    p.W = lw.wgu; p.N = 2 * c->F; p.K = H; p.x = xres; p.ss = ssres; p.nss = H / 16; p.gain = lw.g_ffn;
+    p.act = c->act;
+    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_SWIGLU, s); }
+
+    p = base;
+    p.W = lw.wdown; p.N = H; p.K = c->F; p.xf = c->act; p.out = xres; p.ss_out = ssres;
+    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+}
+
+// The backbone layers of one decode position over the residual in x.
+static void enqueue_layers(pipo_ctx *c, hipStream_t s) {
+    for (int l = 0; l < c->L; ++l)
+        enqueue_layer(c, c->layers[l], c->kc + (int64_t)l * c->Bmax * c->kv_bstride,
+                      c->vc + (int64_t)l * c->Bmax * c->kv_bstride, c->x, c->ss_x, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -353,6 +446,8 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     m.embed = c->embed; m.tokkey = c->best_b;
     m.out = c->hd; m.ss_out = c->ss_hd;
     { PROF(PIPO_K_GEMV_SMALL); launch_gemv(m, PRO_MTP, EPI_STORE, s); }
+    // App. B.2: the MTP head's decoder layer at the current latent position
+    if (c->heads & PIPO_HEADS_MTP_LAYER) enqueue_layer(c, c->mtp, c->kc_mtp, c->vc_mtp, c->hd, c->ss_hd, s);
     // LM head #2 on RMSNorm(h_d; g_mo)
     GemvParams q{};
     q.B = B; q.eps = c->cfg.rms_eps; q.H = H; q.xh = c->xh; q.xl = c->xl; q.part = c->gpart; q.part_cap = c->gpart_cap;
@@ -366,6 +461,15 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
         launch_sample(sp, s);
     }
     GateParams gp{};
+    if (c->heads & PIPO_HEADS_MLP_CONFIDENCE) {
+        // App. B.3: SiLU(W1 RMSNorm([h_b; h_d]; g_c)) into act; the gate takes w2 . act
+        GemvParams f = gemv_base(c, B);
+        f.W = c->conf_w1; f.N = H; f.K = 2 * H;
+        f.x = c->x; f.x2 = c->hd; f.ss = c->ss_x; f.ss2 = c->ss_hd; f.nss = H / 16; f.gain = c->g_conf;
+        f.act = c->act;
+        { PROF(PIPO_K_GEMV_SMALL); launch_gemv(f, PRO_CAT, EPI_SILU, s); }
+        gp.conf_h = c->act; gp.conf_w2 = c->conf_w2;
+    }
     gp.hb = c->x; gp.hd = c->hd; gp.ss_b = c->ss_x; gp.nss_b = nss; gp.ss_d = c->ss_hd; gp.nss_d = H / 16;
     gp.w_conf = c->w_conf; gp.g_conf = c->g_conf; gp.H = H; gp.eps = c->cfg.rms_eps; gp.tau = c->tau;
     gp.best_b = c->best_b; gp.best_d = c->best_d; gp.pad_id = c->pad_id; gp.out = c->out;
@@ -374,62 +478,19 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     launch_gate(gp, s);
 }
 
-// Key splits of the decode attention: at most two 32-key blocks per split at
-// full capacity (both blocks are prefetched), and no more splits than it takes
-// to give the machine about 1024 waves; at most 64 (the merge kernel's limit).
-static int attn_splits(const pipo_ctx *c, int B) {
-    const int blocks = (c->cfg.max_latent + 31) / 32;
-    int sp = (blocks + 1) / 2;
-    const int cap = (1024 + B * c->nkv - 1) / (B * c->nkv);
-    sp = sp < cap ? sp : cap;
-    return sp < 1 ? 1 : (sp > 64 ? 64 : sp);
-}
-
-// The backbone layers of one decode position (eq. 2) over the residual in x.
-static void enqueue_layers(pipo_ctx *c, hipStream_t s) {
-    const int B = c->batch, H = c->H;
-    GemvParams base{};
-    base.B = B; base.eps = c->cfg.rms_eps; base.H = H; base.vocab = c->V; base.xh = c->xh; base.xl = c->xl; base.part = c->gpart; base.part_cap = c->gpart_cap;
-    base.wg_cap = c->n_cu;
-    for (int l = 0; l < c->L; ++l) {
-        const LayerW &lw = c->layers[l];
-        uint16_t *kc = c->kc + (int64_t)l * c->Bmax * c->kv_bstride;
-        uint16_t *vc = c->vc + (int64_t)l * c->Bmax * c->kv_bstride;
-        GemvParams p = base;
-        p.W = lw.wqkv; p.N = c->nqkv; p.K = H;
-        p.x = c->x; p.ss = c->ss_x; p.nss = H / 16; p.gain = lw.g_attn;
-        p.q = c->qbuf; p.kc = kc; p.vc = vc; p.pos = c->pos; p.rope_cos = c->rope_cos; p.rope_sin = c->rope_sin;
-        p.n_q = c->nq; p.n_kv = c->nkv; p.d = c->d; p.lmax_pad = c->lmax_pad; p.kv_bstride = c->kv_bstride;
-        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_QKV, s); }
-
-        AttnDecodeParams ap{};
-        ap.q = c->qbuf; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.pos = c->pos;
-        ap.B = B; ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad;
-        ap.splits = attn_splits(c, B); ap.part = c->apart; ap.out = c->attn_out;
-        { PROF(PIPO_K_ATTN_DECODE); launch_attn_decode(ap, s); }
-
-        p = base;
-        p.W = lw.wo; p.N = H; p.K = c->qdim; p.xf = c->attn_out; p.out = c->x; p.ss_out = c->ss_x;
-        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
-
-        p = base;
-        p.W = lw.wgu; p.N = 2 * c->F; p.K = H; p.x = c->x; p.ss = c->ss_x; p.nss = H / 16; p.gain = lw.g_ffn;
-        p.act = c->act;
-        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_SWIGLU, s); }
-
-        p = base;
-        p.W = lw.wdown; p.N = H; p.K = c->F; p.xf = c->act; p.out = c->x; p.ss_out = c->ss_x;
-        { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
-    }
-}
-
 // One pair-decode step (eq. 1 on the pending pair, eq. 2 one position, heads).
 static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
-    {   // pair-in compressor
-        GemvParams p{};
-        p.B = B; p.eps = c->cfg.rms_eps; p.H = H; p.vocab = c->V; p.xh = c->xh; p.xl = c->xl; p.part = c->gpart; p.part_cap = c->gpart_cap;
-        p.wg_cap = c->n_cu;
+    if (c->heads & PIPO_HEADS_MLP_COMPRESSOR) {   // Table 4 MLP: E[a] + E[b] + W2 SiLU(W1 [E[a]; E[b]])
+        GemvParams p = gemv_base(c, B);
+        p.W = c->comp_w1; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed; p.act = c->act;
+        { PROF(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_PAIR, EPI_SILU, s); }
+        { PROF(PIPO_K_GEMV_SMALL); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 1, s); }
+        p = gemv_base(c, B);
+        p.W = c->comp_w2; p.N = H; p.K = H; p.xf = c->act; p.out = c->x; p.ss_out = c->ss_x;
+        { PROF(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+    } else {   // pair-in compressor, Linear (eq. 1)
+        GemvParams p = gemv_base(c, B);
         p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;
         p.out = c->x; p.bias = c->b_comp; p.ss_out = c->ss_x;
         PROF(PIPO_K_GEMV_SMALL);
@@ -504,6 +565,14 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
         if (regular) {
             PROF(PIPO_K_PREFILL_MISC);
             launch_gather_tokens(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_x, s);
+        } else if (c->heads & PIPO_HEADS_MLP_COMPRESSOR) {
+            { PROF(PIPO_K_PREFILL_MISC); launch_gather_pairs(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_xin, s); }
+            p.W = c->comp_w1; p.X = c->p_xin; p.N = H; p.K = 2 * H; p.epi = EPI_SILU; p.act_hi = c->p_act; p.act_lo = c->p_act_lo;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+            { PROF(PIPO_K_PREFILL_MISC); launch_gather_pair_sum(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_x, s); }
+            p = gp;
+            p.W = c->comp_w2; p.X = c->p_act; p.Xlo = c->p_act_lo; p.N = H; p.K = H; p.epi = EPI_RESID; p.out = c->p_x;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
         } else {
             { PROF(PIPO_K_PREFILL_MISC); launch_gather_pairs(d_tokens, c->embed, H, c->V, c->pad_id, g, c->p_xin, s); }
             p.W = c->w_comp; p.X = c->p_xin; p.N = H; p.K = 2 * H; p.epi = EPI_STORE; p.out = c->p_x; p.bias = c->b_comp;
@@ -532,6 +601,37 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
             p.W = lw.wdown; p.X = c->p_act; p.Xlo = c->p_act_lo; p.N = H; p.K = F; p.epi = EPI_RESID; p.out = c->p_x;
             { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
         }
+        if (!regular && (c->heads & PIPO_HEADS_MTP_LAYER)) {
+            // App. B.2 over the chunk's latents (their K/V fill the MTP cache);
+            // the MTP stream lives in p_xin, free once the compressor has run
+            float *xm = (float *)c->p_xin;
+            { PROF(PIPO_K_PREFILL_MISC);
+              launch_mtp_rows(c->p_x, d_tokens, c->embed, c->g_mtp_h, c->g_mtp_e, H, c->V, c->pad_id, c->cfg.rms_eps, g, M,
+                              c->p_act, c->p_act_lo, s); }
+            p = gp;
+            p.W = c->w_fc; p.X = c->p_act; p.Xlo = c->p_act_lo; p.N = H; p.K = 2 * H; p.epi = EPI_STORE; p.out = xm;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+            const LayerW &lw = c->mtp;
+            { PROF(PIPO_K_PREFILL_MISC); launch_rmsnorm_tiled(xm, lw.g_attn, H, c->cfg.rms_eps, M, c->p_xn, c->p_xn_lo, s); }
+            p = gp;
+            p.W = lw.wqkv; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q;
+            p.kc = c->kc_mtp; p.vc = c->vc_mtp;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+            AttnPrefillParams ap{};
+            ap.q = c->p_q; ap.kc = c->kc_mtp; ap.vc = c->vc_mtp; ap.kv_bstride = c->kv_bstride; ap.g = g;
+            ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad; ap.out_hi = c->p_o; ap.out_lo = c->p_o_lo;
+            { PROF(PIPO_K_PREFILL_ATTN); launch_attn_prefill(ap, s); }
+            p = gp;
+            p.W = lw.wo; p.X = c->p_o; p.Xlo = c->p_o_lo; p.N = H; p.K = c->qdim; p.epi = EPI_RESID; p.out = xm;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+            { PROF(PIPO_K_PREFILL_MISC); launch_rmsnorm_tiled(xm, lw.g_ffn, H, c->cfg.rms_eps, M, c->p_xn, c->p_xn_lo, s); }
+            p = gp;
+            p.W = lw.wgu; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = 2 * F; p.K = H; p.epi = EPI_SWIGLU; p.act_hi = c->p_act; p.act_lo = c->p_act_lo;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+            p = gp;
+            p.W = lw.wdown; p.X = c->p_act; p.Xlo = c->p_act_lo; p.N = H; p.K = F; p.epi = EPI_RESID; p.out = xm;
+            { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
+        }
     }
     { PROF(PIPO_K_PREFILL_MISC); launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, positions, s); }
     c->len = positions;
@@ -547,7 +647,7 @@ extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     c->prefilled = false;
     int rc = prefill_backbone(c, batch, d_tokens, n, smp, false, s);
     if (rc) return rc;
-    enqueue_heads(c, batch, 1, 0, s);
+    enqueue_heads(c, batch, c->H / 16, 1, s);
     HIP_TRY(c, hipGetLastError());
     rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
     if (rc) return rc;
@@ -579,7 +679,7 @@ static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, hipS
 // backbone layers as the pair step (eq. 2 for one position), the heads above.
 static void enqueue_regular_decode(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
-    { PROF(PIPO_K_GEMV_SMALL); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, s); }
+    { PROF(PIPO_K_GEMV_SMALL); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 0, s); }
     enqueue_layers(c, s);
     enqueue_regular_heads(c, B, H / 16, 1, s);
 }
@@ -599,7 +699,7 @@ extern "C" int pipo_regular_prefill(pipo_ctx *c, int32_t batch, const int32_t *d
     c->prefilled = false;
     int rc = prefill_backbone(c, batch, d_tokens, n, smp, true, s);
     if (rc) return rc;
-    enqueue_regular_heads(c, batch, 1, 0, s);
+    enqueue_regular_heads(c, batch, c->H / 16, 1, s);
     HIP_TRY(c, hipGetLastError());
     rc = copy_tokens(c, d_tok, d_logits, s);
     if (rc) return rc;
@@ -738,7 +838,11 @@ extern "C" int pipo_read_weight(pipo_ctx *c, const char *name, int64_t start, in
     int perm = PERM_NONE, half = 0;
     std::string nm(name);
     int layer = -1;
-    if (nm.size() > 1 && nm[0] == 'l' && nm.find('.') != std::string::npos) {
+    if (nm.rfind("mtp.", 0) == 0) {
+        if (!(c->heads & PIPO_HEADS_MTP_LAYER)) return fail(c, PIPO_EINVAL, "no MTP layer in this model: %s", name);
+        layer = c->L;   // the MTP head's decoder layer
+        nm = nm.substr(4);
+    } else if (nm.size() > 1 && nm[0] == 'l' && nm.find('.') != std::string::npos) {
         layer = atoi(nm.c_str() + 1);
         if (layer < 0 || layer >= c->L) return fail(c, PIPO_EINVAL, "layer out of range in %s", name);
         nm = nm.substr(nm.find('.') + 1);
@@ -754,8 +858,12 @@ extern "C" int pipo_read_weight(pipo_ctx *c, const char *name, int64_t start, in
         else if (nm == "g_mtp_e") { vec = c->g_mtp_e; N = H; }
         else if (nm == "g_mtp_o") { vec = c->g_mtp_o; N = H; }
         else if (nm == "g_conf") { vec = c->g_conf; N = 2 * H; }
+        else if (nm == "comp_w1" && c->comp_w1) { src = c->comp_w1; N = H; K = 2 * H; }
+        else if (nm == "comp_w2" && c->comp_w2) { src = c->comp_w2; N = H; K = H; }
+        else if (nm == "conf_w1" && c->conf_w1) { src = c->conf_w1; N = H; K = 2 * H; }
+        else if (nm == "conf_w2" && c->conf_w2) { vec = c->conf_w2; N = H; }
     } else {
-        const LayerW &lw = c->layers[layer];
+        const LayerW &lw = layer < c->L ? c->layers[layer] : c->mtp;
         if (nm == "wq") { src = lw.wqkv; N = c->qdim; K = H; perm = PERM_QK; half = c->d / 2; }
         else if (nm == "wk") { src = lw.wqkv; N = c->kvdim; K = H; perm = PERM_QK; half = c->d / 2; row_base = c->qdim; }
         else if (nm == "wv") { src = lw.wqkv; N = c->kvdim; K = H; row_base = c->qdim + c->kvdim; }

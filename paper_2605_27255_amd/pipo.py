@@ -33,7 +33,7 @@ class PipoConfig(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
                 ("pad_id", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_latent", ctypes.c_int32),
-                ("prefill_chunk", ctypes.c_int32), ("gain_mode", ctypes.c_int32)]
+                ("prefill_chunk", ctypes.c_int32), ("gain_mode", ctypes.c_int32), ("heads", ctypes.c_int32)]
 
 
 class PipoSampling(ctypes.Structure):
@@ -80,7 +80,8 @@ def make_config(model, max_batch: int, max_latent: int, prefill_chunk: int = 409
     """A PipoConfig from any object with the model-shape attributes."""
     return PipoConfig(model.n_layers, model.hidden, model.n_q_heads, model.n_kv_heads, model.head_dim,
                       model.ffn, model.vocab, float(model.rope_base), float(model.rms_eps), -1,
-                      max_batch, max_latent, prefill_chunk, int(getattr(model, "gain_mode", 0)))
+                      max_batch, max_latent, prefill_chunk, int(getattr(model, "gain_mode", 0)),
+                      int(getattr(model, "heads", 0)))
 
 
 def _ptr(t):

@@ -68,7 +68,8 @@ def _check_token(rep, tag, gpu_tok, ref_tok, gpu_row, ref_row, max_abs, smp, u):
         rep.failures.append(f"{tag}: sampled {gpu_tok}, oracle {ref_tok}, rule on GPU logits {again}")
 
 
-def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=LOGIT_MEAN_REL):
+def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=LOGIT_MEAN_REL, conf_tol=CONF_TOL,
+                 max_abs_tol=LOGIT_MAX_ABS):
     tok_b, tok_d, conf, acc = out_np
     rep.steps += 1
     for i, r in enumerate(recs):
@@ -78,7 +79,7 @@ def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=
             ma, mr = _row_err(g, ref)
             rep.max_abs = max(rep.max_abs, ma)
             rep.max_mean_rel = max(rep.max_mean_rel, mr)
-            if ma > LOGIT_MAX_ABS or mr > mean_rel_tol:
+            if ma > max_abs_tol or mr > mean_rel_tol:
                 rep.failures.append(f"{t} {name}: max_abs {ma:.3g} mean_rel {mr:.3g}")
         u_b = rspec.uniform_draw(seeds[i], step, 0) if smp.temperature > 0 else None
         u_d = rspec.uniform_draw(seeds[i], step, 1) if smp.temperature > 0 else None
@@ -88,10 +89,10 @@ def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=
         _check_token(rep, t + " draft", int(tok_d[i]), r["tok_d"], ld[i], r["logits_d"], ma_d, smp, u_d)
         ce = abs(float(conf[i]) - r["conf"])
         rep.max_conf_err = max(rep.max_conf_err, ce)
-        if ce > CONF_TOL:
+        if ce > conf_tol:
             rep.failures.append(f"{t}: conf {conf[i]:.6f} vs {r['conf']:.6f}")
         if bool(acc[i]) != r["accept"]:
-            if abs(r["conf"] - smp.tau) <= CONF_TOL:
+            if abs(r["conf"] - smp.tau) <= conf_tol:
                 rep.ambiguous_accepts += 1
             else:
                 rep.failures.append(f"{t}: accept {acc[i]} vs {r['accept']} (c_ref {r['conf']:.6f})")
@@ -100,7 +101,8 @@ def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=
             rep.failures.append(f"{t}: accept flag inconsistent with conf {conf[i]} and tau {smp.tau}")
 
 
-def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_MEAN_REL):
+def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_MEAN_REL, conf_tol=CONF_TOL,
+               max_abs_tol=LOGIT_MAX_ABS):
     """Run the GPU free for ``steps`` pair steps after prefill; replay on the oracle."""
     import torch
     from paper_2605_27255_amd import unpack_pairs
@@ -125,7 +127,7 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
             prev = host[s - 1][0]
             pairs = [(int(prev[0][i]), int(prev[1][i]) if prev[3][i] else W.cfg.pad_id) for i in range(B)]
             recs = orc.decode_step(in_pairs=pairs, force_b=force)
-        compare_step(rep, f"step {s}", o, lb, ld, recs, smp, seeds, s, mean_rel_tol)
+        compare_step(rep, f"step {s}", o, lb, ld, recs, smp, seeds, s, mean_rel_tol, conf_tol, max_abs_tol)
     log(f"parity: steps {rep.steps} rows {rep.rows} max_abs {rep.max_abs:.3g} "
         f"max_mean_rel {rep.max_mean_rel:.3g} conf_err {rep.max_conf_err:.3g} "
         f"ambiguous tokens {rep.ambiguous_tokens} accepts {rep.ambiguous_accepts}")

@@ -42,15 +42,17 @@ def test_struct_layout_matches_header(tmp_path):
 #include <stddef.h>
 #include "{HEADER}"
 int main(void) {{
-  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(pipo_config), sizeof(pipo_sampling), sizeof(pipo_pair),
-         offsetof(pipo_config, gain_mode), offsetof(pipo_sampling, seeds), offsetof(pipo_pair, accept));
+  printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(pipo_config), sizeof(pipo_sampling), sizeof(pipo_pair),
+         offsetof(pipo_config, gain_mode), offsetof(pipo_sampling, seeds), offsetof(pipo_pair, accept),
+         offsetof(pipo_config, heads));
   return 0;
 }}''')
     exe = tmp_path / "layout"
     subprocess.run(["gcc", str(src), "-o", str(exe)], check=True)
     got = list(map(int, subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()))
     assert got == [ctypes.sizeof(pipo.PipoConfig), ctypes.sizeof(pipo.PipoSampling), ctypes.sizeof(pipo.PipoPair),
-                   pipo.PipoConfig.gain_mode.offset, pipo.PipoSampling.seeds.offset, pipo.PipoPair.accept.offset]
+                   pipo.PipoConfig.gain_mode.offset, pipo.PipoSampling.seeds.offset, pipo.PipoPair.accept.offset,
+                   pipo.PipoConfig.heads.offset]
     assert got[2] == 16
 
 
@@ -65,7 +67,7 @@ def _cfg(**kw):
 
 @pytest.mark.parametrize("field,value", [("head_dim", 96), ("hidden", 250), ("ffn", 1000), ("vocab", 4090),
                                          ("max_batch", 33), ("max_batch", 0), ("n_kv_heads", 3),
-                                         ("prefill_chunk", 0), ("max_latent", 0), ("gain_mode", 2),
+                                         ("prefill_chunk", 0), ("max_latent", 0), ("gain_mode", 2), ("heads", 8),
                                          ("pad_id", 5000)])
 def test_bad_config_is_rejected_before_device_work(lib, field, value):
     from paper_2605_27255_amd import pipo

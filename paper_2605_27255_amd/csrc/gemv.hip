@@ -21,10 +21,14 @@
 // a strip are reduced through LDS in wave order (deterministic, no atomics,
 // no cross-workgroup traffic) and a fused epilogue writes the result (bias,
 // residual add, SwiGLU, RoPE + KV append, logits + argmax).
+#include <hip/hip_ext.h>
+
 #include "device_common.h"
 #include "kernels.h"
 
 namespace pipo {
+
+thread_local GemvTiming g_gemv_timing = {nullptr, nullptr, false};
 
 constexpr int kNW = 8;                       // waves per workgroup
 constexpr int kGemvOneLdsBytes = 72 * 1024;  // budget for wave-private X (two workgroups per CU)
@@ -1003,6 +1007,9 @@ __global__ __launch_bounds__(64) void k_gemv_fin(GemvParams p) {
 }
 
 template <int NBT, int KS, int PRO, int EPI, int U>
+static void launch_multi(GemvParams &q, hipStream_t s);
+
+template <int NBT, int KS, int PRO, int EPI, int U>
 static void launch_t(const GemvParams &p, hipStream_t s) {
     GemvParams q = p;
     const int KT = q.K >> 5;
@@ -1015,10 +1022,27 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     const int lds_one = planes * kNW * q.B * (nmax * 32 + 8) * 2 + red;
     if (lds_one <= kGemvOneLdsBytes) {
         if (q.wg_cap > 0 && grid > q.wg_cap) grid = q.wg_cap;
-        hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s, q);
+        if (g_gemv_timing.pending) {
+            hipExtLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s,
+                                  g_gemv_timing.start, g_gemv_timing.stop, 0, q);
+            g_gemv_timing.pending = false;
+        } else {
+            hipLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s, q);
+        }
         return;
     }
-    // otherwise, below the vocabulary head: k-ranges whose X slices fit
+    // the other paths launch several kernels: the events bracket them
+    const bool timed = g_gemv_timing.pending;
+    g_gemv_timing.pending = false;
+    if (timed) hipEventRecord(g_gemv_timing.start, s);
+    launch_multi<NBT, KS, PRO, EPI, U>(q, s);
+    if (timed) hipEventRecord(g_gemv_timing.stop, s);
+}
+
+template <int NBT, int KS, int PRO, int EPI, int U>
+static void launch_multi(GemvParams &q, hipStream_t s) {
+    const int KT = q.K >> 5;
+    // below the vocabulary head: k-ranges whose X slices fit
     if constexpr (EPI != EPI_LOGITS) {
         // k-tiles per range: the X slice (hi + lo bf16) within the LDS budget
         // and the per-thread chunk count, and enough ranges x strips for the

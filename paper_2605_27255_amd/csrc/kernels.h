@@ -54,6 +54,12 @@ struct GemvParams {
     int xseg;                     // 2048-column segments per row of the X planes (set by launch_gemv)
 };
 void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s);
+// Profiling of the next launch_gemv on this thread: with `pending` set, the
+// call records `start` / `stop` around its kernels (the batch-1 kernel through
+// hipExtLaunchKernelGGL, so the interval is the kernel's own execution) and
+// clears `pending`.
+struct GemvTiming { hipEvent_t start, stop; bool pending; };
+extern thread_local GemvTiming g_gemv_timing;
 int gemv_num_groups(int N);
 
 // ----------------------------------------------------------------------------

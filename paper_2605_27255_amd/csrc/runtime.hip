@@ -100,9 +100,13 @@ struct pipo_ctx {
 };
 
 // Launch bracket: record an event before and after a launch when profiling.
+// Around one launch_gemv call (gemv = true) the events go to the GEMV
+// launcher instead, which records them around its kernels (the batch-1
+// kernel times itself, without the gaps an event recorded between two
+// launches adds).
 struct ProfScope {
-    pipo_ctx *c; hipStream_t s; int cls; size_t i0 = 0;
-    ProfScope(pipo_ctx *c_, hipStream_t s_, int cls_) : c(c_), s(s_), cls(cls_) {
+    pipo_ctx *c; hipStream_t s; int cls; bool gemv; size_t i0 = 0;
+    ProfScope(pipo_ctx *c_, hipStream_t s_, int cls_, bool gemv_ = false) : c(c_), s(s_), cls(cls_), gemv(gemv_) {
         if (!c->prof_on) return;
         while (c->ev_pool.size() < c->ev_next + 2) {
             hipEvent_t e;
@@ -111,17 +115,25 @@ struct ProfScope {
         }
         i0 = c->ev_next;
         c->ev_next += 2;
-        hipEventRecord(c->ev_pool[i0], s);
+        if (gemv) g_gemv_timing = GemvTiming{c->ev_pool[i0], c->ev_pool[i0 + 1], true};
+        else hipEventRecord(c->ev_pool[i0], s);
     }
     ~ProfScope() {
         if (!c->prof_on) return;
-        hipEventRecord(c->ev_pool[i0 + 1], s);
+        if (!gemv) {
+            hipEventRecord(c->ev_pool[i0 + 1], s);
+        } else if (g_gemv_timing.pending) {   // nothing was launched: an empty interval
+            g_gemv_timing.pending = false;
+            hipEventRecord(c->ev_pool[i0], s);
+            hipEventRecord(c->ev_pool[i0 + 1], s);
+        }
         c->pending.push_back({cls, i0});
     }
 };
 #define PROF_CAT2(a, b) a##b
 #define PROF_CAT(a, b) PROF_CAT2(a, b)
 #define PROF(cls) ProfScope PROF_CAT(prof_scope_, __LINE__)(c, s, cls)
+#define PROF_GEMV(cls) ProfScope PROF_CAT(prof_scope_, __LINE__)(c, s, cls, true)
 
 static int fail(pipo_ctx *c, int code, const char *fmt, ...) {
     char buf[512];
@@ -389,7 +401,7 @@ static void enqueue_layer(pipo_ctx *c, const LayerW &lw, uint16_t *kc, uint16_t 
     p.x = xres; p.ss = ssres; p.nss = H / 16; p.gain = lw.g_attn;
     p.q = c->qbuf; p.kc = kc; p.vc = vc; p.pos = c->pos; p.rope_cos = c->rope_cos; p.rope_sin = c->rope_sin;
     p.n_q = c->nq; p.n_kv = c->nkv; p.d = c->d; p.lmax_pad = c->lmax_pad; p.kv_bstride = c->kv_bstride;
-    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_QKV, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_QKV, s); }
 
     AttnDecodeParams ap{};
     ap.q = c->qbuf; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.pos = c->pos;
@@ -399,16 +411,16 @@ static void enqueue_layer(pipo_ctx *c, const LayerW &lw, uint16_t *kc, uint16_t 
 
     p = base;
     p.W = lw.wo; p.N = H; p.K = c->qdim; p.xf = c->attn_out; p.out = xres; p.ss_out = ssres;
-    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
 
     p = base;
     p.W = lw.wgu; p.N = 2 * c->F; p.K = H; p.x = xres; p.ss = ssres; p.nss = H / 16; p.gain = lw.g_ffn;
     p.act = c->act;
-    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_SWIGLU, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_SWIGLU, s); }
 
     p = base;
     p.W = lw.wdown; p.N = H; p.K = c->F; p.xf = c->act; p.out = xres; p.ss_out = ssres;
-    { PROF(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
 }
 
 // The backbone layers of one decode position over the residual in x.
@@ -431,7 +443,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     p.W = c->embed; p.N = c->V; p.K = H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
     p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
-    { PROF(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         SampleParams sp{c->logits_b, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 0, c->best_b};
         PROF(PIPO_K_SAMPLE);
@@ -445,7 +457,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     m.x = c->x; m.ss = c->ss_x; m.nss = nss; m.gain = c->g_mtp_h; m.gain2 = c->g_mtp_e;
     m.embed = c->embed; m.tokkey = c->best_b;
     m.out = c->hd; m.ss_out = c->ss_hd;
-    { PROF(PIPO_K_GEMV_SMALL); launch_gemv(m, PRO_MTP, EPI_STORE, s); }
+    { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(m, PRO_MTP, EPI_STORE, s); }
     // App. B.2: the MTP head's decoder layer at the current latent position
     if (c->heads & PIPO_HEADS_MTP_LAYER) enqueue_layer(c, c->mtp, c->kc_mtp, c->vc_mtp, c->hd, c->ss_hd, s);
     // LM head #2 on RMSNorm(h_d; g_mo)
@@ -454,7 +466,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     q.W = c->embed; q.N = c->V; q.K = H;
     q.x = c->hd; q.ss = c->ss_hd; q.nss = H / 16; q.gain = c->g_mtp_o;
     q.out = c->logits_d; q.best = greedy ? c->best_d : nullptr;
-    { PROF(PIPO_K_GEMV_LMHEAD); launch_gemv(q, PRO_NORM, EPI_LOGITS, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(q, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         SampleParams sp{c->logits_d, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 1, c->best_d};
         PROF(PIPO_K_SAMPLE);
@@ -467,7 +479,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
         f.W = c->conf_w1; f.N = H; f.K = 2 * H;
         f.x = c->x; f.x2 = c->hd; f.ss = c->ss_x; f.ss2 = c->ss_hd; f.nss = H / 16; f.gain = c->g_conf;
         f.act = c->act;
-        { PROF(PIPO_K_GEMV_SMALL); launch_gemv(f, PRO_CAT, EPI_SILU, s); }
+        { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(f, PRO_CAT, EPI_SILU, s); }
         gp.conf_h = c->act; gp.conf_w2 = c->conf_w2;
     }
     gp.hb = c->x; gp.hd = c->hd; gp.ss_b = c->ss_x; gp.nss_b = nss; gp.ss_d = c->ss_hd; gp.nss_d = H / 16;
@@ -484,16 +496,16 @@ static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
     if (c->heads & PIPO_HEADS_MLP_COMPRESSOR) {   // Table 4 MLP: E[a] + E[b] + W2 SiLU(W1 [E[a]; E[b]])
         GemvParams p = gemv_base(c, B);
         p.W = c->comp_w1; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed; p.act = c->act;
-        { PROF(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_PAIR, EPI_SILU, s); }
-        { PROF(PIPO_K_GEMV_SMALL); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 1, s); }
+        { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_PAIR, EPI_SILU, s); }
+        { PROF(PIPO_K_GATE); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 1, s); }
         p = gemv_base(c, B);
         p.W = c->comp_w2; p.N = H; p.K = H; p.xf = c->act; p.out = c->x; p.ss_out = c->ss_x;
-        { PROF(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+        { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_F32, EPI_RESID, s); }
     } else {   // pair-in compressor, Linear (eq. 1)
         GemvParams p = gemv_base(c, B);
         p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;
         p.out = c->x; p.bias = c->b_comp; p.ss_out = c->ss_x;
-        PROF(PIPO_K_GEMV_SMALL);
+        PROF_GEMV(PIPO_K_GEMV_SMALL);
         launch_gemv(p, PRO_PAIR, EPI_STORE, s);
     }
     enqueue_layers(c, s);
@@ -665,7 +677,7 @@ static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, hipS
     p.W = c->embed; p.N = c->V; p.K = c->H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
     p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
-    { PROF(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         SampleParams sp{c->logits_b, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 0, c->best_b};
         PROF(PIPO_K_SAMPLE);
@@ -679,7 +691,7 @@ static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, hipS
 // backbone layers as the pair step (eq. 2 for one position), the heads above.
 static void enqueue_regular_decode(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
-    { PROF(PIPO_K_GEMV_SMALL); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 0, s); }
+    { PROF(PIPO_K_GATE); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 0, s); }
     enqueue_layers(c, s);
     enqueue_regular_heads(c, B, H / 16, 1, s);
 }

@@ -435,10 +435,13 @@ void launch_gemm(const GemmParams &p, hipStream_t s) {
 // requested into registers before the current one is multiplied.  Per stage
 // the scores of all 64 keys are formed first (both query tiles), then one
 // online-softmax update per query tile (the causal mask only on stages that
-// reach the diagonal), so the accumulator rescale and the row max / sum
-// shuffles happen once per 64 keys.  Scores stay unscaled; the softmax scale
-// 1/sqrt(d) (times log2 e) enters through one fma per score in the exponent.
-// Two workgroups fit per CU so that one's softmax overlaps the other's MFMAs.
+// reach the diagonal), so the row max / sum shuffles happen once per 64 keys,
+// and the accumulators are rescaled only when the running max grows by more
+// than 2^8.  Scores stay unscaled; the softmax scale 1/sqrt(d) (times log2 e)
+// enters through one fma per score in the exponent, and the exponentials are
+// the hardware exp2 (results below the normal range flush to zero, which the
+// softmax weights can afford).  Two workgroups fit per CU so that one's
+// softmax overlaps the other's MFMAs.
 constexpr int kAQ = 32;         // queries per workgroup
 constexpr int kAK = 64;         // keys per LDS stage
 
@@ -520,6 +523,80 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             }
         }
     };
+    // One 64-key stage: scores S^T for the four 16-key tiles and both query
+    // tiles, one online-softmax update per query tile, then O^T += V^T P^T.
+    // The running max only moves when some column's max grows by more than
+    // 2^8 (in exp2 units), so the accumulators are rarely rescaled and every
+    // exponent stays at most 256; o / l at the end is the same quotient.
+    auto attend = [&](const uint16_t *ks, const uint16_t *vs, int kb0, bool diag) {
+        f32x4 sc[2][4];
+#pragma unroll
+        for (int tau = 0; tau < 4; ++tau) {
+            u32x4 kf[NC];
+#pragma unroll
+            for (int c = 0; c < NC; ++c) kf[c] = *(const u32x4 *)(&ks[(16 * tau + j) * KS + 32 * c + 8 * g]);
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                sc[ct][tau] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int c = 0; c < NC; ++c) sc[ct][tau] = mfma16(kf[c], qb[ct][c], sc[ct][tau]);
+            }
+        }
+        u32x4 pt[2][2];
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+            // keys past this column's query are masked (only on diagonal stages)
+            const int lim = diag ? qpos0 + 16 * ct + j - kb0 - 4 * g : 64;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    float sv = sc[ct][tau][v];
+                    if (diag) sv = 16 * tau + v <= lim ? sv : -INFINITY;
+                    sc[ct][tau][v] = sv;
+                    mx = fmaxf(mx, sv);
+                }
+            mx = col_max(mx);
+            // a query row sees key 0 in the first stage, so the max is finite from then on
+            const float m_cand = fmaxf(m_run[ct], mx * scale);
+            if (__any(m_cand > m_run[ct] + 8.0f)) {
+                const float alpha = __builtin_amdgcn_exp2f(m_run[ct] - m_cand);
+                l_run[ct] *= alpha;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) o[ct][t] *= alpha;
+                m_run[ct] = m_cand;
+            }
+            const float m_use = m_run[ct];
+            float ps = 0.f;
+#pragma unroll
+            for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float e = __builtin_amdgcn_exp2f(fmaf(sc[ct][tau][v], scale, -m_use));
+                    sc[ct][tau][v] = e;
+                    ps += e;
+                }
+            l_run[ct] += col_sum(ps);
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                pt[ct][half][0] = pack_bf2_hw(sc[ct][2 * half][0], sc[ct][2 * half][1]);
+                pt[ct][half][1] = pack_bf2_hw(sc[ct][2 * half][2], sc[ct][2 * half][3]);
+                pt[ct][half][2] = pack_bf2_hw(sc[ct][2 * half + 1][0], sc[ct][2 * half + 1][1]);
+                pt[ct][half][3] = pack_bf2_hw(sc[ct][2 * half + 1][2], sc[ct][2 * half + 1][3]);
+            }
+        }
+        // O^T += V^T P^T, each V fragment serving both query tiles
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const u32x4 vf = *(const u32x4 *)(&vs[(half * D + 16 * t + j) * VS + 8 * g]);
+#pragma unroll
+                for (int ct = 0; ct < 2; ++ct) o[ct][t] = mfma16(vf, pt[ct][half], o[ct][t]);
+            }
+    };
+
     stage_load(0);
     stage_store(0);
     __syncthreads();
@@ -531,69 +608,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
         stage_load(kb0 + kAK);
         const uint16_t *ks = ks2[buf], *vs = vs2[buf];
         if (active) {
-            // scores S^T for 64 keys (four 16-key tiles) and both query tiles
-            f32x4 sc[2][4];
-#pragma unroll
-            for (int tau = 0; tau < 4; ++tau) {
-                u32x4 kf[NC];
-#pragma unroll
-                for (int c = 0; c < NC; ++c) kf[c] = *(const u32x4 *)(&ks[(16 * tau + j) * KS + 32 * c + 8 * g]);
-#pragma unroll
-                for (int ct = 0; ct < 2; ++ct) {
-                    sc[ct][tau] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int c = 0; c < NC; ++c) sc[ct][tau] = mfma16(kf[c], qb[ct][c], sc[ct][tau]);
-                }
-            }
-            const bool diag = kb0 + kAK - 1 > qpos0;   // some key may lie past some query
-            u32x4 pt[2][2];
-#pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
-                const int qabs = qpos0 + 16 * ct + j;
-                float mx = -INFINITY;
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        float sv = sc[ct][tau][v];
-                        if (diag) sv = kb0 + 16 * tau + 4 * g + v <= qabs ? sv : -INFINITY;
-                        sc[ct][tau][v] = sv;
-                        mx = fmaxf(mx, sv);
-                    }
-                mx = col_max(mx);
-                // a query row sees key 0 in the first stage, so m_new is finite
-                const float m_new = fmaxf(m_run[ct], mx * scale);
-                const float alpha = exp2f(m_run[ct] - m_new);
-                float ps = 0.f;
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const float e = exp2f(fmaf(sc[ct][tau][v], scale, -m_new));
-                        sc[ct][tau][v] = e;
-                        ps += e;
-                    }
-                l_run[ct] = l_run[ct] * alpha + col_sum(ps);
-                m_run[ct] = m_new;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) o[ct][t] *= alpha;
-#pragma unroll
-                for (int half = 0; half < 2; ++half) {
-                    pt[ct][half][0] = pack_bf2_hw(sc[ct][2 * half][0], sc[ct][2 * half][1]);
-                    pt[ct][half][1] = pack_bf2_hw(sc[ct][2 * half][2], sc[ct][2 * half][3]);
-                    pt[ct][half][2] = pack_bf2_hw(sc[ct][2 * half + 1][0], sc[ct][2 * half + 1][1]);
-                    pt[ct][half][3] = pack_bf2_hw(sc[ct][2 * half + 1][2], sc[ct][2 * half + 1][3]);
-                }
-            }
-            // O^T += V^T P^T, each V fragment serving both query tiles
-#pragma unroll
-            for (int half = 0; half < 2; ++half)
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const u32x4 vf = *(const u32x4 *)(&vs[(half * D + 16 * t + j) * VS + 8 * g]);
-#pragma unroll
-                    for (int ct = 0; ct < 2; ++ct) o[ct][t] = mfma16(vf, pt[ct][half], o[ct][t]);
-                }
+            // the causal mask only where some key of the stage lies past some query
+            attend(ks, vs, kb0, kb0 + kAK - 1 > qpos0);
         }
         stage_store(buf ^ 1);
         __syncthreads();

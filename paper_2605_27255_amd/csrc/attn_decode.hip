@@ -107,13 +107,13 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
             }
         mx = col_max(mx);
         const float m_new = fmaxf(m_run, mx);
-        const float alpha = exp2f(m_run - m_new);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
         float ps = 0.f;
 #pragma unroll
         for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const float e = exp2f(st[tau][v] - m_new);
+                const float e = __builtin_amdgcn_exp2f(st[tau][v] - m_new);
                 st[tau][v] = e;
                 ps += e;
             }
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
         const float ms = t < S ? msr : -INFINITY;
         const float ls = t < S ? lsr : 0.f;
         const float M = wave_max(ms);
-        const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
+        const float w = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M);
         const float L = wave_sum(w * ls);
         s_w[t] = w;
         if (t == 0) s_inv = 1.0f / L;

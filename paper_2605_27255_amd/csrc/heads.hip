@@ -120,7 +120,9 @@ void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_
 
 // ---------------------------------------------------------------------------
 // Temperature + top-p selection, one 1024-thread workgroup per sequence.
-//   e_j = exp((l_j - max l) / T); masses are fixed point, E_j = round(e_j 2^40),
+//   e_j = exp((l_j - max l) / T) (the hardware exp2; values below the normal
+//   range flush to zero, as their fixed-point masses round to zero anyway);
+//   masses are fixed point, E_j = round(e_j 2^40),
 //   so every sum is an exact integer sum (order independent).
 //   theta* = the largest e-value whose upper mass sum_{e_i >= theta} E_i
 //   reaches top_p * sum E: found exactly by a 4-pass radix select over the
@@ -188,7 +190,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
         float v[4];
         load4(t, v);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) tot += valid(t, e) ? fixed_mass(exp2f((v[e] - mx) * kT)) : 0ull;
+        for (int e = 0; e < 4; ++e) tot += valid(t, e) ? fixed_mass(__builtin_amdgcn_exp2f((v[e] - mx) * kT)) : 0ull;
     }
     for (int o = 32; o > 0; o >>= 1) {
         const uint32_t lo = __shfl_xor((uint32_t)tot, o), hi = __shfl_xor((uint32_t)(tot >> 32), o);
@@ -212,7 +214,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
             load4(t, v);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float ev = exp2f((v[e] - mx) * kT);
+                const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
                 const uint32_t key = __float_as_uint(ev);
                 if (valid(t, e) && (pass == 0 || (key >> (shift + 8)) == prefix))
                     atomicAdd(&hist[wave][(key >> shift) & 255u], fixed_mass(ev));
@@ -261,7 +263,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
         load4(t, v);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float ev = exp2f((v[e] - mx) * kT);
+            const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
             wm += (valid(t, e) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
         }
     }
@@ -282,7 +284,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
         unsigned long long m4[4], loc = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float ev = exp2f((v[e] - mx) * kT);
+            const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
             m4[e] = (valid(t, e) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
             loc += m4[e];
         }

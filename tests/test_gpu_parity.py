@@ -398,3 +398,40 @@ def test_4b_width_paper_heads(torch):
                             max_abs_tol=APPB_MAX_ABS)
         rep.check()
         m.close()
+
+
+# ------------------------------------------------------------ edge cases
+
+def test_tiny_degenerate_and_tile_boundary_prompts(torch):
+    """Prompts of 1, 2 and 3 tokens (a single latent, PAD at the odd slot for
+    odd n) and latent counts on both sides of the 32-key decode tile and the
+    64-key prefill stage, each followed by pair steps that cross the next
+    boundary; one context, re-prefilled per prompt."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    W = O.OracleWeights.generate(cfg, seed=17, precision="bf16")
+    m = _model(cfg, seed=17, max_batch=1, max_latent=70, prefill_chunk=32)
+    for n, steps in ((1, 3), (2, 3), (3, 2), (62, 3), (64, 2), (66, 1), (126, 3), (128, 2), (130, 2)):
+        log(f"prompt of {n} tokens, {steps} steps")
+        prompts = rspec.prompt_tokens(1, n, cfg.vocab, seed=100 + n)
+        rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log)
+        rep.check()
+    m.close()
+
+
+def test_tiny_top_p_floor_is_greedy(torch):
+    """A nucleus mass far below any single token's probability keeps only the
+    most probable token, so top-p sampling must return the greedy choice."""
+    from paper_2605_27255_amd import unpack_pairs
+    prompts = rspec.prompt_tokens(2, 30, TINY.vocab, seed=31)
+    m = _model(TINY, seed=4, max_batch=2, max_latent=24, prefill_chunk=16)
+    t = torch.from_numpy(prompts).cuda()
+    greedy = [m.prefill(t, 0.5)[0]] + [m.decode_step()[0] for _ in range(4)]
+    sampled = [m.prefill(t, 0.5, temperature=0.7, top_p=1e-6, seeds=[5, 6])[0]] + \
+              [m.decode_step()[0] for _ in range(4)]
+    torch.cuda.synchronize()
+    for g, s_ in zip(greedy, sampled):
+        gb, gd, _, _ = unpack_pairs(g)
+        sb, sd, _, _ = unpack_pairs(s_)
+        np.testing.assert_array_equal(gb, sb)
+        np.testing.assert_array_equal(gd, sd)
+    m.close()

@@ -573,9 +573,8 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 // bf16 hi / lo planes.  k_gemv_wide: a workgroup owns 128 weight rows (one
 // 16-row strip per wave) over the whole K; chunks of X (all B rows, hi and
 // lo) pass through LDS once per workgroup and are shared by its eight waves.
-// Weights stream one chunk ahead of the chunk being multiplied.  (The kernel
-// can also take a k-range with partial sums for k_gemv_fin; the head never
-// splits K, since its argmax epilogue is workgroup-wide.)
+// Weights stream one chunk ahead of the chunk being multiplied.  The head
+// never splits K: its argmax epilogue is workgroup-wide.
 template <int PRO>
 __global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
     // workgroup (b, segment): columns [2048 seg, 2048 seg + 2048) of row b
@@ -666,13 +665,10 @@ __global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
-    const int rtiles = (nstrips + kNW - 1) / kNW;
-    const int rt = blockIdx.x % rtiles, ksi = blockIdx.x / rtiles;
-    const int strip = rt * kNW + wave;
+    const int strip = blockIdx.x * kNW + wave;
     const bool sok = strip < nstrips;
     const int KT = p.K >> 5, K = p.K, B = p.B;
-    const int NC = (KT + CK - 1) / CK;     // chunks over the whole K
-    const int c0 = (ksi * NC) / p.ksplit, c1 = ((ksi + 1) * NC) / p.ksplit;
+    const int c0 = 0, c1 = (KT + CK - 1) / CK;   // chunks over the whole K
     const int nch = c1 - c0;
     const uint16_t *wp = p.W + (int64_t)(sok ? strip : 0) * KT * 512 + lane * 8;
     const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
@@ -729,7 +725,7 @@ __global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
     for (int bt = 0; bt < NBT; ++bt) {
         const int b = bt * 16 + j;
         resid[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (EPI == EPI_RESID && p.ksplit == 1)
+        if (EPI == EPI_RESID)
             resid[bt] = *(const f32x4 *)(p.out + ((sok && b < B) ? (int64_t)b * p.N + strip * 16 + 4 * g : 0));
     }
     // chunk c: X regs loaded one chunk ahead and written to LDS buffer c % 2
@@ -775,16 +771,7 @@ __global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
     f32x4 fin[NBT];
 #pragma unroll
     for (int bt = 0; bt < NBT; ++bt) fin[bt] = acc[bt];
-    if (p.ksplit == 1) {
-        gemv_epilogue<NBT, EPI>(p, fin, resid, strip, sok);
-        return;
-    }
-    // partial sums of this k-range: part[ksi][b][row]
-#pragma unroll
-    for (int bt = 0; bt < NBT; ++bt) {
-        const int b = bt * 16 + j;
-        if (sok && b < B) *(f32x4 *)(p.part + ((int64_t)ksi * B + b) * p.N + strip * 16 + 4 * g) = fin[bt];
-    }
+    gemv_epilogue<NBT, EPI>(p, fin, resid, strip, sok);
 }
 
 // ---------------------------------------------------------------------------
@@ -1075,7 +1062,6 @@ static void launch_multi(GemvParams &q, hipStream_t s) {
     q.xseg = (q.K + 2047) / 2048;
     hipLaunchKernelGGL((k_xprep<PRO>), dim3(q.B * q.xseg), dim3(256), 0, s, q);
     const int rtiles = ((q.N >> 4) + kNW - 1) / kNW;
-    q.ksplit = 1;
     const int lds_w = 2 * 2 * q.B * (kWideChunk * 32 + 8) * 2 + 16;
     hipLaunchKernelGGL((k_gemv_wide<NBT, EPI>), dim3(rtiles), dim3(kNW * 64), lds_w, s, q);
 }

@@ -233,6 +233,29 @@ def select_top_p(logits, temperature, top_p, u):
     return int(nucleus[hit[0]] if hit.size else nucleus[-1])
 
 
+def repetition_penalty(logits, seen, theta):
+    """CTRL-style repetition penalty: the logit of every token in ``seen`` is
+    divided by ``theta`` when positive and multiplied by it otherwise."""
+    y = np.asarray(logits, F64).copy()
+    idx = np.fromiter(sorted(set(int(t) for t in seen)), dtype=np.int64)
+    if idx.size and theta != 1.0:
+        v = y[idx]
+        y[idx] = np.where(v > 0, v / theta, v * theta)
+    return y
+
+
+def select_eval(logits, seen, temperature, top_k, top_p, theta, u):
+    """The paper's evaluation sampler (Sec. 4, after Qwen3.5): repetition
+    penalty, temperature, top-k (every value at least the k-th largest, ties
+    kept), then top-p over the kept tokens and the inverse-CDF draw of
+    ``select_top_p`` (ids of the kept set scanned upwards)."""
+    y = repetition_penalty(logits, seen, theta) / F64(temperature)
+    if 0 < top_k < y.size:
+        kth = np.sort(y)[::-1][top_k - 1]
+        y = np.where(y >= kth, y, -np.inf)
+    return select_top_p(y, 1.0, top_p, u)
+
+
 # ------------------------------------------------------------------- weights
 
 class OracleWeights:
@@ -364,6 +387,8 @@ class Sampling:
     temperature: float = 0.0       # <= 0: greedy
     top_p: float = 1.0
     seeds: tuple = ()              # one per sequence (sampling only)
+    top_k: int = 0                 # 0: no top-k (sampling only)
+    rep_penalty: float = 1.0       # 1: none (sampling only)
 
 
 class PipoOracle:
@@ -393,7 +418,7 @@ class PipoOracle:
         if cfg.heads & HEADS_MTP_LAYER:
             h_d = layer_step(cfg, mtp_layer(W), h_d, pos, self.mtp_caches[seq], self.kv_bf16)
         logits_d = lm_logits(W["embed"], W["g_mtp_o"], h_d, eps)
-        d = self._select(logits_d, seq, step, 1)
+        d = self._select(logits_d, seq, step, 1, extra=(b_used,))   # b precedes d in the output
         if cfg.heads & HEADS_MLP_CONFIDENCE:
             s, c = confidence_mlp(W["conf_w1"], W["conf_w2"], W["g_conf"], h_b, h_d, eps)
         else:
@@ -401,11 +426,14 @@ class PipoOracle:
         return dict(tok_b=b, tok_d=d, s=float(s), conf=float(c), accept=gate(c, smp.tau),
                     logits_b=logits_b, logits_d=logits_d, h_b=h_b, h_d=h_d)
 
-    def _select(self, logits, seq, step, slot):
+    def _select(self, logits, seq, step, slot, extra=()):
         smp = self.sampling
         if smp.temperature <= 0:
             return select_greedy(logits)
         u = rspec.uniform_draw(smp.seeds[seq], step, slot)
+        if smp.top_k or smp.rep_penalty != 1.0:
+            return select_eval(logits, self.seen[seq] | set(extra), smp.temperature, smp.top_k, smp.top_p,
+                               smp.rep_penalty, u)
         return select_top_p(logits, smp.temperature, smp.top_p, u)
 
     def prefill(self, prompts, sampling: Sampling, force_b=None):
@@ -413,6 +441,7 @@ class PipoOracle:
         self.sampling = sampling
         W, cfg = self.W, self.cfg
         self.caches, self.length, self.step_idx, self.next_pairs, self.mtp_caches = [], [], [], [], []
+        self.seen = [set(int(t) for t in p) for p in np.asarray(prompts)]   # tokens the penalty applies to
         out = []
         for i, prompt in enumerate(np.asarray(prompts)):
             pairs = prompt_pairs(prompt, cfg.pad_id)
@@ -440,12 +469,20 @@ class PipoOracle:
     def _next_pair(self, rec):
         return (rec["tok_b"], rec["tok_d"] if rec["accept"] else self.cfg.pad_id)
 
+    def _emitted(self, seq, pair):
+        """The tokens a pair step emitted, (b, d) or (b, PAD), join the penalised
+        set when they come back as the next input pair (PAD never does)."""
+        self.seen[seq].add(int(pair[0]))
+        if int(pair[1]) != self.cfg.pad_id:
+            self.seen[seq].add(int(pair[1]))
+
     def decode_step(self, in_pairs=None, force_b=None):
         """One pair step for every sequence; ``in_pairs`` teacher-forces the input."""
         W = self.W
         out = []
         for i in range(len(self.caches)):
             pair = self.next_pairs[i] if in_pairs is None else tuple(int(v) for v in in_pairs[i])
+            self._emitted(i, pair)
             z = self._compress(np.array([pair]))[0]
             pos = self.length[i]
             h_b = backbone_step(W, z, pos, self.caches[i], self.kv_bf16)
@@ -476,6 +513,8 @@ class RegularOracle:
         if smp.temperature <= 0:
             return select_greedy(logits)
         u = rspec.uniform_draw(smp.seeds[seq], step, 0)
+        if smp.top_k or smp.rep_penalty != 1.0:
+            return select_eval(logits, self.seen[seq], smp.temperature, smp.top_k, smp.top_p, smp.rep_penalty, u)
         return select_top_p(logits, smp.temperature, smp.top_p, u)
 
     def _head(self, h, seq, step):
@@ -487,6 +526,7 @@ class RegularOracle:
         self.sampling = sampling
         W = self.W
         self.caches, self.length, self.step_idx, self.next_tok = [], [], [], []
+        self.seen = [set(int(t) for t in p) for p in np.asarray(prompts)]
         out = []
         for i, prompt in enumerate(np.asarray(prompts)):
             X, caches = backbone_full(W, W["embed"][np.asarray(prompt)], self.kv_bf16)
@@ -504,6 +544,7 @@ class RegularOracle:
         out = []
         for i in range(len(self.caches)):
             t = self.next_tok[i] if in_tok is None else int(in_tok[i])
+            self.seen[i].add(t)
             h = backbone_step(W, W["embed"][t], self.length[i], self.caches[i], self.kv_bf16)
             self.length[i] += 1
             rec = self._head(h, i, self.step_idx[i])

@@ -587,3 +587,39 @@ def test_paper_heads_session_equals_brute_force(paper_w):
         np.testing.assert_allclose(rec["h_d"], Hd[L0 - 1 + k], rtol=1e-10, atol=1e-12)
         s, c = O.confidence_mlp(W["conf_w1"], W["conf_w2"], W["g_conf"], rec["h_b"], rec["h_d"], cfg.rms_eps)
         assert abs(c - rec["conf"]) < 1e-15
+
+
+# --------------------------------------------- evaluation sampler (Sec. 4)
+
+def test_repetition_penalty_closed_form():
+    l = np.array([2.0, -1.0, 0.5, 3.0, -4.0])
+    y = O.repetition_penalty(l, {0, 1, 4}, 1.5)
+    np.testing.assert_array_equal(y, [2.0 / 1.5, -1.5, 0.5, 3.0, -6.0])
+    np.testing.assert_array_equal(O.repetition_penalty(l, {0, 1}, 1.0), l)
+
+
+def test_eval_sampler_limits():
+    rng = np.random.default_rng(0)
+    l = rng.standard_normal(200)
+    # top_k = 1: the argmax of the penalised logits, for any draw
+    seen = {int(np.argmax(l))}
+    pen = O.repetition_penalty(l, seen, 1.5)
+    for u in (0.0, 0.3, 0.999):
+        assert O.select_eval(l, seen, 1.0, 1, 0.95, 1.5, u) == int(np.argmax(pen))
+    # top_k >= V and no penalty: the plain top-p rule
+    for u in (0.1, 0.5, 0.9):
+        assert O.select_eval(l, set(), 0.8, 500, 0.9, 1.0, u) == O.select_top_p(l, 0.8, 0.9, u)
+    # top_k keeps ties at the k-th value whole
+    t = np.array([1.0, 3.0, 2.0, 2.0, 0.5])
+    kept = {O.select_eval(t, set(), 1.0, 2, 1.0, 1.0, u) for u in np.linspace(0, 0.999, 200)}
+    assert kept == {1, 2, 3}
+
+
+def test_eval_sampler_worked_example():
+    # logits [ln 4, ln 2, ln 1, ln 8] with token 3 penalised by 1.5 (positive: divided),
+    # T = 1, top-k 3 keeps ids {0, 1, 3}: p ~ (4, 2, 8^(1/1.5) = 4) / 10; top-p 0.7:
+    # masses sorted 0.4, 0.4, 0.2 -> theta* = 0.4 (upper mass 0.8 >= 0.7), nucleus {0, 3},
+    # mass 0.8; u = 0.6 -> t = 0.48 -> running mass 0.4 (id 0), 0.8 (id 3) -> id 3
+    l = np.log(np.array([4.0, 2.0, 1.0, 8.0]))
+    assert O.select_eval(l, {3}, 1.0, 3, 0.7, 1.5, 0.6) == 3
+    assert O.select_eval(l, {3}, 1.0, 3, 0.7, 1.5, 0.3) == 0

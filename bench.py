@@ -112,7 +112,9 @@ def cpu_baseline(wl, accept_rate, budget_s=12.0):
                 rng.standard_normal((m2.n_kv_heads, T, m2.head_dim))] for _ in range(2)]
     orc = O.PipoOracle(W)
     orc.sampling = O.Sampling(tau=wl.tau, temperature=wl.temperature, top_p=wl.top_p,
-                              seeds=(wl.sample_seed_base,))
+                              seeds=(wl.sample_seed_base,), top_k=wl.top_k, rep_penalty=wl.rep_penalty)
+    from synth import rspec
+    orc.seen = [set(int(t) for t in rspec.prompt_tokens(1, wl.prompt_tokens, m2.vocab, wl.prompt_seed)[0])]
     mtp0 = [rng.standard_normal((m2.n_kv_heads, T, m2.head_dim)), rng.standard_normal((m2.n_kv_heads, T, m2.head_dim))]
     z = rng.standard_normal(m2.hidden)
     t_layers, t_heads, reps = [], [], 0
@@ -157,7 +159,7 @@ def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_
     def job(ev=None):
         if ev:
             ev[0].record(stream)
-        model.regular_prefill(prompts, wl.temperature, wl.top_p, seeds)
+        model.regular_prefill(prompts, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty)
         if ev:
             ev[1].record(stream)
         for s in range(steps):
@@ -206,6 +208,9 @@ def main():
     ap.add_argument("--no-regular", action="store_true", help="skip the regular-decoding baseline leg")
     ap.add_argument("--heads", choices=("linear", "paper"), default="linear",
                     help="linear: the workloads' one-linear heads; paper: the App. B forms of all three heads")
+    ap.add_argument("--sampler", choices=("workload", "eval"), default="workload",
+                    help="workload: the workload's own selection; eval: the paper's evaluation sampler "
+                         "(T 1.0, top-p 0.95, top-k 20, repetition penalty 1.5)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration) and exit")
     args = ap.parse_args()
@@ -236,6 +241,8 @@ def main():
         wl = replace(wl, decode_steps=args.decode_steps)
     if args.heads == "paper":
         wl = replace(wl, name=wl.name + "+appB-heads", model=replace(wl.model, heads=HEADS_PAPER))
+    if args.sampler == "eval":
+        wl = replace(wl, name=wl.name + "+eval-sampler", temperature=1.0, top_p=0.95, top_k=20, rep_penalty=1.5)
     m = wl.model
     B, steps = wl.batch, wl.decode_steps
     torch.cuda.set_device(0)
@@ -255,7 +262,8 @@ def main():
     def job(ev=None):
         if ev:
             ev[0].record(stream)
-        first, _, _ = model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds)
+        first, _, _ = model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k,
+                                    rep_penalty=wl.rep_penalty)
         if ev:
             ev[1].record(stream)
         for s in range(steps):
@@ -301,7 +309,9 @@ def main():
                    "heads_q_kv": [m.n_q_heads, m.n_kv_heads], "head_dim": m.head_dim, "vocab": m.vocab,
                    "batch": B, "prompt_tokens": wl.prompt_tokens, "latents": wl.latents,
                    "decode_steps": steps, "tau": wl.tau,
-                   "sampling": "greedy" if wl.temperature <= 0 else f"T{wl.temperature} top-p{wl.top_p}",
+                   "sampling": ("greedy" if wl.temperature <= 0 else f"T{wl.temperature} top-p{wl.top_p}"
+                                + (f" top-k{wl.top_k} rep-penalty{wl.rep_penalty}"
+                                   if wl.top_k or wl.rep_penalty != 1.0 else "")),
                    "parallelism": "none (1 GPU)"},
         "ttft_ms": round(ttft, 3),
         "decode": {"ms_per_pair_step": round(ms_step, 4), "pair_steps_per_s": round(1e3 / ms_step, 2),
@@ -315,7 +325,7 @@ def main():
     if not args.no_profile:
         psteps = min(steps, 16)
         model.profile(True)
-        model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds)
+        model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty)
         torch.cuda.synchronize()
         pre = model.profile_read()
         model.profile(True)

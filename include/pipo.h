@@ -82,7 +82,20 @@ typedef struct {
     float top_p;             /* nucleus mass in (0, 1]; used when temperature > 0   */
     const uint64_t *seeds;   /* host [batch] per-sequence sampler seeds; may be NULL
                                 when greedy                                          */
+    int32_t top_k;           /* sampling only: keep the tokens whose logit is at
+                                least the k-th largest (ties kept); 0 or >= vocab
+                                = off; negative: PIPO_EINVAL                        */
+    float rep_penalty;       /* sampling only, > 0: logits of penalised tokens are
+                                divided by it when positive, multiplied otherwise
+                                (1 = off)                                           */
 } pipo_sampling;
+/* With top_k > 0 or rep_penalty != 1, selection is the evaluation sampler of
+ * Sec. 4: repetition penalty, temperature, top-k, then top-p over the kept
+ * tokens, drawn as in the plain top-p sampler.  The penalised tokens of a
+ * sequence are its prompt's tokens and every token a decode step took as
+ * input (the first of the pair, and the second unless PAD); the draft of a
+ * pair also penalises that pair's backbone token.  Under greedy decoding
+ * (temperature <= 0) top_k must be 0 and rep_penalty 1 (else PIPO_EINVAL). */
 
 /* One pair step's result for one sequence (16 bytes). */
 typedef struct {

@@ -1,10 +1,28 @@
 // Output side of a pair step: the confidence gate and next-pair builder
-// (eq. 6 and the PAD fallback of Sec. 3.2), and temperature / top-p token
-// selection.
+// (eq. 6 and the PAD fallback of Sec. 3.2), and token selection: temperature
+// + top-p, and the evaluation sampler of Sec. 4 (repetition penalty,
+// temperature, top-k, top-p).
 #include "device_common.h"
 #include "kernels.h"
 
 namespace pipo {
+
+// Set token t's bit in a penalised-token bitmap row (ids outside [0, V) are
+// not tokens and are skipped).
+__device__ __forceinline__ void seen_set(uint32_t *row, int32_t t, int V) {
+    if (t >= 0 && t < V) atomicOr(row + (t >> 5), 1u << (t & 31));
+}
+
+__global__ __launch_bounds__(256) void k_seen_mark(const int32_t *tokens, int n, int V, uint32_t *seen,
+                                                   int seen_words) {
+    const int b = blockIdx.y;
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i < n) seen_set(seen + (int64_t)b * seen_words, tokens[(int64_t)b * n + i], V);
+}
+
+void launch_seen_mark(const int32_t *tokens, int n, int B, int V, uint32_t *seen, int seen_words, hipStream_t s) {
+    hipLaunchKernelGGL(k_seen_mark, dim3((n + 255) / 256, B), dim3(256), 0, s, tokens, n, V, seen, seen_words);
+}
 
 struct PairOut { int32_t tok_b, tok_d; float conf; int32_t accept; };
 
@@ -43,6 +61,11 @@ __global__ __launch_bounds__(512) void k_gate(GateParams p) {
         const int acc = c >= p.tau ? 1 : 0;
         const int32_t tb = argmax_key_id(p.best_b[b]);
         const int32_t td = argmax_key_id(p.best_d[b]);
+        if (p.seen) {   // the tokens this step took as input were emitted: later steps penalise them
+            uint32_t *row = p.seen + (int64_t)b * p.seen_words;
+            seen_set(row, p.pairs[2 * b], p.V);
+            if (p.pairs[2 * b + 1] != p.pad_id) seen_set(row, p.pairs[2 * b + 1], p.V);
+        }
         PairOut *o = (PairOut *)p.out + b;
         o->tok_b = tb;
         o->tok_d = td;
@@ -99,10 +122,12 @@ void launch_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V
 }
 
 // Step output: the selected token, which is also the next step's input.
+// With a bitmap, the step's input token joins the sequence's penalised set.
 __global__ void k_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_t pad_id, int32_t *pos,
-                              int32_t *step, int advance, int B) {
+                              int32_t *step, int advance, int B, uint32_t *seen, int seen_words, int V) {
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B) return;
+    if (seen) seen_set(seen + (int64_t)b * seen_words, pairs[2 * b], V);
     const int32_t t = argmax_key_id(best[b]);
     out_tok[b] = t;
     pairs[2 * b] = t;
@@ -113,9 +138,9 @@ __global__ void k_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, 
 }
 
 void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_t pad_id, int32_t *pos,
-                        int32_t *step, int advance, int B, hipStream_t s) {
+                        int32_t *step, int advance, int B, uint32_t *seen, int seen_words, int V, hipStream_t s) {
     hipLaunchKernelGGL(k_regular_out, dim3((B + 63) / 64), dim3(64), 0, s, best, out_tok, pairs, pad_id, pos, step,
-                       advance, B);
+                       advance, B, seen, seen_words, V);
 }
 
 // ---------------------------------------------------------------------------
@@ -129,6 +154,11 @@ void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_
 //   float bit patterns of e (positive floats order like their bits).
 //   nucleus N = {j : e_j >= theta*}, mass M; t = floor(u M); the token is the
 //   first id, scanning upwards through N, whose running mass exceeds t.
+// The evaluation sampler (EVAL) first replaces every penalised logit l by
+// l / theta_r if l > 0, else l theta_r (theta_r = rep_penalty), and with
+// top_k keeps the tokens whose penalised logit is at least the k-th largest
+// (ties kept): a 4-pass radix select for the k-th largest over an order-
+// preserving integer image of the floats; top-p then runs on the kept set.
 // ---------------------------------------------------------------------------
 constexpr int kSampThreads = 1024;
 
@@ -141,12 +171,19 @@ __device__ __forceinline__ uint64_t fixed_mass(float e) {
     return (uint64_t)__double2ull_rn((double)e * 1099511627776.0);   // 2^40
 }
 
+// Unsigned image of a float that orders like the float (-0 taken as +0).
+__device__ __forceinline__ uint32_t order_key(float f) {
+    const uint32_t u = __float_as_uint(f + 0.0f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
 // Wave w of the workgroup owns the contiguous ids [w R, (w + 1) R), R a
 // multiple of 256, read as 256-element sub-tiles (lane l: ids base + 4 l ..
 // base + 4 l + 3, one float4), so every pass is coalesced and id order is
 // (wave, sub-tile, lane, element).
 constexpr int kSampWaves = kSampThreads / 64;
 
+template <bool EVAL>
 __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
     __shared__ unsigned long long hist[kSampWaves][256];
     __shared__ float s_red[kSampWaves];
@@ -160,11 +197,33 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
     const int V = p.V;
     const int R = ((V + kSampWaves * 256 - 1) / (kSampWaves * 256)) * 256;   // ids per wave
     const int w0 = wave * R;
-    // the four logits of this lane in sub-tile t (ids past V read id 0, masked)
+    // penalised ids besides the bitmap: the step's input pair (the second
+    // unless PAD) and the extra token; -1: none
+    int ex0 = -1, ex1 = -1, ex2 = -1;
+    const uint32_t *seen = nullptr;
+    if constexpr (EVAL) {
+        if (p.seen) seen = p.seen + (int64_t)b * p.seen_words;
+        if (p.pairs) {
+            ex0 = p.pairs[2 * b];
+            ex1 = p.pairs[2 * b + 1] == p.pad_id ? -1 : p.pairs[2 * b + 1];
+        }
+        if (p.extra_key) ex2 = argmax_key_id(p.extra_key[b]);
+    }
+    // the four (penalised) logits of this lane in sub-tile t (ids past V read
+    // id 0, masked)
     auto load4 = [&](int t, float (&v)[4]) {
         const int id = w0 + t * 256 + 4 * lane;
         const float4 q = *(const float4 *)(lg + (id + 3 < V ? id : 0));
         v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+        if constexpr (EVAL) {
+            const uint32_t bits = (seen && id < V) ? seen[id >> 5] >> (id & 31) : 0u;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int j = id + e;
+                if (((bits >> e) & 1u) || j == ex0 || j == ex1 || j == ex2)
+                    v[e] = v[e] > 0.f ? v[e] / p.rep_penalty : v[e] * p.rep_penalty;
+            }
+        }
     };
     auto valid = [&](int t, int e) { return w0 + t * 256 + 4 * lane + e < V; };
     const int nt = R / 256;
@@ -184,13 +243,61 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
     for (int w = 1; w < kSampWaves; ++w) mx = fmaxf(mx, s_red[w]);
     const float kT = 1.4426950408889634f / p.temperature;
 
+    // top-k: kstar = image of the k-th largest penalised logit; kept = key >= kstar
+    uint32_t kstar = 0;
+    if constexpr (EVAL) {
+        if (p.top_k > 0 && p.top_k < V) {
+            __shared__ uint32_t s_kpre, s_krem;
+            if (tid == 0) { s_kpre = 0; s_krem = (uint32_t)p.top_k; }
+            for (int pass = 0; pass < 4; ++pass) {
+                const int shift = 24 - 8 * pass;
+                for (int i = tid; i < kSampWaves * 256; i += kSampThreads) (&hist[0][0])[i] = 0;
+                __syncthreads();
+                const uint32_t prefix = s_kpre;
+#pragma unroll 2
+                for (int t = 0; t < nt; ++t) {
+                    float v[4];
+                    load4(t, v);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t key = order_key(v[e]);
+                        if (valid(t, e) && (pass == 0 || (key >> (shift + 8)) == prefix))
+                            atomicAdd(&hist[wave][(key >> shift) & 255u], 1ull);
+                    }
+                }
+                __syncthreads();
+                if (tid < 256) {
+                    unsigned long long h = 0;
+                    for (int w = 0; w < kSampWaves; ++w) h += hist[w][tid];
+                    hist[0][tid] = h;
+                }
+                __syncthreads();
+                if (tid == 0) {   // the digit holding the rank-krem element, counting down
+                    uint32_t rem = s_krem;
+                    int d = 255;
+                    for (; d > 0; --d) {
+                        if (hist[0][d] >= rem) break;
+                        rem -= (uint32_t)hist[0][d];
+                    }
+                    s_kpre = (prefix << 8) | (uint32_t)d;
+                    s_krem = rem;
+                }
+                __syncthreads();
+            }
+            kstar = s_kpre;
+        }
+    }
+    // kept: in the vocabulary and, with top-k, at least the k-th largest
+    auto kept = [&](int t, int e, float v) { return valid(t, e) && (!EVAL || order_key(v) >= kstar); };
+
     unsigned long long tot = 0;
 #pragma unroll 4
     for (int t = 0; t < nt; ++t) {
         float v[4];
         load4(t, v);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) tot += valid(t, e) ? fixed_mass(__builtin_amdgcn_exp2f((v[e] - mx) * kT)) : 0ull;
+        for (int e = 0; e < 4; ++e)
+            tot += kept(t, e, v[e]) ? fixed_mass(__builtin_amdgcn_exp2f((v[e] - mx) * kT)) : 0ull;
     }
     for (int o = 32; o > 0; o >>= 1) {
         const uint32_t lo = __shfl_xor((uint32_t)tot, o), hi = __shfl_xor((uint32_t)(tot >> 32), o);
@@ -216,7 +323,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
             for (int e = 0; e < 4; ++e) {
                 const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
                 const uint32_t key = __float_as_uint(ev);
-                if (valid(t, e) && (pass == 0 || (key >> (shift + 8)) == prefix))
+                if (kept(t, e, v[e]) && (pass == 0 || (key >> (shift + 8)) == prefix))
                     atomicAdd(&hist[wave][(key >> shift) & 255u], fixed_mass(ev));
             }
         }
@@ -234,7 +341,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
                 if ((double)(above + hist[0][k]) >= target) { beta = k; break; }
                 above += hist[0][k];
             }
-            if (beta < 0) {   // no value reaches top_p (rounding): every token
+            if (beta < 0) {   // no value reaches top_p (rounding): every kept token
                 s_all = 1;
                 beta = 0;
                 above = s_above;
@@ -264,7 +371,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
-            wm += (valid(t, e) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
+            wm += (kept(t, e, v[e]) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
         }
     }
     for (int o = 32; o > 0; o >>= 1) {
@@ -285,7 +392,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
-            m4[e] = (valid(t, e) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
+            m4[e] = (kept(t, e, v[e]) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
             loc += m4[e];
         }
         unsigned long long inc = loc;
@@ -311,7 +418,10 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
 }
 
 void launch_sample(const SampleParams &p, hipStream_t s) {
-    hipLaunchKernelGGL(k_sample, dim3(p.B), dim3(kSampThreads), 0, s, p);
+    if (p.top_k > 0 || p.rep_penalty != 1.f)
+        hipLaunchKernelGGL(k_sample<true>, dim3(p.B), dim3(kSampThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(k_sample<false>, dim3(p.B), dim3(kSampThreads), 0, s, p);
 }
 
 }  // namespace pipo

@@ -87,6 +87,8 @@ struct GateParams {
     void *out;                  // pipo_pair [B]
     int32_t *pairs, *pos, *step; int advance;
     int B;
+    uint32_t *seen; int seen_words;   // non-NULL: the input pair's tokens join the penalised-token bitmap
+    int V;
 };
 void launch_gate(const GateParams &p, hipStream_t s);
 
@@ -94,13 +96,21 @@ void launch_gate(const GateParams &p, hipStream_t s);
 void launch_embed_step(const int32_t *pairs, const uint16_t *embed, int H, int V, float *x, float *ss, int B,
                        int both, hipStream_t s);
 void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_t pad_id, int32_t *pos,
-                        int32_t *step, int advance, int B, hipStream_t s);
+                        int32_t *step, int advance, int B, uint32_t *seen, int seen_words, int V, hipStream_t s);
+// Penalised-token bitmaps [B][seen_words] (bit t of word t/32: token t):
+// set the bit of every prompt token (ids outside [0, V) are skipped).
+void launch_seen_mark(const int32_t *tokens, int n, int B, int V, uint32_t *seen, int seen_words, hipStream_t s);
 
 struct SampleParams {
     const float *logits; int V; int B;
     float temperature, top_p;
     const uint64_t *seeds; const int32_t *step; int slot;
     uint64_t *best;
+    // the evaluation sampler, when top_k > 0 or rep_penalty != 1
+    int top_k; float rep_penalty;
+    const uint32_t *seen; int seen_words;   // penalised tokens per sequence
+    const int32_t *pairs; int32_t pad_id;   // the step's input pair, also penalised (NULL: none)
+    const uint64_t *extra_key;              // argmax key of one more penalised token (NULL: none)
 };
 void launch_sample(const SampleParams &p, hipStream_t s);
 

@@ -69,6 +69,7 @@ struct pipo_ctx {
     int n_cu;             // compute units: workgroups of the batch-1 GEMV
     uint64_t *best_b, *best_d, *seeds;
     int32_t *pairs, *pos, *step;
+    uint32_t *seen; int seen_words;   // penalised-token bitmap per sequence (evaluation sampler)
     pipo_pair *out;
     // prefill activations
     uint16_t *p_xin, *p_xn, *p_xn_lo, *p_q, *p_o, *p_o_lo, *p_act, *p_act_lo;
@@ -85,6 +86,8 @@ struct pipo_ctx {
     hipGraphExec_t graph_reg = nullptr;
     bool graph_reg_dirty = true;
     float tau = 0.5f, temperature = 0.f, top_p = 1.f;
+    int top_k = 0; float rep_penalty = 1.f;
+    bool eval_smp = false;          // top-k or repetition penalty in use
 
     hipGraphExec_t graph = nullptr;
     bool graph_dirty = true;
@@ -281,6 +284,8 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->best_d = a.take<uint64_t>(B);
         c->seeds = a.take<uint64_t>(B);
         c->pairs = a.take<int32_t>(2 * B);
+        c->seen_words = (V + 31) / 32;
+        c->seen = a.take<uint32_t>((int64_t)B * c->seen_words);
         c->pos = a.take<int32_t>(B);
         c->step = a.take<int32_t>(B);
         c->out = a.take<pipo_pair>(B);
@@ -430,11 +435,29 @@ static void enqueue_layers(pipo_ctx *c, hipStream_t s) {
                       c->vc + (int64_t)l * c->Bmax * c->kv_bstride, c->x, c->ss_x, s);
 }
 
+// Selection of one slot's tokens from `logits` into `best`.  `in_pair`: the
+// step's input pair is in c->pairs (a decode step, not a prefill); `extra`:
+// the argmax key of one more token the repetition penalty applies to.
+static SampleParams sample_params(pipo_ctx *c, const float *logits, int B, int slot, uint64_t *best, bool in_pair,
+                                  const uint64_t *extra) {
+    SampleParams sp{};
+    sp.logits = logits; sp.V = c->V; sp.B = B; sp.temperature = c->temperature; sp.top_p = c->top_p;
+    sp.seeds = c->seeds; sp.step = c->step; sp.slot = slot; sp.best = best;
+    sp.top_k = c->top_k; sp.rep_penalty = c->rep_penalty;
+    if (c->eval_smp) {
+        sp.seen = c->seen; sp.seen_words = c->seen_words;
+        sp.pairs = in_pair ? c->pairs : nullptr; sp.pad_id = c->pad_id;
+        sp.extra_key = extra;
+    }
+    return sp;
+}
+
 // ---------------------------------------------------------------------------
 // The heads of a pair step (eqs. 3-6): LM head + selection of the backbone
 // token, MTP head, LM head + selection of the draft, confidence gate.
-// `nss` is the number of sum-of-squares parts describing x (h_b).
-static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t s) {
+// `nss` is the number of sum-of-squares parts describing x (h_b); `in_pair`:
+// a decode step, whose input pair joins the penalised tokens.
+static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, bool in_pair, hipStream_t s) {
     const int H = c->H;
     const bool greedy = c->temperature <= 0.f;
     GemvParams p{};
@@ -445,9 +468,8 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
     { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
-        SampleParams sp{c->logits_b, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 0, c->best_b};
         PROF(PIPO_K_SAMPLE);
-        launch_sample(sp, s);
+        launch_sample(sample_params(c, c->logits_b, B, 0, c->best_b, in_pair, nullptr), s);
     }
     // MTP head: W_fc [RMSNorm(h_b; g_mh); RMSNorm(E[b]; g_me)]
     GemvParams m{};
@@ -468,9 +490,9 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     q.out = c->logits_d; q.best = greedy ? c->best_d : nullptr;
     { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(q, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
-        SampleParams sp{c->logits_d, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 1, c->best_d};
+        // the draft's penalised set also holds its pair's backbone token
         PROF(PIPO_K_SAMPLE);
-        launch_sample(sp, s);
+        launch_sample(sample_params(c, c->logits_d, B, 1, c->best_d, in_pair, c->best_b), s);
     }
     GateParams gp{};
     if (c->heads & PIPO_HEADS_MLP_CONFIDENCE) {
@@ -486,6 +508,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t 
     gp.w_conf = c->w_conf; gp.g_conf = c->g_conf; gp.H = H; gp.eps = c->cfg.rms_eps; gp.tau = c->tau;
     gp.best_b = c->best_b; gp.best_d = c->best_d; gp.pad_id = c->pad_id; gp.out = c->out;
     gp.pairs = c->pairs; gp.pos = c->pos; gp.step = c->step; gp.advance = advance; gp.B = B;
+    if (c->eval_smp && in_pair) { gp.seen = c->seen; gp.seen_words = c->seen_words; gp.V = c->V; }
     PROF(PIPO_K_GATE);
     launch_gate(gp, s);
 }
@@ -509,7 +532,7 @@ static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
         launch_gemv(p, PRO_PAIR, EPI_STORE, s);
     }
     enqueue_layers(c, s);
-    enqueue_heads(c, B, H / 16, 1, s);
+    enqueue_heads(c, B, H / 16, 1, true, s);
 }
 
 static int check_sampling(pipo_ctx *c, const pipo_sampling *smp, int batch) {
@@ -518,6 +541,10 @@ static int check_sampling(pipo_ctx *c, const pipo_sampling *smp, int batch) {
     if (smp->temperature > 0.f) {
         if (!(smp->top_p > 0.f && smp->top_p <= 1.f)) return fail(c, PIPO_EINVAL, "top_p must be in (0, 1]");
         if (!smp->seeds) return fail(c, PIPO_EINVAL, "sampling needs per-sequence seeds");
+        if (smp->top_k < 0) return fail(c, PIPO_EINVAL, "top_k must be >= 0");
+        if (!(smp->rep_penalty > 0.f)) return fail(c, PIPO_EINVAL, "rep_penalty must be > 0");
+    } else if (smp->top_k != 0 || smp->rep_penalty != 1.f) {
+        return fail(c, PIPO_EINVAL, "top_k and rep_penalty apply to sampling (temperature > 0) only");
     }
     (void)batch;
     return PIPO_OK;
@@ -549,7 +576,8 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
                     c->cfg.max_latent);
     HIP_TRY(c, hipGetLastError());
 
-    if (c->batch != batch || c->tau != smp->tau || c->temperature != smp->temperature || c->top_p != smp->top_p) {
+    if (c->batch != batch || c->tau != smp->tau || c->temperature != smp->temperature || c->top_p != smp->top_p ||
+        c->top_k != smp->top_k || c->rep_penalty != smp->rep_penalty) {
         c->graph_dirty = true;
         c->graph_reg_dirty = true;
     }
@@ -557,6 +585,14 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     c->tau = smp->tau;
     c->temperature = smp->temperature;
     c->top_p = smp->top_p;
+    c->top_k = smp->top_k;
+    c->rep_penalty = smp->rep_penalty;
+    c->eval_smp = smp->temperature > 0.f && (smp->top_k > 0 || smp->rep_penalty != 1.f);
+    if (c->eval_smp) {   // the prompt's tokens start each sequence's penalised set
+        PROF(PIPO_K_PREFILL_MISC);
+        launch_fill_u32(c->seen, 0u, (int64_t)batch * c->seen_words, s);
+        launch_seen_mark(d_tokens, n, batch, c->V, c->seen, c->seen_words, s);
+    }
     if (smp->temperature > 0.f) {
         HIP_TRY(c, hipEventSynchronize(c->seeds_done));
         memcpy(c->h_seeds, smp->seeds, sizeof(uint64_t) * batch);
@@ -659,7 +695,7 @@ extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     c->prefilled = false;
     int rc = prefill_backbone(c, batch, d_tokens, n, smp, false, s);
     if (rc) return rc;
-    enqueue_heads(c, batch, c->H / 16, 1, s);
+    enqueue_heads(c, batch, c->H / 16, 1, false, s);
     HIP_TRY(c, hipGetLastError());
     rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
     if (rc) return rc;
@@ -670,7 +706,7 @@ extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
 
 // Regular decoding's heads: eq. 3 alone (tied LM head on RMSNorm(h; g_final),
 // greedy or top-p in sampler slot 0), then the token becomes the next input.
-static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, hipStream_t s) {
+static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, bool in_tok, hipStream_t s) {
     const bool greedy = c->temperature <= 0.f;
     GemvParams p{};
     p.B = B; p.eps = c->cfg.rms_eps; p.H = c->H; p.xh = c->xh; p.xl = c->xl; p.part = c->gpart; p.part_cap = c->gpart_cap;
@@ -679,12 +715,13 @@ static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, hipS
     p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
     { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
-        SampleParams sp{c->logits_b, c->V, B, c->temperature, c->top_p, c->seeds, c->step, 0, c->best_b};
         PROF(PIPO_K_SAMPLE);
-        launch_sample(sp, s);
+        launch_sample(sample_params(c, c->logits_b, B, 0, c->best_b, in_tok, nullptr), s);
     }
     PROF(PIPO_K_GATE);
-    launch_regular_out(c->best_b, c->out_tok, c->pairs, c->pad_id, c->pos, c->step, advance, B, s);
+    const bool mark = c->eval_smp && in_tok;   // the step's input token joins the penalised set
+    launch_regular_out(c->best_b, c->out_tok, c->pairs, c->pad_id, c->pos, c->step, advance, B,
+                       mark ? c->seen : nullptr, c->seen_words, c->V, s);
 }
 
 // One regular decoding step: x = E[token] at the next position, the same
@@ -693,7 +730,7 @@ static void enqueue_regular_decode(pipo_ctx *c, hipStream_t s) {
     const int B = c->batch, H = c->H;
     { PROF(PIPO_K_GATE); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 0, s); }
     enqueue_layers(c, s);
-    enqueue_regular_heads(c, B, H / 16, 1, s);
+    enqueue_regular_heads(c, B, H / 16, 1, true, s);
 }
 
 static int copy_tokens(pipo_ctx *c, int32_t *d_tok, float *d_logits, hipStream_t s) {
@@ -711,7 +748,7 @@ extern "C" int pipo_regular_prefill(pipo_ctx *c, int32_t batch, const int32_t *d
     c->prefilled = false;
     int rc = prefill_backbone(c, batch, d_tokens, n, smp, true, s);
     if (rc) return rc;
-    enqueue_regular_heads(c, batch, c->H / 16, 1, s);
+    enqueue_regular_heads(c, batch, c->H / 16, 1, false, s);
     HIP_TRY(c, hipGetLastError());
     rc = copy_tokens(c, d_tok, d_logits, s);
     if (rc) return rc;

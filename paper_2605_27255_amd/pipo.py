@@ -38,7 +38,8 @@ class PipoConfig(ctypes.Structure):
 
 class PipoSampling(ctypes.Structure):
     _fields_ = [("tau", ctypes.c_float), ("temperature", ctypes.c_float), ("top_p", ctypes.c_float),
-                ("seeds", ctypes.POINTER(ctypes.c_uint64))]
+                ("seeds", ctypes.POINTER(ctypes.c_uint64)), ("top_k", ctypes.c_int32),
+                ("rep_penalty", ctypes.c_float)]
 
 
 class PipoPair(ctypes.Structure):
@@ -120,12 +121,13 @@ class PipoModel:
         return out, lb, ld
 
     @staticmethod
-    def _sampling(tau, temperature, top_p, seeds):
+    def _sampling(tau, temperature, top_p, seeds, top_k=0, rep_penalty=1.0):
         seed_arr = None
         if seeds is not None:
             seed_arr = (ctypes.c_uint64 * len(seeds))(*[int(s) for s in seeds])
         smp = PipoSampling(tau, temperature, top_p,
-                           ctypes.cast(seed_arr, ctypes.POINTER(ctypes.c_uint64)) if seed_arr else None)
+                           ctypes.cast(seed_arr, ctypes.POINTER(ctypes.c_uint64)) if seed_arr else None,
+                           int(top_k), float(rep_penalty))
         return smp, seed_arr
 
     def _tokens(self, tokens):
@@ -134,10 +136,10 @@ class PipoModel:
         return tokens.shape
 
     def prefill(self, tokens, tau: float, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
-                logits: bool = False):
+                logits: bool = False, top_k: int = 0, rep_penalty: float = 1.0):
         """tokens: int32 CUDA tensor [B, n].  Returns (pairs [B,4] int32, logits_b, logits_d)."""
         B, n = self._tokens(tokens)
-        smp, _keep = self._sampling(tau, temperature, top_p, seeds)
+        smp, _keep = self._sampling(tau, temperature, top_p, seeds, top_k, rep_penalty)
         out, lb, ld = self._outputs(B, logits)
         self._check(self.lib.pipo_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(out),
                                           _ptr(lb), _ptr(ld), self._stream()))
@@ -158,11 +160,11 @@ class PipoModel:
                                               _ptr(logits_d), self._stream()))
 
     def regular_prefill(self, tokens, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
-                        logits: bool = False):
+                        logits: bool = False, top_k: int = 0, rep_penalty: float = 1.0):
         """Regular decoding's prefill over the n prompt tokens.  Returns (tok [B] int32, logits)."""
         t = self.torch
         B, n = self._tokens(tokens)
-        smp, _keep = self._sampling(0.0, temperature, top_p, seeds)
+        smp, _keep = self._sampling(0.0, temperature, top_p, seeds, top_k, rep_penalty)
         tok = t.empty(B, dtype=t.int32, device="cuda")
         lg = t.empty((B, self.model.vocab), dtype=t.float32, device="cuda") if logits else None
         self._check(self.lib.pipo_regular_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(tok),

@@ -103,6 +103,8 @@ class Workload:
     tau: float
     temperature: float = 0.0     # <= 0: greedy
     top_p: float = 1.0
+    top_k: int = 0               # evaluation sampler (Sec. 4): 0 = off
+    rep_penalty: float = 1.0     # evaluation sampler: 1 = off
     prefill_chunk: int = 4096    # latent positions per prefill chunk
     weight_precision: str = "bf16"   # precision of the stored weights
     seed: int = 0

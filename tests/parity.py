@@ -14,7 +14,8 @@ output is compared:
   either answer is correct for); then the step is counted as ambiguous, and
   the GPU token must still be the argmax of the GPU's own logits;
 * sampled tokens: equal, or else the oracle's selection rule applied to the
-  GPU's logits must give the GPU token (a boundary case moved by logit error).
+  GPU's logits must give the GPU token (a boundary case moved by logit error);
+  the evaluation sampler's rule takes the oracle's penalised set of that step.
 """
 from __future__ import annotations
 
@@ -39,6 +40,7 @@ class ParityReport:
     max_conf_err: float = 0.0
     ambiguous_tokens: int = 0
     ambiguous_accepts: int = 0
+    penalty_decisive: int = 0   # rows whose oracle token the repetition penalty changed
     failures: list = field(default_factory=list)
 
     def check(self):
@@ -50,7 +52,17 @@ def _row_err(gpu_row, ref_row):
     return float(d.max()), float(d.sum() / np.abs(ref_row).sum())
 
 
-def _check_token(rep, tag, gpu_tok, ref_tok, gpu_row, ref_row, max_abs, smp, u):
+def _rule(smp, u, seen):
+    """The oracle's selection rule for one row (sampling only)."""
+    if smp.top_k or smp.rep_penalty != 1.0:
+        return lambda row: O.select_eval(row, seen, smp.temperature, smp.top_k, smp.top_p, smp.rep_penalty, u)
+    return lambda row: O.select_top_p(row, smp.temperature, smp.top_p, u)
+
+
+def _check_token(rep, tag, gpu_tok, ref_tok, gpu_row, ref_row, max_abs, smp, u, seen=()):
+    if smp.temperature > 0 and smp.rep_penalty != 1.0:
+        plain = O.select_eval(ref_row, (), smp.temperature, smp.top_k, smp.top_p, 1.0, u)
+        rep.penalty_decisive += int(plain != ref_tok)
     if gpu_tok == ref_tok:
         return
     if smp.temperature <= 0:
@@ -61,7 +73,7 @@ def _check_token(rep, tag, gpu_tok, ref_tok, gpu_row, ref_row, max_abs, smp, u):
         rep.failures.append(f"{tag}: token {gpu_tok} != oracle {ref_tok} (margin {margin:.3g}, "
                             f"max_abs {max_abs:.3g})")
     else:
-        again = O.select_top_p(gpu_row.astype(np.float64), smp.temperature, smp.top_p, u)
+        again = _rule(smp, u, seen)(gpu_row.astype(np.float64))
         if again == gpu_tok:
             rep.ambiguous_tokens += 1
             return
@@ -69,7 +81,7 @@ def _check_token(rep, tag, gpu_tok, ref_tok, gpu_row, ref_row, max_abs, smp, u):
 
 
 def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=LOGIT_MEAN_REL, conf_tol=CONF_TOL,
-                 max_abs_tol=LOGIT_MAX_ABS):
+                 max_abs_tol=LOGIT_MAX_ABS, seen=None):
     tok_b, tok_d, conf, acc = out_np
     rep.steps += 1
     for i, r in enumerate(recs):
@@ -85,8 +97,11 @@ def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=
         u_d = rspec.uniform_draw(seeds[i], step, 1) if smp.temperature > 0 else None
         ma_b, _ = _row_err(lb[i], r["logits_b"])
         ma_d, _ = _row_err(ld[i], r["logits_d"])
-        _check_token(rep, t + " backbone", int(tok_b[i]), r["tok_b"], lb[i], r["logits_b"], ma_b, smp, u_b)
-        _check_token(rep, t + " draft", int(tok_d[i]), r["tok_d"], ld[i], r["logits_d"], ma_d, smp, u_d)
+        sb = seen[i] if seen is not None else set()
+        _check_token(rep, t + " backbone", int(tok_b[i]), r["tok_b"], lb[i], r["logits_b"], ma_b, smp, u_b, sb)
+        # the draft penalises its pair's backbone token too (the GPU's, which the oracle was forced to)
+        _check_token(rep, t + " draft", int(tok_d[i]), r["tok_d"], ld[i], r["logits_d"], ma_d, smp, u_d,
+                     sb | {int(tok_b[i])})
         ce = abs(float(conf[i]) - r["conf"])
         rep.max_conf_err = max(rep.max_conf_err, ce)
         if ce > conf_tol:
@@ -111,7 +126,8 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
     seeds = list(smp.seeds) if smp.seeds else [0] * B
     tokens = torch.from_numpy(np.ascontiguousarray(prompts, dtype=np.int32)).cuda()
     outs = [gpu_model.prefill(tokens, smp.tau, smp.temperature, smp.top_p,
-                              seeds if smp.temperature > 0 else None, logits=True)]
+                              seeds if smp.temperature > 0 else None, logits=True, top_k=smp.top_k,
+                              rep_penalty=smp.rep_penalty)]
     for _ in range(steps):
         outs.append(gpu_model.decode_step(logits=True))
     torch.cuda.synchronize()
@@ -127,10 +143,12 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
             prev = host[s - 1][0]
             pairs = [(int(prev[0][i]), int(prev[1][i]) if prev[3][i] else W.cfg.pad_id) for i in range(B)]
             recs = orc.decode_step(in_pairs=pairs, force_b=force)
-        compare_step(rep, f"step {s}", o, lb, ld, recs, smp, seeds, s, mean_rel_tol, conf_tol, max_abs_tol)
+        compare_step(rep, f"step {s}", o, lb, ld, recs, smp, seeds, s, mean_rel_tol, conf_tol, max_abs_tol,
+                     seen=[set(x) for x in orc.seen])
     log(f"parity: steps {rep.steps} rows {rep.rows} max_abs {rep.max_abs:.3g} "
         f"max_mean_rel {rep.max_mean_rel:.3g} conf_err {rep.max_conf_err:.3g} "
-        f"ambiguous tokens {rep.ambiguous_tokens} accepts {rep.ambiguous_accepts}")
+        f"ambiguous tokens {rep.ambiguous_tokens} accepts {rep.ambiguous_accepts} "
+        f"penalty-decisive {rep.penalty_decisive}")
     return rep, host
 
 
@@ -144,7 +162,8 @@ def run_regular_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_to
     seeds = list(smp.seeds) if smp.seeds else [0] * B
     tokens = torch.from_numpy(np.ascontiguousarray(prompts, dtype=np.int32)).cuda()
     outs = [gpu_model.regular_prefill(tokens, smp.temperature, smp.top_p,
-                                      seeds if smp.temperature > 0 else None, logits=True)]
+                                      seeds if smp.temperature > 0 else None, logits=True, top_k=smp.top_k,
+                                      rep_penalty=smp.rep_penalty)]
     for _ in range(steps):
         outs.append(gpu_model.regular_step(logits=True))
     torch.cuda.synchronize()
@@ -164,7 +183,8 @@ def run_regular_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_to
             if ma > LOGIT_MAX_ABS or mr > mean_rel_tol:
                 rep.failures.append(f"{t} logits: max_abs {ma:.3g} mean_rel {mr:.3g}")
             u = rspec.uniform_draw(seeds[i], s, 0) if smp.temperature > 0 else None
-            _check_token(rep, t, int(tok[i]), r["tok"], lg[i], r["logits"], ma, smp, u)
+            _check_token(rep, t, int(tok[i]), r["tok"], lg[i], r["logits"], ma, smp, u, set(orc.seen[i]))
     log(f"regular parity: steps {rep.steps} rows {rep.rows} max_abs {rep.max_abs:.3g} "
-        f"max_mean_rel {rep.max_mean_rel:.3g} ambiguous tokens {rep.ambiguous_tokens}")
+        f"max_mean_rel {rep.max_mean_rel:.3g} ambiguous tokens {rep.ambiguous_tokens} "
+        f"penalty-decisive {rep.penalty_decisive}")
     return rep, host

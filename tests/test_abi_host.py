@@ -42,9 +42,9 @@ def test_struct_layout_matches_header(tmp_path):
 #include <stddef.h>
 #include "{HEADER}"
 int main(void) {{
-  printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(pipo_config), sizeof(pipo_sampling), sizeof(pipo_pair),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(pipo_config), sizeof(pipo_sampling), sizeof(pipo_pair),
          offsetof(pipo_config, gain_mode), offsetof(pipo_sampling, seeds), offsetof(pipo_pair, accept),
-         offsetof(pipo_config, heads));
+         offsetof(pipo_config, heads), offsetof(pipo_sampling, top_k), offsetof(pipo_sampling, rep_penalty));
   return 0;
 }}''')
     exe = tmp_path / "layout"
@@ -52,7 +52,8 @@ int main(void) {{
     got = list(map(int, subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()))
     assert got == [ctypes.sizeof(pipo.PipoConfig), ctypes.sizeof(pipo.PipoSampling), ctypes.sizeof(pipo.PipoPair),
                    pipo.PipoConfig.gain_mode.offset, pipo.PipoSampling.seeds.offset, pipo.PipoPair.accept.offset,
-                   pipo.PipoConfig.heads.offset]
+                   pipo.PipoConfig.heads.offset, pipo.PipoSampling.top_k.offset,
+                   pipo.PipoSampling.rep_penalty.offset]
     assert got[2] == 16
 
 

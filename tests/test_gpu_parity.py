@@ -435,3 +435,78 @@ def test_tiny_top_p_floor_is_greedy(torch):
         np.testing.assert_array_equal(gb, sb)
         np.testing.assert_array_equal(gd, sd)
     m.close()
+
+
+# ------------------------------------------- the evaluation sampler (Sec. 4)
+
+def _eval_smp(B, tau=0.5, base=500):
+    """The paper's evaluation settings: T 1.0, top-p 0.95, top-k 20, repetition penalty 1.5."""
+    return O.Sampling(tau=tau, temperature=1.0, top_p=0.95, seeds=tuple(base + b for b in range(B)), top_k=20,
+                      rep_penalty=1.5)
+
+
+def test_tiny_eval_sampler_parity(torch):
+    """Pair path, batch 3, odd prompt, 8 steps: penalised set = prompt + input
+    pairs (+ the pair's backbone token for the draft), top-k 20 over 4096."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    B, n, steps = 3, 41, 8
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=40)
+    m = _model(cfg, seed=5, max_batch=4, max_latent=21 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(cfg, seed=5, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, _eval_smp(B), log)
+    rep.check()
+    assert rep.penalty_decisive > 0      # the penalty changed some draws: the test can see it
+    assert rep.ambiguous_tokens <= rep.rows // 10
+    m.close()
+
+
+def test_tiny_regular_eval_sampler_parity(torch):
+    B, n, steps = 2, 25, 8
+    prompts = rspec.prompt_tokens(B, n, TINY.vocab, seed=41)
+    m = _model(TINY, seed=6, max_batch=2, max_latent=n + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(TINY, seed=6, precision="bf16")
+    rep, _ = run_regular_parity(m, W, prompts, steps, _eval_smp(B, tau=0.0), log)
+    rep.check()
+    assert rep.penalty_decisive > 0
+    assert rep.ambiguous_tokens <= rep.rows // 10
+    m.close()
+
+
+def test_4b_width_eval_sampler_parity(torch):
+    """Full 151936-token vocabulary, two layers, batch 4: the radix top-k and
+    the bitmap over every vocabulary tile."""
+    cfg = DENSE_4B.with_layers(2)
+    B, n, steps = 4, 64, 3
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=42)
+    m = _model(cfg, seed=4, max_batch=4, max_latent=32 + steps + 1, prefill_chunk=4096)
+    W = O.OracleWeights.generate(cfg, seed=4, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, _eval_smp(B, tau=0.7), log)
+    rep.check()
+    m.close()
+
+
+def test_tiny_eval_sampler_top1_is_greedy_and_bad_settings(torch):
+    """top-k 1 without a penalty keeps only the argmax, so it must return the
+    greedy tokens (pair and regular paths); invalid settings are refused."""
+    from paper_2605_27255_amd import unpack_pairs, PipoError, PIPO_EINVAL
+    prompts = rspec.prompt_tokens(2, 30, TINY.vocab, seed=43)
+    m = _model(TINY, seed=4, max_batch=2, max_latent=40, prefill_chunk=16)
+    t = torch.from_numpy(prompts).cuda()
+    greedy = [m.prefill(t, 0.5)[0]] + [m.decode_step()[0] for _ in range(4)]
+    top1 = [m.prefill(t, 0.5, temperature=1.0, seeds=[5, 6], top_k=1)[0]] + [m.decode_step()[0] for _ in range(4)]
+    rg = [m.regular_prefill(t)[0]] + [m.regular_step()[0] for _ in range(4)]
+    r1 = [m.regular_prefill(t, temperature=1.0, seeds=[5, 6], top_k=1)[0]] + [m.regular_step()[0] for _ in range(4)]
+    torch.cuda.synchronize()
+    for g, s_ in zip(greedy, top1):
+        gb, gd, _, _ = unpack_pairs(g)
+        sb, sd, _, _ = unpack_pairs(s_)
+        np.testing.assert_array_equal(gb, sb)
+        np.testing.assert_array_equal(gd, sd)
+    for g, s_ in zip(rg, r1):
+        np.testing.assert_array_equal(g.cpu().numpy(), s_.cpu().numpy())
+    for kw in (dict(temperature=1.0, seeds=[1, 2], top_k=-1), dict(temperature=1.0, seeds=[1, 2], rep_penalty=0.0),
+               dict(top_k=5), dict(rep_penalty=1.5)):
+        with pytest.raises(PipoError) as e:
+            m.prefill(t, 0.5, **kw)
+        assert e.value.code == PIPO_EINVAL
+    m.close()

@@ -124,6 +124,18 @@ int pipo_prefill(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, int32_t 
                  const pipo_sampling *smp, pipo_pair *d_out,
                  float *d_logits_b, float *d_logits_d, void *stream);
 
+/* Ragged batch (the serving shape of Sec. 4: requests of different prompt
+ * lengths decoded together): as pipo_prefill, but sequence i's prompt is the
+ * first lens[i] tokens of row i of d_tokens (device int32 [batch][stride]),
+ * lens a host int32 [batch] array read before the call returns, each in
+ * [1, stride].  Sequence i gets ceil(lens[i]/2) latents; its pair steps then
+ * run at its own positions.  Errors: as pipo_prefill, PIPO_EINVAL for a NULL
+ * lens or a length outside [1, stride], PIPO_ECAPACITY when the longest
+ * prompt's latents + 1 exceed max_latent. */
+int pipo_prefill_ragged(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, int32_t stride,
+                        const int32_t *lens, const pipo_sampling *smp, pipo_pair *d_out,
+                        float *d_logits_b, float *d_logits_d, void *stream);
+
 /* One pair-decode step for every sequence of the last prefill.  The input
  * pair is d_in_pairs (device int32 [batch][2]) when non-NULL (teacher
  * forcing), else the pair the previous call produced on the device:
@@ -147,6 +159,13 @@ int pipo_decode_step(pipo_ctx *ctx, const int32_t *d_in_pairs, pipo_pair *d_out,
 int pipo_regular_prefill(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, int32_t n,
                          const pipo_sampling *smp, int32_t *d_tok, float *d_logits,
                          void *stream);
+
+/* Ragged regular prefill: as pipo_regular_prefill with sequence i's prompt
+ * the first lens[i] tokens of row i of d_tokens ([batch][stride]); lens as in
+ * pipo_prefill_ragged. */
+int pipo_regular_prefill_ragged(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, int32_t stride,
+                                const int32_t *lens, const pipo_sampling *smp, int32_t *d_tok,
+                                float *d_logits, void *stream);
 
 /* One regular decoding step: feed one token per sequence, append one
  * position, emit the next token.  The input is d_in_tok (device int32

@@ -441,9 +441,10 @@ class PipoOracle:
         self.sampling = sampling
         W, cfg = self.W, self.cfg
         self.caches, self.length, self.step_idx, self.next_pairs, self.mtp_caches = [], [], [], [], []
-        self.seen = [set(int(t) for t in p) for p in np.asarray(prompts)]   # tokens the penalty applies to
+        prompts = [np.asarray(p) for p in prompts]   # a ragged batch: prompts of their own lengths
+        self.seen = [set(int(t) for t in p) for p in prompts]   # tokens the penalty applies to
         out = []
-        for i, prompt in enumerate(np.asarray(prompts)):
+        for i, prompt in enumerate(prompts):
             pairs = prompt_pairs(prompt, cfg.pad_id)
             Z = self._compress(pairs)
             X, caches = backbone_full(W, Z, self.kv_bf16)
@@ -526,9 +527,10 @@ class RegularOracle:
         self.sampling = sampling
         W = self.W
         self.caches, self.length, self.step_idx, self.next_tok = [], [], [], []
-        self.seen = [set(int(t) for t in p) for p in np.asarray(prompts)]
+        prompts = [np.asarray(p) for p in prompts]
+        self.seen = [set(int(t) for t in p) for p in prompts]
         out = []
-        for i, prompt in enumerate(np.asarray(prompts)):
+        for i, prompt in enumerate(prompts):
             X, caches = backbone_full(W, W["embed"][np.asarray(prompt)], self.kv_bf16)
             self.caches.append([[k, v] for k, v in caches])
             self.length.append(len(prompt))

@@ -13,15 +13,16 @@ __device__ __forceinline__ void seen_set(uint32_t *row, int32_t t, int V) {
     if (t >= 0 && t < V) atomicOr(row + (t >> 5), 1u << (t & 31));
 }
 
-__global__ __launch_bounds__(256) void k_seen_mark(const int32_t *tokens, int n, int V, uint32_t *seen,
-                                                   int seen_words) {
+__global__ __launch_bounds__(256) void k_seen_mark(const int32_t *tokens, int n, const int32_t *ntok, int V,
+                                                   uint32_t *seen, int seen_words) {
     const int b = blockIdx.y;
     const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i < n) seen_set(seen + (int64_t)b * seen_words, tokens[(int64_t)b * n + i], V);
+    if (i < (ntok ? ntok[b] : n)) seen_set(seen + (int64_t)b * seen_words, tokens[(int64_t)b * n + i], V);
 }
 
-void launch_seen_mark(const int32_t *tokens, int n, int B, int V, uint32_t *seen, int seen_words, hipStream_t s) {
-    hipLaunchKernelGGL(k_seen_mark, dim3((n + 255) / 256, B), dim3(256), 0, s, tokens, n, V, seen, seen_words);
+void launch_seen_mark(const int32_t *tokens, int n, const int32_t *ntok, int B, int V, uint32_t *seen, int seen_words,
+                      hipStream_t s) {
+    hipLaunchKernelGGL(k_seen_mark, dim3((n + 255) / 256, B), dim3(256), 0, s, tokens, n, ntok, V, seen, seen_words);
 }
 
 struct PairOut { int32_t tok_b, tok_d; float conf; int32_t accept; };

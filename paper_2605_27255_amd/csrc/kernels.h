@@ -99,7 +99,10 @@ void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_
                         int32_t *step, int advance, int B, uint32_t *seen, int seen_words, int V, hipStream_t s);
 // Penalised-token bitmaps [B][seen_words] (bit t of word t/32: token t):
 // set the bit of every prompt token (ids outside [0, V) are skipped).
-void launch_seen_mark(const int32_t *tokens, int n, int B, int V, uint32_t *seen, int seen_words, hipStream_t s);
+// `ntok` (device [B], or NULL: n each) bounds each sequence's prompt inside
+// its row of stride n.
+void launch_seen_mark(const int32_t *tokens, int n, const int32_t *ntok, int B, int V, uint32_t *seen, int seen_words,
+                      hipStream_t s);
 
 struct SampleParams {
     const float *logits; int V; int B;
@@ -137,10 +140,13 @@ void launch_copy_bytes(void *dst, const void *src, int64_t n, hipStream_t s);
 // ----------------------------------------------------------------------------
 struct PrefillGeom {
     int B;           // sequences
-    int c0, clen;    // chunk start latent and latents in this chunk
+    int c0, clen;    // chunk start latent and latents in this chunk (the longest sequence's)
     int mpad;        // per-sequence row stride (clen rounded up to 16)
-    int n_tok;       // prompt tokens per sequence
+    int n_tok;       // row stride of the token array, and every prompt's length when ntok is NULL
+    const int32_t *ntok;   // per-sequence prompt lengths [B] (ragged batch), or NULL
 };
+// Prompt tokens of sequence b.
+__device__ __forceinline__ int seq_tokens(const PrefillGeom &g, int b) { return g.ntok ? g.ntok[b] : g.n_tok; }
 void launch_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
                          const PrefillGeom &g, uint16_t *xin, hipStream_t s);
 void launch_gather_pair_sum(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
@@ -173,7 +179,9 @@ struct AttnPrefillParams {
     uint16_t *out_hi, *out_lo;  // tiled [B*mpad][n_q*d], hi and lo planes
 };
 void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s);
+// After a chunk: every sequence whose last position (ceil(n_b / 2) - 1, or
+// n_b - 1 with `regular`) lies in the chunk takes that row as its step state.
 void launch_pick_last(const float *x, int H, const PrefillGeom &g, float *xdec, float *ss,
-                      int32_t *pos, int32_t *step, int latents, hipStream_t s);
+                      int32_t *pos, int32_t *step, int regular, hipStream_t s);
 
 }  // namespace pipo

@@ -24,9 +24,9 @@ __global__ void k_gather_pairs(const int32_t *tokens, const uint16_t *embed, int
         const int k = (int)(idx - (int64_t)m * cpr) << 3;
         const int b = m / g.mpad, i = m - b * g.mpad;
         int row = pad_id;
-        if (i < g.clen) {
+        if (i < g.clen) {   // rows past a sequence's prompt (ragged batch) hold (PAD, PAD)
             const int t = 2 * (g.c0 + i) + (k < H ? 0 : 1);
-            row = t < g.n_tok ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+            row = t < seq_tokens(g, b) ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
         }
         const u32x4 v = *(const u32x4 *)(embed + tiled_index(row, k < H ? k : k - H, H));
         *(u32x4 *)(xin + tiled_index(m, k, 2 * H)) = v;
@@ -53,9 +53,9 @@ __global__ void k_gather_pair_sum(const int32_t *tokens, const uint16_t *embed, 
         const int b = m / g.mpad, i = m - b * g.mpad;
         int ra = pad_id, rb = pad_id;
         if (i < g.clen) {
-            const int t = 2 * (g.c0 + i);
-            ra = t < g.n_tok ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
-            rb = t + 1 < g.n_tok ? clamp_id(tokens[(int64_t)b * g.n_tok + t + 1], V) : pad_id;
+            const int t = 2 * (g.c0 + i), nb = seq_tokens(g, b);
+            ra = t < nb ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+            rb = t + 1 < nb ? clamp_id(tokens[(int64_t)b * g.n_tok + t + 1], V) : pad_id;
         }
         const u32x4 va = *(const u32x4 *)(embed + tiled_index(ra, k, H));
         const u32x4 vb = *(const u32x4 *)(embed + tiled_index(rb, k, H));
@@ -88,7 +88,7 @@ __global__ __launch_bounds__(256) void k_mtp_rows(const float *xb, const int32_t
     if (m >= M) return;
     const int b = m / g.mpad, i = m - b * g.mpad;
     const int t = 2 * (g.c0 + i) + 2;
-    const int tok = (i < g.clen && t < g.n_tok) ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+    const int tok = (i < g.clen && t < seq_tokens(g, b)) ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
     const float *xr = xb + (int64_t)m * H;
     float a = 0.f, e = 0.f;
     for (int k = lane * 8; k < H; k += 512) {
@@ -144,7 +144,7 @@ __global__ void k_gather_tokens(const int32_t *tokens, const uint16_t *embed, in
         const int k = (int)(idx - (int64_t)m * cpr) << 3;
         const int b = m / g.mpad, i = m - b * g.mpad;
         const int t = g.c0 + i;
-        const int row = (i < g.clen && t < g.n_tok) ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
+        const int row = (i < g.clen && t < seq_tokens(g, b)) ? clamp_id(tokens[(int64_t)b * g.n_tok + t], V) : pad_id;
         const u32x4 v = *(const u32x4 *)(embed + tiled_index(row, k, H));
         float4 *dst = (float4 *)(x + (int64_t)m * H + k);
         dst[0] = make_float4(bf_lo(v[0]), bf_hi(v[0]), bf_lo(v[1]), bf_hi(v[1]));
@@ -650,9 +650,12 @@ void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s) {
 // them); pos is set to that position, so the heads that follow run there and
 // advance it, and the step counter restarts.
 __global__ __launch_bounds__(256) void k_pick_last(const float *x, int H, PrefillGeom g, float *xdec,
-                                                   float *ss, int32_t *pos, int32_t *step, int latents) {
+                                                   float *ss, int32_t *pos, int32_t *step, int regular) {
     const int b = blockIdx.x;
-    const float *xr = x + ((int64_t)b * g.mpad + g.clen - 1) * H;
+    const int nb = seq_tokens(g, b);
+    const int last = (regular ? nb : (nb + 1) / 2) - 1;   // the sequence's last position
+    if (last < g.c0 || last >= g.c0 + g.clen) return;
+    const float *xr = x + ((int64_t)b * g.mpad + last - g.c0) * H;
     for (int k = threadIdx.x; k < H; k += 256) xdec[(int64_t)b * H + k] = xr[k];
     for (int st = threadIdx.x; st < (H >> 4); st += 256) {
         float a = 0.f;
@@ -661,14 +664,14 @@ __global__ __launch_bounds__(256) void k_pick_last(const float *x, int H, Prefil
         ss[(int64_t)b * (H >> 4) + st] = a;
     }
     if (threadIdx.x == 0) {
-        pos[b] = latents - 1;
+        pos[b] = last;
         step[b] = 0;
     }
 }
 
 void launch_pick_last(const float *x, int H, const PrefillGeom &g, float *xdec, float *ss, int32_t *pos,
-                      int32_t *step, int latents, hipStream_t s) {
-    hipLaunchKernelGGL(k_pick_last, dim3(g.B), dim3(256), 0, s, x, H, g, xdec, ss, pos, step, latents);
+                      int32_t *step, int regular, hipStream_t s) {
+    hipLaunchKernelGGL(k_pick_last, dim3(g.B), dim3(256), 0, s, x, H, g, xdec, ss, pos, step, regular);
 }
 
 }  // namespace pipo

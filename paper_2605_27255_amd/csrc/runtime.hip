@@ -77,6 +77,9 @@ struct pipo_ctx {
 
     uint64_t *h_seeds = nullptr;     // pinned staging for sampler seeds
     hipEvent_t seeds_done = nullptr;
+    int32_t *h_lens = nullptr;       // pinned staging for the prompt lengths of a ragged batch
+    hipEvent_t lens_done = nullptr;
+    int32_t *ntok = nullptr;         // device: prompt lengths of the last ragged prefill [Bmax]
     hipStream_t cap_stream = nullptr;
 
     int batch = 0, len = 0;
@@ -284,6 +287,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->best_d = a.take<uint64_t>(B);
         c->seeds = a.take<uint64_t>(B);
         c->pairs = a.take<int32_t>(2 * B);
+        c->ntok = a.take<int32_t>(B);
         c->seen_words = (V + 31) / 32;
         c->seen = a.take<uint32_t>((int64_t)B * c->seen_words);
         c->pos = a.take<int32_t>(B);
@@ -357,6 +361,8 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
     if (e != hipSuccess) return cleanup_fail(fail(c, PIPO_EHIP, "init launch: %s", hipGetErrorString(e)));
     if (hipHostMalloc((void **)&c->h_seeds, sizeof(uint64_t) * B, hipHostMallocDefault) != hipSuccess ||
         hipEventCreateWithFlags(&c->seeds_done, hipEventDisableTiming) != hipSuccess ||
+        hipHostMalloc((void **)&c->h_lens, sizeof(int32_t) * B, hipHostMallocDefault) != hipSuccess ||
+        hipEventCreateWithFlags(&c->lens_done, hipEventDisableTiming) != hipSuccess ||
         hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess)
         return cleanup_fail(fail(c, PIPO_EHIP, "host staging / event / stream creation failed"));
     e = hipStreamSynchronize(s);
@@ -562,7 +568,9 @@ static int copy_outputs(pipo_ctx *c, pipo_pair *d_out, float *d_lb, float *d_ld,
 // the chunked backbone over `positions` (PIPO: ceil(n/2) latents of
 // compressed pairs, eq. 1; regular: the n tokens themselves), and the last
 // position's residual into x.
-static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
+// `n` is the row stride of d_tokens; `lens` (host [batch], or NULL: n each)
+// the prompt lengths of a ragged batch.
+static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n, const int32_t *lens,
                             const pipo_sampling *smp, bool regular, hipStream_t s) {
     if (!d_tokens) return fail(c, PIPO_EINVAL, "d_tokens must be non-NULL");
     if (n < 1) return fail(c, PIPO_EINVAL, "prompt length must be >= 1 (got %d)", n);
@@ -570,7 +578,16 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     int rc = check_sampling(c, smp, batch);
     if (rc) return rc;
     if (batch > c->Bmax) return fail(c, PIPO_ECAPACITY, "batch %d exceeds max_batch %d", batch, c->Bmax);
-    const int positions = regular ? n : (n + 1) / 2;
+    int nmax = n;
+    if (lens) {
+        nmax = 0;
+        for (int b = 0; b < batch; ++b) {
+            if (lens[b] < 1 || lens[b] > n)
+                return fail(c, PIPO_EINVAL, "lens[%d] = %d outside [1, %d]", b, lens[b], n);
+            nmax = std::max(nmax, (int)lens[b]);
+        }
+    }
+    const int positions = regular ? nmax : (nmax + 1) / 2;   // the longest sequence's
     if (positions + 1 > c->cfg.max_latent)
         return fail(c, PIPO_ECAPACITY, "%d positions leave no room for a step (max_latent %d)", positions,
                     c->cfg.max_latent);
@@ -588,10 +605,18 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     c->top_k = smp->top_k;
     c->rep_penalty = smp->rep_penalty;
     c->eval_smp = smp->temperature > 0.f && (smp->top_k > 0 || smp->rep_penalty != 1.f);
+    const int32_t *ntok = nullptr;
+    if (lens) {
+        HIP_TRY(c, hipEventSynchronize(c->lens_done));
+        memcpy(c->h_lens, lens, sizeof(int32_t) * batch);
+        HIP_TRY(c, hipMemcpyAsync(c->ntok, c->h_lens, sizeof(int32_t) * batch, hipMemcpyHostToDevice, s));
+        HIP_TRY(c, hipEventRecord(c->lens_done, s));
+        ntok = c->ntok;
+    }
     if (c->eval_smp) {   // the prompt's tokens start each sequence's penalised set
         PROF(PIPO_K_PREFILL_MISC);
         launch_fill_u32(c->seen, 0u, (int64_t)batch * c->seen_words, s);
-        launch_seen_mark(d_tokens, n, batch, c->V, c->seen, c->seen_words, s);
+        launch_seen_mark(d_tokens, n, ntok, batch, c->V, c->seen, c->seen_words, s);
     }
     if (smp->temperature > 0.f) {
         HIP_TRY(c, hipEventSynchronize(c->seeds_done));
@@ -603,7 +628,7 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     PrefillGeom g{};
     for (int c0 = 0; c0 < positions; c0 += c->chunk) {
         g.B = batch; g.c0 = c0; g.clen = std::min(c->chunk, positions - c0);
-        g.mpad = (int)round_up(g.clen, 32); g.n_tok = n;
+        g.mpad = (int)round_up(g.clen, 32); g.n_tok = n; g.ntok = ntok;
         const int M = batch * g.mpad;
         GemmParams gp{};
         gp.g = g; gp.M = M;
@@ -649,6 +674,8 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
             p.W = lw.wdown; p.X = c->p_act; p.Xlo = c->p_act_lo; p.N = H; p.K = F; p.epi = EPI_RESID; p.out = c->p_x;
             { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
         }
+        // sequences whose last position is in this chunk take it as their step state
+        { PROF(PIPO_K_PREFILL_MISC); launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, regular, s); }
         if (!regular && (c->heads & PIPO_HEADS_MTP_LAYER)) {
             // App. B.2 over the chunk's latents (their K/V fill the MTP cache);
             // the MTP stream lives in p_xin, free once the compressor has run
@@ -681,19 +708,18 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
             { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
         }
     }
-    { PROF(PIPO_K_PREFILL_MISC); launch_pick_last(c->p_x, H, g, c->x, c->ss_x, c->pos, c->step, positions, s); }
     c->len = positions;
     return PIPO_OK;
 }
 
-extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
-                            const pipo_sampling *smp, pipo_pair *d_out, float *d_logits_b, float *d_logits_d,
-                            void *stream) {
+static int prefill_pair(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n, const int32_t *lens,
+                        const pipo_sampling *smp, pipo_pair *d_out, float *d_logits_b, float *d_logits_d,
+                        void *stream) {
     if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
     if (!d_out) return fail(c, PIPO_EINVAL, "d_out must be non-NULL");
     hipStream_t s = (hipStream_t)stream;
     c->prefilled = false;
-    int rc = prefill_backbone(c, batch, d_tokens, n, smp, false, s);
+    int rc = prefill_backbone(c, batch, d_tokens, n, lens, smp, false, s);
     if (rc) return rc;
     enqueue_heads(c, batch, c->H / 16, 1, false, s);
     HIP_TRY(c, hipGetLastError());
@@ -702,6 +728,19 @@ extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     c->prefilled = true;
     c->regular = false;
     return PIPO_OK;
+}
+
+extern "C" int pipo_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
+                            const pipo_sampling *smp, pipo_pair *d_out, float *d_logits_b, float *d_logits_d,
+                            void *stream) {
+    return prefill_pair(c, batch, d_tokens, n, nullptr, smp, d_out, d_logits_b, d_logits_d, stream);
+}
+
+extern "C" int pipo_prefill_ragged(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t stride,
+                                   const int32_t *lens, const pipo_sampling *smp, pipo_pair *d_out,
+                                   float *d_logits_b, float *d_logits_d, void *stream) {
+    if (!lens) return fail(c, PIPO_EINVAL, "lens must be non-NULL");
+    return prefill_pair(c, batch, d_tokens, stride, lens, smp, d_out, d_logits_b, d_logits_d, stream);
 }
 
 // Regular decoding's heads: eq. 3 alone (tied LM head on RMSNorm(h; g_final),
@@ -740,13 +779,13 @@ static int copy_tokens(pipo_ctx *c, int32_t *d_tok, float *d_logits, hipStream_t
     return PIPO_OK;
 }
 
-extern "C" int pipo_regular_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
-                                    const pipo_sampling *smp, int32_t *d_tok, float *d_logits, void *stream) {
+static int prefill_regular(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n, const int32_t *lens,
+                           const pipo_sampling *smp, int32_t *d_tok, float *d_logits, void *stream) {
     if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
     if (!d_tok) return fail(c, PIPO_EINVAL, "d_tok must be non-NULL");
     hipStream_t s = (hipStream_t)stream;
     c->prefilled = false;
-    int rc = prefill_backbone(c, batch, d_tokens, n, smp, true, s);
+    int rc = prefill_backbone(c, batch, d_tokens, n, lens, smp, true, s);
     if (rc) return rc;
     enqueue_regular_heads(c, batch, c->H / 16, 1, false, s);
     HIP_TRY(c, hipGetLastError());
@@ -755,6 +794,18 @@ extern "C" int pipo_regular_prefill(pipo_ctx *c, int32_t batch, const int32_t *d
     c->prefilled = true;
     c->regular = true;
     return PIPO_OK;
+}
+
+extern "C" int pipo_regular_prefill(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t n,
+                                    const pipo_sampling *smp, int32_t *d_tok, float *d_logits, void *stream) {
+    return prefill_regular(c, batch, d_tokens, n, nullptr, smp, d_tok, d_logits, stream);
+}
+
+extern "C" int pipo_regular_prefill_ragged(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int32_t stride,
+                                           const int32_t *lens, const pipo_sampling *smp, int32_t *d_tok,
+                                           float *d_logits, void *stream) {
+    if (!lens) return fail(c, PIPO_EINVAL, "lens must be non-NULL");
+    return prefill_regular(c, batch, d_tokens, stride, lens, smp, d_tok, d_logits, stream);
 }
 
 extern "C" int pipo_regular_step(pipo_ctx *c, const int32_t *d_in_tok, int32_t *d_tok, float *d_logits,
@@ -867,6 +918,8 @@ extern "C" int pipo_free(pipo_ctx *c) {
     if (c->cap_stream) hipStreamDestroy(c->cap_stream);
     if (c->seeds_done) hipEventDestroy(c->seeds_done);
     if (c->h_seeds) hipHostFree(c->h_seeds);
+    if (c->lens_done) hipEventDestroy(c->lens_done);
+    if (c->h_lens) hipHostFree(c->h_lens);
     if (c->wmem) hipFree(c->wmem);
     if (c->amem) hipFree(c->amem);
     delete c;

@@ -14,9 +14,9 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libpipo.so")
 
 PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -1, -2, -3, -4, -5
-EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_regular_prefill",
-            "pipo_regular_step", "pipo_free", "pipo_last_error", "pipo_read_weight", "pipo_profile_enable",
-            "pipo_profile_read")
+EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step",
+            "pipo_regular_prefill", "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free",
+            "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read")
 #: kernel classes of the profiling counters (PIPO_K_* in include/pipo.h)
 KERNEL_CLASSES = ("gemv_layer", "gemv_lmhead", "gemv_small", "attn_decode", "sample", "gate",
                   "prefill_gemm", "prefill_attn", "prefill_misc")
@@ -63,6 +63,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_prefill.argtypes = [vp, i32, vp, i32, ctypes.POINTER(PipoSampling), vp, vp, vp, vp]
     lib.pipo_decode_step.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.pipo_regular_prefill.argtypes = [vp, i32, vp, i32, ctypes.POINTER(PipoSampling), vp, vp, vp]
+    lib.pipo_prefill_ragged.argtypes = [vp, i32, vp, i32, ctypes.POINTER(i32), ctypes.POINTER(PipoSampling),
+                                        vp, vp, vp, vp]
+    lib.pipo_regular_prefill_ragged.argtypes = [vp, i32, vp, i32, ctypes.POINTER(i32), ctypes.POINTER(PipoSampling),
+                                                vp, vp, vp]
     lib.pipo_regular_step.argtypes = [vp, vp, vp, vp, vp]
     lib.pipo_free.argtypes = [vp]
     lib.pipo_last_error.argtypes = [vp]
@@ -70,8 +74,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_read_weight.argtypes = [vp, ctypes.c_char_p, i64, i64, vp]
     lib.pipo_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.pipo_profile_read.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
-    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_decode_step", "pipo_regular_prefill",
-               "pipo_regular_step", "pipo_free", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read"):
+    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step", "pipo_regular_prefill",
+               "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free", "pipo_read_weight",
+               "pipo_profile_enable", "pipo_profile_read"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -135,14 +140,26 @@ class PipoModel:
         assert tokens.dtype == t.int32 and tokens.is_cuda and tokens.dim() == 2 and tokens.is_contiguous()
         return tokens.shape
 
+    @staticmethod
+    def _lens(lens, B):
+        arr = (ctypes.c_int32 * B)(*[int(v) for v in lens])
+        return arr
+
     def prefill(self, tokens, tau: float, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
-                logits: bool = False, top_k: int = 0, rep_penalty: float = 1.0):
-        """tokens: int32 CUDA tensor [B, n].  Returns (pairs [B,4] int32, logits_b, logits_d)."""
+                logits: bool = False, top_k: int = 0, rep_penalty: float = 1.0, lens=None):
+        """tokens: int32 CUDA tensor [B, n]; lens: optional per-sequence prompt
+        lengths (a ragged batch, each the first lens[i] tokens of row i).
+        Returns (pairs [B,4] int32, logits_b, logits_d)."""
         B, n = self._tokens(tokens)
         smp, _keep = self._sampling(tau, temperature, top_p, seeds, top_k, rep_penalty)
         out, lb, ld = self._outputs(B, logits)
-        self._check(self.lib.pipo_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(out),
-                                          _ptr(lb), _ptr(ld), self._stream()))
+        if lens is None:
+            self._check(self.lib.pipo_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(out),
+                                              _ptr(lb), _ptr(ld), self._stream()))
+        else:
+            self._check(self.lib.pipo_prefill_ragged(self.ctx, B, _ptr(tokens), n, self._lens(lens, B),
+                                                     ctypes.byref(smp), _ptr(out), _ptr(lb), _ptr(ld),
+                                                     self._stream()))
         self.batch = B
         self._keep = tokens
         return out, lb, ld
@@ -160,15 +177,21 @@ class PipoModel:
                                               _ptr(logits_d), self._stream()))
 
     def regular_prefill(self, tokens, temperature: float = 0.0, top_p: float = 1.0, seeds=None,
-                        logits: bool = False, top_k: int = 0, rep_penalty: float = 1.0):
-        """Regular decoding's prefill over the n prompt tokens.  Returns (tok [B] int32, logits)."""
+                        logits: bool = False, top_k: int = 0, rep_penalty: float = 1.0, lens=None):
+        """Regular decoding's prefill over the n prompt tokens (lens: ragged
+        batch, as in prefill).  Returns (tok [B] int32, logits)."""
         t = self.torch
         B, n = self._tokens(tokens)
         smp, _keep = self._sampling(0.0, temperature, top_p, seeds, top_k, rep_penalty)
         tok = t.empty(B, dtype=t.int32, device="cuda")
         lg = t.empty((B, self.model.vocab), dtype=t.float32, device="cuda") if logits else None
-        self._check(self.lib.pipo_regular_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(tok),
-                                                  _ptr(lg), self._stream()))
+        if lens is None:
+            self._check(self.lib.pipo_regular_prefill(self.ctx, B, _ptr(tokens), n, ctypes.byref(smp), _ptr(tok),
+                                                      _ptr(lg), self._stream()))
+        else:
+            self._check(self.lib.pipo_regular_prefill_ragged(self.ctx, B, _ptr(tokens), n, self._lens(lens, B),
+                                                             ctypes.byref(smp), _ptr(tok), _ptr(lg),
+                                                             self._stream()))
         self.batch = B
         self._keep = tokens
         return tok, lg

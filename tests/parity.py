@@ -117,8 +117,10 @@ def compare_step(rep, tag, out_np, lb, ld, recs, smp, seeds, step, mean_rel_tol=
 
 
 def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_MEAN_REL, conf_tol=CONF_TOL,
-               max_abs_tol=LOGIT_MAX_ABS):
-    """Run the GPU free for ``steps`` pair steps after prefill; replay on the oracle."""
+               max_abs_tol=LOGIT_MAX_ABS, lens=None):
+    """Run the GPU free for ``steps`` pair steps after prefill; replay on the
+    oracle.  ``lens``: a ragged batch, sequence i's prompt being the first
+    lens[i] tokens of row i of ``prompts``."""
     import torch
     from paper_2605_27255_amd import unpack_pairs
 
@@ -127,7 +129,7 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
     tokens = torch.from_numpy(np.ascontiguousarray(prompts, dtype=np.int32)).cuda()
     outs = [gpu_model.prefill(tokens, smp.tau, smp.temperature, smp.top_p,
                               seeds if smp.temperature > 0 else None, logits=True, top_k=smp.top_k,
-                              rep_penalty=smp.rep_penalty)]
+                              rep_penalty=smp.rep_penalty, lens=lens)]
     for _ in range(steps):
         outs.append(gpu_model.decode_step(logits=True))
     torch.cuda.synchronize()
@@ -138,7 +140,7 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
     for s, (o, lb, ld) in enumerate(host):
         force = [int(v) for v in o[0]]
         if s == 0:
-            recs = orc.prefill(prompts, smp, force_b=force)
+            recs = orc.prefill(_own_prompts(prompts, lens), smp, force_b=force)
         else:
             prev = host[s - 1][0]
             pairs = [(int(prev[0][i]), int(prev[1][i]) if prev[3][i] else W.cfg.pad_id) for i in range(B)]
@@ -152,7 +154,11 @@ def run_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_
     return rep, host
 
 
-def run_regular_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_MEAN_REL):
+def _own_prompts(prompts, lens):
+    return prompts if lens is None else [prompts[i][:int(n)] for i, n in enumerate(lens)]
+
+
+def run_regular_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_tol=LOGIT_MEAN_REL, lens=None):
     """Regular decoding: the GPU runs free for ``steps`` token steps after its
     prefill; the oracle replays the GPU's tokens as inputs.  Logits and tokens
     are held to the bounds of the pair path."""
@@ -163,7 +169,7 @@ def run_regular_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_to
     tokens = torch.from_numpy(np.ascontiguousarray(prompts, dtype=np.int32)).cuda()
     outs = [gpu_model.regular_prefill(tokens, smp.temperature, smp.top_p,
                                       seeds if smp.temperature > 0 else None, logits=True, top_k=smp.top_k,
-                                      rep_penalty=smp.rep_penalty)]
+                                      rep_penalty=smp.rep_penalty, lens=lens)]
     for _ in range(steps):
         outs.append(gpu_model.regular_step(logits=True))
     torch.cuda.synchronize()
@@ -172,7 +178,8 @@ def run_regular_parity(gpu_model, W, prompts, steps, smp, log=print, mean_rel_to
     orc = O.RegularOracle(W, kv_bf16=True)
     rep = ParityReport()
     for s, (tok, lg) in enumerate(host):
-        recs = orc.prefill(prompts, smp) if s == 0 else orc.step(in_tok=[int(v) for v in host[s - 1][0]])
+        recs = orc.prefill(_own_prompts(prompts, lens), smp) if s == 0 else \
+            orc.step(in_tok=[int(v) for v in host[s - 1][0]])
         rep.steps += 1
         for i, r in enumerate(recs):
             rep.rows += 1

@@ -88,6 +88,11 @@ def test_null_arguments(lib):
     assert lib.pipo_prefill(None, 1, None, 4, ctypes.byref(smp), None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_decode_step(None, None, None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_regular_prefill(None, 1, None, 4, ctypes.byref(smp), None, None, None) == pipo.PIPO_EINVAL
+    lens = (ctypes.c_int32 * 1)(4)
+    assert lib.pipo_prefill_ragged(None, 1, None, 4, lens, ctypes.byref(smp), None, None, None, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_prefill_ragged(None, 1, None, 4, None, ctypes.byref(smp), None, None, None, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_regular_prefill_ragged(None, 1, None, 4, lens, ctypes.byref(smp), None, None,
+                                           None) == pipo.PIPO_EINVAL
     assert lib.pipo_regular_step(None, None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_read_weight(None, b"embed", 0, 1, None) == pipo.PIPO_EINVAL
     assert lib.pipo_free(None) == pipo.PIPO_OK

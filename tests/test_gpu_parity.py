@@ -510,3 +510,103 @@ def test_tiny_eval_sampler_top1_is_greedy_and_bad_settings(torch):
             m.prefill(t, 0.5, **kw)
         assert e.value.code == PIPO_EINVAL
     m.close()
+
+
+# ------------------------------------------------------------- ragged batches
+
+def _ragged(B, lens, vocab, seed):
+    """Prompts of their own lengths in one [B][max] array; the tail of each
+    row holds other random tokens, which must never be read."""
+    stride = max(lens)
+    full = rspec.prompt_tokens(B, stride, vocab, seed=seed)
+    junk = rspec.prompt_tokens(B, stride, vocab, seed=seed + 1000)
+    for i, n in enumerate(lens):
+        full[i, n:] = junk[i, n:]
+    return full
+
+
+def test_tiny_ragged_pair_parity(torch):
+    """Five prompts of 1, 2, 37, 64 and 17 tokens (1 to 32 latents) in chunks
+    of 16: sequences end in different chunks and step at their own positions."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    lens = [1, 2, 37, 64, 17]
+    B, steps = len(lens), 6
+    prompts = _ragged(B, lens, cfg.vocab, 50)
+    m = _model(cfg, seed=5, max_batch=8, max_latent=32 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(cfg, seed=5, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log, lens=lens)
+    rep.check()
+    rep, _ = run_parity(m, W, prompts, steps, _eval_smp(B, base=700), log, lens=lens)
+    rep.check()
+    m.close()
+
+
+def test_tiny_ragged_equal_lengths_match_uniform(torch):
+    """A ragged prefill whose lengths are all equal is the uniform prefill, bit for bit."""
+    from paper_2605_27255_amd import unpack_pairs
+    prompts = rspec.prompt_tokens(3, 33, TINY.vocab, seed=51)
+    m = _model(TINY, seed=2, max_batch=3, max_latent=30, prefill_chunk=8)
+    t = torch.from_numpy(prompts).cuda()
+    a = [m.prefill(t, 0.5, logits=True)] + [m.decode_step(logits=True) for _ in range(3)]
+    b = [m.prefill(t, 0.5, logits=True, lens=[33, 33, 33])] + [m.decode_step(logits=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    for (oa, la, da), (ob, lb, db) in zip(a, b):
+        for x, y in zip(unpack_pairs(oa), unpack_pairs(ob)):
+            np.testing.assert_array_equal(x, y)
+        assert torch.equal(la, lb) and torch.equal(da, db)
+    m.close()
+
+
+def test_tiny_ragged_regular_parity(torch):
+    lens = [5, 33, 20]
+    B, steps = len(lens), 6
+    prompts = _ragged(B, lens, TINY.vocab, 52)
+    m = _model(TINY, seed=3, max_batch=4, max_latent=33 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(TINY, seed=3, precision="bf16")
+    rep, _ = run_regular_parity(m, W, prompts, steps, O.Sampling(tau=0.0), log, lens=lens)
+    rep.check()
+    smp = O.Sampling(tau=0.0, temperature=0.7, top_p=0.9, seeds=tuple(90 + b for b in range(B)))
+    rep, _ = run_regular_parity(m, W, prompts, steps, smp, log, lens=lens)
+    rep.check()
+    m.close()
+
+
+def test_tiny_ragged_paper_heads_parity(torch):
+    """App. B heads: the MTP layer's prompt rows stop at each sequence's own end."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1, "heads": HEADS_PAPER})
+    lens = [3, 30, 15]
+    B, steps = len(lens), 5
+    prompts = _ragged(B, lens, cfg.vocab, 53)
+    m = _model(cfg, seed=13, max_batch=3, max_latent=15 + steps + 1, prefill_chunk=8)
+    W = O.OracleWeights.generate(cfg, seed=13, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log, conf_tol=APPB_CONF,
+                        max_abs_tol=APPB_MAX_ABS, lens=lens)
+    rep.check()
+    m.close()
+
+
+def test_4b_width_ragged_pair_parity(torch):
+    """4B width, two layers: prompts of 100, 513 and 257 tokens over chunks of 128 latents."""
+    cfg = DENSE_4B.with_layers(2)
+    lens = [100, 513, 257]
+    B, steps = len(lens), 3
+    prompts = _ragged(B, lens, cfg.vocab, 54)
+    m = _model(cfg, seed=4, max_batch=4, max_latent=257 + steps + 1, prefill_chunk=128)
+    W = O.OracleWeights.generate(cfg, seed=4, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log, lens=lens)
+    rep.check()
+    m.close()
+
+
+def test_ragged_bad_lengths(torch):
+    from paper_2605_27255_amd import PipoError, PIPO_EINVAL, PIPO_ECAPACITY
+    m = _model(TINY, seed=0, max_batch=2, max_latent=12, prefill_chunk=16)
+    t = torch.from_numpy(rspec.prompt_tokens(2, 30, TINY.vocab)).cuda()
+    for lens, code in (([0, 5], PIPO_EINVAL), ([5, 31], PIPO_EINVAL), ([4, 30], PIPO_ECAPACITY)):
+        with pytest.raises(PipoError) as e:
+            m.prefill(t, 0.5, lens=lens)
+        assert e.value.code == code
+    m.prefill(t, 0.5, lens=[4, 22])      # 11 latents + 1 fits
+    m.decode_step()
+    torch.cuda.synchronize()
+    m.close()

@@ -47,7 +47,7 @@ typedef struct pipo_ctx pipo_ctx;   /* opaque; owns weights, KV cache, workspace
 /* Model shape and capacities.  Constraints (PIPO_EINVAL otherwise):
  * hidden % 32 == 0, ffn % 32 == 0, vocab % 16 == 0, head_dim in {64, 128},
  * n_q_heads % n_kv_heads == 0 and n_q_heads / n_kv_heads <= 16,
- * (n_q_heads*head_dim) % 32 == 0, 1 <= max_batch <= 32, max_latent >= 1,
+ * (n_q_heads*head_dim) % 32 == 0, 1 <= max_batch <= 64, max_latent >= 1,
  * prefill_chunk >= 1. */
 typedef struct {
     int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;

@@ -31,8 +31,11 @@ namespace pipo {
 thread_local GemvTiming g_gemv_timing = {nullptr, nullptr, false};
 
 constexpr int kNW = 8;                       // waves per workgroup
+constexpr int kMaxB = 64;                    // columns (sequences) at most: four 16-column tiles
 constexpr int kGemvOneLdsBytes = 72 * 1024;  // budget for wave-private X (two workgroups per CU)
-constexpr int kWideChunk = 8;                // k-tiles per shared X chunk (larger batches)
+// k-tiles per shared X chunk (larger batches); beyond 32 columns half as
+// many, so that the X and weight registers of two chunks in flight fit
+constexpr int wide_chunk(int nbt) { return nbt <= 2 ? 8 : 4; }
 constexpr int kXR = 3;                       // prologue chunks per thread loaded ahead of the weights
 
 __device__ __forceinline__ float silu_f(float u) { return u / (1.0f + __expf(-u)); }
@@ -304,7 +307,7 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams &p, f32x4 (&fin)[
     const int row0 = strip * 16 + 4 * g;
     if (EPI == EPI_LOGITS) {
         // every wave reaches here; waves without a strip contribute key 0
-        __shared__ uint64_t s_best[kNW][32];
+        __shared__ uint64_t s_best[kNW][kMaxB];
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) {
             const int b = bt * 16 + j;
@@ -433,7 +436,7 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     constexpr int NA = NAcc<PRO>::n;
     constexpr bool HASLO = PRO != PRO_PAIR;   // gathered embeddings are exact in bf16
     extern __shared__ __align__(16) uint16_t xs[];
-    __shared__ float sc0[32], sc1[32];
+    __shared__ float sc0[kMaxB], sc1[kMaxB];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
@@ -658,9 +661,9 @@ __global__ __launch_bounds__(256) void k_xprep(GemvParams p) {
 
 template <int NBT, int EPI>
 __global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
-    constexpr int CK = kWideChunk;         // k-tiles per X chunk
+    constexpr int CK = wide_chunk(NBT);    // k-tiles per X chunk
     constexpr int RS = CK * 32 + 8;        // LDS row stride (elements) of a chunk plane
-    constexpr int XU = 2 * NBT;            // 16-byte X units per thread per chunk (2 B CK 4 / 512)
+    constexpr int XU = 2 * NBT * CK / 8;   // 16-byte X units per thread per chunk (2 B CK 4 / 512)
     extern __shared__ __align__(16) uint16_t xsm[];   // [2 buffers][2 planes][B][RS]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
@@ -788,14 +791,15 @@ __global__ __launch_bounds__(512) void k_gemv_wide(GemvParams p) {
 // ranges in range order.
 constexpr int kKrLdsBytes = 128 * 1024;      // X slice budget of a k-range workgroup (one per CU)
 constexpr int kKrChunks = 8;                 // X chunks per thread: B * k-tiles * 4 <= 8 * 512
-template <int PRO>   // the MTP's chunks hold both halves' sources, so fewer fit in registers
-struct KrChunks { static constexpr int n = PRO == PRO_MTP ? 6 : kKrChunks; };
+template <int PRO>   // the MTP's chunks hold both halves' sources, and PRO_CAT keeps two sets of
+                     // RMSNorm parts, so fewer fit in registers
+struct KrChunks { static constexpr int n = (PRO == PRO_MTP || PRO == PRO_CAT) ? 6 : kKrChunks; };
 constexpr int kKrWaves = 1280;               // streaming waves the ranges aim for (~20 MB in flight)
 template <int NBT, int PRO, int EPI, int U>
 __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
     constexpr int NA = NAcc<PRO>::n;
     extern __shared__ __align__(16) uint16_t xs[];
-    __shared__ float sc0[32], sc1[32];
+    __shared__ float sc0[kMaxB], sc1[kMaxB];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
@@ -1007,7 +1011,7 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     // wave-private X when every wave's slices fit
     const int nmax = (KT + KS - 1) / KS;
     const int lds_one = planes * kNW * q.B * (nmax * 32 + 8) * 2 + red;
-    if (lds_one <= kGemvOneLdsBytes) {
+    if (NBT <= 2 && lds_one <= kGemvOneLdsBytes) {   // (never fits beyond 32 columns)
         if (q.wg_cap > 0 && grid > q.wg_cap) grid = q.wg_cap;
         if (g_gemv_timing.pending) {
             hipExtLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s,
@@ -1062,7 +1066,7 @@ static void launch_multi(GemvParams &q, hipStream_t s) {
     q.xseg = (q.K + 2047) / 2048;
     hipLaunchKernelGGL((k_xprep<PRO>), dim3(q.B * q.xseg), dim3(256), 0, s, q);
     const int rtiles = ((q.N >> 4) + kNW - 1) / kNW;
-    const int lds_w = 2 * 2 * q.B * (kWideChunk * 32 + 8) * 2 + 16;
+    const int lds_w = 2 * 2 * q.B * (wide_chunk(NBT) * 32 + 8) * 2 + 16;
     hipLaunchKernelGGL((k_gemv_wide<NBT, EPI>), dim3(rtiles), dim3(kNW * 64), lds_w, s, q);
 }
 
@@ -1079,7 +1083,9 @@ static void launch_u(const GemvParams &p, hipStream_t s) {
 template <int KS, int PRO, int EPI>
 static void launch_nbt(const GemvParams &p, hipStream_t s) {
     if (p.B <= 16) launch_u<1, KS, PRO, EPI>(p, s);
-    else launch_u<2, KS, PRO, EPI>(p, s);
+    else if (p.B <= 32) launch_u<2, KS, PRO, EPI>(p, s);
+    else if (p.B <= 48) launch_u<3, KS, PRO, EPI>(p, s);
+    else launch_u<4, KS, PRO, EPI>(p, s);
 }
 
 int gemv_num_groups(int N) { return N >> 4; }

@@ -9,7 +9,7 @@ namespace pipo {
 // Weight-streaming skinny GEMM for the decode step:  Y^T[N][B] = W[N][K] X^T.
 // W is tiled (16x32 tiles, see device_common.h), X is produced on the fly by
 // the prologue into LDS as a bf16 pair (hi + lo, about 16 significant bits),
-// B <= 32.
+// B <= 64.
 // ----------------------------------------------------------------------------
 enum GemvPro : int {
     PRO_NORM = 0,   // X = bf16(RMSNorm(x) * gain): x fp32 [B][K], sum-of-squares parts

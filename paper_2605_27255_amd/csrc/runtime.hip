@@ -170,7 +170,7 @@ static int check_config(const pipo_config *c) {
     if (c->n_q_heads % c->n_kv_heads || c->n_q_heads / c->n_kv_heads > 16)
         return fail(nullptr, PIPO_EINVAL, "n_q_heads must be a multiple of n_kv_heads, at most 16x");
     if ((c->n_q_heads * c->head_dim) % 32) return fail(nullptr, PIPO_EINVAL, "n_q_heads*head_dim % 32 != 0");
-    if (c->max_batch < 1 || c->max_batch > 32) return fail(nullptr, PIPO_EINVAL, "max_batch must be in [1, 32]");
+    if (c->max_batch < 1 || c->max_batch > 64) return fail(nullptr, PIPO_EINVAL, "max_batch must be in [1, 64]");
     if (c->max_latent < 1 || c->prefill_chunk < 1) return fail(nullptr, PIPO_EINVAL, "max_latent and prefill_chunk must be >= 1");
     if (c->pad_id < -1 || c->pad_id >= c->vocab) return fail(nullptr, PIPO_EINVAL, "pad_id out of range");
     if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return fail(nullptr, PIPO_EINVAL, "bad rms_eps or rope_base");

@@ -67,7 +67,7 @@ def _cfg(**kw):
 
 
 @pytest.mark.parametrize("field,value", [("head_dim", 96), ("hidden", 250), ("ffn", 1000), ("vocab", 4090),
-                                         ("max_batch", 33), ("max_batch", 0), ("n_kv_heads", 3),
+                                         ("max_batch", 65), ("max_batch", 0), ("n_kv_heads", 3),
                                          ("prefill_chunk", 0), ("max_latent", 0), ("gain_mode", 2), ("heads", 8),
                                          ("pad_id", 5000)])
 def test_bad_config_is_rejected_before_device_work(lib, field, value):

@@ -610,3 +610,33 @@ def test_ragged_bad_lengths(torch):
     m.decode_step()
     torch.cuda.synchronize()
     m.close()
+
+
+def test_tiny_batch64_ragged_eval_sampler(torch):
+    """64 sequences (four 16-column tiles), ragged prompts of 1..64 tokens,
+    the evaluation sampler; then greedy."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1})
+    B, steps = 64, 4
+    lens = [1 + (7 * i) % 64 for i in range(B)]
+    prompts = _ragged(B, lens, cfg.vocab, 60)
+    m = _model(cfg, seed=8, max_batch=64, max_latent=32 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(cfg, seed=8, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, _eval_smp(B, base=900), log, lens=lens)
+    rep.check()
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.5), log, lens=lens)
+    rep.check()
+    m.close()
+
+
+def test_4b_width_batch64_top_p(torch):
+    """4B width, two layers, 64 sequences: the k-range and wide GEMV forms at
+    four column tiles, T 0.6, top-p 0.95, tau 0.7."""
+    cfg = DENSE_4B.with_layers(2)
+    B, n, steps = 64, 48, 2
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=61)
+    smp = O.Sampling(tau=0.7, temperature=0.6, top_p=0.95, seeds=tuple(2000 + b for b in range(B)))
+    m = _model(cfg, seed=4, max_batch=64, max_latent=24 + steps + 1, prefill_chunk=4096)
+    W = O.OracleWeights.generate(cfg, seed=4, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, smp, log)
+    rep.check()
+    m.close()

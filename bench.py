@@ -208,6 +208,7 @@ def main():
     ap.add_argument("--no-regular", action="store_true", help="skip the regular-decoding baseline leg")
     ap.add_argument("--heads", choices=("linear", "paper"), default="linear",
                     help="linear: the workloads' one-linear heads; paper: the App. B forms of all three heads")
+    ap.add_argument("--batch", type=int, default=None, help="override the workload's batch (up to 64)")
     ap.add_argument("--sampler", choices=("workload", "eval"), default="workload",
                     help="workload: the workload's own selection; eval: the paper's evaluation sampler "
                          "(T 1.0, top-p 0.95, top-k 20, repetition penalty 1.5)")
@@ -241,6 +242,8 @@ def main():
         wl = replace(wl, decode_steps=args.decode_steps)
     if args.heads == "paper":
         wl = replace(wl, name=wl.name + "+appB-heads", model=replace(wl.model, heads=HEADS_PAPER))
+    if args.batch is not None:
+        wl = replace(wl, name=f"{wl.name}@bs{args.batch}", batch=args.batch)
     if args.sampler == "eval":
         wl = replace(wl, name=wl.name + "+eval-sampler", temperature=1.0, top_p=0.95, top_k=20, rep_penalty=1.5)
     m = wl.model

@@ -256,6 +256,55 @@ def select_eval(logits, seen, temperature, top_k, top_p, theta, u):
     return select_top_p(y, 1.0, top_p, u)
 
 
+# ------------------------------------------------------- OPD targets (App. C)
+
+def opd_teacher_rows(tokens, pad_id):
+    """PAD compaction of the OPD teacher pass (App. C, OPD training): the
+    teacher runs on the trajectory with every PAD removed, and position t of
+    the PAD-augmented trajectory takes the teacher row of the last non-PAD
+    position at or before t (the row index is the count of non-PAD tokens in
+    tokens[0..t], minus one; -1 where there is none yet)."""
+    keep = np.asarray(tokens) != pad_id
+    return np.cumsum(keep) - 1
+
+
+def log_softmax_at(logits, y):
+    """log p(y) for p = softmax(logits): logits[y] - log sum_j exp(logits[j])."""
+    l = np.asarray(logits, F64)
+    m = np.max(l)
+    return float(l[y] - (m + np.log(np.sum(np.exp(l - m)))))
+
+
+def opd_targets(logits_s, logits_t, rows, labels):
+    """Per-position sampled reverse-KL term and confidence target (App. C):
+    d_t = log p_s(y_t) - log p_t(y_t) with the teacher row rows[t], and
+    alpha_t = exp(-max(d_t, 0)) = min(p_t(y_t) / p_s(y_t), 1).  Positions with
+    a negative label are not scored (d = 0, alpha = 1).  Returns (d, alpha)."""
+    T = len(labels)
+    d = np.zeros(T)
+    alpha = np.ones(T)
+    for t in range(T):
+        y = int(labels[t])
+        if y < 0:
+            continue
+        d[t] = log_softmax_at(logits_s[t], y) - log_softmax_at(logits_t[int(rows[t])], y)
+        alpha[t] = np.exp(-max(d[t], 0.0))
+    return d, alpha
+
+
+def opd_loss_sums(d, labels):
+    """The sampled-KL loss's sums, kept apart for even positions (backbone
+    head) and odd positions (MTP head): [sum_even, n_even, sum_odd, n_odd]
+    over the scored positions."""
+    d = np.asarray(d, F64)
+    lab = np.asarray(labels)
+    out = []
+    for par in (0, 1):
+        sel = (np.arange(len(lab)) % 2 == par) & (lab >= 0)
+        out += [float(np.sum(d[sel])), float(np.count_nonzero(sel))]
+    return out
+
+
 # ------------------------------------------------------------------- weights
 
 class OracleWeights:

@@ -623,3 +623,65 @@ def test_eval_sampler_worked_example():
     l = np.log(np.array([4.0, 2.0, 1.0, 8.0]))
     assert O.select_eval(l, {3}, 1.0, 3, 0.7, 1.5, 0.6) == 3
     assert O.select_eval(l, {3}, 1.0, 3, 0.7, 1.5, 0.3) == 0
+
+
+# ------------------------------------------------- OPD targets (App. C)
+
+def test_opd_teacher_rows_worked_example():
+    P = 99
+    # non-PAD prefix counts minus one; a PAD inherits the row before it
+    assert list(O.opd_teacher_rows([5, P, 7, 8, P, P, 9], P)) == [0, 0, 1, 2, 2, 2, 3]
+    assert list(O.opd_teacher_rows([P, 4], P)) == [-1, 0]
+
+
+def test_opd_targets_closed_forms():
+    rng = np.random.default_rng(3)
+    V, T = 50, 12
+    ls = rng.standard_normal((T, V)) * 2
+    lt = rng.standard_normal((T, V)) * 2
+    y = rng.integers(0, V, T)
+    y[3] = -1
+    rows = np.arange(T)
+    d, a = O.opd_targets(ls, lt, rows, y)
+    # alpha = min(p_t / p_s, 1) from the probabilities themselves
+    ps = np.exp(ls) / np.exp(ls).sum(1, keepdims=True)
+    pt = np.exp(lt) / np.exp(lt).sum(1, keepdims=True)
+    for t in range(T):
+        if y[t] < 0:
+            assert d[t] == 0 and a[t] == 1
+            continue
+        np.testing.assert_allclose(a[t], min(pt[t, y[t]] / ps[t, y[t]], 1.0), rtol=1e-12)
+        np.testing.assert_allclose(d[t], np.log(ps[t, y[t]]) - np.log(pt[t, y[t]]), rtol=1e-10, atol=1e-12)
+    # a student equal to its teacher: d = 0, alpha = 1
+    d0, a0 = O.opd_targets(ls, ls, rows, np.abs(y))
+    np.testing.assert_allclose(d0, 0, atol=1e-12)
+    np.testing.assert_allclose(a0, 1, atol=1e-12)
+    # shifting a whole logit row changes nothing
+    d1, _ = O.opd_targets(ls + 7.5, lt - 3.0, rows, y)
+    np.testing.assert_allclose(d1, d, atol=1e-10)
+    # the teacher row map is honoured
+    rows2 = np.maximum(np.arange(T) - 1, 0)
+    d2, _ = O.opd_targets(ls, lt, rows2, y)
+    t = 5
+    np.testing.assert_allclose(d2[t], np.log(ps[t, y[t]]) - np.log(pt[t - 1, y[t]]), rtol=1e-10)
+
+
+def test_opd_sampled_kl_is_unbiased():
+    # E_{y ~ p_s}[log p_s(y) - log p_t(y)] = KL(p_s || p_t): the mean of d over
+    # draws from the student converges to the full-sum divergence
+    rng = np.random.default_rng(4)
+    V, N = 20, 40000
+    ls, lt = rng.standard_normal(V), rng.standard_normal(V)
+    ps = np.exp(ls) / np.exp(ls).sum()
+    pt = np.exp(lt) / np.exp(lt).sum()
+    kl = float(np.sum(ps * np.log(ps / pt)))
+    y = rng.choice(V, size=N, p=ps)
+    d, _ = O.opd_targets(np.tile(ls, (N, 1)), lt[None, :], np.zeros(N, int), y)
+    sd = np.std(d) / np.sqrt(N)
+    assert abs(d.mean() - kl) < 4 * sd
+
+
+def test_opd_loss_sums_by_parity():
+    d = np.array([1.0, 2.0, 3.0, 4.0, 5.0])
+    lab = np.array([1, 1, -1, 1, 1])
+    assert O.opd_loss_sums(d, lab) == [6.0, 2.0, 6.0, 2.0]

@@ -175,6 +175,33 @@ int pipo_regular_prefill_ragged(pipo_ctx *ctx, int32_t batch, const int32_t *d_t
 int pipo_regular_step(pipo_ctx *ctx, const int32_t *d_in_tok, int32_t *d_tok, float *d_logits,
                       void *stream);
 
+/* ---- OPD training targets (App. C; no context needed) ---------------------
+ * pipo_opd_teacher_rows: PAD compaction of the teacher pass.  For a
+ * trajectory d_tokens (device int32 [T]) whose PADs the teacher never saw,
+ * d_rows[t] (device int32 [T]) = (number of non-PAD tokens in tokens[0..t])
+ * - 1: the teacher row of the last non-PAD position at or before t (-1 where
+ * there is none).  Errors: PIPO_EINVAL (NULL pointers, T < 0).
+ *
+ * pipo_opd_targets: for each position t < T with label y = d_labels[t] >= 0,
+ *   d_kl[t]    = log p_s(y) - log p_t(y), the sampled reverse-KL term,
+ *   d_alpha[t] = exp(-max(d_kl[t], 0)) = min(p_t(y) / p_s(y), 1), the
+ *                confidence head's target,
+ * with p_s = softmax(d_logits_s[t]) (device float [T][V]) and p_t =
+ * softmax(d_logits_t[r]) (device float [Tt][V]), r = d_teacher_rows[t]
+ * (device int32 [T]; NULL: r = t).  Positions with a negative label are not
+ * scored (kl 0, alpha 1); a scored position whose row is outside [0, Tt) or
+ * whose label is >= V gets NaN.  When d_sums (device double [4]) is
+ * non-NULL it receives {sum of kl, count} over the scored even positions
+ * (backbone head), then over the odd ones (MTP head), added in a fixed
+ * order.  The paper calls this per chunk of up to 2048 positions; T = 0 is
+ * allowed (the arrays may then be NULL).  Errors: PIPO_EINVAL (NULL pointers
+ * with T > 0, T < 0, V or Tt < 1, V not a multiple of 4, logit arrays not
+ * 16-byte aligned), PIPO_EHIP (launch failure). */
+int pipo_opd_teacher_rows(const int32_t *d_tokens, int32_t T, int32_t pad_id, int32_t *d_rows, void *stream);
+int pipo_opd_targets(int32_t T, int32_t V, const float *d_logits_s, const float *d_logits_t, int32_t Tt,
+                     const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl, float *d_alpha,
+                     double *d_sums, void *stream);
+
 /* Release a context and all its device memory.  NULL is a no-op (returns 0). */
 int pipo_free(pipo_ctx *ctx);
 

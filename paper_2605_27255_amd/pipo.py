@@ -16,7 +16,8 @@ LIB_PATH = os.path.join(PKG_DIR, "libpipo.so")
 PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -1, -2, -3, -4, -5
 EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step",
             "pipo_regular_prefill", "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free",
-            "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read")
+            "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read",
+            "pipo_opd_teacher_rows", "pipo_opd_targets")
 #: kernel classes of the profiling counters (PIPO_K_* in include/pipo.h)
 KERNEL_CLASSES = ("gemv_layer", "gemv_lmhead", "gemv_small", "attn_decode", "sample", "gate",
                   "prefill_gemm", "prefill_attn", "prefill_misc")
@@ -74,9 +75,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_read_weight.argtypes = [vp, ctypes.c_char_p, i64, i64, vp]
     lib.pipo_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.pipo_profile_read.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
+    lib.pipo_opd_teacher_rows.argtypes = [vp, i32, i32, vp, vp]
+    lib.pipo_opd_targets.argtypes = [i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     for fn in ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step", "pipo_regular_prefill",
                "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free", "pipo_read_weight",
-               "pipo_profile_enable", "pipo_profile_read"):
+               "pipo_profile_enable", "pipo_profile_read", "pipo_opd_teacher_rows", "pipo_opd_targets"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -245,3 +248,38 @@ def unpack_pairs(out):
     import numpy as np
     a = out.cpu().numpy()
     return a[:, 0].copy(), a[:, 1].copy(), a[:, 2].copy().view(np.float32), a[:, 3].copy()
+
+
+def _opd_check(lib, rc):
+    if rc != PIPO_OK:
+        raise PipoError(rc, "pipo_opd_*: invalid arguments or launch failure")
+
+
+def opd_teacher_rows(tokens, pad_id: int):
+    """PAD-compaction teacher rows of a trajectory (int32 CUDA tensor [T])."""
+    import torch
+    lib = load_library()
+    assert tokens.dtype == torch.int32 and tokens.is_cuda and tokens.dim() == 1 and tokens.is_contiguous()
+    rows = torch.empty_like(tokens)
+    _opd_check(lib, lib.pipo_opd_teacher_rows(_ptr(tokens), tokens.numel(), int(pad_id), _ptr(rows),
+                                              ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
+    return rows
+
+
+def opd_targets(logits_s, logits_t, labels, rows=None, sums: bool = True):
+    """Sampled reverse-KL terms and confidence targets of the OPD loss.
+    logits_s: float32 CUDA [T, V]; logits_t: float32 CUDA [Tt, V]; labels:
+    int32 CUDA [T] (negative: not scored); rows: int32 CUDA [T] teacher rows
+    (None: row t).  Returns (kl [T], alpha [T], sums [4] float64 or None)."""
+    import torch
+    lib = load_library()
+    for x in (logits_s, logits_t):
+        assert x.dtype == torch.float32 and x.is_cuda and x.dim() == 2 and x.is_contiguous()
+    T, V = logits_s.shape
+    kl = torch.empty(T, dtype=torch.float32, device="cuda")
+    alpha = torch.empty(T, dtype=torch.float32, device="cuda")
+    sm = torch.empty(4, dtype=torch.float64, device="cuda") if sums else None
+    _opd_check(lib, lib.pipo_opd_targets(T, V, _ptr(logits_s), _ptr(logits_t), logits_t.shape[0], _ptr(rows),
+                                         _ptr(labels), _ptr(kl), _ptr(alpha), _ptr(sm),
+                                         ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
+    return kl, alpha, sm

@@ -88,6 +88,15 @@ def test_null_arguments(lib):
     assert lib.pipo_prefill(None, 1, None, 4, ctypes.byref(smp), None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_decode_step(None, None, None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_regular_prefill(None, 1, None, 4, ctypes.byref(smp), None, None, None) == pipo.PIPO_EINVAL
+    # OPD targets: argument checks come before any device work
+    fake = ctypes.c_void_p(16)
+    assert lib.pipo_opd_teacher_rows(None, 4, 0, fake, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_opd_teacher_rows(fake, -1, 0, fake, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_opd_targets(4, 8, None, fake, 4, None, fake, fake, fake, None, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_opd_targets(4, 6, fake, fake, 4, None, fake, fake, fake, None, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_opd_targets(4, 8, ctypes.c_void_p(20), fake, 4, None, fake, fake, fake, None,
+                                None) == pipo.PIPO_EINVAL
+    assert lib.pipo_opd_targets(4, 8, fake, fake, 0, None, fake, fake, fake, None, None) == pipo.PIPO_EINVAL
     lens = (ctypes.c_int32 * 1)(4)
     assert lib.pipo_prefill_ragged(None, 1, None, 4, lens, ctypes.byref(smp), None, None, None, None) == pipo.PIPO_EINVAL
     assert lib.pipo_prefill_ragged(None, 1, None, 4, None, ctypes.byref(smp), None, None, None, None) == pipo.PIPO_EINVAL

@@ -140,6 +140,39 @@ def cpu_baseline(wl, accept_rate, budget_s=12.0):
                        f"tokens per pair step 1 + {accept_rate:.3f} (GPU-measured acceptance)")}
 
 
+def opd_leg(T=2048, V=151936, reps=20):
+    """The OPD target kernel (App. C) on one chunk of the paper's size: T
+    positions of student and teacher logits over V tokens, already in HBM.
+    Algorithmic bytes: both fp32 logit rows of every position, plus labels,
+    rows and the two fp32 outputs."""
+    import torch
+    from paper_2605_27255_amd import opd_targets
+    g = torch.Generator(device="cuda").manual_seed(0)
+    ls = torch.randn((T, V), generator=g, device="cuda", dtype=torch.float32) * 3.0
+    lt = ls + torch.randn((T, V), generator=g, device="cuda", dtype=torch.float32) * 0.5
+    labels = torch.randint(0, V, (T,), generator=g, device="cuda", dtype=torch.int32)
+    for _ in range(3):
+        opd_targets(ls, lt, labels, None, sums=False)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        opd_targets(ls, lt, labels, None, sums=False)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = 2 * T * V * 4 + T * 4 * 3
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    del ls, lt
+    torch.cuda.empty_cache()
+    log(f"OPD targets: {T} x {V}: {ms * 1e3:.1f} us per chunk, {gbs:.0f} GB/s")
+    return {"kernel": "k_opd", "positions": T, "vocab": V, "us_per_chunk": round(ms * 1e3, 2),
+            "algorithmic_bytes": nbytes, "achieved_gbs": round(gbs, 1), "bound": "hbm",
+            "frac_of_8tbs": round(gbs / HBM_PEAK_GBS, 4),
+            "timing": "torch events on the launching stream around 20 launches (the kernel is the only work)"}
+
+
 def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_s, emitted, reps):
     """Regular decoding of the same prompt on the same kernels: one timed job is
     the n-position prefill plus as many token steps as the pair decoder ran
@@ -206,6 +239,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-regular", action="store_true", help="skip the regular-decoding baseline leg")
+    ap.add_argument("--no-opd", action="store_true", help="skip the OPD target kernel leg")
     ap.add_argument("--heads", choices=("linear", "paper"), default="linear",
                     help="linear: the workloads' one-linear heads; paper: the App. B forms of all three heads")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch (up to 64)")
@@ -363,6 +397,8 @@ def main():
     if not args.no_regular:
         result["regular"] = regular_leg(wl, prompts, seeds, ttft, ms_step, acc_rate, wall / args.steps,
                                         emitted_per_job, max(1, min(args.steps, 2)))
+    if not args.no_opd:
+        result["opd"] = opd_leg()
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         result["cpu_baseline"] = cpu_baseline(wl, acc_rate)

@@ -160,36 +160,59 @@ void launch_gather_tokens(const int32_t *tokens, const uint16_t *embed, int H, i
     hipLaunchKernelGGL(k_gather_tokens, dim3(grid), dim3(256), 0, s, tokens, embed, H, V, pad_id, g, x);
 }
 
-// ---- RMSNorm of fp32 rows into the tiled bf16 layout (one wave per row) ----
+// ---- RMSNorm of fp32 rows into the tiled bf16 layout ----------------------
+// One workgroup per 16-row tile row: wave w first forms the sums of squares
+// of rows 4w..4w+3 (the four rows' loads interleaved), then writes every
+// fourth 16x32 tile whole: lane l normalises row l mod 16, columns
+// 8 (l / 16) .. + 7 of the tile, so each store instruction covers one
+// contiguous 1 KB tile (full cache lines, no partial-line writes shared with
+// other workgroups).
 __global__ __launch_bounds__(256) void k_rmsnorm_tiled(const float *x, const float *gain, int H, float eps,
                                                        int M, uint16_t *xh, uint16_t *xl) {
-    const int lane = threadIdx.x & 63;
-    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (m >= M) return;
-    const float *xr = x + (int64_t)m * H;
-    float a = 0.f;
-    for (int k = lane * 4; k < H; k += 256) {
-        const float4 v = *(const float4 *)(xr + k);
-        a += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    __shared__ float s_sc[16];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r0 = blockIdx.x * 16;
+    if (r0 >= M) return;
+    {
+        const float *xr = x + (int64_t)(r0 + 4 * wave) * H;
+        float a[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int k = lane * 4; k < H; k += 256) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float4 v = *(const float4 *)(xr + (int64_t)q * H + k);
+                a[q] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float t = wave_sum(a[q]);
+            if (lane == 0) s_sc[4 * wave + q] = rsqrtf(t / (float)H + eps);
+        }
     }
-    a = wave_sum(a);
-    const float sc = rsqrtf(a / (float)H + eps);
-    for (int k = lane * 8; k < H; k += 512) {
+    __syncthreads();
+    const int j = lane & 15, c = lane >> 4;
+    const float sc = s_sc[j];
+    const float *xr = x + (int64_t)(r0 + j) * H;
+    const int KT = H >> 5;
+    uint16_t *th = xh + (int64_t)(r0 >> 4) * KT * 512 + lane * 8;
+    uint16_t *tl = xl + (int64_t)(r0 >> 4) * KT * 512 + lane * 8;
+    for (int kt = wave; kt < KT; kt += 4) {
+        const int k = kt * 32 + c * 8;
         const float4 x0 = *(const float4 *)(xr + k), x1 = *(const float4 *)(xr + k + 4);
         const float4 g0 = *(const float4 *)(gain + k), g1 = *(const float4 *)(gain + k + 4);
         const float f[8] = {x0.x * sc * g0.x, x0.y * sc * g0.y, x0.z * sc * g0.z, x0.w * sc * g0.w,
                             x1.x * sc * g1.x, x1.y * sc * g1.y, x1.z * sc * g1.z, x1.w * sc * g1.w};
         u32x4 hi, lo;
         split8(f, hi, lo);
-        const int64_t at = tiled_index(m, k, H);
-        *(u32x4 *)(xh + at) = hi;
-        *(u32x4 *)(xl + at) = lo;
+        *(u32x4 *)(th + (int64_t)kt * 512) = hi;
+        *(u32x4 *)(tl + (int64_t)kt * 512) = lo;
     }
 }
 
 void launch_rmsnorm_tiled(const float *x, const float *gain, int H, float eps, int M, uint16_t *xh,
                           uint16_t *xl, hipStream_t s) {
-    hipLaunchKernelGGL(k_rmsnorm_tiled, dim3((M + 3) / 4), dim3(256), 0, s, x, gain, H, eps, M, xh, xl);
+    // M is a multiple of 16 (chunk rows are padded to 32 per sequence)
+    hipLaunchKernelGGL(k_rmsnorm_tiled, dim3((M + 15) / 16), dim3(256), 0, s, x, gain, H, eps, M, xh, xl);
 }
 
 // ---- MFMA GEMM  C^T[N][M] = W[N][K] X[M][K]^T, both operands tiled ---------

@@ -168,8 +168,10 @@ __device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int d) {
     return ((uint64_t)hi << 32) | lo;
 }
 
+// round(e 2^40) for e in [0, 1]: exact in double, rounded to nearest even,
+// converted without branches (so the loads of a pass stay in flight)
 __device__ __forceinline__ uint64_t fixed_mass(float e) {
-    return (uint64_t)__double2ull_rn((double)e * 1099511627776.0);   // 2^40
+    return (uint64_t)__builtin_rint((double)e * 1099511627776.0);   // 2^40
 }
 
 // Unsigned image of a float that orders like the float (-0 taken as +0).
@@ -226,17 +228,59 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
             }
         }
     };
-    auto valid = [&](int t, int e) { return w0 + t * 256 + 4 * lane + e < V; };
+    // V is a multiple of 16, so a lane's four ids are all in range or all out.
+    // Conditions are combined with & and masses masked arithmetically (no
+    // short-circuit, no select around a load's use): otherwise the compiler
+    // sinks each load into its branch and a pass keeps one load in flight.
+    auto valid = [&](int t, int e) { (void)e; return w0 + t * 256 + 4 * lane < V; };
+    auto masked = [](bool ok, uint64_t m) { return m & (0ull - (uint64_t)ok); };
     const int nt = R / 256;
+    // every pass: four sub-tiles' loads issued together, then their use
+    auto for_tiles = [&](auto &&f) {
+        int t = 0;
+        for (; t + 4 <= nt; t += 4) {
+            float v[4][4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) load4(t + u, v[u]);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) f(t + u, v[u]);
+        }
+        for (; t < nt; ++t) {
+            float v[4];
+            load4(t, v);
+            f(t, v);
+        }
+    };
+    // Suffix sums S_k = sum_{k' >= k} hist[0][k'] of the merged histogram
+    // into s_suf (threads 0..255, a reversed wave scan); then each bin tests
+    // its own suffix, so the digit is one parallel step instead of a serial
+    // 256-step scan.
+    __shared__ unsigned long long s_suf[257], s_wtot[4];
+    __shared__ int s_dig;
+    auto suffix_sums = [&]() {
+        unsigned long long x = 0;
+        if (tid < 256) {
+            x = hist[0][255 - tid];
+            for (int d = 1; d < 64; d <<= 1) {
+                const unsigned long long y = shfl_up_u64(x, d);
+                if (lane >= d) x += y;
+            }
+            if (lane == 63) s_wtot[wave] = x;
+        }
+        if (tid == 0) { s_dig = -1; s_suf[256] = 0; }
+        __syncthreads();
+        if (tid < 256) {
+            for (int w = 0; w < wave; ++w) x += s_wtot[w];
+            s_suf[255 - tid] = x;
+        }
+        __syncthreads();
+    };
 
     float mx = -INFINITY;
-#pragma unroll 4
-    for (int t = 0; t < nt; ++t) {
-        float v[4];
-        load4(t, v);
+    for_tiles([&](int t, const float (&v)[4]) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) mx = valid(t, e) ? fmaxf(mx, v[e]) : mx;
-    }
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, valid(t, e) ? v[e] : -INFINITY);
+    });
     mx = wave_max(mx);
     if (lane == 0) s_red[wave] = mx;
     __syncthreads();
@@ -255,17 +299,14 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
                 for (int i = tid; i < kSampWaves * 256; i += kSampThreads) (&hist[0][0])[i] = 0;
                 __syncthreads();
                 const uint32_t prefix = s_kpre;
-#pragma unroll 2
-                for (int t = 0; t < nt; ++t) {
-                    float v[4];
-                    load4(t, v);
+                for_tiles([&](int t, const float (&v)[4]) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const uint32_t key = order_key(v[e]);
-                        if (valid(t, e) && (pass == 0 || (key >> (shift + 8)) == prefix))
+                        if (valid(t, e) & ((pass == 0) | ((key >> (shift + 8)) == prefix)))
                             atomicAdd(&hist[wave][(key >> shift) & 255u], 1ull);
                     }
-                }
+                });
                 __syncthreads();
                 if (tid < 256) {
                     unsigned long long h = 0;
@@ -273,15 +314,15 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
                     hist[0][tid] = h;
                 }
                 __syncthreads();
-                if (tid == 0) {   // the digit holding the rank-krem element, counting down
-                    uint32_t rem = s_krem;
-                    int d = 255;
-                    for (; d > 0; --d) {
-                        if (hist[0][d] >= rem) break;
-                        rem -= (uint32_t)hist[0][d];
-                    }
+                suffix_sums();
+                // the digit holding the rank-krem element: the largest d with S_d >= krem
+                const uint32_t krem = s_krem;
+                if (tid < 256 && s_suf[tid] >= krem) atomicMax(&s_dig, tid);
+                __syncthreads();
+                if (tid == 0) {
+                    const int d = s_dig < 0 ? 0 : s_dig;
                     s_kpre = (prefix << 8) | (uint32_t)d;
-                    s_krem = rem;
+                    s_krem = krem - (uint32_t)s_suf[d + 1];
                 }
                 __syncthreads();
             }
@@ -289,17 +330,14 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
         }
     }
     // kept: in the vocabulary and, with top-k, at least the k-th largest
-    auto kept = [&](int t, int e, float v) { return valid(t, e) && (!EVAL || order_key(v) >= kstar); };
+    auto kept = [&](int t, int e, float v) { return valid(t, e) & (!EVAL || order_key(v) >= kstar); };
 
     unsigned long long tot = 0;
-#pragma unroll 4
-    for (int t = 0; t < nt; ++t) {
-        float v[4];
-        load4(t, v);
+    for_tiles([&](int t, const float (&v)[4]) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            tot += kept(t, e, v[e]) ? fixed_mass(__builtin_amdgcn_exp2f((v[e] - mx) * kT)) : 0ull;
-    }
+            tot += masked(kept(t, e, v[e]), fixed_mass(__builtin_amdgcn_exp2f((v[e] - mx) * kT)));
+    });
     for (int o = 32; o > 0; o >>= 1) {
         const uint32_t lo = __shfl_xor((uint32_t)tot, o), hi = __shfl_xor((uint32_t)(tot >> 32), o);
         tot += ((unsigned long long)hi << 32) | lo;
@@ -316,18 +354,15 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
         for (int i = tid; i < kSampWaves * 256; i += kSampThreads) (&hist[0][0])[i] = 0;
         __syncthreads();
         const uint32_t prefix = s_prefix;
-#pragma unroll 2
-        for (int t = 0; t < nt; ++t) {
-            float v[4];
-            load4(t, v);
+        for_tiles([&](int t, const float (&v)[4]) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
                 const uint32_t key = __float_as_uint(ev);
-                if (kept(t, e, v[e]) && (pass == 0 || (key >> (shift + 8)) == prefix))
+                if (kept(t, e, v[e]) & ((pass == 0) | ((key >> (shift + 8)) == prefix)))
                     atomicAdd(&hist[wave][(key >> shift) & 255u], fixed_mass(ev));
             }
-        }
+        });
         __syncthreads();
         if (tid < 256) {   // merge the per-wave histograms
             unsigned long long h = 0;
@@ -335,22 +370,20 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
             hist[0][tid] = h;
         }
         __syncthreads();
+        suffix_sums();
+        // beta: the largest digit whose upper mass (the bins above it and
+        // itself) reaches the target
+        const unsigned long long above = s_above;
+        if (tid < 256 && (double)(above + s_suf[tid]) >= target) atomicMax(&s_dig, tid);
+        __syncthreads();
         if (tid == 0) {
-            unsigned long long above = s_above;
-            int beta = -1;
-            for (int k = 255; k >= 0; --k) {
-                if ((double)(above + hist[0][k]) >= target) { beta = k; break; }
-                above += hist[0][k];
-            }
+            const int beta = s_dig;
             if (beta < 0) {   // no value reaches top_p (rounding): every kept token
                 s_all = 1;
-                beta = 0;
-                above = s_above;
-            }
-            if (!s_all) {
-                s_above = above;
+            } else {
+                s_above = above + s_suf[beta + 1];
                 s_prefix = (prefix << 8) | (uint32_t)beta;
-                s_mass = above + hist[0][beta];
+                s_mass = above + s_suf[beta];
             }
         }
         __syncthreads();
@@ -365,16 +398,13 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
 
     // nucleus mass of each wave's id range, exclusive prefix over waves
     unsigned long long wm = 0;
-#pragma unroll 4
-    for (int t = 0; t < nt; ++t) {
-        float v[4];
-        load4(t, v);
+    for_tiles([&](int t, const float (&v)[4]) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
-            wm += (kept(t, e, v[e]) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
+            wm += masked(kept(t, e, v[e]) & (__float_as_uint(ev) >= theta), fixed_mass(ev));
         }
-    }
+    });
     for (int o = 32; o > 0; o >>= 1) {
         const uint32_t lo = __shfl_xor((uint32_t)wm, o), hi = __shfl_xor((uint32_t)(wm >> 32), o);
         wm += ((unsigned long long)hi << 32) | lo;
@@ -393,7 +423,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
-            m4[e] = (kept(t, e, v[e]) && __float_as_uint(ev) >= theta) ? fixed_mass(ev) : 0ull;
+            m4[e] = masked(kept(t, e, v[e]) & (__float_as_uint(ev) >= theta), fixed_mass(ev));
             loc += m4[e];
         }
         unsigned long long inc = loc;

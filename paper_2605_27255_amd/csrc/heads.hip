@@ -212,21 +212,27 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
         }
         if (p.extra_key) ex2 = argmax_key_id(p.extra_key[b]);
     }
-    // the four (penalised) logits of this lane in sub-tile t (ids past V read
-    // id 0, masked)
+    // The four logits of this lane in sub-tile t (ids past V read id 0,
+    // masked).  EVAL: the first pass reads the raw logits, applies the
+    // penalty and keeps the penalised row in p.pen (each lane rereads only
+    // what it wrote itself); every later pass reads that row.
+    const float *src = lg;
+    float *pen = EVAL ? p.pen + (int64_t)b * V : nullptr;
     auto load4 = [&](int t, float (&v)[4]) {
         const int id = w0 + t * 256 + 4 * lane;
-        const float4 q = *(const float4 *)(lg + (id + 3 < V ? id : 0));
+        const float4 q = *(const float4 *)(src + (id + 3 < V ? id : 0));
         v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
-        if constexpr (EVAL) {
-            const uint32_t bits = (seen && id < V) ? seen[id >> 5] >> (id & 31) : 0u;
+    };
+    auto penalise = [&](int t, float (&v)[4]) {
+        const int id = w0 + t * 256 + 4 * lane;
+        const uint32_t bits = (seen && id < V) ? seen[id >> 5] >> (id & 31) : 0u;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int j = id + e;
-                if (((bits >> e) & 1u) || j == ex0 || j == ex1 || j == ex2)
-                    v[e] = v[e] > 0.f ? v[e] / p.rep_penalty : v[e] * p.rep_penalty;
-            }
+        for (int e = 0; e < 4; ++e) {
+            const int j = id + e;
+            if (((bits >> e) & 1u) || j == ex0 || j == ex1 || j == ex2)
+                v[e] = v[e] > 0.f ? v[e] / p.rep_penalty : v[e] * p.rep_penalty;
         }
+        if (id + 3 < V) *(float4 *)(pen + id) = make_float4(v[0], v[1], v[2], v[3]);
     };
     // V is a multiple of 16, so a lane's four ids are all in range or all out.
     // Conditions are combined with & and masses masked arithmetically (no
@@ -277,10 +283,13 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
     };
 
     float mx = -INFINITY;
-    for_tiles([&](int t, const float (&v)[4]) {
+    for_tiles([&](int t, const float (&v0)[4]) {
+        float v[4] = {v0[0], v0[1], v0[2], v0[3]};
+        if constexpr (EVAL) penalise(t, v);
 #pragma unroll
         for (int e = 0; e < 4; ++e) mx = fmaxf(mx, valid(t, e) ? v[e] : -INFINITY);
     });
+    if constexpr (EVAL) src = pen;
     mx = wave_max(mx);
     if (lane == 0) s_red[wave] = mx;
     __syncthreads();

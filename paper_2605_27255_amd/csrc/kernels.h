@@ -114,6 +114,7 @@ struct SampleParams {
     const uint32_t *seen; int seen_words;   // penalised tokens per sequence
     const int32_t *pairs; int32_t pad_id;   // the step's input pair, also penalised (NULL: none)
     const uint64_t *extra_key;              // argmax key of one more penalised token (NULL: none)
+    float *pen;                             // workspace [B][V]: the penalised logits
 };
 void launch_sample(const SampleParams &p, hipStream_t s);
 

@@ -70,6 +70,7 @@ struct pipo_ctx {
     uint64_t *best_b, *best_d, *seeds;
     int32_t *pairs, *pos, *step;
     uint32_t *seen; int seen_words;   // penalised-token bitmap per sequence (evaluation sampler)
+    float *pen;                       // penalised logits [Bmax][V] (evaluation sampler workspace)
     pipo_pair *out;
     // prefill activations
     uint16_t *p_xin, *p_xn, *p_xn_lo, *p_q, *p_o, *p_o_lo, *p_act, *p_act_lo;
@@ -290,6 +291,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->ntok = a.take<int32_t>(B);
         c->seen_words = (V + 31) / 32;
         c->seen = a.take<uint32_t>((int64_t)B * c->seen_words);
+        c->pen = a.take<float>((int64_t)B * V);
         c->pos = a.take<int32_t>(B);
         c->step = a.take<int32_t>(B);
         c->out = a.take<pipo_pair>(B);
@@ -454,6 +456,7 @@ static SampleParams sample_params(pipo_ctx *c, const float *logits, int B, int s
         sp.seen = c->seen; sp.seen_words = c->seen_words;
         sp.pairs = in_pair ? c->pairs : nullptr; sp.pad_id = c->pad_id;
         sp.extra_key = extra;
+        sp.pen = c->pen;
     }
     return sp;
 }

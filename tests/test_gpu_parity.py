@@ -640,3 +640,30 @@ def test_4b_width_batch64_top_p(torch):
     rep, _ = run_parity(m, W, prompts, steps, smp, log)
     rep.check()
     m.close()
+
+
+def test_tiny_paper_heads_ragged_eval_sampler(torch):
+    """All three App. B heads, a ragged batch and the evaluation sampler
+    together: the draft penalises its pair's backbone token, which is also the
+    MTP layer's input."""
+    cfg = ModelConfig(**{**TINY.__dict__, "gain_mode": 1, "heads": HEADS_PAPER})
+    lens = [2, 27, 40, 9]
+    B, steps = len(lens), 5
+    prompts = _ragged(B, lens, cfg.vocab, 70)
+    m = _model(cfg, seed=13, max_batch=4, max_latent=20 + steps + 1, prefill_chunk=8)
+    W = O.OracleWeights.generate(cfg, seed=13, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, _eval_smp(B, base=1100), log, conf_tol=APPB_CONF,
+                        max_abs_tol=APPB_MAX_ABS, lens=lens)
+    rep.check()
+    m.close()
+
+
+def test_tiny_regular_ragged_eval_sampler(torch):
+    lens = [3, 31, 18]
+    B, steps = len(lens), 6
+    prompts = _ragged(B, lens, TINY.vocab, 71)
+    m = _model(TINY, seed=6, max_batch=3, max_latent=31 + steps + 1, prefill_chunk=16)
+    W = O.OracleWeights.generate(TINY, seed=6, precision="bf16")
+    rep, _ = run_regular_parity(m, W, prompts, steps, _eval_smp(B, tau=0.0, base=1200), log, lens=lens)
+    rep.check()
+    m.close()

@@ -388,6 +388,21 @@ def main():
                                         "eager profiling pass after the timed region"}
         result["kernel_ms_per_pair_step"] = per_class
         result["prefill_kernel_ms"] = {k: round(v[0], 3) for k, v in pre.items() if v[1]}
+        if pre.get("prefill_gemm", (0, 0))[1]:
+            # the prefill GEMMs (k_gemm_wd): 2 flops per weight per latent row; every
+            # layer GEMM also multiplies the activations' lo plane (a second MFMA)
+            h, f, L = m.hidden, m.ffn, m.n_layers
+            layer_w = (m.q_dim + 2 * m.kv_dim) * h + h * m.q_dim + 2 * f * h + h * f
+            rows = B * wl.latents
+            useful = 2.0 * rows * (L * layer_w + 2 * h * h)
+            issued = 2.0 * rows * (2 * L * layer_w + 2 * h * h)
+            sec = pre["prefill_gemm"][0] * 1e-3
+            result["prefill_gemm"] = {
+                "kernel": "k_gemm_wd", "bound": "mfma", "peak_tflops": 2500.0,
+                "useful_tflops": round(useful / sec / 1e12, 1), "issued_tflops": round(issued / sec / 1e12, 1),
+                "issued_frac": round(issued / sec / 1e12 / 2500.0, 4),
+                "note": "issued counts the lo-plane MFMAs (activations carried as bf16 hi + lo); times are the "
+                        "profiling pass's HIP events around every prefill GEMM launch"}
         log("per-class decode ms/step:", {k: v["ms_per_step"] for k, v in per_class.items()})
         log("prefill kernel ms:", result["prefill_kernel_ms"])
 

@@ -164,12 +164,24 @@ def opd_leg(T=2048, V=151936, reps=20):
     ms = e0.elapsed_time(e1) / reps
     nbytes = 2 * T * V * 4 + T * 4 * 3
     gbs = nbytes / (ms * 1e-3) / 1e9
+    # the same chunk with bf16 logit rows
+    ls, lt = ls.to(torch.bfloat16), lt.to(torch.bfloat16)
+    for _ in range(3):
+        opd_targets(ls, lt, labels, None, sums=False)
+    e0.record(stream)
+    for _ in range(reps):
+        opd_targets(ls, lt, labels, None, sums=False)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms16 = e0.elapsed_time(e1) / reps
+    gbs16 = (2 * T * V * 2 + T * 4 * 3) / (ms16 * 1e-3) / 1e9
     del ls, lt
     torch.cuda.empty_cache()
-    log(f"OPD targets: {T} x {V}: {ms * 1e3:.1f} us per chunk, {gbs:.0f} GB/s")
+    log(f"OPD targets: {T} x {V}: {ms * 1e3:.1f} us per chunk, {gbs:.0f} GB/s (bf16 rows {ms16 * 1e3:.1f} us)")
     return {"kernel": "k_opd", "positions": T, "vocab": V, "us_per_chunk": round(ms * 1e3, 2),
             "algorithmic_bytes": nbytes, "achieved_gbs": round(gbs, 1), "bound": "hbm",
             "frac_of_8tbs": round(gbs / HBM_PEAK_GBS, 4),
+            "bf16_rows": {"us_per_chunk": round(ms16 * 1e3, 2), "achieved_gbs": round(gbs16, 1)},
             "timing": "torch events on the launching stream around 20 launches (the kernel is the only work)"}
 
 

@@ -201,6 +201,11 @@ int pipo_opd_teacher_rows(const int32_t *d_tokens, int32_t T, int32_t pad_id, in
 int pipo_opd_targets(int32_t T, int32_t V, const float *d_logits_s, const float *d_logits_t, int32_t Tt,
                      const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl, float *d_alpha,
                      double *d_sums, void *stream);
+/* As pipo_opd_targets, with bf16 logit rows (device uint16 bit patterns,
+ * [T][V] and [Tt][V], 8-byte aligned); the arithmetic is the same fp32. */
+int pipo_opd_targets_bf16(int32_t T, int32_t V, const uint16_t *d_logits_s, const uint16_t *d_logits_t, int32_t Tt,
+                          const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl, float *d_alpha,
+                          double *d_sums, void *stream);
 
 /* Release a context and all its device memory.  NULL is a no-op (returns 0). */
 int pipo_free(pipo_ctx *ctx);

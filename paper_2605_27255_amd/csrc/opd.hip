@@ -65,7 +65,27 @@ __device__ __forceinline__ Lse lse_merge(Lse a, Lse b) {
     return Lse{m, a.s * exp_e(a.m - m) + b.s * exp_e(b.m - m)};
 }
 
-__global__ __launch_bounds__(kOpdThreads) void k_opd(const float *ls, const float *lt, const int32_t *rows,
+// Four consecutive logits as floats: fp32 rows (one 16-byte load) or bf16
+// rows (one 8-byte load, widened exactly).
+template <typename L> struct Logit4;
+template <> struct Logit4<float> {
+    static __device__ __forceinline__ f32x4 load(const float *row, int i) {
+        return __builtin_nontemporal_load((const f32x4 *)row + i);
+    }
+    static __device__ __forceinline__ float at(const float *row, int y) { return row[y]; }
+};
+template <> struct Logit4<uint16_t> {
+    static __device__ __forceinline__ f32x4 load(const uint16_t *row, int i) {
+        const u32x2 w = __builtin_nontemporal_load((const u32x2 *)row + i);
+        return f32x4{bf_lo(w[0]), bf_hi(w[0]), bf_lo(w[1]), bf_hi(w[1])};
+    }
+    static __device__ __forceinline__ float at(const uint16_t *row, int y) {
+        return __uint_as_float((uint32_t)row[y] << 16);
+    }
+};
+
+template <typename L>
+__global__ __launch_bounds__(kOpdThreads) void k_opd(const L *ls, const L *lt, const int32_t *rows,
                                                      const int32_t *labels, int T, int V, int Tt, float *kl,
                                                      float *alpha) {
     __shared__ Lse s_red[2][kOpdThreads / 64];
@@ -80,13 +100,13 @@ __global__ __launch_bounds__(kOpdThreads) void k_opd(const float *ls, const floa
         if (tid == 0) { kl[t] = __builtin_nanf(""); alpha[t] = __builtin_nanf(""); }
         return;
     }
-    const float *rs = ls + (int64_t)t * V;
-    const float *rt = lt + (int64_t)r * V;
+    const L *rs = ls + (int64_t)t * V;
+    const L *rt = lt + (int64_t)r * V;
     Lse a{-INFINITY, 0.f}, b{-INFINITY, 0.f};
     const int V4 = V >> 2;
     for (int i = tid; i < V4; i += kOpdThreads) {
-        a = lse_add4(a, __builtin_nontemporal_load((const f32x4 *)rs + i));
-        b = lse_add4(b, __builtin_nontemporal_load((const f32x4 *)rt + i));
+        a = lse_add4(a, Logit4<L>::load(rs, i));
+        b = lse_add4(b, Logit4<L>::load(rt, i));
     }
     for (int o = 32; o > 0; o >>= 1) {
         a = lse_merge(a, Lse{__shfl_xor(a.m, o), __shfl_xor(a.s, o)});
@@ -100,8 +120,8 @@ __global__ __launch_bounds__(kOpdThreads) void k_opd(const float *ls, const floa
             A = lse_merge(A, s_red[0][w]);
             Bt = lse_merge(Bt, s_red[1][w]);
         }
-        const float lps = rs[y] - (A.m + logf(A.s));
-        const float lpt = rt[y] - (Bt.m + logf(Bt.s));
+        const float lps = Logit4<L>::at(rs, y) - (A.m + logf(A.s));
+        const float lpt = Logit4<L>::at(rt, y) - (Bt.m + logf(Bt.s));
         const float d = lps - lpt;
         kl[t] = d;
         alpha[t] = expf(-fmaxf(d, 0.f));
@@ -143,17 +163,32 @@ extern "C" int pipo_opd_teacher_rows(const int32_t *d_tokens, int32_t T, int32_t
     return hipGetLastError() == hipSuccess ? PIPO_OK : PIPO_EHIP;
 }
 
-extern "C" int pipo_opd_targets(int32_t T, int32_t V, const float *d_logits_s, const float *d_logits_t, int32_t Tt,
-                                const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl, float *d_alpha,
-                                double *d_sums, void *stream) {
+template <typename L>
+static int opd_targets(int32_t T, int32_t V, const L *d_logits_s, const L *d_logits_t, int32_t Tt,
+                       const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl, float *d_alpha,
+                       double *d_sums, void *stream) {
     if (T < 0 || V < 1 || Tt < 1 || V % 4) return PIPO_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     if (T > 0) {   // an empty chunk needs no arrays (its sums are zero)
         if (!d_logits_s || !d_logits_t || !d_labels || !d_kl || !d_alpha) return PIPO_EINVAL;
-        if (((uintptr_t)d_logits_s | (uintptr_t)d_logits_t) & 15) return PIPO_EINVAL;   // float4 rows
-        hipLaunchKernelGGL(k_opd, dim3(T), dim3(kOpdThreads), 0, s, d_logits_s, d_logits_t, d_teacher_rows, d_labels,
-                           T, V, Tt, d_kl, d_alpha);
+        if (((uintptr_t)d_logits_s | (uintptr_t)d_logits_t) & (4 * sizeof(L) - 1)) return PIPO_EINVAL;   // 4-value rows
+        hipLaunchKernelGGL(k_opd<L>, dim3(T), dim3(kOpdThreads), 0, s, d_logits_s, d_logits_t, d_teacher_rows,
+                           d_labels, T, V, Tt, d_kl, d_alpha);
     }
     if (d_sums) hipLaunchKernelGGL(k_opd_sums, dim3(1), dim3(1024), 0, s, d_kl, d_labels, T, d_sums);
     return hipGetLastError() == hipSuccess ? PIPO_OK : PIPO_EHIP;
+}
+
+extern "C" int pipo_opd_targets(int32_t T, int32_t V, const float *d_logits_s, const float *d_logits_t, int32_t Tt,
+                                const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl, float *d_alpha,
+                                double *d_sums, void *stream) {
+    return opd_targets<float>(T, V, d_logits_s, d_logits_t, Tt, d_teacher_rows, d_labels, d_kl, d_alpha, d_sums,
+                              stream);
+}
+
+extern "C" int pipo_opd_targets_bf16(int32_t T, int32_t V, const uint16_t *d_logits_s, const uint16_t *d_logits_t,
+                                     int32_t Tt, const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl,
+                                     float *d_alpha, double *d_sums, void *stream) {
+    return opd_targets<uint16_t>(T, V, d_logits_s, d_logits_t, Tt, d_teacher_rows, d_labels, d_kl, d_alpha, d_sums,
+                                 stream);
 }

@@ -17,7 +17,7 @@ PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -
 EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step",
             "pipo_regular_prefill", "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free",
             "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read",
-            "pipo_opd_teacher_rows", "pipo_opd_targets")
+            "pipo_opd_teacher_rows", "pipo_opd_targets", "pipo_opd_targets_bf16")
 #: kernel classes of the profiling counters (PIPO_K_* in include/pipo.h)
 KERNEL_CLASSES = ("gemv_layer", "gemv_lmhead", "gemv_small", "attn_decode", "sample", "gate",
                   "prefill_gemm", "prefill_attn", "prefill_misc")
@@ -77,9 +77,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_profile_read.argtypes = [vp, ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     lib.pipo_opd_teacher_rows.argtypes = [vp, i32, i32, vp, vp]
     lib.pipo_opd_targets.argtypes = [i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
+    lib.pipo_opd_targets_bf16.argtypes = [i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     for fn in ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step", "pipo_regular_prefill",
                "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free", "pipo_read_weight",
-               "pipo_profile_enable", "pipo_profile_read", "pipo_opd_teacher_rows", "pipo_opd_targets"):
+               "pipo_profile_enable", "pipo_profile_read", "pipo_opd_teacher_rows", "pipo_opd_targets",
+               "pipo_opd_targets_bf16"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -268,18 +270,20 @@ def opd_teacher_rows(tokens, pad_id: int):
 
 def opd_targets(logits_s, logits_t, labels, rows=None, sums: bool = True):
     """Sampled reverse-KL terms and confidence targets of the OPD loss.
-    logits_s: float32 CUDA [T, V]; logits_t: float32 CUDA [Tt, V]; labels:
+    logits_s: float32 or bfloat16 CUDA [T, V]; logits_t: the same dtype, [Tt, V]; labels:
     int32 CUDA [T] (negative: not scored); rows: int32 CUDA [T] teacher rows
     (None: row t).  Returns (kl [T], alpha [T], sums [4] float64 or None)."""
     import torch
     lib = load_library()
     for x in (logits_s, logits_t):
-        assert x.dtype == torch.float32 and x.is_cuda and x.dim() == 2 and x.is_contiguous()
+        assert x.dtype in (torch.float32, torch.bfloat16) and x.is_cuda and x.dim() == 2 and x.is_contiguous()
+    assert logits_s.dtype == logits_t.dtype
+    fn = lib.pipo_opd_targets if logits_s.dtype == torch.float32 else lib.pipo_opd_targets_bf16
     T, V = logits_s.shape
     kl = torch.empty(T, dtype=torch.float32, device="cuda")
     alpha = torch.empty(T, dtype=torch.float32, device="cuda")
     sm = torch.empty(4, dtype=torch.float64, device="cuda") if sums else None
-    _opd_check(lib, lib.pipo_opd_targets(T, V, _ptr(logits_s), _ptr(logits_t), logits_t.shape[0], _ptr(rows),
+    _opd_check(lib, fn(T, V, _ptr(logits_s), _ptr(logits_t), logits_t.shape[0], _ptr(rows),
                                          _ptr(labels), _ptr(kl), _ptr(alpha), _ptr(sm),
                                          ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
     return kl, alpha, sm

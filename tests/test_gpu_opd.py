@@ -111,3 +111,21 @@ def test_opd_targets_edges(torch):
     kl, alpha, _ = opd_targets(ls, ls, lab, rows)
     torch.cuda.synchronize()
     assert torch.isnan(kl[7]) and torch.isnan(alpha[7]) and not torch.isnan(kl[:7]).any()
+
+
+def test_opd_targets_bf16_rows(torch):
+    """bf16 logit rows: the oracle on the same bf16 values (exact in float64)."""
+    from paper_2605_27255_amd import opd_targets
+    T, V = 96, 151936
+    tok, labels, ls, lt, pad = _inputs(T, V, seed=9)
+    rows = O.opd_teacher_rows(tok, pad)
+    ls_b = torch.from_numpy(ls).cuda().to(torch.bfloat16)
+    lt_b = torch.from_numpy(lt).cuda().to(torch.bfloat16)
+    kl, alpha, sums = opd_targets(ls_b, lt_b, torch.from_numpy(labels).cuda(),
+                                  torch.from_numpy(rows.astype(np.int32)).cuda())
+    torch.cuda.synchronize()
+    ls64 = ls_b.float().cpu().numpy().astype(np.float64)
+    lt64 = lt_b.float().cpu().numpy().astype(np.float64)
+    d_ref, a_ref = O.opd_targets(ls64, lt64, rows, labels)
+    assert np.max(np.abs(kl.cpu().numpy() - d_ref)) <= KL_TOL
+    assert np.max(np.abs(alpha.cpu().numpy() - a_ref)) <= KL_TOL

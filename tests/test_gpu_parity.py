@@ -667,3 +667,20 @@ def test_tiny_regular_ragged_eval_sampler(torch):
     rep, _ = run_regular_parity(m, W, prompts, steps, _eval_smp(B, tau=0.0, base=1200), log, lens=lens)
     rep.check()
     m.close()
+
+
+def test_empty_inputs_are_refused(torch):
+    """An empty prompt or an empty batch is refused with PIPO_EINVAL before any device work."""
+    from paper_2605_27255_amd import PipoError, PIPO_EINVAL
+    m = _model(TINY, seed=0, max_batch=2, max_latent=16, prefill_chunk=16)
+    for shape in ((1, 0), (0, 8)):
+        t = torch.zeros(shape, dtype=torch.int32, device="cuda")
+        for call in (lambda: m.prefill(t, 0.5), lambda: m.regular_prefill(t)):
+            with pytest.raises(PipoError) as e:
+                call()
+            assert e.value.code == PIPO_EINVAL
+    # the context still works afterwards
+    m.prefill(torch.from_numpy(rspec.prompt_tokens(2, 6, TINY.vocab)).cuda(), 0.5)
+    m.decode_step()
+    torch.cuda.synchronize()
+    m.close()

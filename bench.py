@@ -185,7 +185,7 @@ def opd_leg(T=2048, V=151936, reps=20):
             "timing": "torch events on the launching stream around 20 launches (the kernel is the only work)"}
 
 
-def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_s, emitted, reps):
+def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_s, lens, emitted, reps):
     """Regular decoding of the same prompt on the same kernels: one timed job is
     the n-position prefill plus as many token steps as the pair decoder ran
     pair steps; ``reps`` timed jobs after one warm-up."""
@@ -204,7 +204,8 @@ def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_
     def job(ev=None):
         if ev:
             ev[0].record(stream)
-        model.regular_prefill(prompts, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty)
+        model.regular_prefill(prompts, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty,
+                              lens=lens)
         if ev:
             ev[1].record(stream)
         for s in range(steps):
@@ -255,6 +256,8 @@ def main():
     ap.add_argument("--heads", choices=("linear", "paper"), default="linear",
                     help="linear: the workloads' one-linear heads; paper: the App. B forms of all three heads")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch (up to 64)")
+    ap.add_argument("--ragged", action="store_true",
+                    help="a ragged batch: sequence b's prompt is the first n - (7919 b mod n/2) tokens of its row")
     ap.add_argument("--sampler", choices=("workload", "eval"), default="workload",
                     help="workload: the workload's own selection; eval: the paper's evaluation sampler "
                          "(T 1.0, top-p 0.95, top-k 20, repetition penalty 1.5)")
@@ -290,6 +293,8 @@ def main():
         wl = replace(wl, name=wl.name + "+appB-heads", model=replace(wl.model, heads=HEADS_PAPER))
     if args.batch is not None:
         wl = replace(wl, name=f"{wl.name}@bs{args.batch}", batch=args.batch)
+    if args.ragged:
+        wl = replace(wl, name=wl.name + "+ragged")
     if args.sampler == "eval":
         wl = replace(wl, name=wl.name + "+eval-sampler", temperature=1.0, top_p=0.95, top_k=20, rep_penalty=1.5)
     m = wl.model
@@ -301,6 +306,9 @@ def main():
     model = PipoModel(m, seed=wl.seed, max_batch=B, max_latent=wl.latents + steps + 1,
                       prefill_chunk=wl.prefill_chunk)
     prompts = torch.from_numpy(rspec.prompt_tokens(B, wl.prompt_tokens, m.vocab, wl.prompt_seed)).cuda()
+    n_tok = wl.prompt_tokens
+    lens = [n_tok - (7919 * b) % max(1, n_tok // 2) for b in range(B)] if args.ragged else None
+    lat = [(n + 1) // 2 for n in lens] if lens else [wl.latents] * B
     seeds = [wl.sample_seed_base + b for b in range(B)] if wl.temperature > 0 else None
     outs = torch.empty((steps, B, 4), dtype=torch.int32, device="cuda")
     torch.cuda.synchronize()
@@ -312,7 +320,7 @@ def main():
         if ev:
             ev[0].record(stream)
         first, _, _ = model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k,
-                                    rep_penalty=wl.rep_penalty)
+                                    rep_penalty=wl.rep_penalty, lens=lens)
         if ev:
             ev[1].record(stream)
         for s in range(steps):
@@ -344,7 +352,7 @@ def main():
     dec_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     ms_step = dec_ms / max(steps, 1)
     acc_rate = accepts / pairs
-    kv_mean = float(np.mean([kv_step_bytes(m, B, wl.latents + s) for s in range(max(steps, 1))]))
+    kv_mean = float(np.mean([sum(kv_step_bytes(m, 1, L + s) for L in lat) for s in range(max(steps, 1))]))
     step_bytes = gemv_step_bytes(m, B) + kv_mean
     log(f"timed {args.steps} requests in {wall:.3f} s: TTFT {ttft:.2f} ms, decode {ms_step:.3f} ms/pair step, "
         f"acceptance {acc_rate:.3f}, {value:.1f} output tokens/s")
@@ -357,6 +365,7 @@ def main():
         "config": {"workload": wl.name, "layers": m.n_layers, "hidden": m.hidden, "ffn": m.ffn,
                    "heads_q_kv": [m.n_q_heads, m.n_kv_heads], "head_dim": m.head_dim, "vocab": m.vocab,
                    "batch": B, "prompt_tokens": wl.prompt_tokens, "latents": wl.latents,
+                   "prompt_lengths": ("ragged, mean %.0f" % np.mean(lens)) if lens else "uniform",
                    "decode_steps": steps, "tau": wl.tau,
                    "sampling": ("greedy" if wl.temperature <= 0 else f"T{wl.temperature} top-p{wl.top_p}"
                                 + (f" top-k{wl.top_k} rep-penalty{wl.rep_penalty}"
@@ -375,7 +384,8 @@ def main():
         settle = min(4, steps // 4)          # eager steps before the counted ones
         psteps = max(1, min(steps - settle, 32))
         model.profile(True)
-        model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty)
+        model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty,
+                      lens=lens)
         torch.cuda.synchronize()
         pre = model.profile_read()
         model.profile(True)
@@ -428,7 +438,7 @@ def main():
     del model
     torch.cuda.empty_cache()
     if not args.no_regular:
-        result["regular"] = regular_leg(wl, prompts, seeds, ttft, ms_step, acc_rate, wall / args.steps,
+        result["regular"] = regular_leg(wl, prompts, seeds, ttft, ms_step, acc_rate, wall / args.steps, lens,
                                         emitted_per_job, max(1, min(args.steps, 2)))
     if not args.no_opd:
         result["opd"] = opd_leg()

@@ -145,6 +145,7 @@ struct PrefillGeom {
     int mpad;        // per-sequence row stride (clen rounded up to 16)
     int n_tok;       // row stride of the token array, and every prompt's length when ntok is NULL
     const int32_t *ntok;   // per-sequence prompt lengths [B] (ragged batch), or NULL
+    int tok_per_pos;       // prompt tokens per position: 2 (pairs), 1 (regular decoding)
 };
 // Prompt tokens of sequence b.
 __device__ __forceinline__ int seq_tokens(const PrefillGeom &g, int b) { return g.ntok ? g.ntok[b] : g.n_tok; }

@@ -328,6 +328,10 @@ __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
     const int nbn = (p.N + kWdRows - 1) / kWdRows, nbm = (p.M + kWdToks - 1) / kWdToks;
     int bn, bm;
     if (!wd_tile(blockIdx.x, nbn, nbm, bn, bm)) return;
+    if (p.g.ntok) {   // a ragged batch: a token tile wholly past its sequence's last position holds only PAD rows
+        const int m0 = bm * kWdToks, sb = m0 / p.g.mpad;   // (mpad is a multiple of the tile there)
+        if (p.g.c0 + (m0 - sb * p.g.mpad) >= (p.g.ntok[sb] + p.g.tok_per_pos - 1) / p.g.tok_per_pos) return;
+    }
     const int KT = p.K >> 5;
     const int NI = (KT + 1) >> 1;                              // iterations of two k tiles
     const int NS = p.N >> 4, MS = p.M >> 4;
@@ -492,6 +496,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     const int q0 = qblk * kAQ;                 // chunk-local first query
     const int qpos0 = p.g.c0 + q0;             // absolute position of the first query
     const float scale = 1.4426950408889634f / sqrtf((float)D);
+    // a ragged batch: a block wholly past this sequence's last position holds
+    // only PAD rows, whose outputs nothing reads
+    if (p.g.ntok && qpos0 >= (p.g.ntok[b] + p.g.tok_per_pos - 1) / p.g.tok_per_pos) return;
 
     u32x4 qb[2][NC];
 #pragma unroll

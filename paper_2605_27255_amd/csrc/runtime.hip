@@ -253,7 +253,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
 
     // ---- KV cache, RoPE table, activations ------------------------------
     Arena a;
-    const int64_t mcap = (int64_t)B * round_up(c->chunk, 32);
+    const int64_t mcap = (int64_t)B * round_up(c->chunk, 64);   // rows per chunk: ragged batches pad to 64
     const int S_att = 64;
     for (int pass = 0; pass < 2; ++pass) {
         a.used = 0;
@@ -631,7 +631,9 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
     PrefillGeom g{};
     for (int c0 = 0; c0 < positions; c0 += c->chunk) {
         g.B = batch; g.c0 = c0; g.clen = std::min(c->chunk, positions - c0);
-        g.mpad = (int)round_up(g.clen, 32); g.n_tok = n; g.ntok = ntok;
+        // ragged batches pad each sequence's rows to whole 64-row GEMM tiles, so
+        // that tiles past a shorter prompt can be skipped
+        g.mpad = (int)round_up(g.clen, ntok ? 64 : 32); g.n_tok = n; g.ntok = ntok; g.tok_per_pos = regular ? 1 : 2;
         const int M = batch * g.mpad;
         GemmParams gp{};
         gp.g = g; gp.M = M;

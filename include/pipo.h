@@ -25,6 +25,10 @@
  *     call leaves the context unchanged.  A device fault from earlier work
  *     surfaces as PIPO_EHIP.  Nothing aborts; no C++ exception crosses the ABI.
  *   - pipo_last_error() returns the message of the most recent failure.
+ *   - Debugging: with PIPO_CHECK=1 in the environment when a context is
+ *     created, that context launches every kernel eagerly (no HIP graph),
+ *     waits for the stream after each one, and returns the first failure as
+ *     PIPO_EHIP with its launch site in pipo_last_error().
  */
 #ifndef PIPO_H
 #define PIPO_H
@@ -105,7 +109,10 @@ typedef struct {
     int32_t accept;          /* 1 iff conf >= tau: the draft is emitted             */
 } pipo_pair;
 
-/* Create a context: allocate weights, KV cache and workspaces on the current
+/* The model of Sec. 3.1: the pair-in compressor (eq. 1; App. B.1 Table 4), the
+ * backbone (eq. 2), the tied LM head (eq. 3), the MTP head (eqs. 4-5; App.
+ * B.2) and the confidence head (eq. 6; App. B.3).
+ * Create a context: allocate weights, KV cache and workspaces on the current
  * device and fill every weight tensor from the counter-based generator
  * (SplitMix64-derived, N(0, 0.02)-shaped, bf16 storage) for `seed`.
  * On success *out receives the context (released by pipo_free).  Returns
@@ -136,7 +143,9 @@ int pipo_prefill_ragged(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, i
                         const int32_t *lens, const pipo_sampling *smp, pipo_pair *d_out,
                         float *d_logits_b, float *d_logits_d, void *stream);
 
-/* One pair-decode step for every sequence of the last prefill.  The input
+/* The pair-in, pair-out step of Sec. 3.2 (eqs. 1-6: compress the input pair,
+ * one backbone position, backbone token, MTP draft, confidence gate).
+ * One pair-decode step for every sequence of the last prefill.  The input
  * pair is d_in_pairs (device int32 [batch][2]) when non-NULL (teacher
  * forcing), else the pair the previous call produced on the device:
  * (tok_b, accept ? tok_d : pad_id).  Appends one latent per sequence.
@@ -207,14 +216,17 @@ int pipo_opd_targets_bf16(int32_t T, int32_t V, const uint16_t *d_logits_s, cons
                           const int32_t *d_teacher_rows, const int32_t *d_labels, float *d_kl, float *d_alpha,
                           double *d_sums, void *stream);
 
-/* Release a context and all its device memory.  NULL is a no-op (returns 0). */
+/* Release a context made by pipo_init_weights and all its device memory.
+ * NULL is a no-op (returns 0). */
 int pipo_free(pipo_ctx *ctx);
 
-/* Message of the most recent failure on ctx (or of pipo_init_weights when
- * ctx is NULL).  Never NULL; valid until the next call on the same context. */
+/* Error reporting of this ABI (no passage of the paper): message of the most
+ * recent failure on ctx (or of pipo_init_weights when ctx is NULL).  Never NULL; valid until the next call on the same context. */
 const char *pipo_last_error(const pipo_ctx *ctx);
 
-/* Copy `count` elements, starting at logical element `start` of the
+/* Testing aid (no passage of the paper): read the weights of the Sec. 3.1
+ * model back in logical layout.
+ * Copy `count` elements, starting at logical element `start` of the
  * row-major [out][in] tensor `name` (e.g. "embed", "w_comp", "l3.wq",
  * "l0.g_attn"), to host memory as bf16 bit patterns, undoing the device
  * packing.  Synchronous.  For verifying the device weight generator.
@@ -234,13 +246,16 @@ int pipo_read_weight(pipo_ctx *ctx, const char *name, int64_t start, int64_t cou
 #define PIPO_K_PREFILL_MISC 8   /* prefill gather, RMSNorm, last-latent pick           */
 #define PIPO_K_CLASSES      9
 
-/* Profiling: while on (on != 0), the prefill and step calls of both decoders launch
+/* Measurement aid (no passage of the paper; it times the kernels of Sec. 3.2
+ * and Sec. 4.3).
+ * Profiling: while on (on != 0), the prefill and step calls of both decoders launch
  * eagerly (no graph) with a HIP event recorded on the call's stream before
  * and after every kernel; durations accumulate per kernel class.  Turning it
  * on clears the accumulators.  Errors: PIPO_EINVAL (NULL ctx). */
 int pipo_profile_enable(pipo_ctx *ctx, int on);
 
-/* Synchronise the pending profiling events and return, for kernel class
+/* Measurement aid, as pipo_profile_enable.
+ * Synchronise the pending profiling events and return, for kernel class
  * `kclass` (PIPO_K_*), the summed duration in milliseconds and the number of
  * launches since profiling was turned on.  Errors: PIPO_EINVAL. */
 int pipo_profile_read(pipo_ctx *ctx, int kclass, double *total_ms, int64_t *launches);

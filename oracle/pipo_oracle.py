@@ -56,9 +56,12 @@ silent:
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass
 
 import numpy as np
+from threadpoolctl import threadpool_limits
 
 from synth import rspec
 from synth.configs import (ModelConfig, model_tensor_shapes, HEADS_MLP_COMPRESSOR, HEADS_MTP_LAYER,
@@ -156,17 +159,21 @@ def attention_decode(q, K, V):
     return out, probs
 
 
-def attention_causal(Q, K, V, block=2048):
+def attention_causal(Q, K, V, block=256):
     """Causal grouped-query attention over a whole sequence.
 
     ``Q``: [n_q, T, d]; ``K``, ``V``: [n_kv, T, d].  Query row ``i`` attends to
     keys ``0..i``.  Rows are independent; they are processed ``block`` at a
-    time only to bound memory.
+    time only to bound memory.  Heads are independent too: they run
+    concurrently on a thread pool, each head's arithmetic in one thread (its
+    matrix products single-threaded), so the values do not depend on the
+    number of threads.
     """
     n_q, T, d = Q.shape
     n_kv = K.shape[0]
     out = np.empty_like(Q, dtype=F64)
-    for h in range(n_q):
+
+    def one_head(h):
         g = h * n_kv // n_q
         for r0 in range(0, T, block):
             r1 = min(T, r0 + block)
@@ -175,6 +182,10 @@ def attention_causal(Q, K, V, block=2048):
             cols = np.arange(r1)[None, :]
             s = np.where(cols <= rows, s, -np.inf)
             out[h, r0:r1] = softmax(s) @ V[g, :r1]
+
+    workers = max(1, min(n_q, 16, len(os.sched_getaffinity(0))))
+    with threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
+        list(ex.map(one_head, range(n_q)))
     return out
 
 
@@ -213,8 +224,9 @@ def select_greedy(logits):
     return int(np.argmax(logits))
 
 
-def select_top_p(logits, temperature, top_p, u):
-    """Temperature + nucleus sampling by inverse CDF in id order (see header)."""
+def top_p_nucleus(logits, temperature, top_p):
+    """``p = softmax(logits / T)`` and the nucleus threshold ``theta*`` (see
+    header): the largest ``p_j`` whose upper mass reaches ``top_p``."""
     y = np.asarray(logits, F64) / F64(temperature)
     e = np.exp(y - np.max(y))
     p = e / np.sum(e)
@@ -225,6 +237,12 @@ def select_top_p(logits, temperature, top_p, u):
     last_of_group = np.searchsorted(-desc, -desc, side="right") - 1
     ok = upper[last_of_group] >= top_p
     theta = desc[np.argmax(ok)] if ok.any() else desc[-1]
+    return p, theta
+
+
+def select_top_p(logits, temperature, top_p, u):
+    """Temperature + nucleus sampling by inverse CDF in id order (see header)."""
+    p, theta = top_p_nucleus(logits, temperature, top_p)
     nucleus = np.nonzero(p >= theta)[0]
     mass = np.sum(p[nucleus])
     t = u * mass
@@ -249,11 +267,17 @@ def select_eval(logits, seen, temperature, top_k, top_p, theta, u):
     penalty, temperature, top-k (every value at least the k-th largest, ties
     kept), then top-p over the kept tokens and the inverse-CDF draw of
     ``select_top_p`` (ids of the kept set scanned upwards)."""
+    return select_top_p(eval_scores(logits, seen, temperature, top_k, theta), 1.0, top_p, u)
+
+
+def eval_scores(logits, seen, temperature, top_k, theta):
+    """The evaluation sampler's scores before its top-p draw: penalised logits
+    over the temperature, with every token below the k-th largest at -inf."""
     y = repetition_penalty(logits, seen, theta) / F64(temperature)
     if 0 < top_k < y.size:
         kth = np.sort(y)[::-1][top_k - 1]
         y = np.where(y >= kth, y, -np.inf)
-    return select_top_p(y, 1.0, top_p, u)
+    return y
 
 
 # ------------------------------------------------------- OPD targets (App. C)
@@ -362,11 +386,15 @@ def _layer_ffn(cfg, L, x):
     return x + (silu(n @ L["wgate"].T) * (n @ L["wup"].T)) @ L["wdown"].T
 
 
-def backbone_full(W: OracleWeights, Z, kv_bf16=False):
+def backbone_full(W: OracleWeights, Z, kv_bf16=False, last_only=False):
     """Eq. 2 by brute force: all latent positions 0..T-1 from scratch.
 
     Returns the final residual states [T, H] (before the final norm) and the
-    per-layer caches ``[(K, V)]`` with K, V of shape [n_kv, T, d].
+    per-layer caches ``[(K, V)]`` with K, V of shape [n_kv, T, d].  With
+    ``last_only`` the states returned are the last position's alone ([1, H]):
+    the last layer then forms its keys and values at every position (the
+    cache) but attends and runs its FFN for the last query only, which is
+    all that position's state depends on.
     """
     cfg = W.cfg
     x = np.asarray(Z, F64).copy()
@@ -375,10 +403,16 @@ def backbone_full(W: OracleWeights, Z, kv_bf16=False):
     for li in range(cfg.n_layers):
         L = W.layer(li)
         q, k, v = _layer_qkv(cfg, L, x, np.arange(T), kv_bf16)
-        o = attention_causal(q, k, v)
-        x = x + o.transpose(1, 0, 2).reshape(T, cfg.q_dim) @ L["wo"].T
+        if last_only and li == cfg.n_layers - 1:
+            o, _ = attention_decode(q[:, -1], k, v)
+            x = x[-1:] + o.reshape(1, cfg.q_dim) @ L["wo"].T
+        else:
+            o = attention_causal(q, k, v)
+            x = x + o.transpose(1, 0, 2).reshape(T, cfg.q_dim) @ L["wo"].T
         x = _layer_ffn(cfg, L, x)
         caches.append((k, v))
+    if last_only and cfg.n_layers == 0:
+        x = x[-1:]
     return x, caches
 
 
@@ -485,18 +519,33 @@ class PipoOracle:
                                smp.rep_penalty, u)
         return select_top_p(logits, smp.temperature, smp.top_p, u)
 
-    def prefill(self, prompts, sampling: Sampling, force_b=None):
-        """Compressed-prompt prefill of every sequence; returns the first pair."""
+    def prefill(self, prompts, sampling: Sampling, force_b=None, forced_pairs=None):
+        """Compressed-prompt prefill of every sequence; returns the first pair.
+
+        ``forced_pairs`` (one list per sequence, all of the same length k):
+        the input pairs of the first k decode steps after the prefill,
+        teacher-forced.  Their latents follow the prompt's, and eq. 2 is
+        causal, so running the backbone over all of them at once gives the
+        same states as the prefill followed by k steps; the records returned
+        are then those of step k (sampler step index k), and the session
+        continues from there."""
         self.sampling = sampling
         W, cfg = self.W, self.cfg
         self.caches, self.length, self.step_idx, self.next_pairs, self.mtp_caches = [], [], [], [], []
         prompts = [np.asarray(p) for p in prompts]   # a ragged batch: prompts of their own lengths
         self.seen = [set(int(t) for t in p) for p in prompts]   # tokens the penalty applies to
+        nforced = 0 if forced_pairs is None else len(forced_pairs[0])
         out = []
         for i, prompt in enumerate(prompts):
             pairs = prompt_pairs(prompt, cfg.pad_id)
+            if nforced:
+                fp = np.asarray(forced_pairs[i], dtype=np.int64).reshape(nforced, 2)
+                for pair in fp:
+                    self._emitted(i, pair)
+                pairs = np.concatenate([pairs, fp])
             Z = self._compress(pairs)
-            X, caches = backbone_full(W, Z, self.kv_bf16)
+            # the heads read the last latent only; the MTP layer of App. B reads every latent's state
+            X, caches = backbone_full(W, Z, self.kv_bf16, last_only=not cfg.heads & HEADS_MTP_LAYER)
             self.caches.append([[k, v] for k, v in caches])
             self.length.append(len(pairs))
             if cfg.heads & HEADS_MTP_LAYER:
@@ -510,9 +559,9 @@ class PipoOracle:
                     k = np.zeros((cfg.n_kv_heads, 0, cfg.head_dim))
                     v = np.zeros((cfg.n_kv_heads, 0, cfg.head_dim))
                 self.mtp_caches.append([k, v])
-            rec = self.heads(X[-1], i, 0, len(pairs) - 1, None if force_b is None else force_b[i])
+            rec = self.heads(X[-1], i, nforced, len(pairs) - 1, None if force_b is None else force_b[i])
             out.append(rec)
-            self.step_idx.append(1)
+            self.step_idx.append(nforced + 1)
             self.next_pairs.append(self._next_pair(rec))
         return out
 
@@ -580,7 +629,7 @@ class RegularOracle:
         self.seen = [set(int(t) for t in p) for p in prompts]
         out = []
         for i, prompt in enumerate(prompts):
-            X, caches = backbone_full(W, W["embed"][np.asarray(prompt)], self.kv_bf16)
+            X, caches = backbone_full(W, W["embed"][np.asarray(prompt)], self.kv_bf16, last_only=True)
             self.caches.append([[k, v] for k, v in caches])
             self.length.append(len(prompt))
             rec = self._head(X[-1], i, 0)

@@ -1092,8 +1092,9 @@ int gemv_num_groups(int N) { return N >> 4; }
 
 // One instantiation per (prologue, epilogue) pair the decode step uses.
 // Waves per strip (the K split), from a sweep on MI355X at batch 1: the LM
-// head (151936 rows) splits K in four, every other matrix in eight.
-void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s) {
+// head (151936 rows) splits K in four, every other matrix in eight.  Any
+// other pair launches nothing and returns -1.
+int launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s) {
     if (pro == PRO_PAIR && epi == EPI_STORE) launch_nbt<8, PRO_PAIR, EPI_STORE>(p, s);
     else if (pro == PRO_NORM && epi == EPI_QKV) launch_nbt<8, PRO_NORM, EPI_QKV>(p, s);
     else if (pro == PRO_F32 && epi == EPI_RESID) launch_nbt<8, PRO_F32, EPI_RESID>(p, s);
@@ -1103,6 +1104,8 @@ void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s) {
     else if (pro == PRO_NORM && epi == EPI_STORE) launch_nbt<8, PRO_NORM, EPI_STORE>(p, s);
     else if (pro == PRO_PAIR && epi == EPI_SILU) launch_nbt<8, PRO_PAIR, EPI_SILU>(p, s);
     else if (pro == PRO_CAT && epi == EPI_SILU) launch_nbt<8, PRO_CAT, EPI_SILU>(p, s);
+    else return -1;
+    return 0;
 }
 
 }  // namespace pipo

@@ -53,7 +53,9 @@ struct GemvParams {
     int krt;                      // k-tiles per range of the k-range kernel (set by launch_gemv)
     int xseg;                     // 2048-column segments per row of the X planes (set by launch_gemv)
 };
-void launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s);
+// Returns 0, or -1 (nothing launched) for a (pro, epi) pair without an
+// instantiation.
+int launch_gemv(const GemvParams &p, int pro, int epi, hipStream_t s);
 // Profiling of the next launch_gemv on this thread: with `pending` set, the
 // call records `start` / `stop` around its kernels (the batch-1 kernel through
 // hipExtLaunchKernelGGL, so the interval is the kernel's own execution) and
@@ -168,13 +170,14 @@ struct GemmParams {
     int epi;                                // EPI_STORE (bias), EPI_RESID, EPI_SWIGLU, EPI_QKV, EPI_SILU
     PrefillGeom g;
     float *out; const float *bias; uint16_t *act_hi, *act_lo;
-    uint16_t *q; uint16_t *kc; uint16_t *vc;
+    uint16_t *q, *q_lo;                     // EPI_QKV: the query as hi and lo planes
+    uint16_t *kc; uint16_t *vc;
     const float *rope_cos; const float *rope_sin;
     int n_q, n_kv, d, lmax_pad; int64_t kv_bstride;
 };
 void launch_gemm(const GemmParams &p, hipStream_t s);
 struct AttnPrefillParams {
-    const uint16_t *q;          // bf16 [B][n_q][mpad][d]
+    const uint16_t *q, *q_lo;   // bf16 [B][n_q][mpad][d] each: the query as hi + lo
     const uint16_t *kc, *vc; int64_t kv_bstride;
     PrefillGeom g;
     int n_q, n_kv, d, lmax_pad;

@@ -269,12 +269,19 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
 #pragma unroll
             for (int v = 0; v < 4; ++v)
                 r[v] = (g < 2) ? val[v] * cs[v] - other[v] * sn[v] : val[v] * cs[v] + other[v] * sn[v];
-            u32x2 w;
-            w[0] = pack_bf2(r[0], r[1]);
-            w[1] = pack_bf2(r[2], r[3]);
-            uint16_t *dst = isq ? p.q + (((int64_t)b * p.n_q + head) * p.g.mpad + i) * d + dim0
-                                : p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0;
-            *(u32x2 *)dst = w;
+            if (isq) {   // the query as a bf16 pair hi + lo (two planes)
+                uint32_t h[4], l[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) split_bf(r[v], h[v], l[v]);
+                const int64_t at = (((int64_t)b * p.n_q + head) * p.g.mpad + i) * d + dim0;
+                *(u32x2 *)(p.q + at) = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+                *(u32x2 *)(p.q_lo + at) = u32x2{l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
+            } else {     // the key, stored in bf16 (the cache's format)
+                u32x2 w;
+                w[0] = pack_bf2(r[0], r[1]);
+                w[1] = pack_bf2(r[2], r[3]);
+                *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
+            }
         } else {
             const int r0 = (strip - qs - ks) * 16 + 4 * g;
             const int kvh = r0 / d, dim = r0 - kvh * d;
@@ -500,12 +507,15 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     // only PAD rows, whose outputs nothing reads
     if (p.g.ntok && qpos0 >= (p.g.ntok[b] + p.g.tok_per_pos - 1) / p.g.tok_per_pos) return;
 
-    u32x4 qb[2][NC];
+    u32x4 qb[2][NC], ql[2][NC];   // the query rows as a bf16 pair hi + lo
 #pragma unroll
     for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
-            qb[ct][c] = *(const u32x4 *)(p.q + (((int64_t)b * p.n_q + head) * p.g.mpad + q0 + 16 * ct + j) * D + 32 * c + 8 * g);
+        for (int c = 0; c < NC; ++c) {
+            const int64_t at = (((int64_t)b * p.n_q + head) * p.g.mpad + q0 + 16 * ct + j) * D + 32 * c + 8 * g;
+            qb[ct][c] = *(const u32x4 *)(p.q + at);
+            ql[ct][c] = *(const u32x4 *)(p.q_lo + at);
+        }
 
     const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
     const uint16_t *vbase = p.vc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
@@ -569,10 +579,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             for (int ct = 0; ct < 2; ++ct) {
                 sc[ct][tau] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int c = 0; c < NC; ++c) sc[ct][tau] = mfma16(kf[c], qb[ct][c], sc[ct][tau]);
+                for (int c = 0; c < NC; ++c) {
+                    sc[ct][tau] = mfma16(kf[c], qb[ct][c], sc[ct][tau]);
+                    sc[ct][tau] = mfma16(kf[c], ql[ct][c], sc[ct][tau]);
+                }
             }
         }
-        u32x4 pt[2][2];
+        u32x4 pt[2][2], pl[2][2];   // P^T as a bf16 pair hi + lo
 #pragma unroll
         for (int ct = 0; ct < 2; ++ct) {
             // keys past this column's query are masked (only on diagonal stages)
@@ -610,10 +623,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             l_run[ct] += col_sum(ps);
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
-                pt[ct][half][0] = pack_bf2_hw(sc[ct][2 * half][0], sc[ct][2 * half][1]);
-                pt[ct][half][1] = pack_bf2_hw(sc[ct][2 * half][2], sc[ct][2 * half][3]);
-                pt[ct][half][2] = pack_bf2_hw(sc[ct][2 * half + 1][0], sc[ct][2 * half + 1][1]);
-                pt[ct][half][3] = pack_bf2_hw(sc[ct][2 * half + 1][2], sc[ct][2 * half + 1][3]);
+                const float f[8] = {sc[ct][2 * half][0], sc[ct][2 * half][1], sc[ct][2 * half][2],
+                                    sc[ct][2 * half][3], sc[ct][2 * half + 1][0], sc[ct][2 * half + 1][1],
+                                    sc[ct][2 * half + 1][2], sc[ct][2 * half + 1][3]};
+                split8(f, pt[ct][half], pl[ct][half]);
             }
         }
         // O^T += V^T P^T, each V fragment serving both query tiles
@@ -623,7 +636,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             for (int t = 0; t < NT; ++t) {
                 const u32x4 vf = *(const u32x4 *)(&vs[(half * D + 16 * t + j) * VS + 8 * g]);
 #pragma unroll
-                for (int ct = 0; ct < 2; ++ct) o[ct][t] = mfma16(vf, pt[ct][half], o[ct][t]);
+                for (int ct = 0; ct < 2; ++ct) {
+                    o[ct][t] = mfma16(vf, pt[ct][half], o[ct][t]);
+                    o[ct][t] = mfma16(vf, pl[ct][half], o[ct][t]);
+                }
             }
     };
 

@@ -73,7 +73,7 @@ struct pipo_ctx {
     float *pen;                       // penalised logits [Bmax][V] (evaluation sampler workspace)
     pipo_pair *out;
     // prefill activations
-    uint16_t *p_xin, *p_xn, *p_xn_lo, *p_q, *p_o, *p_o_lo, *p_act, *p_act_lo;
+    uint16_t *p_xin, *p_xn, *p_xn_lo, *p_q, *p_q_lo, *p_o, *p_o_lo, *p_act, *p_act_lo;
     float *p_x;
 
     uint64_t *h_seeds = nullptr;     // pinned staging for sampler seeds
@@ -96,6 +96,10 @@ struct pipo_ctx {
     hipGraphExec_t graph = nullptr;
     bool graph_dirty = true;
     bool use_graph = true;
+    // PIPO_CHECK=1 in the environment at init: launch eagerly, wait for the
+    // stream after every kernel and report the first failure with its site
+    bool check = false;
+    int enq_rc = PIPO_OK;            // first failure while enqueueing the current call
 
     // profiling: events around every launch, summed per kernel class
     bool prof_on = false;
@@ -106,14 +110,18 @@ struct pipo_ctx {
     int64_t prof_n[PIPO_K_CLASSES] = {};
 };
 
-// Launch bracket: record an event before and after a launch when profiling.
+static void check_launch(pipo_ctx *c, hipStream_t s, int cls, int line);
+
+// Launch bracket: record an event before and after a launch when profiling;
+// in check mode, wait for the launch and take its error.
 // Around one launch_gemv call (gemv = true) the events go to the GEMV
 // launcher instead, which records them around its kernels (the batch-1
 // kernel times itself, without the gaps an event recorded between two
 // launches adds).
 struct ProfScope {
-    pipo_ctx *c; hipStream_t s; int cls; bool gemv; size_t i0 = 0;
-    ProfScope(pipo_ctx *c_, hipStream_t s_, int cls_, bool gemv_ = false) : c(c_), s(s_), cls(cls_), gemv(gemv_) {
+    pipo_ctx *c; hipStream_t s; int cls; int line; bool gemv; size_t i0 = 0;
+    ProfScope(pipo_ctx *c_, hipStream_t s_, int cls_, int line_, bool gemv_ = false)
+        : c(c_), s(s_), cls(cls_), line(line_), gemv(gemv_) {
         if (!c->prof_on) return;
         while (c->ev_pool.size() < c->ev_next + 2) {
             hipEvent_t e;
@@ -126,6 +134,7 @@ struct ProfScope {
         else hipEventRecord(c->ev_pool[i0], s);
     }
     ~ProfScope() {
+        if (c->check) check_launch(c, s, cls, line);
         if (!c->prof_on) return;
         if (!gemv) {
             hipEventRecord(c->ev_pool[i0 + 1], s);
@@ -139,8 +148,8 @@ struct ProfScope {
 };
 #define PROF_CAT2(a, b) a##b
 #define PROF_CAT(a, b) PROF_CAT2(a, b)
-#define PROF(cls) ProfScope PROF_CAT(prof_scope_, __LINE__)(c, s, cls)
-#define PROF_GEMV(cls) ProfScope PROF_CAT(prof_scope_, __LINE__)(c, s, cls, true)
+#define PROF(cls) ProfScope PROF_CAT(prof_scope_, __LINE__)(c, s, cls, __LINE__)
+#define PROF_GEMV(cls) ProfScope PROF_CAT(prof_scope_, __LINE__)(c, s, cls, __LINE__, true)
 
 static int fail(pipo_ctx *c, int code, const char *fmt, ...) {
     char buf[512];
@@ -151,6 +160,21 @@ static int fail(pipo_ctx *c, int code, const char *fmt, ...) {
     if (c) c->err = buf;
     else g_init_error = buf;
     return code;
+}
+
+static void check_launch(pipo_ctx *c, hipStream_t s, int cls, int line) {
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = hipGetLastError();
+    if (e != hipSuccess && c->enq_rc == PIPO_OK)
+        c->enq_rc = fail(c, PIPO_EHIP, "PIPO_CHECK: kernel of class %d launched at runtime.hip:%d failed: %s", cls,
+                         line, hipGetErrorString(e));
+}
+
+// launch_gemv; a (prologue, epilogue) pair it has no kernel for is the call's error
+static void gemv(pipo_ctx *c, const GemvParams &p, int pro, int epi, hipStream_t s) {
+    if (launch_gemv(p, pro, epi, s) != 0 && c->enq_rc == PIPO_OK)
+        c->enq_rc = fail(c, PIPO_EINVAL, "no decode GEMV kernel for prologue %d with epilogue %d", pro, epi);
 }
 
 #define HIP_TRY(ctx, expr)                                                                     \
@@ -302,6 +326,7 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->p_xn = a.take<uint16_t>(mcap * H);
         c->p_xn_lo = a.take<uint16_t>(mcap * H);
         c->p_q = a.take<uint16_t>(mcap * c->qdim);
+        c->p_q_lo = a.take<uint16_t>(mcap * c->qdim);
         c->p_o = a.take<uint16_t>(mcap * c->qdim);
         c->p_o_lo = a.take<uint16_t>(mcap * c->qdim);
         c->p_act = a.take<uint16_t>(mcap * F);
@@ -380,7 +405,9 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         if (wc && atoi(wc) > 0) c->n_cu = atoi(wc);
     }
     const char *ng = getenv("PIPO_NO_GRAPH");
-    c->use_graph = !(ng && ng[0] == '1');
+    const char *ck = getenv("PIPO_CHECK");
+    c->check = ck && ck[0] == '1';
+    c->use_graph = !(ng && ng[0] == '1') && !c->check;
     *out = c;
     return PIPO_OK;
 }
@@ -414,7 +441,7 @@ static void enqueue_layer(pipo_ctx *c, const LayerW &lw, uint16_t *kc, uint16_t 
     p.x = xres; p.ss = ssres; p.nss = H / 16; p.gain = lw.g_attn;
     p.q = c->qbuf; p.kc = kc; p.vc = vc; p.pos = c->pos; p.rope_cos = c->rope_cos; p.rope_sin = c->rope_sin;
     p.n_q = c->nq; p.n_kv = c->nkv; p.d = c->d; p.lmax_pad = c->lmax_pad; p.kv_bstride = c->kv_bstride;
-    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_QKV, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); gemv(c, p, PRO_NORM, EPI_QKV, s); }
 
     AttnDecodeParams ap{};
     ap.q = c->qbuf; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.pos = c->pos;
@@ -424,16 +451,16 @@ static void enqueue_layer(pipo_ctx *c, const LayerW &lw, uint16_t *kc, uint16_t 
 
     p = base;
     p.W = lw.wo; p.N = H; p.K = c->qdim; p.xf = c->attn_out; p.out = xres; p.ss_out = ssres;
-    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); gemv(c, p, PRO_F32, EPI_RESID, s); }
 
     p = base;
     p.W = lw.wgu; p.N = 2 * c->F; p.K = H; p.x = xres; p.ss = ssres; p.nss = H / 16; p.gain = lw.g_ffn;
     p.act = c->act;
-    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_NORM, EPI_SWIGLU, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); gemv(c, p, PRO_NORM, EPI_SWIGLU, s); }
 
     p = base;
     p.W = lw.wdown; p.N = H; p.K = c->F; p.xf = c->act; p.out = xres; p.ss_out = ssres;
-    { PROF_GEMV(PIPO_K_GEMV_LAYER); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LAYER); gemv(c, p, PRO_F32, EPI_RESID, s); }
 }
 
 // The backbone layers of one decode position over the residual in x.
@@ -475,7 +502,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, bool in_pair
     p.W = c->embed; p.N = c->V; p.K = H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
     p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
-    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); gemv(c, p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         PROF(PIPO_K_SAMPLE);
         launch_sample(sample_params(c, c->logits_b, B, 0, c->best_b, in_pair, nullptr), s);
@@ -488,7 +515,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, bool in_pair
     m.x = c->x; m.ss = c->ss_x; m.nss = nss; m.gain = c->g_mtp_h; m.gain2 = c->g_mtp_e;
     m.embed = c->embed; m.tokkey = c->best_b;
     m.out = c->hd; m.ss_out = c->ss_hd;
-    { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(m, PRO_MTP, EPI_STORE, s); }
+    { PROF_GEMV(PIPO_K_GEMV_SMALL); gemv(c, m, PRO_MTP, EPI_STORE, s); }
     // App. B.2: the MTP head's decoder layer at the current latent position
     if (c->heads & PIPO_HEADS_MTP_LAYER) enqueue_layer(c, c->mtp, c->kc_mtp, c->vc_mtp, c->hd, c->ss_hd, s);
     // LM head #2 on RMSNorm(h_d; g_mo)
@@ -497,7 +524,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, bool in_pair
     q.W = c->embed; q.N = c->V; q.K = H;
     q.x = c->hd; q.ss = c->ss_hd; q.nss = H / 16; q.gain = c->g_mtp_o;
     q.out = c->logits_d; q.best = greedy ? c->best_d : nullptr;
-    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(q, PRO_NORM, EPI_LOGITS, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); gemv(c, q, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         // the draft's penalised set also holds its pair's backbone token
         PROF(PIPO_K_SAMPLE);
@@ -510,7 +537,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, bool in_pair
         f.W = c->conf_w1; f.N = H; f.K = 2 * H;
         f.x = c->x; f.x2 = c->hd; f.ss = c->ss_x; f.ss2 = c->ss_hd; f.nss = H / 16; f.gain = c->g_conf;
         f.act = c->act;
-        { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(f, PRO_CAT, EPI_SILU, s); }
+        { PROF_GEMV(PIPO_K_GEMV_SMALL); gemv(c, f, PRO_CAT, EPI_SILU, s); }
         gp.conf_h = c->act; gp.conf_w2 = c->conf_w2;
     }
     gp.hb = c->x; gp.hd = c->hd; gp.ss_b = c->ss_x; gp.nss_b = nss; gp.ss_d = c->ss_hd; gp.nss_d = H / 16;
@@ -528,17 +555,17 @@ static void enqueue_decode(pipo_ctx *c, hipStream_t s) {
     if (c->heads & PIPO_HEADS_MLP_COMPRESSOR) {   // Table 4 MLP: E[a] + E[b] + W2 SiLU(W1 [E[a]; E[b]])
         GemvParams p = gemv_base(c, B);
         p.W = c->comp_w1; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed; p.act = c->act;
-        { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_PAIR, EPI_SILU, s); }
+        { PROF_GEMV(PIPO_K_GEMV_SMALL); gemv(c, p, PRO_PAIR, EPI_SILU, s); }
         { PROF(PIPO_K_GATE); launch_embed_step(c->pairs, c->embed, H, c->V, c->x, c->ss_x, B, 1, s); }
         p = gemv_base(c, B);
         p.W = c->comp_w2; p.N = H; p.K = H; p.xf = c->act; p.out = c->x; p.ss_out = c->ss_x;
-        { PROF_GEMV(PIPO_K_GEMV_SMALL); launch_gemv(p, PRO_F32, EPI_RESID, s); }
+        { PROF_GEMV(PIPO_K_GEMV_SMALL); gemv(c, p, PRO_F32, EPI_RESID, s); }
     } else {   // pair-in compressor, Linear (eq. 1)
         GemvParams p = gemv_base(c, B);
         p.W = c->w_comp; p.N = H; p.K = 2 * H; p.pairs = c->pairs; p.embed = c->embed;
         p.out = c->x; p.bias = c->b_comp; p.ss_out = c->ss_x;
         PROF_GEMV(PIPO_K_GEMV_SMALL);
-        launch_gemv(p, PRO_PAIR, EPI_STORE, s);
+        gemv(c, p, PRO_PAIR, EPI_STORE, s);
     }
     enqueue_layers(c, s);
     enqueue_heads(c, B, H / 16, 1, true, s);
@@ -595,6 +622,9 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
         return fail(c, PIPO_ECAPACITY, "%d positions leave no room for a step (max_latent %d)", positions,
                     c->cfg.max_latent);
     HIP_TRY(c, hipGetLastError());
+    // every host-side check has passed: from here the previous sequences are gone
+    c->prefilled = false;
+    c->enq_rc = PIPO_OK;
 
     if (c->batch != batch || c->tau != smp->tau || c->temperature != smp->temperature || c->top_p != smp->top_p ||
         c->top_k != smp->top_k || c->rep_penalty != smp->rep_penalty) {
@@ -662,10 +692,10 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
             uint16_t *vc = c->vc + (int64_t)l * c->Bmax * c->kv_bstride;
             { PROF(PIPO_K_PREFILL_MISC); launch_rmsnorm_tiled(c->p_x, lw.g_attn, H, c->cfg.rms_eps, M, c->p_xn, c->p_xn_lo, s); }
             p = gp;
-            p.W = lw.wqkv; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q; p.kc = kc; p.vc = vc;
+            p.W = lw.wqkv; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q; p.q_lo = c->p_q_lo; p.kc = kc; p.vc = vc;
             { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
             AttnPrefillParams ap{};
-            ap.q = c->p_q; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.g = g;
+            ap.q = c->p_q; ap.q_lo = c->p_q_lo; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.g = g;
             ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad; ap.out_hi = c->p_o; ap.out_lo = c->p_o_lo;
             { PROF(PIPO_K_PREFILL_ATTN); launch_attn_prefill(ap, s); }
             p = gp;
@@ -694,11 +724,11 @@ static int prefill_backbone(pipo_ctx *c, int32_t batch, const int32_t *d_tokens,
             const LayerW &lw = c->mtp;
             { PROF(PIPO_K_PREFILL_MISC); launch_rmsnorm_tiled(xm, lw.g_attn, H, c->cfg.rms_eps, M, c->p_xn, c->p_xn_lo, s); }
             p = gp;
-            p.W = lw.wqkv; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q;
+            p.W = lw.wqkv; p.X = c->p_xn; p.Xlo = c->p_xn_lo; p.N = c->nqkv; p.K = H; p.epi = EPI_QKV; p.q = c->p_q; p.q_lo = c->p_q_lo;
             p.kc = c->kc_mtp; p.vc = c->vc_mtp;
             { PROF(PIPO_K_PREFILL_GEMM); launch_gemm(p, s); }
             AttnPrefillParams ap{};
-            ap.q = c->p_q; ap.kc = c->kc_mtp; ap.vc = c->vc_mtp; ap.kv_bstride = c->kv_bstride; ap.g = g;
+            ap.q = c->p_q; ap.q_lo = c->p_q_lo; ap.kc = c->kc_mtp; ap.vc = c->vc_mtp; ap.kv_bstride = c->kv_bstride; ap.g = g;
             ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad; ap.out_hi = c->p_o; ap.out_lo = c->p_o_lo;
             { PROF(PIPO_K_PREFILL_ATTN); launch_attn_prefill(ap, s); }
             p = gp;
@@ -723,11 +753,11 @@ static int prefill_pair(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, int
     if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
     if (!d_out) return fail(c, PIPO_EINVAL, "d_out must be non-NULL");
     hipStream_t s = (hipStream_t)stream;
-    c->prefilled = false;
     int rc = prefill_backbone(c, batch, d_tokens, n, lens, smp, false, s);
     if (rc) return rc;
     enqueue_heads(c, batch, c->H / 16, 1, false, s);
     HIP_TRY(c, hipGetLastError());
+    if (c->enq_rc) return c->enq_rc;
     rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
     if (rc) return rc;
     c->prefilled = true;
@@ -757,7 +787,7 @@ static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, bool
     p.W = c->embed; p.N = c->V; p.K = c->H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
     p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
-    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); launch_gemv(p, PRO_NORM, EPI_LOGITS, s); }
+    { PROF_GEMV(PIPO_K_GEMV_LMHEAD); gemv(c, p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         PROF(PIPO_K_SAMPLE);
         launch_sample(sample_params(c, c->logits_b, B, 0, c->best_b, in_tok, nullptr), s);
@@ -789,11 +819,11 @@ static int prefill_regular(pipo_ctx *c, int32_t batch, const int32_t *d_tokens, 
     if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
     if (!d_tok) return fail(c, PIPO_EINVAL, "d_tok must be non-NULL");
     hipStream_t s = (hipStream_t)stream;
-    c->prefilled = false;
     int rc = prefill_backbone(c, batch, d_tokens, n, lens, smp, true, s);
     if (rc) return rc;
     enqueue_regular_heads(c, batch, c->H / 16, 1, false, s);
     HIP_TRY(c, hipGetLastError());
+    if (c->enq_rc) return c->enq_rc;
     rc = copy_tokens(c, d_tok, d_logits, s);
     if (rc) return rc;
     c->prefilled = true;
@@ -832,9 +862,14 @@ extern "C" int pipo_regular_step(pipo_ctx *c, const int32_t *d_in_tok, int32_t *
                 c->graph_reg = nullptr;
             }
             hipGraph_t gr;
+            c->enq_rc = PIPO_OK;
             HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
             enqueue_regular_decode(c, c->cap_stream);
             HIP_TRY(c, hipStreamEndCapture(c->cap_stream, &gr));
+            if (c->enq_rc) {
+                hipGraphDestroy(gr);
+                return c->enq_rc;
+            }
             hipError_t e = hipGraphInstantiate(&c->graph_reg, gr, nullptr, nullptr, 0);
             hipGraphDestroy(gr);
             if (e != hipSuccess) return fail(c, PIPO_EHIP, "graph instantiate: %s", hipGetErrorString(e));
@@ -842,8 +877,10 @@ extern "C" int pipo_regular_step(pipo_ctx *c, const int32_t *d_in_tok, int32_t *
         }
         HIP_TRY(c, hipGraphLaunch(c->graph_reg, s));
     } else {
+        c->enq_rc = PIPO_OK;
         enqueue_regular_decode(c, s);
         HIP_TRY(c, hipGetLastError());
+        if (c->enq_rc) return c->enq_rc;
     }
     int rc = copy_tokens(c, d_tok, d_logits, s);
     if (rc) return rc;
@@ -869,9 +906,14 @@ extern "C" int pipo_decode_step(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pai
                 c->graph = nullptr;
             }
             hipGraph_t gr;
+            c->enq_rc = PIPO_OK;
             HIP_TRY(c, hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
             enqueue_decode(c, c->cap_stream);
             HIP_TRY(c, hipStreamEndCapture(c->cap_stream, &gr));
+            if (c->enq_rc) {
+                hipGraphDestroy(gr);
+                return c->enq_rc;
+            }
             hipError_t e = hipGraphInstantiate(&c->graph, gr, nullptr, nullptr, 0);
             hipGraphDestroy(gr);
             if (e != hipSuccess) return fail(c, PIPO_EHIP, "graph instantiate: %s", hipGetErrorString(e));
@@ -879,8 +921,10 @@ extern "C" int pipo_decode_step(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pai
         }
         HIP_TRY(c, hipGraphLaunch(c->graph, s));
     } else {
+        c->enq_rc = PIPO_OK;
         enqueue_decode(c, s);
         HIP_TRY(c, hipGetLastError());
+        if (c->enq_rc) return c->enq_rc;
     }
     int rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
     if (rc) return rc;

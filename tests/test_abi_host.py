@@ -106,3 +106,18 @@ def test_null_arguments(lib):
     assert lib.pipo_read_weight(None, b"embed", 0, 1, None) == pipo.PIPO_EINVAL
     assert lib.pipo_free(None) == pipo.PIPO_OK
     assert b"ctx" in lib.pipo_last_error(None)
+
+
+def test_gemv_dispatch_refuses_unlisted_variant(lib):
+    """The decode GEMV launcher has one kernel per (prologue, epilogue) pair the
+    step uses; any other pair launches nothing and reports -1, which the
+    runtime turns into PIPO_EINVAL for the call.  The launcher is a C++ symbol
+    of the library, called here on a zeroed parameter block (an unlisted pair
+    returns before reading it, with no HIP call)."""
+    fn = getattr(lib, "_ZN4pipo11launch_gemvERKNS_10GemvParamsEiiP12ihipStream_t")
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    block = ctypes.create_string_buffer(4096)
+    pro_f32, pro_mtp, epi_qkv, epi_logits, epi_swiglu = 1, 3, 3, 4, 2
+    for pro, epi in ((pro_f32, epi_qkv), (pro_mtp, epi_logits), (pro_f32, epi_swiglu), (7, 0), (0, 9)):
+        assert fn(ctypes.addressof(block), pro, epi, None) == -1, (pro, epi)

@@ -216,6 +216,36 @@ def test_brute_force_equals_incremental(small_w):
         np.testing.assert_allclose(caches[li][1], caches_full[li][1], rtol=1e-12, atol=1e-14)
 
 
+def test_last_only_backbone_is_the_full_pass_at_the_last_position(small_w):
+    """The last-position form of the brute-force pass: the same state at the
+    last latent and the same caches, for one, several and zero layers."""
+    rng = np.random.default_rng(5)
+    Z = rng.standard_normal((13, SMALL.hidden))
+    X, caches = O.backbone_full(small_w, Z, kv_bf16=True)
+    Xl, caches_l = O.backbone_full(small_w, Z, kv_bf16=True, last_only=True)
+    assert Xl.shape == (1, SMALL.hidden)
+    np.testing.assert_allclose(Xl[0], X[-1], rtol=1e-12, atol=1e-13)
+    for (k, v), (kl, vl) in zip(caches, caches_l):
+        np.testing.assert_array_equal(k, kl)
+        np.testing.assert_array_equal(v, vl)
+    W1 = O.OracleWeights.generate(SMALL.with_layers(1), seed=3, precision="bf16")
+    X, _ = O.backbone_full(W1, Z)
+    np.testing.assert_allclose(O.backbone_full(W1, Z, last_only=True)[0][0], X[-1], rtol=1e-12, atol=1e-13)
+    W0 = O.OracleWeights.generate(SMALL.with_layers(0), seed=3, precision="bf16")
+    np.testing.assert_array_equal(O.backbone_full(W0, Z, last_only=True)[0][0], Z[-1])
+
+
+def test_attention_threads_do_not_change_values():
+    """Heads run concurrently; each head's values are those of a plain
+    single-head evaluation."""
+    rng = np.random.default_rng(6)
+    Q, K, V = rng.standard_normal((6, 300, 16)), rng.standard_normal((2, 300, 16)), rng.standard_normal((2, 300, 16))
+    out = O.attention_causal(Q, K, V)
+    for h in range(6):
+        np.testing.assert_array_equal(out[h:h + 1], O.attention_causal(Q[h:h + 1], K[h // 3:h // 3 + 1],
+                                                                       V[h // 3:h // 3 + 1]))
+
+
 def test_causality(small_w):
     rng = np.random.default_rng(7)
     Z = rng.standard_normal((9, SMALL.hidden))
@@ -420,6 +450,46 @@ def test_teacher_forcing_reproduces_free_run(small_w):
             assert (x["tok_b"], x["tok_d"], x["accept"]) == (y["tok_b"], y["tok_d"], y["accept"])
 
 
+def _forced_prefill_matches_steps(W, cfg, prompts, smp, k_list):
+    """Prefill + k teacher-forced steps, step by step, against one prefill over
+    the prompt's and the forced pairs' latents together (eq. 2 is causal):
+    the records of step k, the sampler's step index and penalised sets, and
+    the step after it."""
+    B = len(prompts)
+    run = O.PipoOracle(W)
+    recs = [run.prefill(prompts, smp)]
+    history = []
+    for _ in range(max(k_list) + 1):
+        history.append([run.next_pairs[i] for i in range(B)])
+        recs.append(run.decode_step(in_pairs=history[-1]))
+    for k in k_list:
+        jump = O.PipoOracle(W)
+        forced = [[history[s][i] for s in range(k)] for i in range(B)]
+        got = jump.prefill(prompts, smp, force_b=[r["tok_b"] for r in recs[k]], forced_pairs=forced)
+        for x, y in zip(got, recs[k]):
+            for key in ("logits_b", "logits_d", "h_b", "h_d"):
+                np.testing.assert_allclose(x[key], y[key], rtol=1e-9, atol=1e-12, err_msg=f"{key} step {k}")
+            assert (x["tok_b"], x["tok_d"], x["accept"]) == (y["tok_b"], y["tok_d"], y["accept"])
+            assert abs(x["conf"] - y["conf"]) < 1e-12
+        assert jump.length == [run.length[i] - (len(history) - k) for i in range(B)]
+        assert jump.step_idx == [k + 1] * B
+        # the session continues from the jump exactly as from the steps
+        nxt = jump.decode_step(in_pairs=history[k])
+        for x, y in zip(nxt, recs[k + 1]):
+            np.testing.assert_allclose(x["logits_d"], y["logits_d"], rtol=1e-9, atol=1e-12)
+            assert (x["tok_b"], x["tok_d"]) == (y["tok_b"], y["tok_d"])
+
+
+def test_forced_prefill_equals_forced_steps(small_w):
+    """Greedy, and the evaluation sampler (penalised sets and draws follow the
+    step index), over a ragged pair of prompts."""
+    cfg = SMALL
+    prompts = [rspec.prompt_tokens(1, 9, cfg.vocab, seed=31)[0], rspec.prompt_tokens(1, 14, cfg.vocab, seed=32)[0]]
+    _forced_prefill_matches_steps(small_w, cfg, prompts, O.Sampling(tau=0.5), [1, 3])
+    smp = O.Sampling(tau=0.3, temperature=1.0, top_p=0.9, seeds=(7, 8), top_k=10, rep_penalty=1.5)
+    _forced_prefill_matches_steps(small_w, cfg, prompts, smp, [2, 4])
+
+
 def test_tiny_workload_shapes_run():
     """The tiny workload's model runs end to end in the oracle (smoke)."""
     W = O.OracleWeights.generate(TINY, seed=0, precision="fp32")
@@ -587,6 +657,13 @@ def test_paper_heads_session_equals_brute_force(paper_w):
         np.testing.assert_allclose(rec["h_d"], Hd[L0 - 1 + k], rtol=1e-10, atol=1e-12)
         s, c = O.confidence_mlp(W["conf_w1"], W["conf_w2"], W["g_conf"], rec["h_b"], rec["h_d"], cfg.rms_eps)
         assert abs(c - rec["conf"]) < 1e-15
+
+
+def test_paper_heads_forced_prefill_equals_forced_steps(paper_w):
+    """With the App. B MTP layer, the forced latents' MTP inputs take the next
+    pair's first token, which is the backbone token each step selected."""
+    prompts = rspec.prompt_tokens(2, 10, SMALL_P.vocab, seed=12)
+    _forced_prefill_matches_steps(paper_w, SMALL_P, list(prompts), O.Sampling(tau=0.5), [1, 3])
 
 
 # --------------------------------------------- evaluation sampler (Sec. 4)

@@ -154,6 +154,24 @@ int pipo_prefill_ragged(pipo_ctx *ctx, int32_t batch, const int32_t *d_tokens, i
 int pipo_decode_step(pipo_ctx *ctx, const int32_t *d_in_pairs, pipo_pair *d_out,
                      float *d_logits_b, float *d_logits_d, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops): pipo_decode_step with the same arguments,
+ * outputs and errors, launched eagerly on `stream` (no HIP graph is built or
+ * instantiated) and with its scratch (the decode attention's split partials
+ * and the larger-batch GEMVs' k-range partial sums) in a 16 MiB device array
+ * of the library, one per GPU, held until the process ends.  It calls no
+ * hipMalloc or hipFree.  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (two streams, or two contexts on two host
+ * threads) race and must be serialised by the caller.  Nothing in the array
+ * needs to start at zero (each call writes the partials it reads).  Errors
+ * as pipo_decode_step, plus PIPO_ECAPACITY when the attention partials
+ * (batch * n_q_heads * splits * (head_dim + 2) floats, splits <= 64) exceed
+ * the array; k-range partials that do not fit its remainder make those
+ * GEMVs run their whole-K form instead.  Profiling (pipo_profile_enable)
+ * does not time this call. */
+int pipo_decode_step_noalloc(pipo_ctx *ctx, const int32_t *d_in_pairs, pipo_pair *d_out,
+                             float *d_logits_b, float *d_logits_d, void *stream);
+
 /* Regular one-token-per-step decoding on the same weights: the baseline the
  * pair decoder is compared against (Sec. 4.3, Fig. 4: the backbone itself,
  * one position per token, no compressor, MTP or confidence head).

@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -67,6 +68,8 @@ struct pipo_ctx {
     uint16_t *xh, *xl;    // decode GEMV input planes for larger batches [Bmax][Kmax]
     float *gpart; int64_t gpart_cap;   // decode GEMV k-range partial sums
     int n_cu;             // compute units: workgroups of the batch-1 GEMV
+    int dev = 0;          // the device the context lives on
+    void *scratch = nullptr;   // that device's address of the static scratch (pipo_decode_step_noalloc)
     uint64_t *best_b, *best_d, *seeds;
     int32_t *pairs, *pos, *step;
     uint32_t *seen; int seen_words;   // penalised-token bitmap per sequence (evaluation sampler)
@@ -211,6 +214,32 @@ enum { TID_EMBED = 0, TID_WCOMP = 1, TID_BCOMP = 2, TID_WFC = 3, TID_WCONF = 4, 
        TID_CONFW1 = 12, TID_CONFW2 = 13 };
 static uint64_t layer_tid(int l, int slot) { return 100ull + 10ull * (uint64_t)l + (uint64_t)slot; }
 static uint64_t mtp_tid(int slot) { return 90ull + (uint64_t)slot; }   // the MTP head's decoder layer
+
+// ---- scratch of pipo_decode_step_noalloc -----------------------------------
+// A file-scope device array, one copy per GPU held until the process ends:
+// the decode attention's split partials at its start, then the k-range
+// partial sums of the larger-batch GEMVs.  Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in); it uses the
+// per-device address hipGetSymbolAddress returns, taken once per device at
+// context creation with that device current.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void *g_scratch_addr[kMaxDevices] = {};
+
+static hipError_t scratch_address(int dev, void **out) {
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_addr[dev] = ptr;
+    }
+    *out = g_scratch_addr[dev];
+    return hipSuccess;
+}
 
 extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *stream, pipo_ctx **out) {
     if (!out) return fail(nullptr, PIPO_EINVAL, "out is NULL");
@@ -403,6 +432,10 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         // test hook: fewer GEMV workgroups, so small models run several strip groups per workgroup
         const char *wc = getenv("PIPO_GEMV_WG_CAP");
         if (wc && atoi(wc) > 0) c->n_cu = atoi(wc);
+        c->dev = dev;
+        const hipError_t se = scratch_address(dev, &c->scratch);
+        if (se != hipSuccess)
+            return cleanup_fail(fail(c, PIPO_EHIP, "scratch address on device %d: %s", dev, hipGetErrorString(se)));
     }
     const char *ng = getenv("PIPO_NO_GRAPH");
     const char *ck = getenv("PIPO_CHECK");
@@ -926,6 +959,51 @@ extern "C" int pipo_decode_step(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pai
         HIP_TRY(c, hipGetLastError());
         if (c->enq_rc) return c->enq_rc;
     }
+    int rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
+    if (rc) return rc;
+    c->len += 1;
+    return PIPO_OK;
+}
+
+// The pair step of pipo_decode_step, launched eagerly on the caller's stream
+// with the attention and k-range partials in the device's static scratch:
+// no allocation and no graph instantiation, so a caller under HIP graph
+// capture can record it.
+extern "C" int pipo_decode_step_noalloc(pipo_ctx *c, const int32_t *d_in_pairs, pipo_pair *d_out,
+                                        float *d_logits_b, float *d_logits_d, void *stream) {
+    if (!c) return fail(nullptr, PIPO_EINVAL, "ctx is NULL");
+    if (!d_out) return fail(c, PIPO_EINVAL, "d_out must be non-NULL");
+    if (!c->prefilled || c->regular) return fail(c, PIPO_ESTATE, "decode step before a PIPO prefill");
+    if (c->len + 1 > c->cfg.max_latent)
+        return fail(c, PIPO_ECAPACITY, "KV cache full: %d latents, max_latent %d", c->len, c->cfg.max_latent);
+    if (!c->scratch) return fail(c, PIPO_EHIP, "no scratch address for device %d", c->dev);
+    const int64_t attn_floats =
+        round_up((int64_t)c->batch * c->nq * attn_splits(c, c->batch) * (c->d + 2), 64);
+    const int64_t cap_floats = (int64_t)(kScratchBytes / sizeof(float));
+    if (attn_floats > cap_floats)
+        return fail(c, PIPO_ECAPACITY, "attention partials of %lld bytes exceed the %zu-byte scratch",
+                    (long long)(attn_floats * 4), kScratchBytes);
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(c, hipGetLastError());
+    if (d_in_pairs)
+        HIP_TRY(c, hipMemcpyAsync(c->pairs, d_in_pairs, sizeof(int32_t) * 2 * c->batch, hipMemcpyDeviceToDevice, s));
+    // this call's partials live in the scratch; the GEMVs whose k-range
+    // partials do not fit the rest take their whole-K path instead
+    float *const apart = c->apart, *const gpart = c->gpart;
+    const int64_t gcap = c->gpart_cap;
+    const bool prof = c->prof_on;
+    c->apart = (float *)c->scratch;
+    c->gpart = c->apart + attn_floats;
+    c->gpart_cap = cap_floats - attn_floats;
+    c->prof_on = false;   // no events: profiling does not cover this call
+    c->enq_rc = PIPO_OK;
+    enqueue_decode(c, s);
+    c->apart = apart;
+    c->gpart = gpart;
+    c->gpart_cap = gcap;
+    c->prof_on = prof;
+    HIP_TRY(c, hipGetLastError());
+    if (c->enq_rc) return c->enq_rc;
     int rc = copy_outputs(c, d_out, d_logits_b, d_logits_d, s);
     if (rc) return rc;
     c->len += 1;

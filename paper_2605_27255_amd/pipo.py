@@ -14,7 +14,7 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libpipo.so")
 
 PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -1, -2, -3, -4, -5
-EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step",
+EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step", "pipo_decode_step_noalloc",
             "pipo_regular_prefill", "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free",
             "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read",
             "pipo_opd_teacher_rows", "pipo_opd_targets", "pipo_opd_targets_bf16")
@@ -63,6 +63,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_init_weights.argtypes = [ctypes.POINTER(PipoConfig), ctypes.c_uint64, vp, ctypes.POINTER(vp)]
     lib.pipo_prefill.argtypes = [vp, i32, vp, i32, ctypes.POINTER(PipoSampling), vp, vp, vp, vp]
     lib.pipo_decode_step.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.pipo_decode_step_noalloc.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.pipo_regular_prefill.argtypes = [vp, i32, vp, i32, ctypes.POINTER(PipoSampling), vp, vp, vp]
     lib.pipo_prefill_ragged.argtypes = [vp, i32, vp, i32, ctypes.POINTER(i32), ctypes.POINTER(PipoSampling),
                                         vp, vp, vp, vp]
@@ -78,7 +79,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_opd_teacher_rows.argtypes = [vp, i32, i32, vp, vp]
     lib.pipo_opd_targets.argtypes = [i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     lib.pipo_opd_targets_bf16.argtypes = [i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
-    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step", "pipo_regular_prefill",
+    for fn in ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step",
+               "pipo_decode_step_noalloc", "pipo_regular_prefill",
                "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free", "pipo_read_weight",
                "pipo_profile_enable", "pipo_profile_read", "pipo_opd_teacher_rows", "pipo_opd_targets",
                "pipo_opd_targets_bf16"):
@@ -175,6 +177,12 @@ class PipoModel:
         self._check(self.lib.pipo_decode_step(self.ctx, _ptr(in_pairs), _ptr(out), _ptr(lb), _ptr(ld),
                                               self._stream()))
         return out, lb, ld
+
+    def decode_step_noalloc(self, out, in_pairs=None, logits_b=None, logits_d=None):
+        """pipo_decode_step_noalloc into caller-provided tensors: the library
+        allocates nothing and builds no graph (scratch in its static array)."""
+        self._check(self.lib.pipo_decode_step_noalloc(self.ctx, _ptr(in_pairs), _ptr(out), _ptr(logits_b),
+                                                      _ptr(logits_d), self._stream()))
 
     def decode_into(self, out, in_pairs=None, logits_b=None, logits_d=None):
         """decode_step writing into caller-provided tensors (no allocation)."""

@@ -242,6 +242,161 @@ def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_
     return res
 
 
+def measure(wl, n_steps, n_warmup, profile=True, ragged=False):
+    """Time ``n_steps`` whole requests of workload ``wl`` after ``n_warmup``
+    untimed ones (prompts resident in HBM), then, with ``profile``, one eager
+    pass with per-kernel-class HIP events.  Returns the JSON fields of the
+    workload and the figures the other legs reuse."""
+    import numpy as np
+    import torch
+    from paper_2605_27255_amd import PipoModel, unpack_pairs
+    from synth import rspec
+
+    m = wl.model
+    B, steps = wl.batch, wl.decode_steps
+    torch.cuda.set_device(0)
+    log(f"workload {wl.name}: {m.n_layers}L h{m.hidden} B{B} prompt {wl.prompt_tokens} "
+        f"({wl.latents} latents) + {steps} pair steps")
+    t0 = time.perf_counter()
+    model = PipoModel(m, seed=wl.seed, max_batch=B, max_latent=wl.latents + steps + 1,
+                      prefill_chunk=wl.prefill_chunk)
+    prompts = torch.from_numpy(rspec.prompt_tokens(B, wl.prompt_tokens, m.vocab, wl.prompt_seed)).cuda()
+    n_tok = wl.prompt_tokens
+    lens = [n_tok - (7919 * b) % max(1, n_tok // 2) for b in range(B)] if ragged else None
+    lat = [(n + 1) // 2 for n in lens] if lens else [wl.latents] * B
+    seeds = [wl.sample_seed_base + b for b in range(B)] if wl.temperature > 0 else None
+    outs = torch.empty((steps, B, 4), dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    log(f"init (device weight generation) {time.perf_counter() - t0:.1f} s")
+
+    stream = torch.cuda.current_stream()
+
+    def job(ev=None):
+        if ev:
+            ev[0].record(stream)
+        first, _, _ = model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k,
+                                    rep_penalty=wl.rep_penalty, lens=lens)
+        if ev:
+            ev[1].record(stream)
+        for s in range(steps):
+            model.decode_into(outs[s])
+        if ev:
+            ev[2].record(stream)
+        return first
+
+    for _ in range(n_warmup):
+        job()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_steps)]
+    firsts = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(n_steps):
+        firsts.append(job(evs[k]))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    # emitted tokens: the last timed request's records (all requests are identical)
+    fb = unpack_pairs(firsts[-1])
+    acc_all = outs[:, :, 3].cpu().numpy()
+    accepts = int(acc_all.sum()) + int(fb[3].sum())
+    pairs = steps * B + B
+    emitted_per_job = pairs + accepts
+    value = emitted_per_job * n_steps / wall
+    ttft = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    dec_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ms_step = dec_ms / max(steps, 1)
+    acc_rate = accepts / pairs
+    kv_mean = float(np.mean([sum(kv_step_bytes(m, 1, L + s) for L in lat) for s in range(max(steps, 1))]))
+    step_bytes = gemv_step_bytes(m, B) + kv_mean
+    log(f"timed {n_steps} requests in {wall:.3f} s: TTFT {ttft:.2f} ms, decode {ms_step:.3f} ms/pair step, "
+        f"acceptance {acc_rate:.3f}, {value:.1f} output tokens/s")
+    res = {
+        "value": round(value, 3), "ms_per_step": round(wall / n_steps * 1e3, 3),
+        "config": {"workload": wl.name, "layers": m.n_layers, "hidden": m.hidden, "ffn": m.ffn,
+                   "heads_q_kv": [m.n_q_heads, m.n_kv_heads], "head_dim": m.head_dim, "vocab": m.vocab,
+                   "batch": B, "prompt_tokens": wl.prompt_tokens, "latents": wl.latents,
+                   "prompt_lengths": ("ragged, mean %.0f" % np.mean(lens)) if lens else "uniform",
+                   "decode_steps": steps, "tau": wl.tau,
+                   "sampling": ("greedy" if wl.temperature <= 0 else f"T{wl.temperature} top-p{wl.top_p}"
+                                + (f" top-k{wl.top_k} rep-penalty{wl.rep_penalty}"
+                                   if wl.top_k or wl.rep_penalty != 1.0 else "")),
+                   "parallelism": "none (1 GPU)"},
+        "ttft_ms": round(ttft, 3),
+        "decode": {"ms_per_pair_step": round(ms_step, 4), "pair_steps_per_s": round(B * 1e3 / ms_step, 2),
+                   "output_tokens_per_s": round(B * (1 + acc_rate) * 1e3 / ms_step, 2),
+                   "acceptance": round(acc_rate, 4),
+                   "algorithmic_gb_per_step": round(step_bytes / 1e9, 4),
+                   "hbm_gbs": round(step_bytes / ms_step / 1e6, 1),
+                   "hbm_frac": round(step_bytes / ms_step / 1e6 / HBM_PEAK_GBS, 4)},
+    }
+
+    if profile:
+        settle = min(4, steps // 4)          # eager steps before the counted ones
+        psteps = max(1, min(steps - settle, 32))
+        model.profile(True)
+        model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty,
+                      lens=lens)
+        torch.cuda.synchronize()
+        pre = model.profile_read()
+        model.profile(True)
+        for s in range(settle):              # settle the eager path first; not counted
+            model.decode_into(outs[s])
+        torch.cuda.synchronize()
+        model.profile_read()
+        model.profile(True)
+        for s in range(psteps):
+            model.decode_into(outs[settle + s])
+        torch.cuda.synchronize()
+        prof = model.profile_read()
+        model.profile(False)
+        gemv_ms = sum(prof[k][0] for k in ("gemv_layer", "gemv_lmhead", "gemv_small")) / psteps
+        gemv_n = sum(prof[k][1] for k in ("gemv_layer", "gemv_lmhead", "gemv_small")) / psteps
+        gb = gemv_step_bytes(m, B)
+        achieved = gb / (gemv_ms * 1e-3) / 1e9
+        per_class = {k: {"ms_per_step": round(v[0] / psteps, 4), "launches_per_step": v[1] / psteps}
+                     for k, v in prof.items() if v[1]}
+        res["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                           "traffic": measured_traffic(wl.name),
+                           "kernel": "k_gemv (decode weight-streaming GEMM, all launches of a pair step)",
+                           "bytes_per_launch": round(gb / gemv_n), "launches_per_step": gemv_n,
+                           "avg_launch_us": round(gemv_ms / gemv_n * 1e3, 3),
+                           "timing": "HIP events recorded by each k_gemv launch itself "
+                                     "(hipExtLaunchKernelGGL start/stop) on the library stream, in an "
+                                     "eager profiling pass after the timed region"}
+        if prof.get("attn_decode", (0, 0))[1]:
+            att_ms = prof["attn_decode"][0] / psteps
+            res["attn_decode"] = {"ms_per_pair_step": round(att_ms, 4), "kv_gb_per_step": round(kv_mean / 1e9, 4),
+                                  "hbm_gbs": round(kv_mean / att_ms / 1e6, 1),
+                                  "hbm_frac": round(kv_mean / att_ms / 1e6 / HBM_PEAK_GBS, 4)}
+        res["kernel_ms_per_pair_step"] = per_class
+        res["prefill_kernel_ms"] = {k: round(v[0], 3) for k, v in pre.items() if v[1]}
+        if pre.get("prefill_gemm", (0, 0))[1]:
+            # the prefill GEMMs (k_gemm_wd): 2 flops per weight per latent row; every
+            # layer GEMM also multiplies the activations' lo plane (a second MFMA)
+            h, f, L = m.hidden, m.ffn, m.n_layers
+            layer_w = (m.q_dim + 2 * m.kv_dim) * h + h * m.q_dim + 2 * f * h + h * f
+            rows = B * wl.latents
+            useful = 2.0 * rows * (L * layer_w + 2 * h * h)
+            issued = 2.0 * rows * (2 * L * layer_w + 2 * h * h)
+            sec = pre["prefill_gemm"][0] * 1e-3
+            res["prefill_gemm"] = {
+                "kernel": "k_gemm_wd", "bound": "mfma", "peak_tflops": 2500.0,
+                "useful_tflops": round(useful / sec / 1e12, 1), "issued_tflops": round(issued / sec / 1e12, 1),
+                "issued_frac": round(issued / sec / 1e12 / 2500.0, 4),
+                "note": "issued counts the lo-plane MFMAs (activations carried as bf16 hi + lo); times are the "
+                        "profiling pass's HIP events around every prefill GEMM launch"}
+        log("per-class decode ms/step:", {k: v["ms_per_step"] for k, v in per_class.items()})
+        log("prefill kernel ms:", res["prefill_kernel_ms"])
+
+    model.close()
+    del model
+    torch.cuda.empty_cache()
+    info = dict(prompts=prompts, seeds=seeds, ttft=ttft, ms_step=ms_step, acc_rate=acc_rate, wall=wall, lens=lens,
+                emitted_per_job=emitted_per_job)
+    return res, info
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -253,6 +408,8 @@ def main():
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-regular", action="store_true", help="skip the regular-decoding baseline leg")
     ap.add_argument("--no-opd", action="store_true", help="skip the OPD target kernel leg")
+    ap.add_argument("--no-bs32", action="store_true",
+                    help="skip the 4B batch-32 leg that the default (4B batch-1) run adds as the bs32 object")
     ap.add_argument("--heads", choices=("linear", "paper"), default="linear",
                     help="linear: the workloads' one-linear heads; paper: the App. B forms of all three heads")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch (up to 64)")
@@ -279,11 +436,7 @@ def main():
               "one-GPU figure is the per-GPU figure.", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
-    import torch
     from dataclasses import replace
-    from paper_2605_27255_amd import PipoModel, unpack_pairs
-    from synth import rspec
     from synth.configs import WORKLOADS
 
     wl = WORKLOADS[args.workload]
@@ -297,146 +450,24 @@ def main():
         wl = replace(wl, name=wl.name + "+ragged")
     if args.sampler == "eval":
         wl = replace(wl, name=wl.name + "+eval-sampler", temperature=1.0, top_p=0.95, top_k=20, rep_penalty=1.5)
-    m = wl.model
-    B, steps = wl.batch, wl.decode_steps
-    torch.cuda.set_device(0)
-    log(f"workload {wl.name}: {m.n_layers}L h{m.hidden} B{B} prompt {wl.prompt_tokens} "
-        f"({wl.latents} latents) + {steps} pair steps")
-    t0 = time.perf_counter()
-    model = PipoModel(m, seed=wl.seed, max_batch=B, max_latent=wl.latents + steps + 1,
-                      prefill_chunk=wl.prefill_chunk)
-    prompts = torch.from_numpy(rspec.prompt_tokens(B, wl.prompt_tokens, m.vocab, wl.prompt_seed)).cuda()
-    n_tok = wl.prompt_tokens
-    lens = [n_tok - (7919 * b) % max(1, n_tok // 2) for b in range(B)] if args.ragged else None
-    lat = [(n + 1) // 2 for n in lens] if lens else [wl.latents] * B
-    seeds = [wl.sample_seed_base + b for b in range(B)] if wl.temperature > 0 else None
-    outs = torch.empty((steps, B, 4), dtype=torch.int32, device="cuda")
-    torch.cuda.synchronize()
-    log(f"init (device weight generation) {time.perf_counter() - t0:.1f} s")
-
-    stream = torch.cuda.current_stream()
-
-    def job(ev=None):
-        if ev:
-            ev[0].record(stream)
-        first, _, _ = model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k,
-                                    rep_penalty=wl.rep_penalty, lens=lens)
-        if ev:
-            ev[1].record(stream)
-        for s in range(steps):
-            model.decode_into(outs[s])
-        if ev:
-            ev[2].record(stream)
-        return first
-
-    for _ in range(args.warmup):
-        job()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    emitted, accepts, pairs = 0, 0, 0
-    firsts = []
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for k in range(args.steps):
-        firsts.append(job(evs[k]))
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
-    # emitted tokens: the last timed request's records (all requests are identical)
-    fb = unpack_pairs(firsts[-1])
-    acc_all = outs[:, :, 3].cpu().numpy()
-    accepts = int(acc_all.sum()) + int(fb[3].sum())
-    pairs = steps * B + B
-    emitted_per_job = pairs + accepts
-    value = emitted_per_job * args.steps / wall
-    ttft = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    dec_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    ms_step = dec_ms / max(steps, 1)
-    acc_rate = accepts / pairs
-    kv_mean = float(np.mean([sum(kv_step_bytes(m, 1, L + s) for L in lat) for s in range(max(steps, 1))]))
-    step_bytes = gemv_step_bytes(m, B) + kv_mean
-    log(f"timed {args.steps} requests in {wall:.3f} s: TTFT {ttft:.2f} ms, decode {ms_step:.3f} ms/pair step, "
-        f"acceptance {acc_rate:.3f}, {value:.1f} output tokens/s")
-
-    result = {
-        "metric": METRIC, "value": round(value, 3), "unit": "output tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(wall / args.steps * 1e3, 3),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic (R-spec random-init weights and uniform random prompts)",
-        "config": {"workload": wl.name, "layers": m.n_layers, "hidden": m.hidden, "ffn": m.ffn,
-                   "heads_q_kv": [m.n_q_heads, m.n_kv_heads], "head_dim": m.head_dim, "vocab": m.vocab,
-                   "batch": B, "prompt_tokens": wl.prompt_tokens, "latents": wl.latents,
-                   "prompt_lengths": ("ragged, mean %.0f" % np.mean(lens)) if lens else "uniform",
-                   "decode_steps": steps, "tau": wl.tau,
-                   "sampling": ("greedy" if wl.temperature <= 0 else f"T{wl.temperature} top-p{wl.top_p}"
-                                + (f" top-k{wl.top_k} rep-penalty{wl.rep_penalty}"
-                                   if wl.top_k or wl.rep_penalty != 1.0 else "")),
-                   "parallelism": "none (1 GPU)"},
-        "ttft_ms": round(ttft, 3),
-        "decode": {"ms_per_pair_step": round(ms_step, 4), "pair_steps_per_s": round(1e3 / ms_step, 2),
-                   "output_tokens_per_s": round(B * (1 + acc_rate) * 1e3 / ms_step, 2),
-                   "acceptance": round(acc_rate, 4),
-                   "algorithmic_gb_per_step": round(step_bytes / 1e9, 4),
-                   "hbm_gbs": round(step_bytes / ms_step / 1e6, 1),
-                   "hbm_frac": round(step_bytes / ms_step / 1e6 / HBM_PEAK_GBS, 4)},
-    }
-
-    if not args.no_profile:
-        settle = min(4, steps // 4)          # eager steps before the counted ones
-        psteps = max(1, min(steps - settle, 32))
-        model.profile(True)
-        model.prefill(prompts, wl.tau, wl.temperature, wl.top_p, seeds, top_k=wl.top_k, rep_penalty=wl.rep_penalty,
-                      lens=lens)
-        torch.cuda.synchronize()
-        pre = model.profile_read()
-        model.profile(True)
-        for s in range(settle):              # settle the eager path first; not counted
-            model.decode_into(outs[s])
-        torch.cuda.synchronize()
-        model.profile_read()
-        model.profile(True)
-        for s in range(psteps):
-            model.decode_into(outs[settle + s])
-        torch.cuda.synchronize()
-        prof = model.profile_read()
-        model.profile(False)
-        gemv_ms = sum(prof[k][0] for k in ("gemv_layer", "gemv_lmhead", "gemv_small")) / psteps
-        gemv_n = sum(prof[k][1] for k in ("gemv_layer", "gemv_lmhead", "gemv_small")) / psteps
-        gb = gemv_step_bytes(m, B)
-        achieved = gb / (gemv_ms * 1e-3) / 1e9
-        per_class = {k: {"ms_per_step": round(v[0] / psteps, 4), "launches_per_step": v[1] / psteps}
-                     for k, v in prof.items() if v[1]}
-        result["roofline"] = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                              "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                              "traffic": measured_traffic(wl.name),
-                              "kernel": "k_gemv (decode weight-streaming GEMM, all launches of a pair step)",
-                              "bytes_per_launch": round(gb / gemv_n), "launches_per_step": gemv_n,
-                              "avg_launch_us": round(gemv_ms / gemv_n * 1e3, 3),
-                              "timing": "HIP events recorded by each k_gemv launch itself "
-                                        "(hipExtLaunchKernelGGL start/stop) on the library stream, in an "
-                                        "eager profiling pass after the timed region"}
-        result["kernel_ms_per_pair_step"] = per_class
-        result["prefill_kernel_ms"] = {k: round(v[0], 3) for k, v in pre.items() if v[1]}
-        if pre.get("prefill_gemm", (0, 0))[1]:
-            # the prefill GEMMs (k_gemm_wd): 2 flops per weight per latent row; every
-            # layer GEMM also multiplies the activations' lo plane (a second MFMA)
-            h, f, L = m.hidden, m.ffn, m.n_layers
-            layer_w = (m.q_dim + 2 * m.kv_dim) * h + h * m.q_dim + 2 * f * h + h * f
-            rows = B * wl.latents
-            useful = 2.0 * rows * (L * layer_w + 2 * h * h)
-            issued = 2.0 * rows * (2 * L * layer_w + 2 * h * h)
-            sec = pre["prefill_gemm"][0] * 1e-3
-            result["prefill_gemm"] = {
-                "kernel": "k_gemm_wd", "bound": "mfma", "peak_tflops": 2500.0,
-                "useful_tflops": round(useful / sec / 1e12, 1), "issued_tflops": round(issued / sec / 1e12, 1),
-                "issued_frac": round(issued / sec / 1e12 / 2500.0, 4),
-                "note": "issued counts the lo-plane MFMAs (activations carried as bf16 hi + lo); times are the "
-                        "profiling pass's HIP events around every prefill GEMM launch"}
-        log("per-class decode ms/step:", {k: v["ms_per_step"] for k, v in per_class.items()})
-        log("prefill kernel ms:", result["prefill_kernel_ms"])
-
-    model.close()
-    del model
-    torch.cuda.empty_cache()
+    res, info = measure(wl, args.steps, args.warmup, profile=not args.no_profile, ragged=args.ragged)
+    result = {"metric": METRIC, "value": res.pop("value"), "unit": "output tokens/s", "n_gpus": 1,
+              "steps": args.steps, "warmup": args.warmup, "ms_per_step": res.pop("ms_per_step"),
+              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+              "data": "synthetic (R-spec random-init weights and uniform random prompts)"}
+    result.update(res)
+    prompts, seeds, lens = info["prompts"], info["seeds"], info["lens"]
+    ttft, ms_step, acc_rate, wall = info["ttft"], info["ms_step"], info["acc_rate"], info["wall"]
+    emitted_per_job = info["emitted_per_job"]
+    if not args.no_bs32 and wl.name == "4b-bs1-ctx2048":
+        # the batch-32 half of the metric: the 4B batch-32 workload, one timed request
+        wl32 = WORKLOADS["4b-bs32-ctx8192-topp"]
+        r32, _ = measure(wl32, 1, 1, profile=not args.no_profile)
+        result["bs32"] = {"workload": wl32.name, "output_tokens_per_s": r32["value"],
+                          "ms_per_request": r32["ms_per_step"], "ttft_ms": r32["ttft_ms"], **r32["decode"]}
+        for k in ("roofline", "attn_decode", "kernel_ms_per_pair_step"):
+            if k in r32:
+                result["bs32"][k] = r32[k]
     if not args.no_regular:
         result["regular"] = regular_leg(wl, prompts, seeds, ttft, ms_step, acc_rate, wall / args.steps, lens,
                                         emitted_per_job, max(1, min(args.steps, 2)))

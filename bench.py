@@ -185,6 +185,47 @@ def opd_leg(T=2048, V=151936, reps=20):
             "timing": "torch events on the launching stream around 20 launches (the kernel is the only work)"}
 
 
+def ceilings_leg(m, reps=20):
+    """Attainable ceilings on this GPU, from the library's measurement kernels.
+
+    stream: the decode GEMV's weight-stream pattern (1 KB tiles per wave load,
+    nontemporal, two batches of five in flight, 256 x 8 waves) reading each
+    matrix size of one pair step once, each launch from other bytes of a
+    2 GiB buffer (from HBM, as the step's matrices are); ``step_ms`` is the sum over a pair
+    step's matrices (layers, the embedding twice, compressor and MTP), the
+    time a pure weight stream of the step would take launch by launch.
+    mfma: v_mfma_f32_16x16x32_bf16 issue rate with register operands (4 x 4
+    independent accumulators per wave) on random and on zero bf16 data, at
+    1, 2 and 4 waves per SIMD."""
+    import torch
+    from paper_2605_27255_amd import calibrate_stream, calibrate_mfma
+    h, f, v, L = m.hidden, m.ffn, m.vocab, m.n_layers
+    mats = {"qkv": ((m.q_dim + 2 * m.kv_dim) * h * 2, L), "o": (h * m.q_dim * 2, L), "gate_up": (2 * f * h * 2, L),
+            "down": (h * f * 2, L), "lm_head": (v * h * 2, 2), "compressor_mtp": (2 * h * h * 2, 2)}
+    # 2 GiB: each launch reads another window, so nothing is served from L2 or the memory-side cache
+    buf = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    stream, step_us = {}, 0.0
+    for name, (nbytes, count) in mats.items():
+        nb = nbytes // 1024 * 1024
+        us = calibrate_stream(buf, nb, reps)
+        stream[name] = {"bytes": nb, "us": round(us, 2), "gbs": round(nb / (us * 1e3), 1), "per_step": count}
+        step_us += us * count
+    del buf
+    g = torch.Generator(device="cuda").manual_seed(0)
+    rnd = (torch.randn(8192, generator=g, device="cuda") * 0.5).to(torch.bfloat16)
+    zer = torch.zeros(8192, dtype=torch.bfloat16, device="cuda")
+    mfma = {}
+    for w in (1, 2, 4):
+        mfma[f"random_{w}w"] = round(calibrate_mfma(rnd, w, iters=4096 // w), 1)
+        mfma[f"zero_{w}w"] = round(calibrate_mfma(zer, w, iters=4096 // w), 1)
+    torch.cuda.empty_cache()
+    res = {"stream": stream, "stream_step_ms": round(step_us / 1e3, 4), "mfma_bf16_tflops": mfma,
+           "kernels": "k_cal_stream, k_cal_mfma (csrc/calibrate.hip)"}
+    log(f"ceilings: weight stream of a pair step {step_us / 1e3:.3f} ms; "
+        + ", ".join(f"{k} {x['gbs']:.0f} GB/s" for k, x in stream.items()) + f"; MFMA bf16 TF/s {mfma}")
+    return res
+
+
 def regular_leg(wl, prompts, seeds, pipo_ttft, pipo_ms_step, acc_rate, pipo_job_s, lens, emitted, reps):
     """Regular decoding of the same prompt on the same kernels: one timed job is
     the n-position prefill plus as many token steps as the pair decoder ran
@@ -408,6 +449,7 @@ def main():
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-regular", action="store_true", help="skip the regular-decoding baseline leg")
     ap.add_argument("--no-opd", action="store_true", help="skip the OPD target kernel leg")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the stream / MFMA ceiling measurements")
     ap.add_argument("--no-bs32", action="store_true",
                     help="skip the 4B batch-32 leg that the default (4B batch-1) run adds as the bs32 object")
     ap.add_argument("--heads", choices=("linear", "paper"), default="linear",
@@ -418,9 +460,17 @@ def main():
     ap.add_argument("--sampler", choices=("workload", "eval"), default="workload",
                     help="workload: the workload's own selection; eval: the paper's evaluation sampler "
                          "(T 1.0, top-p 0.95, top-k 20, repetition penalty 1.5)")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="only measure the attainable ceilings (weight stream per matrix size, MFMA issue rate)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (counter calibration) and exit")
     args = ap.parse_args()
+    if args.calibrate:
+        import torch
+        from synth.configs import WORKLOADS
+        torch.cuda.set_device(0)
+        print(json.dumps({"ceilings": ceilings_leg(WORKLOADS[args.workload].model)}), flush=True)
+        return
     if args.calibrate_copy:
         import torch
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")      # 1 GiB
@@ -473,6 +523,15 @@ def main():
                                         emitted_per_job, max(1, min(args.steps, 2)))
     if not args.no_opd:
         result["opd"] = opd_leg()
+    if not args.no_ceilings:
+        cl = ceilings_leg(wl.model)
+        kc = result.get("kernel_ms_per_pair_step", {})
+        gm = sum(kc.get(k, {}).get("ms_per_step", 0.0) for k in ("gemv_layer", "gemv_lmhead", "gemv_small"))
+        if gm:
+            # the step's GEMV time against a pure weight stream of the same matrices
+            cl["gemv_ms_per_step"] = round(gm, 4)
+            cl["gemv_over_stream_ceiling"] = round(gm / cl["stream_step_ms"], 3)
+        result["ceilings"] = cl
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         result["cpu_baseline"] = cpu_baseline(wl, acc_rate)

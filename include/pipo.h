@@ -278,6 +278,35 @@ int pipo_profile_enable(pipo_ctx *ctx, int on);
  * launches since profiling was turned on.  Errors: PIPO_EINVAL. */
 int pipo_profile_read(pipo_ctx *ctx, int kclass, double *total_ms, int64_t *launches);
 
+/* Measurement aids (no passage of the paper; they compute nothing of the
+ * method).  They give the attainable ceilings that the kernels of Sec. 3.2
+ * and Sec. 4.3 are compared with.  Both are synchronous: they launch one
+ * untimed and then `reps` timed back-to-back launches on `stream` and wait.
+ *
+ * pipo_calibrate_stream: each launch reads `bytes` of the device buffer
+ * d_buf (`buf_bytes` long) with the decode GEMV's weight-stream pattern (one
+ * contiguous 1 KB tile per wave load, 16 bytes per lane, nontemporal; two
+ * batches of five tiles in flight per wave; 256 workgroups of eight waves).
+ * Launch r reads the window starting at 1 KB tile (r * bytes/1024) mod
+ * ((buf_bytes - bytes)/1024 + 1), so with buf_bytes well above the caches
+ * (256 MB memory-side cache, 4 MB L2 per XCD) every launch reads from HBM.
+ * *us = mean microseconds per launch.  The buffer is only read; its contents
+ * do not matter.  Errors: PIPO_EINVAL (NULL pointer, bytes < 1024 or not a
+ * multiple of 1024, buf_bytes < bytes, reps < 1), PIPO_ENOMEM, PIPO_EHIP.
+ *
+ * pipo_calibrate_mfma: issue rate of v_mfma_f32_16x16x32_bf16 with register
+ * operands, as the prefill GEMM issues them (a 4 x 4 block of independent
+ * accumulators per wave).  `waves_per_simd` (1, 2 or 4) waves run on every
+ * SIMD of every compute unit, each `iters` rounds of 16 MFMAs on eight
+ * operand registers loaded once from d_operands (at least 8 KB, bf16 bit
+ * patterns the caller chooses: random data draws more power than zeros).
+ * *tflops = 16384 flops per MFMA over the mean launch time.
+ * Errors: PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP. */
+int pipo_calibrate_stream(const void *d_buf, int64_t buf_bytes, int64_t bytes, int32_t reps, double *us,
+                          void *stream);
+int pipo_calibrate_mfma(const void *d_operands, int32_t waves_per_simd, int32_t iters, int32_t reps,
+                        double *tflops, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

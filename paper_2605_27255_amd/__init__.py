@@ -2,5 +2,6 @@
 compressed-prompt prefill, behind the C ABI in ``include/pipo.h``."""
 from .pipo import (  # noqa: F401
     PipoModel, PipoError, load_library, make_config, unpack_pairs, LIB_PATH, EXPORTED, opd_teacher_rows, opd_targets,
+    calibrate_stream, calibrate_mfma,
     PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE,
 )

@@ -49,19 +49,21 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
     const uint16_t *vbase = p.vc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
 
-    // K and V fragments of one 32-key block: K rows (16 keys per tile, 32 dims
-    // per MFMA step) and the 32-key V tile, 16 dims per output tile.
+    // K and V fragments of one 32-key block: two 16-key K tiles (one 1 KB
+    // tile per 32 dims, stored in MFMA operand order, so each load is one
+    // contiguous 1 KB read) and the 32-key V tile, 16 dims per output tile.
+    // Every key is read once per step: nontemporal loads.
     u32x4 kf[2][2][NC], vf[2][NT];
     auto load_block = [&](int bsel, int kb) {
 #pragma unroll
         for (int tau = 0; tau < 2; ++tau) {
-            const uint16_t *kr = kbase + (int64_t)(kb + 16 * tau + j) * D + 8 * g;
+            const uint16_t *kt = kbase + ((int64_t)((kb >> 4) + tau) * NC) * 512 + lane * 8;
 #pragma unroll
-            for (int c = 0; c < NC; ++c) kf[bsel][tau][c] = *(const u32x4 *)(kr + 32 * c);
+            for (int c = 0; c < NC; ++c) kf[bsel][tau][c] = __builtin_nontemporal_load((const u32x4 *)(kt + c * 512));
         }
         const uint16_t *vt = vbase + (int64_t)(kb >> 5) * D * 32 + j * 32 + 8 * g;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) vf[bsel][t] = *(const u32x4 *)(vt + t * 16 * 32);
+        for (int t = 0; t < NT; ++t) vf[bsel][t] = __builtin_nontemporal_load((const u32x4 *)(vt + t * 16 * 32));
     };
     // blocks k0 + 32 i, i < nblk; loads past the end re-read the first block
     const int nblk = k0 < k1 ? (k1 - k0 + 31) >> 5 : 0;

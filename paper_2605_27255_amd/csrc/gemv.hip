@@ -410,7 +410,8 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams &p, f32x4 (&fin)[
                     u32x2 w;
                     w[0] = pack_bf2(r[0], r[1]);
                     w[1] = pack_bf2(r[2], r[3]);
-                    *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
+                    *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + (int64_t)head * p.lmax_pad * d +
+                               tiled_index(pos, dim0, d)) = w;
                 }
             } else {
                 const int r0 = (strip - qs - kvs) * 16 + 4 * g;

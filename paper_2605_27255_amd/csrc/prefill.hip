@@ -280,7 +280,8 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
                 u32x2 w;
                 w[0] = pack_bf2(r[0], r[1]);
                 w[1] = pack_bf2(r[2], r[3]);
-                *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + ((int64_t)head * p.lmax_pad + pos) * d + dim0) = w;
+                *(u32x2 *)(p.kc + (int64_t)b * p.kv_bstride + (int64_t)head * p.lmax_pad * d +
+                           tiled_index(pos, dim0, d)) = w;
             }
         } else {
             const int r0 = (strip - qs - ks) * 16 + 4 * g;
@@ -482,9 +483,8 @@ constexpr int kAK = 64;         // keys per LDS stage
 template <int D>
 __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     constexpr int NC = D / 32, NT = D / 16;
-    constexpr int KS = D + 8;           // padded K row (elements)
     constexpr int VS = 40;              // padded V tile row (elements)
-    __shared__ __align__(16) uint16_t ks2[2][kAK * KS];
+    __shared__ __align__(16) uint16_t ks2[2][kAK * D];   // K tiles as in the cache
     __shared__ __align__(16) uint16_t vs2[2][2 * D * VS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -538,9 +538,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
         for (int u = 0; u < KU; ++u) {
             const int c = tid + u * 256;
             const uint16_t *src;
-            if (u * 256 < KCH) {          // K rows (whole unrolled slots, KCH is a multiple of 256)
-                const int r = c / (D / 8), e = (c - r * (D / 8)) * 8;
-                src = kbase + (int64_t)(kb0 + r) * D + e;
+            if (u * 256 < KCH) {          // K tiles (whole unrolled slots, KCH is a multiple of 256):
+                                          // the stage's 64 keys are one contiguous block of the cache
+                src = kbase + (int64_t)kb0 * D + c * 8;
             } else {                      // V tiles: row = tile * D + dim
                 const int cv = c - KCH;
                 const int row = cv >> 2, e = (cv & 3) * 8;
@@ -554,8 +554,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
         for (int u = 0; u < KU; ++u) {
             const int c = tid + u * 256;
             if (u * 256 < KCH) {
-                const int r = c / (D / 8), e = (c - r * (D / 8)) * 8;
-                *(u32x4 *)(&ks2[buf][r * KS + e]) = stg[u];
+                *(u32x4 *)(&ks2[buf][c * 8]) = stg[u];
             } else {
                 const int cv = c - KCH;
                 const int row = cv >> 2, e = (cv & 3) * 8;
@@ -574,7 +573,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
         for (int tau = 0; tau < 4; ++tau) {
             u32x4 kf[NC];
 #pragma unroll
-            for (int c = 0; c < NC; ++c) kf[c] = *(const u32x4 *)(&ks[(16 * tau + j) * KS + 32 * c + 8 * g]);
+            for (int c = 0; c < NC; ++c) kf[c] = *(const u32x4 *)(&ks[(tau * NC + c) * 512 + lane * 8]);
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
                 sc[ct][tau] = f32x4{0.f, 0.f, 0.f, 0.f};

@@ -17,7 +17,8 @@ PIPO_OK, PIPO_EINVAL, PIPO_ENOMEM, PIPO_EHIP, PIPO_ECAPACITY, PIPO_ESTATE = 0, -
 EXPORTED = ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step", "pipo_decode_step_noalloc",
             "pipo_regular_prefill", "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free",
             "pipo_last_error", "pipo_read_weight", "pipo_profile_enable", "pipo_profile_read",
-            "pipo_opd_teacher_rows", "pipo_opd_targets", "pipo_opd_targets_bf16")
+            "pipo_opd_teacher_rows", "pipo_opd_targets", "pipo_opd_targets_bf16",
+            "pipo_calibrate_stream", "pipo_calibrate_mfma")
 #: kernel classes of the profiling counters (PIPO_K_* in include/pipo.h)
 KERNEL_CLASSES = ("gemv_layer", "gemv_lmhead", "gemv_small", "attn_decode", "sample", "gate",
                   "prefill_gemm", "prefill_attn", "prefill_misc")
@@ -79,11 +80,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.pipo_opd_teacher_rows.argtypes = [vp, i32, i32, vp, vp]
     lib.pipo_opd_targets.argtypes = [i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     lib.pipo_opd_targets_bf16.argtypes = [i32, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
+    lib.pipo_calibrate_stream.argtypes = [vp, i64, i64, i32, ctypes.POINTER(ctypes.c_double), vp]
+    lib.pipo_calibrate_mfma.argtypes = [vp, i32, i32, i32, ctypes.POINTER(ctypes.c_double), vp]
     for fn in ("pipo_init_weights", "pipo_prefill", "pipo_prefill_ragged", "pipo_decode_step",
                "pipo_decode_step_noalloc", "pipo_regular_prefill",
                "pipo_regular_prefill_ragged", "pipo_regular_step", "pipo_free", "pipo_read_weight",
                "pipo_profile_enable", "pipo_profile_read", "pipo_opd_teacher_rows", "pipo_opd_targets",
-               "pipo_opd_targets_bf16"):
+               "pipo_opd_targets_bf16", "pipo_calibrate_stream", "pipo_calibrate_mfma"):
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -295,3 +298,33 @@ def opd_targets(logits_s, logits_t, labels, rows=None, sums: bool = True):
                                          _ptr(labels), _ptr(kl), _ptr(alpha), _ptr(sm),
                                          ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
     return kl, alpha, sm
+
+
+def calibrate_stream(buf, nbytes: int, reps: int = 20) -> float:
+    """Mean microseconds per launch of the weight-stream pattern reading
+    ``nbytes`` of the CUDA tensor ``buf``, a different window each launch
+    (measurement only)."""
+    import torch
+    lib = load_library()
+    total = buf.numel() * buf.element_size()
+    assert buf.is_cuda and buf.is_contiguous() and nbytes <= total
+    us = ctypes.c_double()
+    rc = lib.pipo_calibrate_stream(_ptr(buf), int(total), int(nbytes), int(reps), ctypes.byref(us),
+                                   ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    if rc != PIPO_OK:
+        raise PipoError(rc, "pipo_calibrate_stream failed")
+    return us.value
+
+
+def calibrate_mfma(operands, waves_per_simd: int, iters: int = 4096, reps: int = 5) -> float:
+    """bf16 16x16x32 MFMA issue rate in TFLOP/s with register operands taken
+    from the CUDA tensor ``operands`` (at least 8 KB; measurement only)."""
+    import torch
+    lib = load_library()
+    assert operands.is_cuda and operands.is_contiguous() and operands.numel() * operands.element_size() >= 8192
+    tf = ctypes.c_double()
+    rc = lib.pipo_calibrate_mfma(_ptr(operands), int(waves_per_simd), int(iters), int(reps), ctypes.byref(tf),
+                                 ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    if rc != PIPO_OK:
+        raise PipoError(rc, "pipo_calibrate_mfma failed")
+    return tf.value

@@ -106,6 +106,20 @@ def test_null_arguments(lib):
     assert lib.pipo_read_weight(None, b"embed", 0, 1, None) == pipo.PIPO_EINVAL
     assert lib.pipo_free(None) == pipo.PIPO_OK
     assert b"ctx" in lib.pipo_last_error(None)
+    # measurement aids: argument checks before any HIP call
+    us = ctypes.c_double()
+    lib.pipo_calibrate_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                          ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
+    lib.pipo_calibrate_mfma.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
+    assert lib.pipo_calibrate_stream(None, 1024, 1024, 1, ctypes.byref(us), None) == pipo.PIPO_EINVAL
+    assert lib.pipo_calibrate_stream(fake, 4096, 1000, 1, ctypes.byref(us), None) == pipo.PIPO_EINVAL
+    assert lib.pipo_calibrate_stream(fake, 1024, 2048, 1, ctypes.byref(us), None) == pipo.PIPO_EINVAL
+    assert lib.pipo_calibrate_stream(fake, 1024, 1024, 0, ctypes.byref(us), None) == pipo.PIPO_EINVAL
+    assert lib.pipo_calibrate_stream(fake, 1024, 1024, 1, None, None) == pipo.PIPO_EINVAL
+    assert lib.pipo_calibrate_mfma(None, 1, 1, 1, ctypes.byref(us), None) == pipo.PIPO_EINVAL
+    assert lib.pipo_calibrate_mfma(fake, 3, 1, 1, ctypes.byref(us), None) == pipo.PIPO_EINVAL
+    assert lib.pipo_calibrate_mfma(fake, 1, 0, 1, ctypes.byref(us), None) == pipo.PIPO_EINVAL
 
 
 def test_gemv_dispatch_refuses_unlisted_variant(lib):

@@ -483,9 +483,10 @@ constexpr int kAK = 64;         // keys per LDS stage
 template <int D>
 __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     constexpr int NC = D / 32, NT = D / 16;
-    constexpr int VS = 40;              // padded V tile row (elements)
-    __shared__ __align__(16) uint16_t ks2[2][kAK * D];   // K tiles as in the cache
-    __shared__ __align__(16) uint16_t vs2[2][2 * D * VS];
+    // two stage buffers, each the stage's K tiles (as in the cache) then its
+    // V fragments in MFMA operand order; two named arrays, so that reading
+    // one while the other fills is visibly independent
+    __shared__ __align__(16) uint16_t kv_a[2 * kAK * D], kv_b[2 * kAK * D];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = lane & 15, g = lane >> 4;
@@ -528,135 +529,134 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
 
     const int kend = qpos0 + kAQ;              // keys [0, kend) may be visible
-    // K rows and V tiles of one 64-key stage, KU 16-byte chunks per thread
-    constexpr int KCH = kAK * D / 8, VCH = 2 * D * 4;   // chunks per stage
-    constexpr int KU = (KCH + VCH) / 256;
+    // One 64-key stage straight from the cache into LDS (global_load_lds: lane
+    // l of a wave writes 16 bytes at the buffer block's base + 16 l, no
+    // registers): the K tiles are 16 contiguous 1 KB blocks (D = 128) copied
+    // as they are; each 1 KB V block (16 dims x 32 keys of a V tile) is read
+    // with its lanes permuted so that lane l = 16 g + j lands holding dim j,
+    // keys 8 g .. 8 g + 7, the PV MFMA's A operand, read back linearly.
+    constexpr int KBW = D / 32;            // K (and V) blocks per wave per stage
     const int nstage = (kend + kAK - 1) / kAK;
-    u32x4 stg[KU];
-    auto stage_load = [&](int kb0) {
+    using lds_t = __attribute__((address_space(3))) void;
+    auto stage_issue = [&](uint16_t *buf, int kb0) {
 #pragma unroll
-        for (int u = 0; u < KU; ++u) {
-            const int c = tid + u * 256;
-            const uint16_t *src;
-            if (u * 256 < KCH) {          // K tiles (whole unrolled slots, KCH is a multiple of 256):
-                                          // the stage's 64 keys are one contiguous block of the cache
-                src = kbase + (int64_t)kb0 * D + c * 8;
-            } else {                      // V tiles: row = tile * D + dim
-                const int cv = c - KCH;
-                const int row = cv >> 2, e = (cv & 3) * 8;
-                src = vbase + (int64_t)(kb0 >> 5) * D * 32 + (int64_t)row * 32 + e;
-            }
-            stg[u] = *(const u32x4 *)src;
+        for (int u = 0; u < KBW; ++u) {
+            const int blk = wave * KBW + u;
+            const uint16_t *src = kbase + (int64_t)kb0 * D + blk * 512 + lane * 8;
+            __builtin_amdgcn_global_load_lds((const void *)src, (lds_t *)(buf + blk * 512), 16, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < KBW; ++u) {
+            const int vb = wave * KBW + u, h = vb / NT, t = vb - h * NT;
+            const uint16_t *src = vbase + (int64_t)((kb0 >> 5) + h) * D * 32 + (16 * t + j) * 32 + 8 * g;
+            __builtin_amdgcn_global_load_lds((const void *)src, (lds_t *)(buf + kAK * D + vb * 512), 16, 0, 0);
         }
     };
-    auto stage_store = [&](int buf) {
-#pragma unroll
-        for (int u = 0; u < KU; ++u) {
-            const int c = tid + u * 256;
-            if (u * 256 < KCH) {
-                *(u32x4 *)(&ks2[buf][c * 8]) = stg[u];
-            } else {
-                const int cv = c - KCH;
-                const int row = cv >> 2, e = (cv & 3) * 8;
-                *(u32x4 *)(&vs2[buf][row * VS + e]) = stg[u];
-            }
-        }
-    };
-    // One 64-key stage: scores S^T for the four 16-key tiles and both query
-    // tiles, one online-softmax update per query tile, then O^T += V^T P^T.
-    // The running max only moves when some column's max grows by more than
-    // 2^8 (in exp2 units), so the accumulators are rarely rescaled and every
-    // exponent stays at most 256; o / l at the end is the same quotient.
-    auto attend = [&](const uint16_t *ks, const uint16_t *vs, int kb0, bool diag) {
-        f32x4 sc[2][4];
+    // One 64-key stage: the scores of both 16-query tiles, the softmax of
+    // tile 0, then the PV MFMAs of tile 0 with the softmax of tile 1 (VALU
+    // that does not depend on them) issued between them, then tile 1's PV.
+    // The scores are S^T over the four 16-key tiles; the softmax is one
+    // online update per tile and stage; PV is O^T += V^T P^T.  The running
+    // max only moves when some column's max grows by more than 2^8 (in exp2
+    // units), so the accumulators are rarely rescaled and every exponent
+    // stays at most 256; o / l at the end is the same quotient.  The rescale
+    // decision (a branch) is taken before each overlapped phase.
+    auto scores = [&](const uint16_t *ks, f32x4 (&s0)[4], f32x4 (&s1)[4]) {
 #pragma unroll
         for (int tau = 0; tau < 4; ++tau) {
             u32x4 kf[NC];
 #pragma unroll
             for (int c = 0; c < NC; ++c) kf[c] = *(const u32x4 *)(&ks[(tau * NC + c) * 512 + lane * 8]);
+            s0[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
+            s1[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
-                sc[ct][tau] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int c = 0; c < NC; ++c) {
-                    sc[ct][tau] = mfma16(kf[c], qb[ct][c], sc[ct][tau]);
-                    sc[ct][tau] = mfma16(kf[c], ql[ct][c], sc[ct][tau]);
-                }
+            for (int c = 0; c < NC; ++c) {
+                s0[tau] = mfma16(kf[c], qb[0][c], s0[tau]);
+                s1[tau] = mfma16(kf[c], qb[1][c], s1[tau]);
+                s0[tau] = mfma16(kf[c], ql[0][c], s0[tau]);
+                s1[tau] = mfma16(kf[c], ql[1][c], s1[tau]);
             }
         }
-        u32x4 pt[2][2], pl[2][2];   // P^T as a bf16 pair hi + lo
+    };
+    // masked scores (diagonal stages only), the column max and the rescale
+    auto soft_max = [&](int ct, f32x4 (&sct)[4], int kb0, bool diag) {
+        // keys past this column's query are masked
+        const int lim = diag ? qpos0 + 16 * ct + j - kb0 - 4 * g : 64;
+        float mx = -INFINITY;
 #pragma unroll
-        for (int ct = 0; ct < 2; ++ct) {
-            // keys past this column's query are masked (only on diagonal stages)
-            const int lim = diag ? qpos0 + 16 * ct + j - kb0 - 4 * g : 64;
-            float mx = -INFINITY;
+        for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
-            for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    float sv = sc[ct][tau][v];
-                    if (diag) sv = 16 * tau + v <= lim ? sv : -INFINITY;
-                    sc[ct][tau][v] = sv;
-                    mx = fmaxf(mx, sv);
-                }
-            mx = col_max(mx);
-            // a query row sees key 0 in the first stage, so the max is finite from then on
-            const float m_cand = fmaxf(m_run[ct], mx * scale);
-            if (__any(m_cand > m_run[ct] + 8.0f)) {
-                const float alpha = __builtin_amdgcn_exp2f(m_run[ct] - m_cand);
-                l_run[ct] *= alpha;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) o[ct][t] *= alpha;
-                m_run[ct] = m_cand;
+            for (int v = 0; v < 4; ++v) {
+                float sv = sct[tau][v];
+                if (diag) sv = 16 * tau + v <= lim ? sv : -INFINITY;
+                sct[tau][v] = sv;
+                mx = fmaxf(mx, sv);
             }
-            const float m_use = m_run[ct];
-            float ps = 0.f;
+        mx = col_max(mx);
+        // a query row sees key 0 in the first stage, so the max is finite from then on
+        const float m_cand = fmaxf(m_run[ct], mx * scale);
+        if (__any(m_cand > m_run[ct] + 8.0f)) {
+            const float alpha = __builtin_amdgcn_exp2f(m_run[ct] - m_cand);
+            l_run[ct] *= alpha;
 #pragma unroll
-            for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const float e = __builtin_amdgcn_exp2f(fmaf(sc[ct][tau][v], scale, -m_use));
-                    sc[ct][tau][v] = e;
-                    ps += e;
-                }
-            l_run[ct] += col_sum(ps);
-#pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const float f[8] = {sc[ct][2 * half][0], sc[ct][2 * half][1], sc[ct][2 * half][2],
-                                    sc[ct][2 * half][3], sc[ct][2 * half + 1][0], sc[ct][2 * half + 1][1],
-                                    sc[ct][2 * half + 1][2], sc[ct][2 * half + 1][3]};
-                split8(f, pt[ct][half], pl[ct][half]);
-            }
+            for (int t = 0; t < NT; ++t) o[ct][t] *= alpha;
+            m_run[ct] = m_cand;
         }
-        // O^T += V^T P^T, each V fragment serving both query tiles
+    };
+    // probabilities, their sum and the bf16 pair P^T = hi + lo
+    auto soft_exp = [&](int ct, f32x4 (&sct)[4], u32x4 (&ph)[2], u32x4 (&pl)[2]) {
+        const float m_use = m_run[ct];
+        float ps = 0.f;
+#pragma unroll
+        for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float e = __builtin_amdgcn_exp2f(fmaf(sct[tau][v], scale, -m_use));
+                sct[tau][v] = e;
+                ps += e;
+            }
+        l_run[ct] += col_sum(ps);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const float f[8] = {sct[2 * half][0], sct[2 * half][1], sct[2 * half][2], sct[2 * half][3],
+                                sct[2 * half + 1][0], sct[2 * half + 1][1], sct[2 * half + 1][2],
+                                sct[2 * half + 1][3]};
+            split8(f, ph[half], pl[half]);
+        }
+    };
+    auto pv = [&](const uint16_t *vs, int ct, const u32x4 (&ph)[2], const u32x4 (&pl)[2]) {
 #pragma unroll
         for (int half = 0; half < 2; ++half)
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                const u32x4 vf = *(const u32x4 *)(&vs[(half * D + 16 * t + j) * VS + 8 * g]);
-#pragma unroll
-                for (int ct = 0; ct < 2; ++ct) {
-                    o[ct][t] = mfma16(vf, pt[ct][half], o[ct][t]);
-                    o[ct][t] = mfma16(vf, pl[ct][half], o[ct][t]);
-                }
+                const u32x4 vf = *(const u32x4 *)(&vs[(half * NT + t) * 512 + lane * 8]);
+                o[ct][t] = mfma16(vf, ph[half], o[ct][t]);
+                o[ct][t] = mfma16(vf, pl[half], o[ct][t]);
             }
     };
+    auto attend = [&](const uint16_t *ks, const uint16_t *vs, int kb0, bool diag) {
+        f32x4 s0[4], s1[4];
+        u32x4 p0h[2], p0l[2], p1h[2], p1l[2];
+        scores(ks, s0, s1);
+        soft_max(0, s0, kb0, diag);
+        soft_exp(0, s0, p0h, p0l);
+        soft_max(1, s1, kb0, diag);
+        pv(vs, 0, p0h, p0l);
+        soft_exp(1, s1, p1h, p1l);
+        pv(vs, 1, p1h, p1l);
+    };
 
-    stage_load(0);
-    stage_store(0);
+    // stage s + 1 is requested (into the other buffer) before stage s is
+    // computed; one stage past the end stays inside the padded cache
+    stage_issue(kv_a, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    for (int st_i = 0; st_i < nstage; ++st_i) {
-        const int kb0 = st_i * kAK;
-        const int buf = st_i & 1;
-        // the next stage is always requested (one stage past the end stays
-        // inside the padded cache), so the load count per step is fixed
-        stage_load(kb0 + kAK);
-        const uint16_t *ks = ks2[buf], *vs = vs2[buf];
-        if (active) {
-            // the causal mask only where some key of the stage lies past some query
-            attend(ks, vs, kb0, kb0 + kAK - 1 > qpos0);
-        }
-        stage_store(buf ^ 1);
+    for (int st = 0; st < nstage; ++st) {
+        uint16_t *cur = (st & 1) ? kv_b : kv_a, *nxt = (st & 1) ? kv_a : kv_b;
+        stage_issue(nxt, (st + 1) * kAK);
+        // the causal mask only where some key of the stage lies past some query
+        if (active) attend(cur, cur + kAK * D, st * kAK, st * kAK + kAK - 1 > qpos0);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
     if (!active) return;

@@ -23,6 +23,8 @@
 // residual add, SwiGLU, RoPE + KV append, logits + argmax).
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -795,7 +797,10 @@ constexpr int kKrChunks = 8;                 // X chunks per thread: B * k-tiles
 template <int PRO>   // the MTP's chunks hold both halves' sources, and PRO_CAT keeps two sets of
                      // RMSNorm parts, so fewer fit in registers
 struct KrChunks { static constexpr int n = (PRO == PRO_MTP || PRO == PRO_CAT) ? 6 : kKrChunks; };
-constexpr int kKrWaves = 1280;               // streaming waves the ranges aim for (~20 MB in flight)
+// the k-range choice's model (host side): KB per microsecond the chip
+// streams and one wave streams (two 8 KB batches in flight), and the cost of a
+// finishing launch in microseconds
+constexpr double kKrChipRate = 6000.0, kKrWaveRate = 5.0, kKrFinUs = 5.0;
 template <int NBT, int PRO, int EPI, int U>
 __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
     constexpr int NA = NAcc<PRO>::n;
@@ -1041,17 +1046,32 @@ static void launch_multi(GemvParams &q, hipStream_t s) {
         // streaming waves
         int kmax = kKrLdsBytes / (2 * 2 * q.B * 32);
         const int krt_c = KrChunks<PRO>::n * kNW * 64 / (4 * q.B);
-        kmax = (kmax < krt_c ? kmax : krt_c) / 8 * 8;            // whole load batches of 8 tiles
-        int R = (KT + kmax - 1) / kmax;
-        const int r_par = (kKrWaves + (q.N >> 4) - 1) / (q.N >> 4);
-        R = R > r_par ? R : r_par;
-        R = R < KT ? R : KT;
-        int krt = (KT + R - 1) / R;                              // even ranges, rounded to whole batches
-        krt = (krt + 7) / 8 * 8;
-        krt = krt < kmax ? krt : kmax;
-        R = (KT + krt - 1) / krt;
+        kmax = (kmax < krt_c ? kmax : krt_c) / 4 * 4;
+        // the split with the shortest estimated time: ranges of nearly equal
+        // length (a multiple of 4 k-tiles), every range on the same number of
+        // workgroups, each wave streaming its strips in rounds; the stream
+        // takes the longer of the matrix at the chip's bandwidth and one wave's
+        // share at a wave's rate (at most the bandwidth split over the active
+        // waves); more than one range adds the finishing launch and the
+        // partial sums it writes and reads
+        const int S = q.N >> 4, wg = q.wg_cap > 0 ? q.wg_cap : 256;
+        const double total = (double)S * KT;                      // 1 KB tiles
+        int R = 0, krt = 0;
+        double best = 1e30;
+        for (int kt = 4; kt <= kmax; kt += 4) {
+            const int r0 = (KT + kt - 1) / kt;
+            const int ke = ((KT + r0 - 1) / r0 + 3) / 4 * 4;     // even ranges
+            if (ke > kmax) continue;
+            const int r = (KT + ke - 1) / ke;
+            const int nwr = (wg / r > 0 ? wg / r : 1) * kNW;
+            const double active = (double)std::min(S, nwr) * r;
+            const double rate = std::min(kKrWaveRate, kKrChipRate / active);
+            double t = std::max(total / kKrChipRate, (double)((S + nwr - 1) / nwr) * ke / rate);
+            if (r > 1) t += kKrFinUs + 2.0 * r * q.B * q.N * 4 / 1024.0 / kKrChipRate;
+            if (t < best - 1e-9) best = t, R = r, krt = ke;
+        }
         const bool partials = R > 1 && (int64_t)R * q.B * q.N <= q.part_cap;
-        if (kmax >= 8 && (R == 1 || partials)) {
+        if (R > 0 && (R == 1 || partials)) {
             q.ksplit = R;
             q.krt = krt;
             const int lds_kr = 2 * q.B * (krt * 32 + 8) * 2;

@@ -312,7 +312,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const uint32_t key = order_key(v[e]);
-                        if (valid(t, e) & ((pass == 0) | ((key >> (shift + 8)) == prefix)))
+                        if (valid(t, e) & ((pass == 0) | ((key >> ((shift + 8) & 31)) == prefix)))
                             atomicAdd(&hist[wave][(key >> shift) & 255u], 1ull);
                     }
                 });
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
             for (int e = 0; e < 4; ++e) {
                 const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
                 const uint32_t key = __float_as_uint(ev);
-                if (kept(t, e, v[e]) & ((pass == 0) | ((key >> (shift + 8)) == prefix)))
+                if (kept(t, e, v[e]) & ((pass == 0) | ((key >> ((shift + 8) & 31)) == prefix)))
                     atomicAdd(&hist[wave][(key >> shift) & 255u], fixed_mass(ev));
             }
         });
@@ -457,11 +457,230 @@ __global__ __launch_bounds__(kSampThreads) void k_sample(SampleParams p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Temperature + top-p with each row split over `nseg` workgroups, as six
+// short kernels (the same arithmetic and decisions as k_sample, so the same
+// token): the row max is the argmax key the LM head left in best[b];
+// kernels 0-3 each histogram one byte of the e-values' bits (fixed-point
+// masses) over their segment, only among the values whose higher bytes
+// match the prefix chosen so far, and store the segment's histogram; the
+// kernel after each pass adds the segments' histograms in segment order,
+// takes that pass's digit, and its segment-0 workgroup records the state
+// (prefix, mass above, nucleus mass, total) for the next kernel; kernel 4
+// stores each wave's nucleus mass; kernel 5 draws t = floor(u M) and the
+// wave whose id range holds it walks its ids in order.  Integer sums, so
+// every order of adding gives the same masses.
+constexpr int kSegThreads = 256, kSegWaves = 4;
+
+__device__ __forceinline__ float argmax_key_value(uint64_t key) {
+    const uint32_t u = (uint32_t)(key >> 32);
+    return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
+}
+
+template <int PASS>
+__global__ __launch_bounds__(kSegThreads) void k_sample_seg(SampleParams p) {
+    __shared__ unsigned long long hist[kSegWaves][256];
+    __shared__ unsigned long long s_suf[257], s_wtot[4];
+    __shared__ int s_dig;
+    __shared__ SampState s_st;
+    const int nseg = p.nseg, B = p.B, V = p.V;
+    const int b = blockIdx.x / nseg, seg = blockIdx.x - b * nseg;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int R = p.seg_len, RW = R / kSegWaves;              // ids per segment and per wave (multiples of 256)
+    const int w0 = seg * R + wave * RW;
+    const int nt = RW / 256;
+    const float *lg = p.logits + (int64_t)b * V;
+    const float mx = argmax_key_value(p.best[b]);
+    const float kT = 1.4426950408889634f / p.temperature;
+    unsigned long long *H = p.hist + (int64_t)b * 4 * nseg * 256;      // [pass][segment][256]
+
+    // the state before this kernel's pass: the previous kernel's record and
+    // the previous pass's histogram (all segments, in segment order)
+    if (PASS == 0) {
+        if (tid == 0) s_st = SampState{0u, 0, 0ull, 0ull, 0ull};
+        __syncthreads();
+        if (seg == 0 && tid == 0) p.state[b] = s_st;
+    } else if (PASS == 5) {      // the walk takes the final state as kernel 4 recorded it
+        if (tid == 0) s_st = p.state[4 * B + b];
+        __syncthreads();
+    } else {
+        if (tid == 0) s_st = p.state[(PASS - 1) * B + b];
+        __syncthreads();
+        if (!s_st.all) {
+            unsigned long long x = 0;
+            if (tid < 256) {
+                unsigned long long h = 0;
+                for (int sg = 0; sg < nseg; ++sg) h += H[((PASS - 1) * nseg + sg) * 256 + (255 - tid)];
+                x = h;
+                for (int d = 1; d < 64; d <<= 1) {
+                    const unsigned long long y = shfl_up_u64(x, d);
+                    if (lane >= d) x += y;
+                }
+                if (lane == 63) s_wtot[wave] = x;
+            }
+            if (tid == 0) { s_dig = -1; s_suf[256] = 0; }
+            __syncthreads();
+            if (tid < 256) {
+                for (int w = 0; w < wave; ++w) x += s_wtot[w];
+                s_suf[255 - tid] = x;
+            }
+            __syncthreads();
+            // pass 0's histogram holds every token: the total mass
+            const unsigned long long tot = PASS == 1 ? s_suf[0] : s_st.total;
+            const double target = (double)p.top_p * (double)tot;
+            const unsigned long long above = s_st.above;
+            if (tid < 256 && (double)(above + s_suf[tid]) >= target) atomicMax(&s_dig, tid);
+            __syncthreads();
+            if (tid == 0) {
+                const int beta = s_dig;
+                s_st.total = tot;
+                if (beta < 0) {
+                    s_st.all = 1;
+                } else {
+                    s_st.above = above + s_suf[beta + 1];
+                    s_st.mass = above + s_suf[beta];
+                    s_st.prefix = (s_st.prefix << 8) | (uint32_t)beta;
+                }
+            }
+            __syncthreads();
+        }
+        if (seg == 0 && tid == 0) p.state[PASS * B + b] = s_st;
+    }
+    const SampState st = s_st;
+
+    auto load4 = [&](int t, float (&v)[4]) {
+        const int id = w0 + t * 256 + 4 * lane;
+        const float4 q = *(const float4 *)(lg + (id + 3 < V ? id : 0));
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    };
+    auto valid = [&](int t) { return w0 + t * 256 + 4 * lane < V; };
+    auto masked = [](bool ok, uint64_t m) { return m & (0ull - (uint64_t)ok); };
+    auto for_tiles = [&](auto &&f) {
+        int t = 0;
+        for (; t + 4 <= nt; t += 4) {
+            float v[4][4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) load4(t + u, v[u]);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) f(t + u, v[u]);
+        }
+        for (; t < nt; ++t) {
+            float v[4];
+            load4(t, v);
+            f(t, v);
+        }
+    };
+
+    if constexpr (PASS <= 3) {
+        if (st.all) return;
+        const int shift = 24 - 8 * PASS;
+        for (int i = tid; i < kSegWaves * 256; i += kSegThreads) (&hist[0][0])[i] = 0;
+        __syncthreads();
+        const uint32_t prefix = st.prefix;
+        for_tiles([&](int t, const float (&v)[4]) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
+                const uint32_t key = __float_as_uint(ev);
+                // pass 0 takes every value (no shift by 32 of a 32-bit key)
+                const bool match = PASS == 0 ? true : ((key >> ((32 - 8 * PASS) & 31)) == prefix);
+                if (valid(t) & match) atomicAdd(&hist[wave][(key >> shift) & 255u], fixed_mass(ev));
+            }
+        });
+        __syncthreads();
+        if (tid < 256) {
+            unsigned long long h = 0;
+#pragma unroll
+            for (int w = 0; w < kSegWaves; ++w) h += hist[w][tid];
+            H[(PASS * nseg + seg) * 256 + tid] = h;
+        }
+        return;
+    }
+    const uint32_t theta = st.all ? 0u : st.prefix;
+    unsigned long long *WM = p.wmass + (int64_t)b * nseg * kSegWaves;   // nucleus mass of each wave's ids
+    if constexpr (PASS == 4) {
+        unsigned long long wm = 0;
+        for_tiles([&](int t, const float (&v)[4]) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
+                wm += masked(valid(t) & (__float_as_uint(ev) >= theta), fixed_mass(ev));
+            }
+        });
+        for (int o = 32; o > 0; o >>= 1) {
+            const uint32_t lo = __shfl_xor((uint32_t)wm, o), hi = __shfl_xor((uint32_t)(wm >> 32), o);
+            wm += ((unsigned long long)hi << 32) | lo;
+        }
+        if (lane == 0) WM[seg * kSegWaves + wave] = wm;
+        return;
+    }
+    if constexpr (PASS == 5) {
+        const unsigned long long M = st.all ? st.total : st.mass;
+        const uint64_t r24 =
+            splitmix64(rng_key(p.seeds[b], 1ull << 33) + 2ull * (uint64_t)p.step[b] + (uint64_t)p.slot) >> 40;
+        const unsigned long long tsel = __umul64hi(r24 << 40, M);
+        // the waves before this one, in id order
+        const int gw = seg * kSegWaves + wave;
+        unsigned long long run = 0;
+        for (int w = 0; w < gw; ++w) run += WM[w];
+        const unsigned long long wm = WM[gw];
+        if (wm == 0 || tsel < run || tsel >= run + wm) return;
+        for (int t = 0; t < nt; ++t) {
+            float v[4];
+            load4(t, v);
+            unsigned long long m4[4], loc = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float ev = __builtin_amdgcn_exp2f((v[e] - mx) * kT);
+                m4[e] = masked(valid(t) & (__float_as_uint(ev) >= theta), fixed_mass(ev));
+                loc += m4[e];
+            }
+            unsigned long long inc = loc;
+            for (int d = 1; d < 64; d <<= 1) {
+                const unsigned long long o = shfl_up_u64(inc, d);
+                if (lane >= d) inc += o;
+            }
+            const unsigned long long excl = run + inc - loc;
+            if (loc > 0 && excl <= tsel && tsel < excl + loc) {
+                unsigned long long r = excl;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    r += m4[e];
+                    if (m4[e] > 0 && r > tsel) {
+                        p.best[b] = (1ull << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)(w0 + t * 256 + 4 * lane + e));
+                        break;
+                    }
+                }
+            }
+            run += __shfl(inc, 63);
+            if (run > tsel) break;
+        }
+    }
+}
+
+// Rows split over the segmented kernels: about 256 workgroups in all, 4 to 32 per row.
+int sample_segments(int B) {
+    int n = 256 / (B > 0 ? B : 1);
+    return n < 4 ? 4 : (n > 32 ? 32 : n);
+}
+
 void launch_sample(const SampleParams &p, hipStream_t s) {
-    if (p.top_k > 0 || p.rep_penalty != 1.f)
+    if (p.top_k > 0 || p.rep_penalty != 1.f) {
         hipLaunchKernelGGL(k_sample<true>, dim3(p.B), dim3(kSampThreads), 0, s, p);
-    else
+    } else if (p.hist && p.nseg > 0) {
+        SampleParams q = p;
+        // segments of whole 1024-id blocks (four waves of 256-id sub-tiles)
+        q.seg_len = ((p.V + p.nseg * 1024 - 1) / (p.nseg * 1024)) * 1024;
+        const dim3 grid(p.B * p.nseg), block(kSegThreads);
+        hipLaunchKernelGGL(k_sample_seg<0>, grid, block, 0, s, q);
+        hipLaunchKernelGGL(k_sample_seg<1>, grid, block, 0, s, q);
+        hipLaunchKernelGGL(k_sample_seg<2>, grid, block, 0, s, q);
+        hipLaunchKernelGGL(k_sample_seg<3>, grid, block, 0, s, q);
+        hipLaunchKernelGGL(k_sample_seg<4>, grid, block, 0, s, q);
+        hipLaunchKernelGGL(k_sample_seg<5>, grid, block, 0, s, q);
+    } else {
         hipLaunchKernelGGL(k_sample<false>, dim3(p.B), dim3(kSampThreads), 0, s, p);
+    }
 }
 
 }  // namespace pipo

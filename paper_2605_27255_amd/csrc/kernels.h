@@ -106,6 +106,12 @@ void launch_regular_out(uint64_t *best, int32_t *out_tok, int32_t *pairs, int32_
 void launch_seen_mark(const int32_t *tokens, int n, const int32_t *ntok, int B, int V, uint32_t *seen, int seen_words,
                       hipStream_t s);
 
+// State of the segmented top-p selection after each pass (one per row).
+struct SampState {
+    uint32_t prefix;             // the e-value bits chosen so far
+    int all;                     // no value reached top_p (rounding): every token is in the nucleus
+    unsigned long long above, mass, total;   // fixed-point masses above the prefix, of the nucleus, of the row
+};
 struct SampleParams {
     const float *logits; int V; int B;
     float temperature, top_p;
@@ -117,8 +123,15 @@ struct SampleParams {
     const int32_t *pairs; int32_t pad_id;   // the step's input pair, also penalised (NULL: none)
     const uint64_t *extra_key;              // argmax key of one more penalised token (NULL: none)
     float *pen;                             // workspace [B][V]: the penalised logits
+    // temperature + top-p split over nseg workgroups per row (NULL hist: one
+    // workgroup per row); best[b] must hold the row's argmax key on entry
+    int nseg, seg_len;                      // seg_len is set by launch_sample
+    unsigned long long *hist;               // [B][4][nseg][256] per-segment histograms
+    SampState *state;                       // [5][B] state after each pass
+    unsigned long long *wmass;              // [B][nseg][4] nucleus mass per wave
 };
 void launch_sample(const SampleParams &p, hipStream_t s);
+int sample_segments(int B);
 
 // ----------------------------------------------------------------------------
 // Initialisation: R-spec weights into packed layouts, RoPE table.

@@ -74,6 +74,8 @@ struct pipo_ctx {
     int32_t *pairs, *pos, *step;
     uint32_t *seen; int seen_words;   // penalised-token bitmap per sequence (evaluation sampler)
     float *pen;                       // penalised logits [Bmax][V] (evaluation sampler workspace)
+    unsigned long long *samp_hist, *samp_wmass;   // segmented top-p workspace: histograms, wave masses
+    SampState *samp_state;
     pipo_pair *out;
     // prefill activations
     uint16_t *p_xin, *p_xn, *p_xn_lo, *p_q, *p_q_lo, *p_o, *p_o_lo, *p_act, *p_act_lo;
@@ -345,6 +347,10 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->seen_words = (V + 31) / 32;
         c->seen = a.take<uint32_t>((int64_t)B * c->seen_words);
         c->pen = a.take<float>((int64_t)B * V);
+        // at most 256 workgroups over the rows: sample_segments(B) * B <= 256
+        c->samp_hist = a.take<unsigned long long>((int64_t)256 * 4 * 256);
+        c->samp_wmass = a.take<unsigned long long>((int64_t)256 * 4);
+        c->samp_state = a.take<SampState>((int64_t)5 * B);
         c->pos = a.take<int32_t>(B);
         c->step = a.take<int32_t>(B);
         c->out = a.take<pipo_pair>(B);
@@ -512,6 +518,7 @@ static SampleParams sample_params(pipo_ctx *c, const float *logits, int B, int s
     sp.logits = logits; sp.V = c->V; sp.B = B; sp.temperature = c->temperature; sp.top_p = c->top_p;
     sp.seeds = c->seeds; sp.step = c->step; sp.slot = slot; sp.best = best;
     sp.top_k = c->top_k; sp.rep_penalty = c->rep_penalty;
+    sp.nseg = sample_segments(B); sp.hist = c->samp_hist; sp.state = c->samp_state; sp.wmass = c->samp_wmass;
     if (c->eval_smp) {
         sp.seen = c->seen; sp.seen_words = c->seen_words;
         sp.pairs = in_pair ? c->pairs : nullptr; sp.pad_id = c->pad_id;
@@ -534,7 +541,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, bool in_pair
     // LM head #1 on RMSNorm(h_b; g_final)
     p.W = c->embed; p.N = c->V; p.K = H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
-    p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
+    p.out = c->logits_b; p.best = c->best_b;   // sampling reads the row max from the key
     { PROF_GEMV(PIPO_K_GEMV_LMHEAD); gemv(c, p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         PROF(PIPO_K_SAMPLE);
@@ -556,7 +563,7 @@ static void enqueue_heads(pipo_ctx *c, int B, int nss, int advance, bool in_pair
     q.B = B; q.eps = c->cfg.rms_eps; q.H = H; q.xh = c->xh; q.xl = c->xl; q.part = c->gpart; q.part_cap = c->gpart_cap;
     q.W = c->embed; q.N = c->V; q.K = H;
     q.x = c->hd; q.ss = c->ss_hd; q.nss = H / 16; q.gain = c->g_mtp_o;
-    q.out = c->logits_d; q.best = greedy ? c->best_d : nullptr;
+    q.out = c->logits_d; q.best = c->best_d;
     { PROF_GEMV(PIPO_K_GEMV_LMHEAD); gemv(c, q, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         // the draft's penalised set also holds its pair's backbone token
@@ -819,7 +826,7 @@ static void enqueue_regular_heads(pipo_ctx *c, int B, int nss, int advance, bool
     p.B = B; p.eps = c->cfg.rms_eps; p.H = c->H; p.xh = c->xh; p.xl = c->xl; p.part = c->gpart; p.part_cap = c->gpart_cap;
     p.W = c->embed; p.N = c->V; p.K = c->H;
     p.x = c->x; p.ss = c->ss_x; p.nss = nss; p.gain = c->g_final;
-    p.out = c->logits_b; p.best = greedy ? c->best_b : nullptr;
+    p.out = c->logits_b; p.best = c->best_b;   // sampling reads the row max from the key
     { PROF_GEMV(PIPO_K_GEMV_LMHEAD); gemv(c, p, PRO_NORM, EPI_LOGITS, s); }
     if (!greedy) {
         PROF(PIPO_K_SAMPLE);

@@ -7,7 +7,7 @@
 // accumulator holds one head; online softmax runs per column; the
 // probabilities, held as (4g + v, 16 + 4g + v) for lane group g, are already
 // the B operand of O^T[dim][head] += V^T P^T because the V cache stores each
-// 32-key tile in that key order (see vslot in gemv.hip).  The query and the
+// 32-key tile in that key order (vslot).  The query and the
 // probabilities enter the MFMAs as bf16 pairs hi + lo (two MFMAs each), so
 // only the bf16 KV cache itself limits the precision.  Per-split results
 // (m, l, o) go to a partial buffer; a second kernel merges them per head in
@@ -17,7 +17,14 @@
 
 namespace pipo {
 
-template <int D>
+// FUSED: the QKV GEMV left its k-range partial sums [R][B][nqkv] (rows in its
+// strip order: strip t of a q or k head holds dims 8t..8t+7, then their RoPE
+// partners d/2+8t..; v heads in order).  Every split adds the ranges of its
+// group's query rows in range order and applies RoPE in registers; the split
+// that holds the new position first adds that position's key and value rows,
+// rotates the key, writes both to the cache and waits for the stores, before
+// it requests any key block (its last block then reads them back).
+template <int D, bool FUSED>
 __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     constexpr int NC = D / 32;   // 32-wide d chunks (QK^T k-steps)
     constexpr int NT = D / 16;   // 16-wide d tiles (PV output tiles)
@@ -31,24 +38,15 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     const int len = p.pos[b] + 1;
     const int nb = (len + 31) >> 5;
     const int k0 = ((split * nb) / S) * 32;
-    const int k1 = min(len, (((split + 1) * nb) / S) * 32);
+    // FUSED: the last split takes the new key (position len - 1) from
+    // registers, after its blocks, so its blocks stop before it
+    const int k1 = min(len - ((FUSED && split == S - 1) ? 1 : 0), (((split + 1) * nb) / S) * 32);
     const float scale = 1.4426950408889634f / sqrtf((float)D);
 
-    // the query rows (clamped for unused columns, zeroed below) and the first
-    // block are requested together, before any of them is waited for
-    float4 qr[NC][2];
-    {
-        const int jq = j < qpg ? j : 0;
-        const float4 *qp = (const float4 *)(p.q + ((int64_t)b * p.n_q + kvh * qpg + jq) * D + 8 * g);
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            qr[c][0] = qp[8 * c];
-            qr[c][1] = qp[8 * c + 1];
-        }
-    }
     const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
     const uint16_t *vbase = p.vc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
-
+    constexpr int HS = D / 16;                    // strips per head in the QKV row order
+    const int jq = j < qpg ? j : 0;               // unused columns take head 0 (zeroed below)
     // K and V fragments of one 32-key block: two 16-key K tiles (one 1 KB
     // tile per 32 dims, stored in MFMA operand order, so each load is one
     // contiguous 1 KB read) and the 32-key V tile, 16 dims per output tile.
@@ -68,8 +66,148 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     // blocks k0 + 32 i, i < nblk; loads past the end re-read the first block
     const int nblk = k0 < k1 ? (k1 - k0 + 31) >> 5 : 0;
     auto blk = [&](int i) { return i < nblk ? k0 + 32 * i : 0; };
-    load_block(0, blk(0));
-    load_block(1, blk(1));
+
+    float4 qr[NC][2];
+    __shared__ float s_new[2][D];      // FUSED, last split: the new key and value (bf16 values)
+    float s_key = 0.f;                 // FUSED, last split: the new key's scaled score
+    if constexpr (FUSED) {
+        // LDS: the group's rotated query rows [qpg][D] (qpg * D <= 1024) and,
+        // for the last split, the new key and value (bf16 values)
+        __shared__ float s_q[1024];
+        const bool hold = split == S - 1;
+        const int R = p.ksplit, pos = len - 1;
+        const int64_t NB = (int64_t)p.B * p.nqkv;
+        const float *P = p.qkv_part + (int64_t)b * p.nqkv;
+        const int qs = p.n_q * HS, kvs = p.n_kv * HS;
+        // The group's query rows are contiguous (qpg heads of D rows each).
+        // A strip's rows 4 qq .. 4 qq + 3 (dims 8 t + 4 qq ..) pair with rows
+        // 8 + 4 qq .. (their RoPE partners): lane l takes quarter-pairs l and
+        // l + 64, so its RoPE needs only its own loads.
+        const int npair = qpg * D / 8;
+        const float *Pq = P + (int64_t)kvh * qpg * D;
+        int qrow[2];
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+            const int pi = min(lane + 64 * pp, npair - 1);
+            qrow[pp] = (pi >> 1) * 16 + 4 * (pi & 1);
+        }
+        // new key and value (last split, lane l < D/2: dims l and l + D/2)
+        const bool kvl = hold && lane < D / 2;
+        const int jd = lane & (D / 2 - 1);
+        const int krow = (qs + kvh * HS + (jd >> 3)) * 16 + (jd & 7);
+        const int vrow = (qs + kvs + kvh * HS) * 16 + jd;
+        // the partial sums, added in range order
+        static_assert(kAttnFusedRanges == 4, "one round trip of four ranges");
+        float4 qa[2][2], u[4][2][2];
+        float ka = 0.f, kb = 0.f, va = 0.f, vb = 0.f, w[4][4];
+        auto load_parts = [&](int r0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int64_t off = (int64_t)min(r0 + e, R - 1) * NB;
+#pragma unroll
+                for (int pp = 0; pp < 2; ++pp) {
+                    u[e][pp][0] = *(const float4 *)(Pq + off + qrow[pp]);
+                    u[e][pp][1] = *(const float4 *)(Pq + off + qrow[pp] + 8);
+                }
+                // (every lane: a branch here would wait for them one range at a time)
+                w[e][0] = P[off + krow];
+                w[e][1] = P[off + krow + 8];
+                w[e][2] = P[off + vrow];
+                w[e][3] = P[off + vrow + D / 2];
+            }
+        };
+        // ranges past R add zero (selects, not branches, so that no load is
+        // moved into a branch)
+        auto add_parts = [&](int r0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bool on = r0 + e < R;
+#pragma unroll
+                for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        qa[pp][h].x += on ? u[e][pp][h].x : 0.f; qa[pp][h].y += on ? u[e][pp][h].y : 0.f;
+                        qa[pp][h].z += on ? u[e][pp][h].z : 0.f; qa[pp][h].w += on ? u[e][pp][h].w : 0.f;
+                    }
+                ka += on ? w[e][0] : 0.f;
+                kb += on ? w[e][1] : 0.f;
+                va += on ? w[e][2] : 0.f;
+                vb += on ? w[e][3] : 0.f;
+            }
+        };
+        // the ranges (at most kAttnFusedRanges) and the RoPE values go out
+        // before the first blocks' loads, so that waiting for them leaves the
+        // blocks in flight
+        load_parts(0);
+        float4 cq[2], sq[2];
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+            const int pi = min(lane + 64 * pp, npair - 1);
+            const int jr = ((pi >> 1) % HS) * 8 + 4 * (pi & 1);
+            cq[pp] = *(const float4 *)(p.rope_cos + (int64_t)pos * (D / 2) + jr);
+            sq[pp] = *(const float4 *)(p.rope_sin + (int64_t)pos * (D / 2) + jr);
+        }
+        const float ck = p.rope_cos[(int64_t)pos * (D / 2) + jd], sk = p.rope_sin[(int64_t)pos * (D / 2) + jd];
+        __builtin_amdgcn_sched_barrier(0);
+        load_block(0, blk(0));
+        load_block(1, blk(1));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) qa[pp][0] = qa[pp][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+        add_parts(0);
+        // RoPE (dim i < D/2 pairs with i + D/2 at frequency index i) into the
+        // natural [head][dim] order
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+            const int pi = lane + 64 * pp;
+            if (pi < npair) {
+                const int hl = (pi >> 1) / HS, jr = ((pi >> 1) % HS) * 8 + 4 * (pi & 1);
+                const float4 a = qa[pp][0], o = qa[pp][1], cs = cq[pp], sn = sq[pp];
+                *(float4 *)&s_q[hl * D + jr] = make_float4(a.x * cs.x - o.x * sn.x, a.y * cs.y - o.y * sn.y,
+                                                          a.z * cs.z - o.z * sn.z, a.w * cs.w - o.w * sn.w);
+                *(float4 *)&s_q[hl * D + D / 2 + jr] = make_float4(o.x * cs.x + a.x * sn.x, o.y * cs.y + a.y * sn.y,
+                                                                  o.z * cs.z + a.z * sn.z, o.w * cs.w + a.w * sn.w);
+            }
+        }
+        if (kvl) {
+            // the new key, rotated and rounded to bf16 as the cache holds it
+            s_new[0][jd] = __uint_as_float(f2bf(ka * ck - kb * sk) << 16);
+            s_new[0][jd + D / 2] = __uint_as_float(f2bf(kb * ck + ka * sk) << 16);
+            s_new[1][jd] = __uint_as_float(f2bf(va) << 16);
+            s_new[1][jd + D / 2] = __uint_as_float(f2bf(vb) << 16);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            qr[c][0] = *(const float4 *)&s_q[jq * D + 32 * c + 8 * g];
+            qr[c][1] = *(const float4 *)&s_q[jq * D + 32 * c + 8 * g + 4];
+        }
+        if (hold) {
+            // the new key's score per head, from the fp32 query
+            float dot = 0.f;
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const float *kn = &s_new[0][32 * c + 8 * g + 4 * h];
+                    dot += qr[c][h].x * kn[0] + qr[c][h].y * kn[1] + qr[c][h].z * kn[2] + qr[c][h].w * kn[3];
+                }
+            dot += __shfl_xor(dot, 16);
+            dot += __shfl_xor(dot, 32);
+            s_key = dot * scale;
+        }
+    } else {
+        // the query rows and the first two blocks are requested together,
+        // before any of them is waited for
+        const float4 *qp = (const float4 *)(p.q + ((int64_t)b * p.n_q + kvh * qpg + jq) * D + 8 * g);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            qr[c][0] = qp[8 * c];
+            qr[c][1] = qp[8 * c + 1];
+        }
+        load_block(0, blk(0));
+        load_block(1, blk(1));
+    }
     __builtin_amdgcn_sched_barrier(0);
     u32x4 qh[NC], ql[NC];
 #pragma unroll
@@ -143,6 +281,32 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     if (i < nblk) block(0, k0 + 32 * i);
     if (i + 1 < nblk) block(1, k0 + 32 * (i + 1));
 
+    if (FUSED && split == S - 1) {
+        // the new key (its score taken before the blocks): one online-softmax
+        // step and its value row
+        const float sv = s_key;
+        const float m_new = fmaxf(m_run, sv);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        const float pe = __builtin_amdgcn_exp2f(sv - m_new);
+        l_run = l_run * alpha + pe;
+        m_run = m_new;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o[t][v] = o[t][v] * alpha + pe * s_new[1][16 * t + 4 * g + v];
+        // the new key and value into the cache for later steps (stored only
+        // now: a store pending among the block loads would make the compiler
+        // wait for every load in flight)
+        if (lane < D / 2) {
+            const int pos = len - 1;
+            uint16_t *kw = (uint16_t *)kbase, *vw = (uint16_t *)vbase;
+            kw[tiled_index(pos, lane, D)] = (uint16_t)(__float_as_uint(s_new[0][lane]) >> 16);
+            kw[tiled_index(pos, lane + D / 2, D)] = (uint16_t)(__float_as_uint(s_new[0][lane + D / 2]) >> 16);
+            vw[((int64_t)(pos >> 5) * D + lane) * 32 + vslot(pos & 31)] = (uint16_t)(__float_as_uint(s_new[1][lane]) >> 16);
+            vw[((int64_t)(pos >> 5) * D + lane + D / 2) * 32 + vslot(pos & 31)] =
+                (uint16_t)(__float_as_uint(s_new[1][lane + D / 2]) >> 16);
+        }
+    }
     // partial (o, m, l) of this split for each head of the group
     if (j < qpg) {
         float *pr = p.part + (((int64_t)b * p.n_q + kvh * qpg + j) * S + split) * (D + 2);
@@ -190,11 +354,14 @@ __global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
 
 void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s) {
     const int grid = p.B * p.n_kv * p.splits;
+    const bool fused = p.qkv_part != nullptr;
     if (p.d == 128) {
-        hipLaunchKernelGGL(k_attn_decode<128>, dim3(grid), dim3(64), 0, s, p);
+        if (fused) hipLaunchKernelGGL((k_attn_decode<128, true>), dim3(grid), dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((k_attn_decode<128, false>), dim3(grid), dim3(64), 0, s, p);
         hipLaunchKernelGGL(k_attn_merge<128>, dim3(p.B * p.n_q), dim3(128), 0, s, p);
     } else {
-        hipLaunchKernelGGL(k_attn_decode<64>, dim3(grid), dim3(64), 0, s, p);
+        if (fused) hipLaunchKernelGGL((k_attn_decode<64, true>), dim3(grid), dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((k_attn_decode<64, false>), dim3(grid), dim3(64), 0, s, p);
         hipLaunchKernelGGL(k_attn_merge<64>, dim3(p.B * p.n_q), dim3(64), 0, s, p);
     }
 }

@@ -90,6 +90,14 @@ __host__ __device__ __forceinline__ int64_t tiled_index(int64_t r, int64_t k, in
     return (((r >> 4) * (K >> 5) + (k >> 5)) << 9) + ((((k & 31) >> 3) * 16 + (r & 15)) << 3) + (k & 7);
 }
 
+// ---- V cache tile order ------------------------------------------------------
+// Slot of key kappa (0..31) inside a 32-key V tile [d][32]: the order in which
+// the attention kernels hold probabilities as MFMA B operands (accumulator
+// lane group g, element v of 16-key tile tau holds key 16 tau + 4 g + v).
+__host__ __device__ __forceinline__ int vslot(int kappa) {
+    return 8 * ((kappa & 15) >> 2) + 4 * (kappa >> 4) + (kappa & 3);
+}
+
 // ---- SplitMix64 (Steele, Lea and Flood, OOPSLA 2014), as a stateless hash --
 __host__ __device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
     uint64_t z = x + 0x9E3779B97F4A7C15ull;

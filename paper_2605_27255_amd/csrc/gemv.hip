@@ -42,11 +42,6 @@ constexpr int kXR = 3;                       // prologue chunks per thread loade
 
 __device__ __forceinline__ float silu_f(float u) { return u / (1.0f + __expf(-u)); }
 
-// slot of key kappa (0..31) inside a 32-key V tile; matches the order in which
-// the attention kernels hold probabilities as MFMA B operands.
-__device__ __forceinline__ int vslot(int kappa) {
-    return 8 * ((kappa & 15) >> 2) + 4 * (kappa >> 4) + (kappa & 3);
-}
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
     uint32_t lo = __shfl_xor((uint32_t)v, m), hi = __shfl_xor((uint32_t)(v >> 32), m);
@@ -1078,7 +1073,8 @@ static void launch_multi(GemvParams &q, hipStream_t s) {
             const int grid_kr = ((q.wg_cap > 0 ? q.wg_cap : 256) / R) * R;   // whole rounds of ranges
             hipLaunchKernelGGL((k_gemv_kr<NBT, PRO, EPI, 8>), dim3(grid_kr > R ? grid_kr : R), dim3(kNW * 64),
                                lds_kr, s, q);
-            if (R > 1) hipLaunchKernelGGL((k_gemv_fin<NBT, EPI>), dim3(q.N >> 4), dim3(64), 0, s, q);
+            if (EPI == EPI_QKV && R > 1 && R <= kAttnFusedRanges && q.deferred) *q.deferred = R;   // the attention finishes it
+            else if (R > 1) hipLaunchKernelGGL((k_gemv_fin<NBT, EPI>), dim3(q.N >> 4), dim3(64), 0, s, q);
             return;
         }
     }

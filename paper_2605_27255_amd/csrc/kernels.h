@@ -50,6 +50,10 @@ struct GemvParams {
     uint16_t *xh, *xl;            // X planes workspace, [B][K] bf16 each (large batches)
     float *part; int64_t part_cap;  // k-range partial sums workspace (floats)
     int ksplit;                   // k-ranges (set by launch_gemv)
+    int *deferred;                // EPI_QKV: if not NULL and K is cut into 2..kAttnFusedRanges ranges,
+                                  // the range sum, RoPE and KV append are left to the decode attention
+                                  // and *deferred is set to the number of ranges (it stays 0 when the
+                                  // epilogue ran)
     int krt;                      // k-tiles per range of the k-range kernel (set by launch_gemv)
     int xseg;                     // 2048-column segments per row of the X planes (set by launch_gemv)
 };
@@ -67,8 +71,17 @@ int gemv_num_groups(int N);
 // ----------------------------------------------------------------------------
 // Split-K grouped-query flash-decode over the latent KV cache.
 // ----------------------------------------------------------------------------
+// k-ranges of the QKV GEMV whose sum the decode attention takes over (one
+// round trip of partial loads in its prologue)
+constexpr int kAttnFusedRanges = 4;
+
 struct AttnDecodeParams {
     const float *q;             // fp32 [B][n_q][d]
+    // with qkv_part: the QKV GEMV left its k-range partial sums [ksplit][B][nqkv]
+    // (rows in its strip order); the attention adds them, applies RoPE to q and
+    // k and appends k, v at pos (instead of reading q)
+    const float *qkv_part; int ksplit, nqkv;
+    const float *rope_cos, *rope_sin;
     const uint16_t *kc, *vc;    // this layer's caches
     int64_t kv_bstride;
     const int32_t *pos;         // [B]: attend to keys 0..pos[b]

@@ -9,9 +9,6 @@
 namespace pipo {
 
 __device__ __forceinline__ float silu_p(float u) { return u / (1.0f + __expf(-u)); }
-__device__ __forceinline__ int vslot_p(int kappa) {
-    return 8 * ((kappa & 15) >> 2) + 4 * (kappa >> 4) + (kappa & 3);
-}
 
 // ---- pair gather: X_in[m] = [E[a]; E[b]] for latent c0 + i of sequence b ----
 __global__ void k_gather_pairs(const int32_t *tokens, const uint16_t *embed, int H, int V, int pad_id,
@@ -287,7 +284,7 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
             const int r0 = (strip - qs - ks) * 16 + 4 * g;
             const int kvh = r0 / d, dim = r0 - kvh * d;
             uint16_t *dst = p.vc + (int64_t)b * p.kv_bstride +
-                            ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot_p(pos & 31);
+                            ((int64_t)(kvh * (p.lmax_pad >> 5) + (pos >> 5)) * d + dim) * 32 + vslot(pos & 31);
 #pragma unroll
             for (int v = 0; v < 4; ++v) dst[v * 32] = (uint16_t)f2bf(val[v]);
         }

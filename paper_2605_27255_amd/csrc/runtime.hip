@@ -480,10 +480,16 @@ static void enqueue_layer(pipo_ctx *c, const LayerW &lw, uint16_t *kc, uint16_t 
     p.x = xres; p.ss = ssres; p.nss = H / 16; p.gain = lw.g_attn;
     p.q = c->qbuf; p.kc = kc; p.vc = vc; p.pos = c->pos; p.rope_cos = c->rope_cos; p.rope_sin = c->rope_sin;
     p.n_q = c->nq; p.n_kv = c->nkv; p.d = c->d; p.lmax_pad = c->lmax_pad; p.kv_bstride = c->kv_bstride;
+    int ranges = 0;      // k-ranges whose sum (and RoPE, KV append) the attention takes over
+    p.deferred = (c->nq / c->nkv) * c->d <= 1024 ? &ranges : nullptr;   // the attention stages q in 4 KB of LDS
     { PROF_GEMV(PIPO_K_GEMV_LAYER); gemv(c, p, PRO_NORM, EPI_QKV, s); }
 
     AttnDecodeParams ap{};
     ap.q = c->qbuf; ap.kc = kc; ap.vc = vc; ap.kv_bstride = c->kv_bstride; ap.pos = c->pos;
+    if (ranges > 1) {
+        ap.qkv_part = p.part; ap.ksplit = ranges; ap.nqkv = c->nqkv;
+        ap.rope_cos = c->rope_cos; ap.rope_sin = c->rope_sin;
+    }
     ap.B = B; ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad;
     ap.splits = attn_splits(c, B); ap.part = c->apart; ap.out = c->attn_out;
     { PROF(PIPO_K_ATTN_DECODE); launch_attn_decode(ap, s); }

@@ -63,6 +63,22 @@ __device__ __forceinline__ float wave_sum(float v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     return v;
 }
+// The same sum without LDS traffic: DPP within each 16-lane row (pairs,
+// quads, half-row and row mirrors), then the four row sums read into scalar
+// registers and added in row order; every lane gets the result.
+#define PIPO_DPP(v, ctrl) \
+    __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, (v)), (ctrl), 0xF, 0xF, false))
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+    v += PIPO_DPP(v, 0xB1);    // quad_perm [1,0,3,2]
+    v += PIPO_DPP(v, 0x4E);    // quad_perm [2,3,0,1]
+    v += PIPO_DPP(v, 0x141);   // row_half_mirror
+    v += PIPO_DPP(v, 0x140);   // row_mirror
+    const int u = __builtin_bit_cast(int, v);
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(u, 0)) +
+           __builtin_bit_cast(float, __builtin_amdgcn_readlane(u, 16)) +
+           __builtin_bit_cast(float, __builtin_amdgcn_readlane(u, 32)) +
+           __builtin_bit_cast(float, __builtin_amdgcn_readlane(u, 48));
+}
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));

@@ -213,7 +213,7 @@ __device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, P
 #pragma unroll
                 for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? pr.ssv2[r][t] : 0.f;
             }
-            a = wave_sum(a);
+            a = wave_sum_dpp(a);
             if (b < B && lane == 0) sc0[b] = rsqrtf(a / (float)(PRO == PRO_MTP ? p.H : p.K) + p.eps);
         }
     }
@@ -230,7 +230,7 @@ __device__ __forceinline__ void pro_finish(const GemvParams &p, const Pro<NBT, P
                     e2 += lo * lo + hi * hi;
                 }
             }
-            e2 = wave_sum(e2);
+            e2 = wave_sum_dpp(e2);
             if (lane == 0) sc1[b] = rsqrtf(e2 / (float)p.H + p.eps);
         }
     }
@@ -824,20 +824,12 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
         const int strip = wid + sidx * nwr;
         return (const u32x4 *)(q < nq && i < nt ? p.W + ((int64_t)strip * KT + kt0 + i) * 512 + lane * 8 : p.W);
     };
-    // 1. the whole X slice (at most KC 8-column chunks per thread) and
-    //    the RMSNorm inputs requested at once, then two weight batches
+    // 1. the RMSNorm inputs, then the whole X slice (at most KC 8-column
+    //    chunks per thread), requested at once
     constexpr bool NORM = PRO == PRO_NORM || PRO == PRO_MTP || PRO == PRO_CAT;
     const int per_row = nt * 4, count = B * per_row;
     const int col0 = kt0 * 32;
     constexpr int KC = KrChunks<PRO>::n;
-    XSrc src[KC];
-#pragma unroll
-    for (int c = 0; c < KC; ++c) {
-        int idx = threadIdx.x + c * (kNW * 64);
-        idx = idx < count ? idx : 0;
-        const int b = idx / per_row;
-        load_src<PRO>(p, b, col0 + ((idx - b * per_row) << 3), src[c]);
-    }
     constexpr int RPW = 2 * NBT;
     float ssv[RPW][4], ssv2[PRO == PRO_CAT ? RPW : 1][4];
     if (NORM) {
@@ -850,12 +842,14 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
                 if (PRO == PRO_CAT) ssv2[rr][t] = p.ss2[(b < B && i < p.nss) ? b * p.nss + i : 0];
             }
     }
-    u32x4 ra[U], rb[U];
+    XSrc src[KC];
 #pragma unroll
-    for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(wptr(0, u));
-#pragma unroll
-    for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(wptr(1, u));
-    __builtin_amdgcn_sched_barrier(0);
+    for (int c = 0; c < KC; ++c) {
+        int idx = threadIdx.x + c * (kNW * 64);
+        idx = idx < count ? idx : 0;
+        const int b = idx / per_row;
+        load_src<PRO>(p, b, col0 + ((idx - b * per_row) << 3), src[c]);
+    }
     // 2. the slice into LDS (shared by the eight waves), the RMSNorm scalars
 #pragma unroll
     for (int c = 0; c < KC; ++c) {
@@ -868,6 +862,15 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
             if (PRO != PRO_PAIR) *(u32x4 *)(xl + b * rstride + k) = vl;
         }
     }
+    // the weight batches go out once this workgroup's X has arrived (issued
+    // earlier they would queue ahead of it), before the scalars and the barrier
+    __builtin_amdgcn_sched_barrier(0);
+    u32x4 ra[U], rb[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ra[u] = __builtin_nontemporal_load(wptr(0, u));
+#pragma unroll
+    for (int u = 0; u < U; ++u) rb[u] = __builtin_nontemporal_load(wptr(1, u));
+    __builtin_amdgcn_sched_barrier(0);
     if (NORM) {
 #pragma unroll
         for (int rr = 0; rr < RPW; ++rr) {
@@ -879,7 +882,7 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
 #pragma unroll
                 for (int t = 0; t < 4; ++t) a += (lane + 64 * t < p.nss) ? ssv2[rr][t] : 0.f;
             }
-            a = wave_sum(a);
+            a = wave_sum_dpp(a);
             if (b < B && lane == 0) sc0[b] = rsqrtf(a / (float)(PRO == PRO_MTP ? p.H : p.K) + p.eps);
         }
     }
@@ -892,7 +895,7 @@ __global__ __launch_bounds__(512) void k_gemv_kr(GemvParams p) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) e2 += bf_lo(w[i]) * bf_lo(w[i]) + bf_hi(w[i]) * bf_hi(w[i]);
             }
-            e2 = wave_sum(e2);
+            e2 = wave_sum_dpp(e2);
             if (lane == 0) sc1[b] = rsqrtf(e2 / (float)p.H + p.eps);
         }
     }

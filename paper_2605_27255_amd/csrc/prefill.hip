@@ -474,6 +474,24 @@ void launch_gemm(const GemmParams &p, hipStream_t s) {
 // the hardware exp2 (results below the normal range flush to zero, which the
 // softmax weights can afford).  Two workgroups fit per CU so that one's
 // softmax overlaps the other's MFMAs.
+// fp16 operands of the PV product: the probabilities are rounded to fp16
+// (11 significant bits, against 8 for bf16) and V, stored as bf16, is
+// widened to fp16 in LDS, exactly for every value in fp16's normal range
+// (|v| in [2^-14, 65504]; smaller values keep 2^-24 absolute precision;
+// larger ones would overflow, a limit of this prefill kernel only).  Half the
+// PV MFMAs of a bf16 pair hi + lo, at a quarter of a single bf16 plane's
+// rounding error.
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+    const f16x2_t v = {(_Float16)lo, (_Float16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ f32x4 mfma16_f16(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0,
+                                                  0);
+}
+
 constexpr int kAQ = 32;         // queries per workgroup
 constexpr int kAK = 64;         // keys per LDS stage
 
@@ -549,6 +567,19 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_t *)(buf + kAK * D + vb * 512), 16, 0, 0);
         }
     };
+    // V of a stage, bf16 -> fp16 in place: each lane converts the 16 bytes
+    // its own loads wrote (so only its own loads must have completed)
+    auto stage_v_f16 = [&](uint16_t *buf) {
+#pragma unroll
+        for (int u = 0; u < KBW; ++u) {
+            u32x4 *at = (u32x4 *)(buf + kAK * D + (wave * KBW + u) * 512 + lane * 8);
+            const u32x4 w = *at;
+            u32x4 h;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) h[i] = pack_f16x2(bf_lo(w[i]), bf_hi(w[i]));
+            *at = h;
+        }
+    };
     // One 64-key stage: the scores of both 16-query tiles, the softmax of
     // tile 0, then the PV MFMAs of tile 0 with the softmax of tile 1 (VALU
     // that does not depend on them) issued between them, then tile 1's PV.
@@ -600,8 +631,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             m_run[ct] = m_cand;
         }
     };
-    // probabilities, their sum and the bf16 pair P^T = hi + lo
-    auto soft_exp = [&](int ct, f32x4 (&sct)[4], u32x4 (&ph)[2], u32x4 (&pl)[2]) {
+    // probabilities, their sum and P^T in fp16
+    auto soft_exp = [&](int ct, f32x4 (&sct)[4], u32x4 (&ph)[2]) {
         const float m_use = m_run[ct];
         float ps = 0.f;
 #pragma unroll
@@ -614,46 +645,49 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             }
         l_run[ct] += col_sum(ps);
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const float f[8] = {sct[2 * half][0], sct[2 * half][1], sct[2 * half][2], sct[2 * half][3],
-                                sct[2 * half + 1][0], sct[2 * half + 1][1], sct[2 * half + 1][2],
-                                sct[2 * half + 1][3]};
-            split8(f, ph[half], pl[half]);
-        }
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                ph[half][i] = pack_f16x2(sct[2 * half + (i >> 1)][2 * (i & 1)], sct[2 * half + (i >> 1)][2 * (i & 1) + 1]);
     };
-    auto pv = [&](const uint16_t *vs, int ct, const u32x4 (&ph)[2], const u32x4 (&pl)[2]) {
+    auto pv = [&](const uint16_t *vs, int ct, const u32x4 (&ph)[2]) {
 #pragma unroll
         for (int half = 0; half < 2; ++half)
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const u32x4 vf = *(const u32x4 *)(&vs[(half * NT + t) * 512 + lane * 8]);
-                o[ct][t] = mfma16(vf, ph[half], o[ct][t]);
-                o[ct][t] = mfma16(vf, pl[half], o[ct][t]);
+                o[ct][t] = mfma16_f16(vf, ph[half], o[ct][t]);
             }
     };
-    auto attend = [&](const uint16_t *ks, const uint16_t *vs, int kb0, bool diag) {
+    auto attend = [&](const uint16_t *ks, const uint16_t *vs, int kb0, bool diag, uint16_t *nxt) {
         f32x4 s0[4], s1[4];
-        u32x4 p0h[2], p0l[2], p1h[2], p1l[2];
+        u32x4 p0h[2], p1h[2];
         scores(ks, s0, s1);
         soft_max(0, s0, kb0, diag);
-        soft_exp(0, s0, p0h, p0l);
+        soft_exp(0, s0, p0h);
+        // the next stage's V (requested at this stage's start) to fp16 here,
+        // between MFMA phases, rather than on the path to the barrier
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        stage_v_f16(nxt);
         soft_max(1, s1, kb0, diag);
-        pv(vs, 0, p0h, p0l);
-        soft_exp(1, s1, p1h, p1l);
-        pv(vs, 1, p1h, p1l);
+        pv(vs, 0, p0h);
+        soft_exp(1, s1, p1h);
+        pv(vs, 1, p1h);
     };
 
     // stage s + 1 is requested (into the other buffer) before stage s is
     // computed; one stage past the end stays inside the padded cache
     stage_issue(kv_a, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    stage_v_f16(kv_a);
     __syncthreads();
     for (int st = 0; st < nstage; ++st) {
         uint16_t *cur = (st & 1) ? kv_b : kv_a, *nxt = (st & 1) ? kv_a : kv_b;
         stage_issue(nxt, (st + 1) * kAK);
         // the causal mask only where some key of the stage lies past some query
-        if (active) attend(cur, cur + kAK * D, st * kAK, st * kAK + kAK - 1 > qpos0);
+        if (active) attend(cur, cur + kAK * D, st * kAK, st * kAK + kAK - 1 > qpos0, nxt);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if (!active) stage_v_f16(nxt);   // (active waves converted theirs in attend)
         __syncthreads();
     }
     if (!active) return;

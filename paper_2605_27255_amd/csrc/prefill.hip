@@ -461,26 +461,27 @@ void launch_gemm(const GemmParams &p, hipStream_t s) {
 
 // ---- causal grouped-query flash attention for a chunk of queries ----------
 // One workgroup per (sequence, KV group, group of up to four query heads,
-// 32-query block); wave w computes one head for all 32 queries (two 16-column
-// MFMA tiles).  Keys and values of 64 positions at a time are staged in LDS,
-// shared by the workgroup's heads and double-buffered: the next stage is
-// requested into registers before the current one is multiplied.  Per stage
+// 64-query block); eight waves, wave w computes head w % 4 for the block's
+// 32-query half w / 4 (two 16-column MFMA tiles).  Keys and values of 64
+// positions at a time are staged in LDS, shared by the workgroup's heads and
+// halves and double-buffered: the next stage is requested straight into LDS
+// before the current one is multiplied, and each lane widens the 16 bytes it
+// requested from bf16 to fp16 once they have landed (mid-stage).  Per stage
 // the scores of all 64 keys are formed first (both query tiles), then one
 // online-softmax update per query tile (the causal mask only on stages that
-// reach the diagonal), so the row max / sum shuffles happen once per 64 keys,
-// and the accumulators are rescaled only when the running max grows by more
-// than 2^8.  Scores stay unscaled; the softmax scale 1/sqrt(d) (times log2 e)
-// enters through one fma per score in the exponent, and the exponentials are
-// the hardware exp2 (results below the normal range flush to zero, which the
-// softmax weights can afford).  Two workgroups fit per CU so that one's
-// softmax overlaps the other's MFMAs.
-// fp16 operands of the PV product: the probabilities are rounded to fp16
-// (11 significant bits, against 8 for bf16) and V, stored as bf16, is
-// widened to fp16 in LDS, exactly for every value in fp16's normal range
-// (|v| in [2^-14, 65504]; smaller values keep 2^-24 absolute precision;
-// larger ones would overflow, a limit of this prefill kernel only).  Half the
-// PV MFMAs of a bf16 pair hi + lo, at a quarter of a single bf16 plane's
-// rounding error.
+// reach the diagonal; stages wholly past a half's queries are skipped), so
+// the row max / sum shuffles happen once per 64 keys, and the accumulators
+// are rescaled only when the running max grows by more than 2^8.  Scores
+// stay unscaled; the softmax scale 1/sqrt(d) (times log2 e) enters through
+// one fma per score in the exponent, and the exponentials are the hardware
+// exp2 (results below the normal range flush to zero, which the softmax
+// weights can afford).
+// Both products take fp16 operands: the query (its hi + lo pair summed and
+// rounded once) and the probabilities carry 11 significant bits (against 8
+// for bf16), and K and V, stored as bf16, are widened to fp16 exactly for
+// every value in fp16's normal range (|x| in [2^-14, 65504]; smaller values
+// keep 2^-24 absolute precision; larger ones would overflow, a limit of this
+// prefill kernel only).  One MFMA per product instead of a bf16 pair's two.
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
 typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
 __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
@@ -492,11 +493,11 @@ __device__ __forceinline__ f32x4 mfma16_f16(u32x4 a, u32x4 b, f32x4 c) {
                                                   0);
 }
 
-constexpr int kAQ = 32;         // queries per workgroup
+constexpr int kAQ = 64;         // queries per workgroup (two 32-query halves)
 constexpr int kAK = 64;         // keys per LDS stage
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
+__global__ __launch_bounds__(512, 1) void k_attn_prefill(AttnPrefillParams p) {
     constexpr int NC = D / 32, NT = D / 16;
     // two stage buffers, each the stage's K tiles (as in the cache) then its
     // V fragments in MFMA operand order; two named arrays, so that reading
@@ -513,24 +514,29 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     const int rest = blockIdx.x / nqb;
     const int hg = rest % nhg, bk = rest / nhg;
     const int b = bk / p.n_kv, kvh = bk - b * p.n_kv;
-    const int hig = hg * 4 + wave;               // head index inside the KV group
+    const int hig = hg * 4 + (wave & 3);         // head index inside the KV group
     const bool active = hig < qpg;
     const int head = kvh * qpg + (active ? hig : 0);
-    const int q0 = qblk * kAQ;                 // chunk-local first query
-    const int qpos0 = p.g.c0 + q0;             // absolute position of the first query
+    const int q0 = qblk * kAQ;                 // chunk-local first query of the workgroup
+    const int qpos0 = p.g.c0 + q0;             // ... its absolute position
+    const int q0w = q0 + 32 * (wave >> 2);     // this wave's first query (its half)
+    const int qpos0w = p.g.c0 + q0w;
     const float scale = 1.4426950408889634f / sqrtf((float)D);
     // a ragged batch: a block wholly past this sequence's last position holds
     // only PAD rows, whose outputs nothing reads
     if (p.g.ntok && qpos0 >= (p.g.ntok[b] + p.g.tok_per_pos - 1) / p.g.tok_per_pos) return;
 
-    u32x4 qb[2][NC], ql[2][NC];   // the query rows as a bf16 pair hi + lo
+    u32x4 qb[2][NC];   // the query rows in fp16
 #pragma unroll
     for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const int64_t at = (((int64_t)b * p.n_q + head) * p.g.mpad + q0 + 16 * ct + j) * D + 32 * c + 8 * g;
-            qb[ct][c] = *(const u32x4 *)(p.q + at);
-            ql[ct][c] = *(const u32x4 *)(p.q_lo + at);
+            const int row = min(q0w + 16 * ct + j, p.g.mpad - 1);   // rows past the chunk are never written
+            const int64_t at = (((int64_t)b * p.n_q + head) * p.g.mpad + row) * D + 32 * c + 8 * g;
+            const u32x4 h = *(const u32x4 *)(p.q + at), l = *(const u32x4 *)(p.q_lo + at);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                qb[ct][c][i] = pack_f16x2(bf_lo(h[i]) + bf_lo(l[i]), bf_hi(h[i]) + bf_hi(l[i]));
         }
 
     const uint16_t *kbase = p.kc + (int64_t)b * p.kv_bstride + (int64_t)kvh * p.lmax_pad * D;
@@ -550,7 +556,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     // as they are; each 1 KB V block (16 dims x 32 keys of a V tile) is read
     // with its lanes permuted so that lane l = 16 g + j lands holding dim j,
     // keys 8 g .. 8 g + 7, the PV MFMA's A operand, read back linearly.
-    constexpr int KBW = D / 32;            // K (and V) blocks per wave per stage
+    constexpr int KBW = D / 64;            // K (and V) blocks per wave per stage
     const int nstage = (kend + kAK - 1) / kAK;
     using lds_t = __attribute__((address_space(3))) void;
     auto stage_issue = [&](uint16_t *buf, int kb0) {
@@ -567,12 +573,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_t *)(buf + kAK * D + vb * 512), 16, 0, 0);
         }
     };
-    // V of a stage, bf16 -> fp16 in place: each lane converts the 16 bytes
-    // its own loads wrote (so only its own loads must have completed)
-    auto stage_v_f16 = [&](uint16_t *buf) {
+    // K and V of a stage, bf16 -> fp16 in place: each lane converts the
+    // 16-byte pieces its own loads wrote (so only those must have completed)
+    auto stage_f16 = [&](uint16_t *buf) {
 #pragma unroll
-        for (int u = 0; u < KBW; ++u) {
-            u32x4 *at = (u32x4 *)(buf + kAK * D + (wave * KBW + u) * 512 + lane * 8);
+        for (int u = 0; u < 2 * KBW; ++u) {
+            u32x4 *at = (u32x4 *)(buf + (u < KBW ? 0 : kAK * D) + (wave * KBW + (u % KBW)) * 512 + lane * 8);
             const u32x4 w = *at;
             u32x4 h;
 #pragma unroll
@@ -599,17 +605,15 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
             s1[tau] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                s0[tau] = mfma16(kf[c], qb[0][c], s0[tau]);
-                s1[tau] = mfma16(kf[c], qb[1][c], s1[tau]);
-                s0[tau] = mfma16(kf[c], ql[0][c], s0[tau]);
-                s1[tau] = mfma16(kf[c], ql[1][c], s1[tau]);
+                s0[tau] = mfma16_f16(kf[c], qb[0][c], s0[tau]);
+                s1[tau] = mfma16_f16(kf[c], qb[1][c], s1[tau]);
             }
         }
     };
     // masked scores (diagonal stages only), the column max and the rescale
     auto soft_max = [&](int ct, f32x4 (&sct)[4], int kb0, bool diag) {
         // keys past this column's query are masked
-        const int lim = diag ? qpos0 + 16 * ct + j - kb0 - 4 * g : 64;
+        const int lim = diag ? qpos0w + 16 * ct + j - kb0 - 4 * g : 64;
         float mx = -INFINITY;
 #pragma unroll
         for (int tau = 0; tau < 4; ++tau)
@@ -665,10 +669,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
         scores(ks, s0, s1);
         soft_max(0, s0, kb0, diag);
         soft_exp(0, s0, p0h);
-        // the next stage's V (requested at this stage's start) to fp16 here,
+        // the next stage (requested at this stage's start) to fp16 here,
         // between MFMA phases, rather than on the path to the barrier
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        stage_v_f16(nxt);
+        stage_f16(nxt);
         soft_max(1, s1, kb0, diag);
         pv(vs, 0, p0h);
         soft_exp(1, s1, p1h);
@@ -676,25 +680,28 @@ __global__ __launch_bounds__(256, 2) void k_attn_prefill(AttnPrefillParams p) {
     };
 
     // stage s + 1 is requested (into the other buffer) before stage s is
-    // computed; one stage past the end stays inside the padded cache
+    // computed
     stage_issue(kv_a, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    stage_v_f16(kv_a);
+    stage_f16(kv_a);
     __syncthreads();
     for (int st = 0; st < nstage; ++st) {
         uint16_t *cur = (st & 1) ? kv_b : kv_a, *nxt = (st & 1) ? kv_a : kv_b;
-        stage_issue(nxt, (st + 1) * kAK);
+        stage_issue(nxt, min((st + 1) * kAK, p.lmax_pad - kAK));   // (the request past the end reads an unused stage)
         // the causal mask only where some key of the stage lies past some query
-        if (active) attend(cur, cur + kAK * D, st * kAK, st * kAK + kAK - 1 > qpos0, nxt);
+        // a wave skips stages wholly past its queries (the upper half's last
+        // stage for the lower half) but still converts its share of the next
+        const bool live = active && st * kAK <= qpos0w + 31;
+        if (live) attend(cur, cur + kAK * D, st * kAK, st * kAK + kAK - 1 > qpos0w, nxt);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        if (!active) stage_v_f16(nxt);   // (active waves converted theirs in attend)
+        if (!live) stage_f16(nxt);   // (live waves converted theirs in attend)
         __syncthreads();
     }
     if (!active) return;
     const int qd = p.n_q * D;
 #pragma unroll
     for (int ct = 0; ct < 2; ++ct) {
-        const int i = q0 + 16 * ct + j;
+        const int i = q0w + 16 * ct + j;
         if (i >= p.g.clen) continue;
         const float inv = 1.0f / l_run[ct];
         const int64_t m = (int64_t)b * p.g.mpad + i;
@@ -715,7 +722,7 @@ void launch_attn_prefill(const AttnPrefillParams &p, hipStream_t s) {
     const int nhg = (qpg + 3) / 4;
     const int nqb = (p.g.clen + kAQ - 1) / kAQ;
     const int grid = p.g.B * p.n_kv * nhg * nqb;
-    const int threads = 256;   // four waves stage K/V even when the group has fewer heads
+    const int threads = 512;   // eight waves stage K/V even when the group has fewer heads
     if (p.d == 128) hipLaunchKernelGGL(k_attn_prefill<128>, dim3(grid), dim3(threads), 0, s, p);
     else hipLaunchKernelGGL(k_attn_prefill<64>, dim3(grid), dim3(threads), 0, s, p);
 }

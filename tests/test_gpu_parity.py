@@ -182,6 +182,24 @@ def test_4b_full_depth_36_layers(torch):
     m.close()
 
 
+@pytest.mark.parametrize("hidden,nq,nkv", [(2048, 32, 16), (1536, 64, 16)])
+def test_head_dim_64_attention_finishes_qkv(torch, hidden, nq, nkv):
+    """Head dim 64 at batch 32 (hidden 2048 with two query heads per KV group,
+    hidden 1536 with four): the QKV GEMV cuts K into four (three) ranges, so
+    the decode attention sums them, rotates q and k and appends the new key
+    and value itself (the d = 64 form of that path); the steps cross a 32-key
+    block."""
+    cfg = ModelConfig(n_layers=2, hidden=hidden, n_q_heads=nq, n_kv_heads=nkv, head_dim=64, ffn=2048, vocab=4096,
+                      rope_base=1e4)
+    B, n, steps = 32, 64, 3
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=21)
+    m = _model(cfg, seed=8, max_batch=32, max_latent=32 + steps + 1, prefill_chunk=4096)
+    W = O.OracleWeights.generate(cfg, seed=8, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log)
+    rep.check()
+    m.close()
+
+
 def test_4b_width_batch20_top_p(torch):
     """4B width, two layers, 20 sequences (two 16-column MFMA tiles), T 0.6,
     top-p 0.95, tau 0.7, per-sequence seeds."""

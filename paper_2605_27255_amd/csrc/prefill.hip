@@ -464,9 +464,9 @@ void launch_gemm(const GemmParams &p, hipStream_t s) {
 // 64-query block); eight waves, wave w computes head w % 4 for the block's
 // 32-query half w / 4 (two 16-column MFMA tiles).  Keys and values of 64
 // positions at a time are staged in LDS, shared by the workgroup's heads and
-// halves and double-buffered: the next stage is requested straight into LDS
-// before the current one is multiplied, and each lane widens the 16 bytes it
-// requested from bf16 to fp16 once they have landed (mid-stage).  Per stage
+// halves and double-buffered: the next stage is requested into registers
+// before the current one is multiplied, and each lane writes the pieces it
+// requested, widened from bf16 to fp16, into the other buffer mid-stage.  Per stage
 // the scores of all 64 keys are formed first (both query tiles), then one
 // online-softmax update per query tile (the causal mask only on stages that
 // reach the diagonal; stages wholly past a half's queries are skipped), so
@@ -550,40 +550,39 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill(AttnPrefillParams p) {
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
 
     const int kend = qpos0 + kAQ;              // keys [0, kend) may be visible
-    // One 64-key stage straight from the cache into LDS (global_load_lds: lane
-    // l of a wave writes 16 bytes at the buffer block's base + 16 l, no
-    // registers): the K tiles are 16 contiguous 1 KB blocks (D = 128) copied
-    // as they are; each 1 KB V block (16 dims x 32 keys of a V tile) is read
-    // with its lanes permuted so that lane l = 16 g + j lands holding dim j,
-    // keys 8 g .. 8 g + 7, the PV MFMA's A operand, read back linearly.
+    // One 64-key stage: each lane requests 16 bytes of each of its wave's K
+    // and V blocks into registers at the start of the previous stage, and
+    // writes them widened to fp16 into the stage buffer half-way through it,
+    // lane l at the block's base + 16 l (one LDS write per piece, against a
+    // direct-to-LDS load plus a read and a write to convert in place): the K
+    // tiles are 16 contiguous 1 KB blocks (D = 128) kept as they are; each 1 KB
+    // V block (16 dims x 32 keys of a V tile) is read with its lanes permuted
+    // so that lane l = 16 g + j holds dim j, keys 8 g .. 8 g + 7, the PV MFMA's
+    // A operand, read back linearly.
     constexpr int KBW = D / 64;            // K (and V) blocks per wave per stage
     const int nstage = (kend + kAK - 1) / kAK;
-    using lds_t = __attribute__((address_space(3))) void;
-    auto stage_issue = [&](uint16_t *buf, int kb0) {
+    u32x4 stg[2 * KBW];   // this lane's 16-byte pieces of the next stage, in flight
+    auto stage_issue = [&](int kb0) {
 #pragma unroll
         for (int u = 0; u < KBW; ++u) {
             const int blk = wave * KBW + u;
-            const uint16_t *src = kbase + (int64_t)kb0 * D + blk * 512 + lane * 8;
-            __builtin_amdgcn_global_load_lds((const void *)src, (lds_t *)(buf + blk * 512), 16, 0, 0);
+            stg[u] = *(const u32x4 *)(kbase + (int64_t)kb0 * D + blk * 512 + lane * 8);
         }
 #pragma unroll
         for (int u = 0; u < KBW; ++u) {
             const int vb = wave * KBW + u, h = vb / NT, t = vb - h * NT;
-            const uint16_t *src = vbase + (int64_t)((kb0 >> 5) + h) * D * 32 + (16 * t + j) * 32 + 8 * g;
-            __builtin_amdgcn_global_load_lds((const void *)src, (lds_t *)(buf + kAK * D + vb * 512), 16, 0, 0);
+            stg[KBW + u] = *(const u32x4 *)(vbase + (int64_t)((kb0 >> 5) + h) * D * 32 + (16 * t + j) * 32 + 8 * g);
         }
     };
-    // K and V of a stage, bf16 -> fp16 in place: each lane converts the
-    // 16-byte pieces its own loads wrote (so only those must have completed)
+    // the pieces, bf16 -> fp16, into a stage buffer: K blocks as stored, V
+    // blocks in MFMA operand order (each lane's piece at 16 bytes x lane)
     auto stage_f16 = [&](uint16_t *buf) {
 #pragma unroll
         for (int u = 0; u < 2 * KBW; ++u) {
-            u32x4 *at = (u32x4 *)(buf + (u < KBW ? 0 : kAK * D) + (wave * KBW + (u % KBW)) * 512 + lane * 8);
-            const u32x4 w = *at;
             u32x4 h;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) h[i] = pack_f16x2(bf_lo(w[i]), bf_hi(w[i]));
-            *at = h;
+            for (int i = 0; i < 4; ++i) h[i] = pack_f16x2(bf_lo(stg[u][i]), bf_hi(stg[u][i]));
+            *(u32x4 *)(buf + (u < KBW ? 0 : kAK * D) + (wave * KBW + (u % KBW)) * 512 + lane * 8) = h;
         }
     };
     // One 64-key stage: the scores of both 16-query tiles, the softmax of
@@ -663,38 +662,36 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill(AttnPrefillParams p) {
                 o[ct][t] = mfma16_f16(vf, ph[half], o[ct][t]);
             }
     };
-    auto attend = [&](const uint16_t *ks, const uint16_t *vs, int kb0, bool diag, uint16_t *nxt) {
-        f32x4 s0[4], s1[4];
-        u32x4 p0h[2], p1h[2];
-        scores(ks, s0, s1);
-        soft_max(0, s0, kb0, diag);
-        soft_exp(0, s0, p0h);
-        // the next stage (requested at this stage's start) to fp16 here,
-        // between MFMA phases, rather than on the path to the barrier
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        stage_f16(nxt);
-        soft_max(1, s1, kb0, diag);
-        pv(vs, 0, p0h);
-        soft_exp(1, s1, p1h);
-        pv(vs, 1, p1h);
-    };
-
+    f32x4 s0[4], s1[4];
+    u32x4 p0h[2], p1h[2];
     // stage s + 1 is requested (into the other buffer) before stage s is
     // computed
-    stage_issue(kv_a, 0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    stage_issue(0);
     stage_f16(kv_a);
     __syncthreads();
     for (int st = 0; st < nstage; ++st) {
         uint16_t *cur = (st & 1) ? kv_b : kv_a, *nxt = (st & 1) ? kv_a : kv_b;
-        stage_issue(nxt, min((st + 1) * kAK, p.lmax_pad - kAK));   // (the request past the end reads an unused stage)
+        stage_issue(min((st + 1) * kAK, p.lmax_pad - kAK));   // (the request past the end reads an unused stage)
         // the causal mask only where some key of the stage lies past some query
         // a wave skips stages wholly past its queries (the upper half's last
         // stage for the lower half) but still converts its share of the next
         const bool live = active && st * kAK <= qpos0w + 31;
-        if (live) attend(cur, cur + kAK * D, st * kAK, st * kAK + kAK - 1 > qpos0w, nxt);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        if (!live) stage_f16(nxt);   // (live waves converted theirs in attend)
+        const bool diag = st * kAK + kAK - 1 > qpos0w;
+        const uint16_t *vs = cur + kAK * D;
+        if (live) {
+            scores(cur, s0, s1);
+            soft_max(0, s0, st * kAK, diag);
+            soft_exp(0, s0, p0h);
+        }
+        // the next stage's pieces to fp16, between this stage's MFMA phases
+        // (every wave, live or not, writes its share)
+        stage_f16(nxt);
+        if (live) {
+            soft_max(1, s1, st * kAK, diag);
+            pv(vs, 0, p0h);
+            soft_exp(1, s1, p1h);
+            pv(vs, 1, p1h);
+        }
         __syncthreads();
     }
     if (!active) return;

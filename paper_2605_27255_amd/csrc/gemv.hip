@@ -35,6 +35,11 @@ thread_local GemvTiming g_gemv_timing = {nullptr, nullptr, false};
 constexpr int kNW = 8;                       // waves per workgroup
 constexpr int kMaxB = 64;                    // columns (sequences) at most: four 16-column tiles
 constexpr int kGemvOneLdsBytes = 72 * 1024;  // budget for wave-private X (two workgroups per CU)
+// The residual and SwiGLU epilogues may take one workgroup per CU instead
+// (X up to 150 KB, e.g. 8 rows of K = 4096): no k-ranges, so no finishing
+// launch (9B at batch 8: pair step 6.03 -> 5.96 ms).  QKV keeps the k-range
+// path there, whose finish the decode attention takes over.
+constexpr int kGemvOneLdsBytesWide = 150 * 1024;
 // k-tiles per shared X chunk (larger batches); beyond 32 columns half as
 // many, so that the X and weight registers of two chunks in flight fit
 constexpr int wide_chunk(int nbt) { return nbt <= 2 ? 8 : 4; }
@@ -1015,7 +1020,8 @@ static void launch_t(const GemvParams &p, hipStream_t s) {
     // wave-private X when every wave's slices fit
     const int nmax = (KT + KS - 1) / KS;
     const int lds_one = planes * kNW * q.B * (nmax * 32 + 8) * 2 + red;
-    if (NBT <= 2 && lds_one <= kGemvOneLdsBytes) {   // (never fits beyond 32 columns)
+    constexpr int budget = (EPI == EPI_RESID || EPI == EPI_SWIGLU) ? kGemvOneLdsBytesWide : kGemvOneLdsBytes;
+    if (NBT <= 2 && lds_one <= budget) {   // (never fits beyond 32 columns)
         if (q.wg_cap > 0 && grid > q.wg_cap) grid = q.wg_cap;
         if (g_gemv_timing.pending) {
             hipExtLaunchKernelGGL((k_gemv<NBT, KS, PRO, EPI, U>), dim3(grid), dim3(kNW * 64), lds_one, s,

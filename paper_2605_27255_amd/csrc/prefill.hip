@@ -292,7 +292,7 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
 }
 
 // ---- MFMA GEMM  C^T[N][M] = W[N][K] X[M][K]^T, both operands tiled ---------
-// Workgroup tile 256 weight rows x 64 tokens, four waves of 64 x 64 (4 x 4
+// Workgroup tile 256 (or 320) weight rows x 64 tokens, four waves of 64 (80) x 64 (4 (5) x 4
 // fragments).  A wave's 64 weight rows are its own, so their 1 KB tiles go
 // from memory straight into its registers (one contiguous load per tile, no
 // LDS); the token tiles (X hi and lo, 16 KB per 64-wide k step) are shared by
@@ -306,7 +306,7 @@ __device__ __forceinline__ void gemm_epi(const GemmParams &p, f32x4 val, int str
 // takes a contiguous run of tiles in grouped order (8 weight tiles by every
 // token tile), so the ~64 workgroups resident on one XCD cover about 8 x 8
 // tiles and share their weight and token tiles in that XCD's L2.
-constexpr int kWdRows = 256, kWdToks = 64, kWdGroup = 8;
+constexpr int kWdToks = 64, kWdGroup = 8;   // tokens per workgroup tile; weight tiles per XCD group
 
 __device__ __forceinline__ bool wd_tile(int id, int nbn, int nbm, int &bn, int &bm) {
     const int T = nbn * nbm;
@@ -322,7 +322,7 @@ __device__ __forceinline__ bool wd_tile(int id, int nbn, int nbm, int &bn, int &
     return true;
 }
 
-template <int EPI, bool HASLO>
+template <int EPI, bool HASLO, int SW>   // SW: 16-row weight strips per wave (tile of 64 SW rows)
 __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
     constexpr int NP = HASLO ? 2 : 1;
     constexpr int XT = NP * 2 * 4;                            // X tiles per stage: plane x k-tile x token strip
@@ -330,7 +330,8 @@ __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
     extern __shared__ __align__(16) uint16_t lds[];           // [2][XT][512]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = lane & 15;
-    const int nbn = (p.N + kWdRows - 1) / kWdRows, nbm = (p.M + kWdToks - 1) / kWdToks;
+    constexpr int ROWS = 64 * SW;
+    const int nbn = (p.N + ROWS - 1) / ROWS, nbm = (p.M + kWdToks - 1) / kWdToks;
     int bn, bm;
     if (!wd_tile(blockIdx.x, nbn, nbm, bn, bm)) return;
     if (p.g.ntok) {   // a ragged batch: a token tile wholly past its sequence's last position holds only PAD rows
@@ -341,11 +342,11 @@ __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
     const int NI = (KT + 1) >> 1;                              // iterations of two k tiles
     const int NS = p.N >> 4, MS = p.M >> 4;
 
-    // this wave's four weight strips (padding strips read strip 0, masked later)
-    const uint16_t *wsrc[4];
+    // this wave's SW weight strips (padding strips read strip 0, masked later)
+    const uint16_t *wsrc[SW];
 #pragma unroll
-    for (int si = 0; si < 4; ++si) {
-        int strip = bn * 16 + wave * 4 + si;
+    for (int si = 0; si < SW; ++si) {
+        int strip = bn * 4 * SW + wave * SW + si;
         strip = strip < NS ? strip : 0;
         wsrc[si] = p.W + (int64_t)strip * KT * 512 + lane * 8;
     }
@@ -361,11 +362,11 @@ __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
     }
     // k tiles past the end re-read the last one (their products are skipped)
     auto kclamp = [&](int kt) { return kt < KT ? kt : KT - 1; };
-    auto load_w = [&](int it, u32x4 (&w)[2][4]) {
+    auto load_w = [&](int it, u32x4 (&w)[2][SW]) {
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-            for (int si = 0; si < 4; ++si)
+            for (int si = 0; si < SW; ++si)
                 w[kk][si] = *(const u32x4 *)(wsrc[si] + (int64_t)kclamp(2 * it + kk) * 512);
     };
     auto load_x = [&](int it, u32x4 (&x)[XC]) {
@@ -381,13 +382,13 @@ __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
         for (int r = 0; r < XC; ++r) *(u32x4 *)(&lds[(buf * XT * 64 + tid + 256 * r) * 8]) = x[r];
     };
 
-    f32x4 acc[4][4];
+    f32x4 acc[SW][4];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < SW; ++a)
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto mma = [&](int buf, int it, const u32x4 (&w)[2][4]) {
+    auto mma = [&](int buf, int it, const u32x4 (&w)[2][SW]) {
         const uint16_t *L = lds + buf * XT * 512;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
@@ -399,19 +400,19 @@ __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
                 if (HASLO) bl[mi] = *(const u32x4 *)(&L[((1 * 2 + kk) * 4 + mi) * 512 + lane * 8]);
             }
 #pragma unroll
-            for (int si = 0; si < 4; ++si)
+            for (int si = 0; si < SW; ++si)
 #pragma unroll
                 for (int mi = 0; mi < 4; ++mi) acc[si][mi] = mfma16(w[kk][si], bh[mi], acc[si][mi]);
             if (HASLO) {
 #pragma unroll
-                for (int si = 0; si < 4; ++si)
+                for (int si = 0; si < SW; ++si)
 #pragma unroll
                     for (int mi = 0; mi < 4; ++mi) acc[si][mi] = mfma16(w[kk][si], bl[mi], acc[si][mi]);
             }
         }
     };
 
-    u32x4 wa[2][4], wb[2][4], xr[XC];
+    u32x4 wa[2][SW], wb[2][SW], xr[XC];
     load_x(0, xr);
     load_w(0, wa);
     store_x(0, xr);
@@ -432,17 +433,29 @@ __global__ __launch_bounds__(256) void k_gemm_wd(GemmParams p) {
     }
 
 #pragma unroll
-    for (int si = 0; si < 4; ++si)
+    for (int si = 0; si < SW; ++si)
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
-            gemm_epi<EPI>(p, acc[si][mi], bn * 16 + wave * 4 + si, bm * kWdToks + mi * 16 + j);
+            gemm_epi<EPI>(p, acc[si][mi], bn * 4 * SW + wave * SW + si, bm * kWdToks + mi * 16 + j);
 }
 
+// Tile height: 256 or 320 weight rows, whichever gives the busiest compute
+// unit the fewest rows (workgroups are spread evenly over the 256 CUs, so a
+// CU runs ceil(tiles / 256) of them): at N = 2560 the 256-row tile leaves
+// 2.5 workgroups per CU (half the CUs run three), the 320-row tile two.
 template <int EPI, bool HASLO>
 static void launch_gemm_wd(const GemmParams &p, hipStream_t s) {
-    const int nbn = (p.N + kWdRows - 1) / kWdRows, nbm = (p.M + kWdToks - 1) / kWdToks;
+    const int nbm = (p.M + kWdToks - 1) / kWdToks;
+    auto load = [&](int rows) {
+        const int tiles = ((p.N + rows - 1) / rows) * nbm;
+        return (int64_t)((tiles + 255) / 256) * rows;
+    };
+    const bool five = p.N % 320 == 0 && load(320) < load(256);
+    const int nbn = five ? p.N / 320 : (p.N + 255) / 256;
     const int grid = 8 * ((nbn * nbm + 7) / 8);
-    hipLaunchKernelGGL((k_gemm_wd<EPI, HASLO>), dim3(grid), dim3(256), 2 * (HASLO ? 16 : 8) * 1024, s, p);
+    const size_t lds = 2 * (HASLO ? 16 : 8) * 1024;
+    if (five) hipLaunchKernelGGL((k_gemm_wd<EPI, HASLO, 5>), dim3(grid), dim3(256), lds, s, p);
+    else hipLaunchKernelGGL((k_gemm_wd<EPI, HASLO, 4>), dim3(grid), dim3(256), lds, s, p);
 }
 
 void launch_gemm(const GemmParams &p, hipStream_t s) {

@@ -48,7 +48,8 @@ struct GemvParams {
     int64_t kv_bstride;           // elements between consecutive sequences' caches
     uint64_t *best;               // argmax keys [B] (EPI_LOGITS; NULL: none)
     uint16_t *xh, *xl;            // X planes workspace, [B][K] bf16 each (large batches)
-    float *part; int64_t part_cap;  // k-range partial sums workspace (floats)
+    float *part; int64_t part_cap;  // k-range partial sums workspace (floats): [range][B][N], or
+                                    // [range][strip][B][16] above 16 sequences (part_index in gemv.hip)
     int ksplit;                   // k-ranges (set by launch_gemv)
     int *deferred;                // EPI_QKV: if not NULL and K is cut into 2..kAttnFusedRanges ranges,
                                   // the range sum, RoPE and KV append are left to the decode attention

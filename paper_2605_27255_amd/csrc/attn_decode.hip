@@ -24,14 +24,19 @@ namespace pipo {
 // that holds the new position first adds that position's key and value rows,
 // rotates the key, writes both to the cache and waits for the stores, before
 // it requests any key block (its last block then reads them back).
-template <int D, bool FUSED>
-__global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
+// NW: waves per workgroup.  1: one wave per (sequence, KV group, split),
+// partials to global memory for k_attn_merge.  NW > 1: one workgroup per
+// (sequence, KV group) whose NW waves are its splits; their partials are
+// combined in LDS in split order and the workgroup writes the output rows.
+template <int D, bool FUSED, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_decode(AttnDecodeParams p) {
     constexpr int NC = D / 32;   // 32-wide d chunks (QK^T k-steps)
     constexpr int NT = D / 16;   // 16-wide d tiles (PV output tiles)
-    const int lane = threadIdx.x, j = lane & 15, g = lane >> 4;
-    const int S = p.splits;
-    const int split = blockIdx.x % S;
-    const int bk = blockIdx.x / S;               // b * n_kv + kvh
+    const int lane = threadIdx.x & 63, j = lane & 15, g = lane >> 4;
+    const int wave = NW > 1 ? (int)threadIdx.x >> 6 : 0;
+    const int S = NW > 1 ? NW : p.splits;
+    const int split = NW > 1 ? wave : (int)blockIdx.x % S;
+    const int bk = NW > 1 ? (int)blockIdx.x : (int)blockIdx.x / S;   // b * n_kv + kvh
     const int b = bk / p.n_kv, kvh = bk - b * p.n_kv;
     const int qpg = p.n_q / p.n_kv;
     // splits own whole 32-key blocks: split s takes blocks [s*nb/S, (s+1)*nb/S)
@@ -68,12 +73,14 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
     auto blk = [&](int i) { return i < nblk ? k0 + 32 * i : 0; };
 
     float4 qr[NC][2];
-    __shared__ float s_new[2][D];      // FUSED, last split: the new key and value (bf16 values)
+    __shared__ float s_new_all[NW][2][D];   // FUSED, last split: the new key and value (bf16 values)
+    float (&s_new)[2][D] = s_new_all[wave];
     float s_key = 0.f;                 // FUSED, last split: the new key's scaled score
     if constexpr (FUSED) {
         // LDS: the group's rotated query rows [qpg][D] (qpg * D <= 1024) and,
         // for the last split, the new key and value (bf16 values)
-        __shared__ float s_q[1024];
+        __shared__ float s_q_all[NW][1024];
+        float (&s_q)[1024] = s_q_all[wave];
         const bool hold = split == S - 1;
         const int R = p.ksplit, pos = len - 1;
         const int64_t NB = (int64_t)p.B * p.nqkv;
@@ -307,14 +314,47 @@ __global__ __launch_bounds__(64) void k_attn_decode(AttnDecodeParams p) {
                 (uint16_t)(__float_as_uint(s_new[1][lane + D / 2]) >> 16);
         }
     }
-    // partial (o, m, l) of this split for each head of the group
-    if (j < qpg) {
-        float *pr = p.part + (((int64_t)b * p.n_q + kvh * qpg + j) * S + split) * (D + 2);
+    if constexpr (NW == 1) {
+        // partial (o, m, l) of this split for each head of the group
+        if (j < qpg) {
+            float *pr = p.part + (((int64_t)b * p.n_q + kvh * qpg + j) * S + split) * (D + 2);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) *(f32x4 *)(pr + 16 * t + 4 * g) = o[t];
-        if (g == 0) {
-            pr[D] = m_run;
-            pr[D + 1] = l_run;
+            for (int t = 0; t < NT; ++t) *(f32x4 *)(pr + 16 * t + 4 * g) = o[t];
+            if (g == 0) {
+                pr[D] = m_run;
+                pr[D + 1] = l_run;
+            }
+        }
+    } else {
+        // the splits' (o, m, l) through LDS, merged as k_attn_merge does:
+        // weights exp2(m_s - M), L = sum_s w_s l_s, the weighted outputs
+        // added in split order
+        __shared__ float red[NW][16][D + 2];
+        if (j < qpg) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) red[wave][j][16 * t + 4 * g + v] = o[t][v];
+            if (g == 0) {
+                red[wave][j][D] = m_run;
+                red[wave][j][D + 1] = l_run;
+            }
+        }
+        __syncthreads();
+        for (int e = threadIdx.x; e < qpg * D; e += 64 * NW) {
+            const int hj = e / D, dim = e - hj * D;
+            float M = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) M = fmaxf(M, red[w][hj][D]);
+            float L = 0.f, acc = 0.f;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) {
+                const float mw = red[w][hj][D];
+                const float ww = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);
+                L += ww * red[w][hj][D + 1];
+                acc += ww * red[w][hj][dim];
+            }
+            p.out[((int64_t)b * p.n_q + kvh * qpg + hj) * D + dim] = acc * (1.0f / L);
         }
     }
 }
@@ -353,15 +393,27 @@ __global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
 }
 
 void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s) {
-    const int grid = p.B * p.n_kv * p.splits;
     const bool fused = p.qkv_part != nullptr;
+    if (p.splits == kAttnWgSplits) {   // one workgroup per (sequence, KV group), no merge launch
+        const int grid = p.B * p.n_kv;
+        constexpr int NW = kAttnWgSplits;
+        if (p.d == 128) {
+            if (fused) hipLaunchKernelGGL((k_attn_decode<128, true, NW>), dim3(grid), dim3(64 * NW), 0, s, p);
+            else hipLaunchKernelGGL((k_attn_decode<128, false, NW>), dim3(grid), dim3(64 * NW), 0, s, p);
+        } else {
+            if (fused) hipLaunchKernelGGL((k_attn_decode<64, true, NW>), dim3(grid), dim3(64 * NW), 0, s, p);
+            else hipLaunchKernelGGL((k_attn_decode<64, false, NW>), dim3(grid), dim3(64 * NW), 0, s, p);
+        }
+        return;
+    }
+    const int grid = p.B * p.n_kv * p.splits;
     if (p.d == 128) {
-        if (fused) hipLaunchKernelGGL((k_attn_decode<128, true>), dim3(grid), dim3(64), 0, s, p);
-        else hipLaunchKernelGGL((k_attn_decode<128, false>), dim3(grid), dim3(64), 0, s, p);
+        if (fused) hipLaunchKernelGGL((k_attn_decode<128, true, 1>), dim3(grid), dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((k_attn_decode<128, false, 1>), dim3(grid), dim3(64), 0, s, p);
         hipLaunchKernelGGL(k_attn_merge<128>, dim3(p.B * p.n_q), dim3(128), 0, s, p);
     } else {
-        if (fused) hipLaunchKernelGGL((k_attn_decode<64, true>), dim3(grid), dim3(64), 0, s, p);
-        else hipLaunchKernelGGL((k_attn_decode<64, false>), dim3(grid), dim3(64), 0, s, p);
+        if (fused) hipLaunchKernelGGL((k_attn_decode<64, true, 1>), dim3(grid), dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((k_attn_decode<64, false, 1>), dim3(grid), dim3(64), 0, s, p);
         hipLaunchKernelGGL(k_attn_merge<64>, dim3(p.B * p.n_q), dim3(64), 0, s, p);
     }
 }

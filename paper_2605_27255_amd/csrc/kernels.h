@@ -75,6 +75,9 @@ int gemv_num_groups(int N);
 // k-ranges of the QKV GEMV whose sum the decode attention takes over (one
 // round trip of partial loads in its prologue)
 constexpr int kAttnFusedRanges = 4;
+// splits == kAttnWgSplits: one workgroup per (sequence, KV group) whose waves
+// are the splits, merged in LDS (no k_attn_merge launch)
+constexpr int kAttnWgSplits = 8;
 
 struct AttnDecodeParams {
     const float *q;             // fp32 [B][n_q][d]

@@ -455,6 +455,9 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
 // full capacity (both blocks are prefetched), and no more splits than it takes
 // to give the machine about 1024 waves; at most 64 (the merge kernel's limit).
 static int attn_splits(const pipo_ctx *c, int B) {
+    // a workgroup per (sequence, KV group) once they fill every CU: its eight
+    // waves split the keys and merge in LDS, with no merge launch
+    if (B * c->nkv >= c->n_cu) return kAttnWgSplits;
     const int blocks = (c->cfg.max_latent + 31) / 32;
     int sp = (blocks + 1) / 2;
     const int cap = (1024 + B * c->nkv - 1) / (B * c->nkv);

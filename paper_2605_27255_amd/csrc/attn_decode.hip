@@ -7,11 +7,13 @@
 // accumulator holds one head; online softmax runs per column; the
 // probabilities, held as (4g + v, 16 + 4g + v) for lane group g, are already
 // the B operand of O^T[dim][head] += V^T P^T because the V cache stores each
-// 32-key tile in that key order (vslot).  The query and the
-// probabilities enter the MFMAs as bf16 pairs hi + lo (two MFMAs each), so
-// only the bf16 KV cache itself limits the precision.  Per-split results
-// (m, l, o) go to a partial buffer; a second kernel merges them per head in
-// split order (the kernel boundary makes every split's partial visible).
+// 32-key tile in that key order (vslot in device_common.h).  The query and
+// the probabilities enter the MFMAs as bf16 pairs hi + lo (two MFMAs each),
+// so only the bf16 KV cache itself limits the precision.  Per-split results
+// (m, l, o) either go to a partial buffer that a second kernel merges per
+// head in split order (the kernel boundary makes every split's partial
+// visible), or, when the (sequence, KV group) pairs fill the machine, stay in
+// one workgroup whose waves are the splits and merge through LDS.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -20,10 +22,11 @@ namespace pipo {
 // FUSED: the QKV GEMV left its k-range partial sums [R][B][nqkv] (rows in its
 // strip order: strip t of a q or k head holds dims 8t..8t+7, then their RoPE
 // partners d/2+8t..; v heads in order).  Every split adds the ranges of its
-// group's query rows in range order and applies RoPE in registers; the split
-// that holds the new position first adds that position's key and value rows,
-// rotates the key, writes both to the cache and waits for the stores, before
-// it requests any key block (its last block then reads them back).
+// group's query rows in range order and applies RoPE (staging the rotated
+// rows in LDS); the split that holds the new position also adds that
+// position's key and value rows and rotates the key, scores the new key from
+// registers (one online-softmax step after its blocks, which stop before it)
+// and stores the key and value to the cache at its end, for later steps.
 // NW: waves per workgroup.  1: one wave per (sequence, KV group, split),
 // partials to global memory for k_attn_merge.  NW > 1: one workgroup per
 // (sequence, KV group) whose NW waves are its splits; their partials are

@@ -477,24 +477,23 @@ void launch_gemm(const GemmParams &p, hipStream_t s) {
 // 64-query block); eight waves, wave w computes head w % 4 for the block's
 // 32-query half w / 4 (two 16-column MFMA tiles).  Keys and values of 64
 // positions at a time are staged in LDS, shared by the workgroup's heads and
-// halves and double-buffered: the next stage is requested into registers
-// before the current one is multiplied, and each lane writes the pieces it
-// requested, widened from bf16 to fp16, into the other buffer mid-stage.  Per stage
-// the scores of all 64 keys are formed first (both query tiles), then one
-// online-softmax update per query tile (the causal mask only on stages that
-// reach the diagonal; stages wholly past a half's queries are skipped), so
-// the row max / sum shuffles happen once per 64 keys, and the accumulators
-// are rescaled only when the running max grows by more than 2^8.  Scores
-// stay unscaled; the softmax scale 1/sqrt(d) (times log2 e) enters through
-// one fma per score in the exponent, and the exponentials are the hardware
-// exp2 (results below the normal range flush to zero, which the softmax
-// weights can afford).
+// halves and double-buffered: the next stage is requested into registers before
+// the current one is multiplied, and each lane writes the pieces it requested,
+// widened from bf16 to fp16, into the other buffer mid-stage.  Per stage the
+// scores of all 64 keys are formed first (both query tiles), then one online-
+// softmax update per query tile (the causal mask only on stages that reach the
+// diagonal; stages wholly past a half's queries are skipped), so the row max /
+// sum shuffles happen once per 64 keys, and the accumulators are rescaled only
+// when the running max grows by more than 2^8.  Scores stay unscaled; the
+// softmax scale 1/sqrt(d) (times log2 e) enters through one fma per score in
+// the exponent, and the exponentials are the hardware exp2 (results below the
+// normal range flush to zero, which the softmax weights can afford).
 // Both products take fp16 operands: the query (its hi + lo pair summed and
-// rounded once) and the probabilities carry 11 significant bits (against 8
-// for bf16), and K and V, stored as bf16, are widened to fp16 exactly for
-// every value in fp16's normal range (|x| in [2^-14, 65504]; smaller values
-// keep 2^-24 absolute precision; larger ones would overflow, a limit of this
-// prefill kernel only).  One MFMA per product instead of a bf16 pair's two.
+// rounded once) and the probabilities carry 11 significant bits (against 8 for
+// bf16), and K and V, stored as bf16, are widened to fp16 exactly for every
+// value in fp16's normal range (|x| in [2^-14, 65504]; smaller values keep
+// 2^-24 absolute precision; larger ones would overflow, a limit of this prefill
+// kernel only).  One MFMA per product instead of a bf16 pair's two.
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
 typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
 __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
@@ -677,8 +676,8 @@ __global__ __launch_bounds__(512, 1) void k_attn_prefill(AttnPrefillParams p) {
     };
     f32x4 s0[4], s1[4];
     u32x4 p0h[2], p1h[2];
-    // stage s + 1 is requested (into the other buffer) before stage s is
-    // computed
+    // stage s + 1 is requested (into registers) before stage s is computed
+    // and lands in the other buffer half-way through it
     stage_issue(0);
     stage_f16(kv_a);
     __syncthreads();

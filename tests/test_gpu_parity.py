@@ -200,6 +200,24 @@ def test_head_dim_64_attention_finishes_qkv(torch, hidden, nq, nkv):
     m.close()
 
 
+@pytest.mark.parametrize("hidden,nq,nkv,d,B", [(2560, 32, 8, 128, 64), (2048, 32, 8, 64, 32)])
+def test_workgroup_merged_attention_unfused(torch, hidden, nq, nkv, d, B):
+    """Batch x KV groups >= 256, so the decode attention runs one workgroup per
+    (sequence, KV group) and merges its eight splits in LDS, with the QKV
+    GEMV finishing its own k-ranges (five ranges at 4B width and batch 64,
+    eight at head dim 64 and batch 32): the unfused form of that kernel, at
+    d = 128 and 64.  The oracle replays the first and the last sequence."""
+    cfg = ModelConfig(n_layers=1, hidden=hidden, n_q_heads=nq, n_kv_heads=nkv, head_dim=d, ffn=2048, vocab=4096,
+                      rope_base=1e4)
+    n, steps = 96, 3
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=23)
+    m = _model(cfg, seed=12, max_batch=B, max_latent=48 + steps + 1, prefill_chunk=4096)
+    W = O.OracleWeights.generate(cfg, seed=12, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log, seqs=[0, B - 1])
+    rep.check()
+    m.close()
+
+
 def test_4b_width_batch20_top_p(torch):
     """4B width, two layers, 20 sequences (two 16-column MFMA tiles), T 0.6,
     top-p 0.95, tau 0.7, per-sequence seeds."""
@@ -359,10 +377,11 @@ def test_regular_and_pair_sessions_share_one_context(torch):
 #
 # The bench's launch configuration (max_latent = latents + steps + 1, chunks
 # of 4096 latents, the workload's batch), so the decode attention splits the
-# keys as the timed runs do (C3: 4 splits of about 65 blocks, C4: 16 of about
-# 32) and the prefill attention reaches its later chunks; the layer count is
-# cut where the float64 oracle needs it, every other dimension is the
-# workload's.
+# keys as the timed runs do (C3: one workgroup per sequence and KV group,
+# eight splits of 32 blocks merged in LDS; C4: 16 one-wave splits of about 32
+# blocks and the merge kernel) and the prefill attention reaches its later
+# chunks; the layer count is cut where the float64 oracle needs it, every
+# other dimension is the workload's.
 
 from synth.configs import WORKLOADS  # noqa: E402
 
@@ -392,7 +411,8 @@ def test_c3_shape_batch32_8192_latents_top_p(torch):
     """The 4B batch-32 workload's shape (two layers): 32 prompts of 16384
     tokens (8192 latents each, two 4096-latent chunks), T 0.6, top-p 0.95,
     tau 0.7, per-sequence seeds; 6 steps; the oracle replays sequences 0 and
-    31.  Each decode-attention split covers about 65 key blocks."""
+    31.  Each decode-attention split (a wave of the sequence's workgroup)
+    covers 32 key blocks."""
     wl = WORKLOADS["4b-bs32-ctx8192-topp"]
     model, m = _workload_model(wl, layers=2)
     B = wl.batch

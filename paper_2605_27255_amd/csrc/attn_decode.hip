@@ -15,9 +15,69 @@
 // visible), or, when the (sequence, KV group) pairs fill the machine, stay in
 // one workgroup whose waves are the splits and merge through LDS.
 #include "device_common.h"
+#include <vector>
+
 #include "kernels.h"
 
 namespace pipo {
+
+// The merge of one (sequence, KV group) by one wave: the records of its qpg
+// heads and S splits ([qpg][S] in the partial buffer).  16 lanes take a head,
+// D / 16 dimensions each, four heads at a time; the splits go in split order,
+// XU at a time, with the running maximum M and the sums L and o rescaled by
+// exp2(M_old - M_new) as it rises; then o / L.
+template <int D>
+__device__ void xl_merge(const AttnDecodeParams &p, int b, int kvh, int qpg, int S, int lane) {
+    constexpr int RS = attn_part_stride(D), DPL = D / 16, XU = 8;
+    const float *rec = p.part + ((int64_t)b * p.n_q + kvh * qpg) * S * RS;   // [qpg][S][RS]
+    const int d0 = (lane & 15) * DPL;
+    for (int h0 = 0; h0 < qpg; h0 += 4) {
+        const int hj = h0 + (lane >> 4);
+        const float *rh = rec + (int64_t)(hj < qpg ? hj : 0) * S * RS;
+        float M = -INFINITY, L = 0.f, acc[DPL];
+#pragma unroll
+        for (int k = 0; k < DPL; ++k) acc[k] = 0.f;
+        for (int s0 = 0; s0 < S; s0 += XU) {
+            float2 ml[XU];
+            float4 ov[XU][DPL / 4];
+#pragma unroll
+            for (int u = 0; u < XU; ++u) {
+                const float *r = rh + (int64_t)min(s0 + u, S - 1) * RS;
+                ml[u] = *(const float2 *)(r + D);
+#pragma unroll
+                for (int k = 0; k < DPL / 4; ++k) ov[u][k] = ((const float4 *)(r + d0))[k];
+            }
+            float Mn = M;
+#pragma unroll
+            for (int u = 0; u < XU; ++u) Mn = fmaxf(Mn, s0 + u < S ? ml[u].x : -INFINITY);
+            const float sc = Mn == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(M - Mn);
+            L *= sc;
+#pragma unroll
+            for (int k = 0; k < DPL; ++k) acc[k] *= sc;
+#pragma unroll
+            for (int u = 0; u < XU; ++u) {
+                const float w = (s0 + u < S && ml[u].x != -INFINITY) ? __builtin_amdgcn_exp2f(ml[u].x - Mn) : 0.f;
+                L += w * ml[u].y;
+#pragma unroll
+                for (int k = 0; k < DPL / 4; ++k) {
+                    acc[4 * k + 0] += w * ov[u][k].x;
+                    acc[4 * k + 1] += w * ov[u][k].y;
+                    acc[4 * k + 2] += w * ov[u][k].z;
+                    acc[4 * k + 3] += w * ov[u][k].w;
+                }
+            }
+            M = Mn;
+        }
+        if (hj < qpg) {
+            const float inv = 1.0f / L;
+            float *o = p.out + ((int64_t)b * p.n_q + kvh * qpg + hj) * D + d0;
+#pragma unroll
+            for (int k = 0; k < DPL / 4; ++k)
+                *(float4 *)(o + 4 * k) = make_float4(acc[4 * k] * inv, acc[4 * k + 1] * inv, acc[4 * k + 2] * inv,
+                                                     acc[4 * k + 3] * inv);
+        }
+    }
+}
 
 // FUSED: the QKV GEMV left its k-range partial sums [R][B][nqkv] (rows in its
 // strip order: strip t of a q or k head holds dims 8t..8t+7, then their RoPE
@@ -38,8 +98,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn_decode(AttnDecodeParams p) {
     const int lane = threadIdx.x & 63, j = lane & 15, g = lane >> 4;
     const int wave = NW > 1 ? (int)threadIdx.x >> 6 : 0;
     const int S = NW > 1 ? NW : p.splits;
-    const int split = NW > 1 ? wave : (int)blockIdx.x % S;
-    const int bk = NW > 1 ? (int)blockIdx.x : (int)blockIdx.x / S;   // b * n_kv + kvh
+    constexpr int RS = attn_part_stride(D);
+    // XCD-local merge: workgroup i runs on XCD i mod 8, so pair (sequence, KV
+    // group) k takes workgroups ((k / 8) S + split) 8 + k mod 8
+    const bool xl = NW == 1 && p.xl_ctr != nullptr;
+    const int xm = (int)blockIdx.x >> 3;
+    const int split = NW > 1 ? wave : xl ? xm % S : (int)blockIdx.x % S;
+    const int bk = NW > 1 ? (int)blockIdx.x : xl ? (xm / S) * 8 + ((int)blockIdx.x & 7) : (int)blockIdx.x / S;
+    if (xl && bk >= p.B * p.n_kv) return;   // (a one-wave workgroup: no barrier to leave)
     const int b = bk / p.n_kv, kvh = bk - b * p.n_kv;
     const int qpg = p.n_q / p.n_kv;
     // splits own whole 32-key blocks: split s takes blocks [s*nb/S, (s+1)*nb/S)
@@ -320,12 +386,27 @@ __global__ __launch_bounds__(64 * NW) void k_attn_decode(AttnDecodeParams p) {
     if constexpr (NW == 1) {
         // partial (o, m, l) of this split for each head of the group
         if (j < qpg) {
-            float *pr = p.part + (((int64_t)b * p.n_q + kvh * qpg + j) * S + split) * (D + 2);
+            float *pr = p.part + (((int64_t)b * p.n_q + kvh * qpg + j) * S + split) * RS;
 #pragma unroll
             for (int t = 0; t < NT; ++t) *(f32x4 *)(pr + 16 * t + 4 * g) = o[t];
             if (g == 0) {
                 pr[D] = m_run;
                 pr[D + 1] = l_run;
+            }
+        }
+        if (xl) {
+            // the last split of this pair to finish merges it: its stores are
+            // acknowledged by L2 before it counts itself in (the pair's other
+            // splits wrote theirs to the same L2; every record is whole cache
+            // lines, and no load of them happened on this CU before, so the
+            // loads below see them)
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            int old = 0;
+            if (lane == 0) old = __hip_atomic_fetch_add(p.xl_ctr + bk, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+            old = __builtin_amdgcn_readfirstlane(old);
+            if (old == S - 1) {
+                if (lane == 0) __hip_atomic_store(p.xl_ctr + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                xl_merge<D>(p, b, kvh, qpg, S, lane);
             }
         }
     } else {
@@ -374,12 +455,13 @@ __global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
     const int t = threadIdx.x;
     const int S = p.splits;
     const int bh = blockIdx.x;                        // b * n_q + head
-    const float *ph = p.part + (int64_t)bh * S * (D + 2);
+    constexpr int RS = attn_part_stride(D);
+    const float *ph = p.part + (int64_t)bh * S * RS;
     float ov[SMAX];
 #pragma unroll
-    for (int sp = 0; sp < SMAX; ++sp) ov[sp] = ph[(sp < S ? sp : 0) * (D + 2) + t];
+    for (int sp = 0; sp < SMAX; ++sp) ov[sp] = ph[(sp < S ? sp : 0) * RS + t];
     if (t < 64) {
-        const float msr = ph[(t < S ? t : 0) * (D + 2) + D], lsr = ph[(t < S ? t : 0) * (D + 2) + D + 1];
+        const float msr = ph[(t < S ? t : 0) * RS + D], lsr = ph[(t < S ? t : 0) * RS + D + 1];
         const float ms = t < S ? msr : -INFINITY;
         const float ls = t < S ? lsr : 0.f;
         const float M = wave_max(ms);
@@ -393,6 +475,37 @@ __global__ __launch_bounds__(D) void k_attn_merge(AttnDecodeParams p) {
 #pragma unroll
     for (int sp = 0; sp < SMAX; ++sp) acc += sp < S ? s_w[sp] * ov[sp] : 0.f;
     p.out[(int64_t)bh * D + t] = acc * s_inv;
+}
+
+__global__ __launch_bounds__(64) void k_xcd_probe(int *out) {
+    if (threadIdx.x == 0) {
+        unsigned x;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+        out[blockIdx.x] = (int)(x & 0xF);
+    }
+}
+
+hipError_t probe_xcd_round_robin(hipStream_t s, bool *ok) {
+    constexpr int n = 2048;
+    *ok = false;
+    int *d = nullptr;
+    hipError_t e = hipMalloc(&d, n * sizeof(int));
+    if (e != hipSuccess) return e;
+    std::vector<int> h(n);
+    hipLaunchKernelGGL(k_xcd_probe, dim3(n), dim3(64), 0, s, d);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipMemcpyAsync(h.data(), d, n * sizeof(int), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    hipFree(d);
+    if (e != hipSuccess) return e;
+    bool good = true, seen[16] = {};
+    for (int i = 0; i < 8; ++i) {
+        good = good && !seen[h[i]];
+        seen[h[i]] = true;
+    }
+    for (int i = 8; i < n; ++i) good = good && h[i] == h[i % 8];
+    *ok = good;
+    return hipSuccess;
 }
 
 void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s) {
@@ -409,15 +522,17 @@ void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s) {
         }
         return;
     }
-    const int grid = p.B * p.n_kv * p.splits;
+    const bool xl = p.xl_ctr != nullptr;
+    const int pairs = p.B * p.n_kv;
+    const int grid = xl ? 8 * p.splits * ((pairs + 7) / 8) : pairs * p.splits;
     if (p.d == 128) {
         if (fused) hipLaunchKernelGGL((k_attn_decode<128, true, 1>), dim3(grid), dim3(64), 0, s, p);
         else hipLaunchKernelGGL((k_attn_decode<128, false, 1>), dim3(grid), dim3(64), 0, s, p);
-        hipLaunchKernelGGL(k_attn_merge<128>, dim3(p.B * p.n_q), dim3(128), 0, s, p);
+        if (!xl) hipLaunchKernelGGL(k_attn_merge<128>, dim3(p.B * p.n_q), dim3(128), 0, s, p);
     } else {
         if (fused) hipLaunchKernelGGL((k_attn_decode<64, true, 1>), dim3(grid), dim3(64), 0, s, p);
         else hipLaunchKernelGGL((k_attn_decode<64, false, 1>), dim3(grid), dim3(64), 0, s, p);
-        hipLaunchKernelGGL(k_attn_merge<64>, dim3(p.B * p.n_q), dim3(64), 0, s, p);
+        if (!xl) hipLaunchKernelGGL(k_attn_merge<64>, dim3(p.B * p.n_q), dim3(64), 0, s, p);
     }
 }
 

@@ -78,6 +78,10 @@ constexpr int kAttnFusedRanges = 4;
 // splits == kAttnWgSplits: one workgroup per (sequence, KV group) whose waves
 // are the splits, merged in LDS (no k_attn_merge launch)
 constexpr int kAttnWgSplits = 8;
+// the XCD-local merge (AttnDecodeParams::xl_ctr) is used up to this many
+// splits: one wave merges them one after another, and past about two rounds
+// of requests a merge launch of its own finishes sooner
+constexpr int kAttnXcdMergeMaxSplits = 16;
 
 struct AttnDecodeParams {
     const float *q;             // fp32 [B][n_q][d]
@@ -90,10 +94,21 @@ struct AttnDecodeParams {
     int64_t kv_bstride;
     const int32_t *pos;         // [B]: attend to keys 0..pos[b]
     int B, n_q, n_kv, d, lmax_pad, splits;
-    float *part;                // [B][n_q][splits][d + 2]
+    float *part;                // [B][n_q][splits][attn_part_stride(d)]: o[d], m, l, padding
     float *out;                 // fp32 [B][n_q * d]
+    // not NULL: the splits of one (sequence, KV group) run on one XCD (the
+    // grid is laid out for workgroup i to run on XCD i mod 8) and the last
+    // one to finish merges them through that XCD's L2; one counter per
+    // (sequence, KV group), left at zero
+    int *xl_ctr;
 };
+// floats per (head, split) record of the attention partials: o, m, l and
+// padding to a multiple of 128 bytes, so that no two records share a cache line
+constexpr int attn_part_stride(int d) { return d + 32; }
 void launch_attn_decode(const AttnDecodeParams &p, hipStream_t s);
+// Whether workgroup i of a launch runs on XCD i mod 8 (what an XCD-local merge
+// needs): a probe grid records each workgroup's XCD; *ok set from that.
+hipError_t probe_xcd_round_robin(hipStream_t s, bool *ok);
 
 // ----------------------------------------------------------------------------
 // Heads: confidence gate, top-p sampler.

@@ -68,6 +68,8 @@ struct pipo_ctx {
     uint16_t *xh, *xl;    // decode GEMV input planes for larger batches [Bmax][Kmax]
     float *gpart; int64_t gpart_cap;   // decode GEMV k-range partial sums
     int n_cu;             // compute units: workgroups of the batch-1 GEMV
+    int32_t *xl_ctr = nullptr;   // decode attention: per (sequence, KV group) split counters, kept at zero
+    bool xl_merge = false;       // merge the attention splits on their XCD (placement probed at init)
     int dev = 0;          // the device the context lives on
     void *scratch = nullptr;   // that device's address of the static scratch (pipo_decode_step_noalloc)
     uint64_t *best_b, *best_d, *seeds;
@@ -355,7 +357,8 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         c->step = a.take<int32_t>(B);
         c->out = a.take<pipo_pair>(B);
         c->out_tok = a.take<int32_t>(B);
-        c->apart = a.take<float>((int64_t)B * c->nq * S_att * (c->d + 2));
+        c->apart = a.take<float>((int64_t)B * c->nq * S_att * attn_part_stride(c->d));
+        c->xl_ctr = a.take<int32_t>((int64_t)B * c->nkv);
         c->p_xin = a.take<uint16_t>(mcap * 2 * H);
         c->p_x = a.take<float>(mcap * H);
         c->p_xn = a.take<uint16_t>(mcap * H);
@@ -442,6 +445,15 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
         const hipError_t se = scratch_address(dev, &c->scratch);
         if (se != hipSuccess)
             return cleanup_fail(fail(c, PIPO_EHIP, "scratch address on device %d: %s", dev, hipGetErrorString(se)));
+        // PIPO_NO_XCD_MERGE=1: always merge the attention splits in a kernel of their own
+        const char *nx = getenv("PIPO_NO_XCD_MERGE");
+        bool rr = false;
+        if (!(nx && nx[0] == '1')) {
+            const hipError_t pe = probe_xcd_round_robin(s, &rr);
+            if (pe != hipSuccess)
+                return cleanup_fail(fail(c, PIPO_EHIP, "XCD placement probe: %s", hipGetErrorString(pe)));
+        }
+        c->xl_merge = rr;
     }
     const char *ng = getenv("PIPO_NO_GRAPH");
     const char *ck = getenv("PIPO_CHECK");
@@ -495,6 +507,7 @@ static void enqueue_layer(pipo_ctx *c, const LayerW &lw, uint16_t *kc, uint16_t 
     }
     ap.B = B; ap.n_q = c->nq; ap.n_kv = c->nkv; ap.d = c->d; ap.lmax_pad = c->lmax_pad;
     ap.splits = attn_splits(c, B); ap.part = c->apart; ap.out = c->attn_out;
+    ap.xl_ctr = c->xl_merge && ap.splits != kAttnWgSplits && ap.splits <= kAttnXcdMergeMaxSplits ? c->xl_ctr : nullptr;
     { PROF(PIPO_K_ATTN_DECODE); launch_attn_decode(ap, s); }
 
     p = base;
@@ -994,7 +1007,7 @@ extern "C" int pipo_decode_step_noalloc(pipo_ctx *c, const int32_t *d_in_pairs, 
         return fail(c, PIPO_ECAPACITY, "KV cache full: %d latents, max_latent %d", c->len, c->cfg.max_latent);
     if (!c->scratch) return fail(c, PIPO_EHIP, "no scratch address for device %d", c->dev);
     const int64_t attn_floats =
-        round_up((int64_t)c->batch * c->nq * attn_splits(c, c->batch) * (c->d + 2), 64);
+        round_up((int64_t)c->batch * c->nq * attn_splits(c, c->batch) * attn_part_stride(c->d), 64);
     const int64_t cap_floats = (int64_t)(kScratchBytes / sizeof(float));
     if (attn_floats > cap_floats)
         return fail(c, PIPO_ECAPACITY, "attention partials of %lld bytes exceed the %zu-byte scratch",

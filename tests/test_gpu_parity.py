@@ -218,6 +218,25 @@ def test_workgroup_merged_attention_unfused(torch, hidden, nq, nkv, d, B):
     m.close()
 
 
+@pytest.mark.parametrize("max_latent,n,xcd", [(26 * 32, 40, "1"), (26 * 32, 300, "0"), (32 * 32, 300, "1"),
+                                              (34 * 32, 300, "1")])
+def test_attention_split_merges(torch, monkeypatch, max_latent, n, xcd):
+    """4B width, batch 2: 13, 16 and 17 key splits per (sequence, KV group).
+    Up to 16 the last split to finish merges them on its XCD (13 leaves a
+    ragged second round of eight; with a 40-token prompt every split of the
+    first round is empty); 17, or PIPO_NO_XCD_MERGE=1, takes the merge
+    launch."""
+    monkeypatch.setenv("PIPO_NO_XCD_MERGE", "0" if xcd == "1" else "1")
+    cfg = DENSE_4B.with_layers(1)
+    B, steps = 2, 3
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=25)
+    m = _model(cfg, seed=13, max_batch=B, max_latent=max_latent, prefill_chunk=4096)
+    W = O.OracleWeights.generate(cfg, seed=13, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, O.Sampling(tau=0.95), log)
+    rep.check()
+    m.close()
+
+
 def test_4b_width_batch20_top_p(torch):
     """4B width, two layers, 20 sequences (two 16-column MFMA tiles), T 0.6,
     top-p 0.95, tau 0.7, per-sequence seeds."""

@@ -29,6 +29,10 @@
  *     created, that context launches every kernel eagerly (no HIP graph),
  *     waits for the stream after each one, and returns the first failure as
  *     PIPO_EHIP with its launch site in pipo_last_error().
+ *   - Decode attention merges its key splits through the L2 of the XCD they
+ *     ran on when a probe at context creation finds workgroups placed on the
+ *     eight XCDs in turn; PIPO_NO_XCD_MERGE=1 at creation keeps the separate
+ *     merge launch (same results up to rounding order).
  */
 #ifndef PIPO_H
 #define PIPO_H

@@ -79,9 +79,9 @@ constexpr int kAttnFusedRanges = 4;
 // are the splits, merged in LDS (no k_attn_merge launch)
 constexpr int kAttnWgSplits = 8;
 // the XCD-local merge (AttnDecodeParams::xl_ctr) is used up to this many
-// splits: one wave merges them one after another, and past about two rounds
-// of requests a merge launch of its own finishes sooner
-constexpr int kAttnXcdMergeMaxSplits = 16;
+// splits: one wave merges them eight at a time, and past three rounds of
+// requests a merge launch of its own finishes sooner
+constexpr int kAttnXcdMergeMaxSplits = 24;
 
 struct AttnDecodeParams {
     const float *q;             // fp32 [B][n_q][d]

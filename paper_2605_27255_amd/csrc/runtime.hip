@@ -466,13 +466,20 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
 // Key splits of the decode attention: at most two 32-key blocks per split at
 // full capacity (both blocks are prefetched), and no more splits than it takes
 // to give the machine about 1024 waves; at most 64 (the merge kernel's limit).
+// Where at most four blocks per split bring the count within the XCD-local
+// merge's limit, the limit it is: the merge launch saved outweighs the
+// longer splits (4B at batch 1 and 73 blocks: 37 splits and the launch
+// 0.430 ms per step, 24 splits merged on their XCD 0.381 ms; 20: 0.388,
+// 16: 0.393, 12: 0.415).
 static int attn_splits(const pipo_ctx *c, int B) {
     // a workgroup per (sequence, KV group) once they fill every CU: its eight
     // waves split the keys and merge in LDS, with no merge launch
     if (B * c->nkv >= c->n_cu) return kAttnWgSplits;
     const int blocks = (c->cfg.max_latent + 31) / 32;
-    int sp = (blocks + 1) / 2;
     const int cap = (1024 + B * c->nkv - 1) / (B * c->nkv);
+    int sp = (blocks + 1) / 2;
+    if (c->xl_merge && sp > kAttnXcdMergeMaxSplits && blocks <= 4 * kAttnXcdMergeMaxSplits)
+        sp = kAttnXcdMergeMaxSplits;
     sp = sp < cap ? sp : cap;
     return sp < 1 ? 1 : (sp > 64 ? 64 : sp);
 }

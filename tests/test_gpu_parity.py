@@ -218,14 +218,16 @@ def test_workgroup_merged_attention_unfused(torch, hidden, nq, nkv, d, B):
     m.close()
 
 
-@pytest.mark.parametrize("max_latent,n,xcd", [(26 * 32, 40, "1"), (26 * 32, 300, "0"), (32 * 32, 300, "1"),
-                                              (34 * 32, 300, "1")])
+@pytest.mark.parametrize("max_latent,n,xcd", [(26 * 32, 40, "1"), (48 * 32, 300, "1"), (90 * 32, 5000, "1"),
+                                              (90 * 32, 5000, "0"), (100 * 32, 300, "1")])
 def test_attention_split_merges(torch, monkeypatch, max_latent, n, xcd):
-    """4B width, batch 2: 13, 16 and 17 key splits per (sequence, KV group).
-    Up to 16 the last split to finish merges them on its XCD (13 leaves a
-    ragged second round of eight; with a 40-token prompt every split of the
-    first round is empty); 17, or PIPO_NO_XCD_MERGE=1, takes the merge
-    launch."""
+    """4B width, batch 2: the decode attention's key splits and their merges.
+    13 splits (a 40-token prompt leaves every split of the first round of
+    eight empty) and 24 (three rounds) merge on their XCD; at 90 blocks two
+    per split would make 45, so 24 splits of three or four blocks, every one
+    holding keys of the 2500-latent prompt, merge on their XCD, or, with
+    PIPO_NO_XCD_MERGE=1, 45 splits and the merge launch; at 100 blocks, 50
+    splits and the merge launch."""
     monkeypatch.setenv("PIPO_NO_XCD_MERGE", "0" if xcd == "1" else "1")
     cfg = DENSE_4B.with_layers(1)
     B, steps = 2, 3

@@ -92,7 +92,10 @@ __device__ void xl_merge(const AttnDecodeParams &p, int b, int kvh, int qpg, int
 // (sequence, KV group) whose NW waves are its splits; their partials are
 // combined in LDS in split order and the workgroup writes the output rows.
 template <int D, bool FUSED, int NW>
-__global__ __launch_bounds__(64 * NW) void k_attn_decode(AttnDecodeParams p) {
+// (at most 256 registers a lane, so that two waves fit on a SIMD: 9B at batch
+// 8 took 2.86 ms of attention per pair step this way, 2.88 with the 278 the
+// compiler chooses otherwise)
+__global__ __launch_bounds__(64 * NW, 2) void k_attn_decode(AttnDecodeParams p) {
     constexpr int NC = D / 32;   // 32-wide d chunks (QK^T k-steps)
     constexpr int NT = D / 16;   // 16-wide d tiles (PV output tiles)
     const int lane = threadIdx.x & 63, j = lane & 15, g = lane >> 4;

@@ -465,7 +465,10 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
 
 // Key splits of the decode attention: at most two 32-key blocks per split at
 // full capacity (both blocks are prefetched), and no more splits than it takes
-// to give the machine about 1024 waves; at most 64 (the merge kernel's limit).
+// to give the machine about 768 waves, three per CU; at most 64 (the merge
+// kernel's limit).  (9B at batch 8, 64 (sequence, KV group) pairs and 517
+// blocks: 9 to 16 splits took 3.04, 2.86, 2.82, 2.76, 2.97, 2.87 (14) and
+// 2.86 ms of attention per pair step: 12 splits, three waves on every CU.)
 // Where at most four blocks per split bring the count within the XCD-local
 // merge's limit, the limit it is: the merge launch saved outweighs the
 // longer splits (4B at batch 1 and 73 blocks: 37 splits and the launch
@@ -476,7 +479,7 @@ static int attn_splits(const pipo_ctx *c, int B) {
     // waves split the keys and merge in LDS, with no merge launch
     if (B * c->nkv >= c->n_cu) return kAttnWgSplits;
     const int blocks = (c->cfg.max_latent + 31) / 32;
-    const int cap = (1024 + B * c->nkv - 1) / (B * c->nkv);
+    const int cap = (768 + B * c->nkv - 1) / (B * c->nkv);
     int sp = (blocks + 1) / 2;
     if (c->xl_merge && sp > kAttnXcdMergeMaxSplits && blocks <= 4 * kAttnXcdMergeMaxSplits)
         sp = kAttnXcdMergeMaxSplits;

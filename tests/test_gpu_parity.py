@@ -226,8 +226,8 @@ def test_attention_split_merges(torch, monkeypatch, max_latent, n, xcd):
     eight empty) and 24 (three rounds) merge on their XCD; at 90 blocks two
     per split would make 45, so 24 splits of three or four blocks, every one
     holding keys of the 2500-latent prompt, merge on their XCD, or, with
-    PIPO_NO_XCD_MERGE=1, 45 splits and the merge launch; at 100 blocks, 50
-    splits and the merge launch."""
+    PIPO_NO_XCD_MERGE=1, 45 splits and the merge launch; at 100 blocks, 48
+    splits (the three-waves-per-CU cap) and the merge launch."""
     monkeypatch.setenv("PIPO_NO_XCD_MERGE", "0" if xcd == "1" else "1")
     cfg = DENSE_4B.with_layers(1)
     B, steps = 2, 3

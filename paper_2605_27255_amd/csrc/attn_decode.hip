@@ -28,7 +28,7 @@ namespace pipo {
 // exp2(M_old - M_new) as it rises; then o / L.
 template <int D>
 __device__ void xl_merge(const AttnDecodeParams &p, int b, int kvh, int qpg, int S, int lane) {
-    constexpr int RS = attn_part_stride(D), DPL = D / 16, XU = 8;
+    constexpr int RS = attn_part_stride(D), DPL = D / 16, XU = 12;
     const float *rec = p.part + ((int64_t)b * p.n_q + kvh * qpg) * S * RS;   // [qpg][S][RS]
     const int d0 = (lane & 15) * DPL;
     for (int h0 = 0; h0 < qpg; h0 += 4) {

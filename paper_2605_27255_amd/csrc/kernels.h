@@ -79,7 +79,7 @@ constexpr int kAttnFusedRanges = 4;
 // are the splits, merged in LDS (no k_attn_merge launch)
 constexpr int kAttnWgSplits = 8;
 // the XCD-local merge (AttnDecodeParams::xl_ctr) is used up to this many
-// splits: one wave merges them eight at a time, and past three rounds of
+// splits: one wave merges them twelve at a time, and past two rounds of
 // requests a merge launch of its own finishes sooner
 constexpr int kAttnXcdMergeMaxSplits = 24;
 

@@ -223,7 +223,7 @@ def test_workgroup_merged_attention_unfused(torch, hidden, nq, nkv, d, B):
 def test_attention_split_merges(torch, monkeypatch, max_latent, n, xcd):
     """4B width, batch 2: the decode attention's key splits and their merges.
     13 splits (a 40-token prompt leaves every split of the first round of
-    eight empty) and 24 (three rounds) merge on their XCD; at 90 blocks two
+    twelve empty) and 24 (two rounds) merge on their XCD; at 90 blocks two
     per split would make 45, so 24 splits of three or four blocks, every one
     holding keys of the 2500-latent prompt, merge on their XCD, or, with
     PIPO_NO_XCD_MERGE=1, 45 splits and the merge launch; at 100 blocks, 48

@@ -10,10 +10,12 @@
 // 32-key tile in that key order (vslot in device_common.h).  The query and
 // the probabilities enter the MFMAs as bf16 pairs hi + lo (two MFMAs each),
 // so only the bf16 KV cache itself limits the precision.  Per-split results
-// (m, l, o) either go to a partial buffer that a second kernel merges per
-// head in split order (the kernel boundary makes every split's partial
-// visible), or, when the (sequence, KV group) pairs fill the machine, stay in
-// one workgroup whose waves are the splits and merge through LDS.
+// (m, l, o) are merged in split order in one of three ways: when the
+// (sequence, KV group) pairs fill the machine they stay in one workgroup
+// whose waves are the splits and merge through LDS; up to 24 splits the
+// splits of a pair run on one XCD and the last to finish merges their
+// records through that XCD's L2; otherwise a second kernel merges the
+// records per head (the kernel boundary makes every split's record visible).
 #include "device_common.h"
 #include <vector>
 
@@ -88,13 +90,13 @@ __device__ void xl_merge(const AttnDecodeParams &p, int b, int kvh, int qpg, int
 // registers (one online-softmax step after its blocks, which stop before it)
 // and stores the key and value to the cache at its end, for later steps.
 // NW: waves per workgroup.  1: one wave per (sequence, KV group, split),
-// partials to global memory for k_attn_merge.  NW > 1: one workgroup per
-// (sequence, KV group) whose NW waves are its splits; their partials are
-// combined in LDS in split order and the workgroup writes the output rows.
+// partial records to global memory, merged on the XCD (xl_ctr) or by
+// k_attn_merge.  NW > 1: one workgroup per (sequence, KV group) whose NW
+// waves are its splits; their partials are combined in LDS in split order and
+// the workgroup writes the output rows.  At most 256 registers a lane, so
+// that two waves fit on a SIMD (9B at batch 8: 2.86 ms of attention per pair
+// step this way, 2.88 with the 278 the compiler chooses otherwise).
 template <int D, bool FUSED, int NW>
-// (at most 256 registers a lane, so that two waves fit on a SIMD: 9B at batch
-// 8 took 2.86 ms of attention per pair step this way, 2.88 with the 278 the
-// compiler chooses otherwise)
 __global__ __launch_bounds__(64 * NW, 2) void k_attn_decode(AttnDecodeParams p) {
     constexpr int NC = D / 32;   // 32-wide d chunks (QK^T k-steps)
     constexpr int NT = D / 16;   // 16-wide d tiles (PV output tiles)

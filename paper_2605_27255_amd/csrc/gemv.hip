@@ -513,7 +513,11 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
             resid[bt] = pr.resid[bt];
             if (EPI == EPI_RESID && r > 0) {   // later groups read their residual rows here
                 const int b = bt * 16 + j;
-                resid[bt] = *(const f32x4 *)(p.out + ((lead && b < B) ? (int64_t)b * p.N + strip * 16 + 4 * g : 0));
+                f32x4 v = *(const f32x4 *)(p.out + ((lead && b < B) ? (int64_t)b * p.N + strip * 16 + 4 * g : 0));
+                // (opaque, so that the two sources stay two values: merged into
+                // one load through a chosen pointer they would put pr in scratch)
+                asm volatile("" : "+v"(v));
+                resid[bt] = v;
             }
         }
         gemv_epilogue<NBT, EPI>(p, fin, resid, strip, lead);

@@ -296,12 +296,28 @@ __device__ __forceinline__ void tile_mma(f32x4 (&acc)[NAcc<PRO>::n][NBT], u32x4 
     }
 }
 
+// RoPE inputs of one strip, requested ahead of its epilogue (the batch-1
+// GEMV's strip groups): the position of each column's sequence and the
+// cos / sin quadruple of this lane's rows.
+template <int NBT>
+struct QkvPre {
+    int pos[NBT];
+    float4 cs[NBT], sn[NBT];
+};
+
+// The RoPE rotation index of v = 0 for lane group g in a q or k strip.
+__device__ __forceinline__ int rope_jr(int strip, int qs, int hs, int g) {
+    const int sidx = strip < qs ? strip : strip - qs;
+    return 8 * (sidx % hs) + 4 * (g & 1);
+}
+
 // Fused epilogues, one wave per strip (lanes (j, g) hold rows row0 + v of
 // column b = 16 bt + j): bias or residual add with sum-of-squares parts,
-// SwiGLU, RoPE + KV append, logits + argmax key.
+// SwiGLU, RoPE + KV append, logits + argmax key.  pre (EPI_QKV): the RoPE
+// inputs already in registers; NULL: read here.
 template <int NBT, int EPI>
 __device__ __forceinline__ void gemv_epilogue(const GemvParams &p, f32x4 (&fin)[NBT], const f32x4 (&resid)[NBT],
-                                              int strip, bool lead) {
+                                              int strip, bool lead, const QkvPre<NBT> *pre = nullptr) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int j = lane & 15, g = lane >> 4;
     const int nstrips = p.N >> 4;
@@ -392,15 +408,15 @@ __device__ __forceinline__ void gemv_epilogue(const GemvParams &p, f32x4 (&fin)[
 #pragma unroll
             for (int v = 0; v < 4; ++v) other[v] = __shfl_xor(fin[bt][v], 32);
             if (b >= B) continue;
-            const int pos = p.pos[b];
+            const int pos = pre ? pre->pos[bt] : p.pos[b];
             if (strip < qs + kvs) {
                 const bool isq = strip < qs;
                 const int sidx = isq ? strip : strip - qs;
                 const int head = sidx / hs, t = sidx - head * hs;
                 const int jr = 8 * t + 4 * (g & 1);         // rotation index of v = 0
                 const int dim0 = (g < 2) ? jr : (d >> 1) + jr;
-                const float4 cs = *(const float4 *)(p.rope_cos + (int64_t)pos * (d >> 1) + jr);
-                const float4 sn = *(const float4 *)(p.rope_sin + (int64_t)pos * (d >> 1) + jr);
+                const float4 cs = pre ? pre->cs[bt] : *(const float4 *)(p.rope_cos + (int64_t)pos * (d >> 1) + jr);
+                const float4 sn = pre ? pre->sn[bt] : *(const float4 *)(p.rope_sin + (int64_t)pos * (d >> 1) + jr);
                 const float c4[4] = {cs.x, cs.y, cs.z, cs.w}, s4[4] = {sn.x, sn.y, sn.z, sn.w};
                 float r[4];
 #pragma unroll
@@ -468,6 +484,23 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
 #pragma unroll
         for (int bt = 0; bt < NBT; ++bt) acc[a][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // EPI_QKV: the RoPE inputs of group r's strip, requested while the group
+    // streams (the positions once, with the prologue), so that its epilogue
+    // waits on nothing
+    QkvPre<NBT> qpre;
+    auto rope_fetch = [&](int r) {
+        const int strip = strip_of(r);
+        const int hs = p.d >> 4, qs = p.n_q * hs, kvs = p.n_kv * hs;
+        const bool rot = strip < qs + kvs;
+        const int jr = rope_jr(rot ? strip : 0, qs, hs, g);
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int64_t at = (int64_t)qpre.pos[bt] * (p.d >> 1) + jr;
+            qpre.cs[bt] = *(const float4 *)(p.rope_cos + (rot ? at : 0));
+            qpre.sn[bt] = *(const float4 *)(p.rope_sin + (rot ? at : 0));
+        }
+    };
+
     // Strip group r ends: KS partial sums reduced in wave order, RMSNorm
     // scalar, epilogue; the accumulators restart at zero.
     Pro<NBT, PRO, EPI> pr;
@@ -520,7 +553,12 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
                 resid[bt] = v;
             }
         }
-        gemv_epilogue<NBT, EPI>(p, fin, resid, strip, lead);
+        if constexpr (EPI == EPI_QKV) {
+            gemv_epilogue<NBT, EPI>(p, fin, resid, strip, lead, &qpre);
+            if (r + 1 < ngrp) rope_fetch(r + 1);   // the next group's, ahead of its stream's end
+        } else {
+            gemv_epilogue<NBT, EPI>(p, fin, resid, strip, lead);
+        }
     };
 
     // ---- wave-private X, then one pipelined pass over every group's tiles ----
@@ -534,6 +572,13 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     uint16_t *xh = xs + wave * B * rstride, *xl = xh + xplane;
     // 1. prologue / epilogue inputs, before any weights
     pro_load<NBT, PRO, EPI>(p, pr, ks == 0 && strip0 < nstrips, row00, cm, 0);
+    if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+        for (int bt = 0; bt < NBT; ++bt) {
+            const int b = bt * 16 + j;
+            qpre.pos[bt] = p.pos[b < B ? b : 0];
+        }
+    }
     // 2. two batches of weights
     u32x4 ra[U], rb[U];
     auto wptr = [&](int q, int u) -> const u32x4 * {
@@ -551,6 +596,7 @@ __global__ __launch_bounds__(512) void k_gemv(GemvParams p) {
     // 3. scalars and this wave's slices of X; the MTP scales its halves
     //    before the reduction, so it waits for every wave's scalars
     pro_finish<NBT, PRO, EPI>(p, pr, cm, 0, xh, xl, sc0, sc1);
+    if constexpr (EPI == EPI_QKV) rope_fetch(0);
     if (PRO == PRO_MTP) __syncthreads();
     // 4. stream: consume one batch while the next is in flight
     auto mma_batch = [&](const u32x4 (&R)[U], int q) {

@@ -239,6 +239,26 @@ def test_attention_split_merges(torch, monkeypatch, max_latent, n, xcd):
     m.close()
 
 
+@pytest.mark.parametrize("B,max_latent", [(3, 300), (5, 1200)])
+def test_attention_xcd_merge_ragged_pair_grid(torch, B, max_latent):
+    """Head dim 128 with four KV groups: 3 x 4 = 12 and 5 x 4 = 20 (sequence,
+    KV group) pairs, not a multiple of eight, so the XCD-merged grid has
+    workgroups past the last pair that leave at once; 5 and 19 splits of one
+    or two blocks each over prompts of 400 and 2000 tokens, T 0.6, top-p
+    0.9."""
+    cfg = ModelConfig(n_layers=1, hidden=1024, n_q_heads=16, n_kv_heads=4, head_dim=128, ffn=2048, vocab=4096,
+                      rope_base=1e4)
+    n = 400 if B == 3 else 2000
+    steps = 3
+    prompts = rspec.prompt_tokens(B, n, cfg.vocab, seed=27)
+    smp = O.Sampling(tau=0.8, temperature=0.6, top_p=0.9, seeds=tuple(300 + b for b in range(B)))
+    m = _model(cfg, seed=14, max_batch=B, max_latent=max_latent, prefill_chunk=4096)
+    W = O.OracleWeights.generate(cfg, seed=14, precision="bf16")
+    rep, _ = run_parity(m, W, prompts, steps, smp, log)
+    rep.check()
+    m.close()
+
+
 def test_4b_width_batch20_top_p(torch):
     """4B width, two layers, 20 sequences (two 16-column MFMA tiles), T 0.6,
     top-p 0.95, tau 0.7, per-sequence seeds."""

@@ -76,8 +76,9 @@ int gemv_num_groups(int N);
 // round trip of partial loads in its prologue)
 constexpr int kAttnFusedRanges = 4;
 // splits == kAttnWgSplits: one workgroup per (sequence, KV group) whose waves
-// are the splits, merged in LDS (no k_attn_merge launch)
-constexpr int kAttnWgSplits = 8;
+// are the splits, merged in LDS (no k_attn_merge launch); four (4B at batch
+// 32: 9.20 ms per pair step against 9.26 with eight, one wave per SIMD)
+constexpr int kAttnWgSplits = 4;
 // the XCD-local merge (AttnDecodeParams::xl_ctr) is used up to this many
 // splits: one wave merges them twelve at a time, and past two rounds of
 // requests a merge launch of its own finishes sooner

@@ -475,8 +475,8 @@ extern "C" int pipo_init_weights(const pipo_config *cfg, uint64_t seed, void *st
 // 0.430 ms per step, 24 splits merged on their XCD 0.381 ms; 20: 0.388,
 // 16: 0.393, 12: 0.415).
 static int attn_splits(const pipo_ctx *c, int B) {
-    // a workgroup per (sequence, KV group) once they fill every CU: its eight
-    // waves split the keys and merge in LDS, with no merge launch
+    // a workgroup per (sequence, KV group) once they fill every CU: its
+    // kAttnWgSplits waves split the keys and merge in LDS, with no merge launch
     if (B * c->nkv >= c->n_cu) return kAttnWgSplits;
     const int blocks = (c->cfg.max_latent + 31) / 32;
     const int cap = (768 + B * c->nkv - 1) / (B * c->nkv);

@@ -203,7 +203,7 @@ def test_head_dim_64_attention_finishes_qkv(torch, hidden, nq, nkv):
 @pytest.mark.parametrize("hidden,nq,nkv,d,B", [(2560, 32, 8, 128, 64), (2048, 32, 8, 64, 32)])
 def test_workgroup_merged_attention_unfused(torch, hidden, nq, nkv, d, B):
     """Batch x KV groups >= 256, so the decode attention runs one workgroup per
-    (sequence, KV group) and merges its eight splits in LDS, with the QKV
+    (sequence, KV group) and merges its splits (one per wave) in LDS, with the QKV
     GEMV finishing its own k-ranges (five ranges at 4B width and batch 64,
     eight at head dim 64 and batch 32): the unfused form of that kernel, at
     d = 128 and 64.  The oracle replays the first and the last sequence."""
